@@ -1,0 +1,294 @@
+// k_quant.hip -- uniform b-bit min-max quantization (Sec. 2.2 of the paper),
+// optionally wrapped in error feedback (Sec. 2.4), and its decompression.
+//
+// Per group (a sample or a token row): lo = min, hi = max (a -0 reads as +0),
+//   code = min(rint((v - lo) / (hi - lo) * (2^b - 1)), 2^b - 1),
+//   meta = (lo, (hi - lo) / (2^b - 1)),
+// codes packed LSB-first into little-endian 32-bit words; the receiver
+// rebuilds lo + code * scale.  b = 32 sends the binary32 values themselves.
+// A group is spread over P workgroups that exchange their partial min / max
+// through per-workgroup slots and one cross-workgroup barrier; the group's
+// values stay in registers between the reduction and the encode.
+#include <algorithm>
+#include <type_traits>
+
+#include "tc_internal.hpp"
+#include "tc_select.hpp"
+
+namespace tc {
+
+constexpr int QVPT = 32;   // elements per thread: 32 * b bits is a whole number of words
+
+__host__ __device__ constexpr uint64_t quant_group_mem_words(uint32_t P) { return 64u + 2u * P; }
+
+template <int B>
+__device__ __forceinline__ void pack_codes(const uint32_t (&c)[QVPT], uint32_t (&w)[QVPT * B / 32]) {
+#pragma unroll
+  for (int j = 0; j < QVPT * B / 32; ++j) w[j] = 0u;
+#pragma unroll
+  for (int i = 0; i < QVPT; ++i) {
+    const int bit = i * B;
+    w[bit >> 5] |= c[i] << (bit & 31);
+    if ((bit & 31) + B > 32) w[(bit >> 5) + 1] |= c[i] >> (32 - (bit & 31));
+  }
+}
+
+template <int B>
+__device__ __forceinline__ void unpack_codes(const uint32_t (&w)[QVPT * B / 32], uint32_t (&c)[QVPT]) {
+  constexpr uint32_t M = (1u << B) - 1u;
+#pragma unroll
+  for (int i = 0; i < QVPT; ++i) {
+    const int bit = i * B;
+    uint32_t x = w[bit >> 5] >> (bit & 31);
+    if ((bit & 31) + B > 32) x |= w[(bit >> 5) + 1] << (32 - (bit & 31));
+    c[i] = x & M;
+  }
+}
+
+template <typename InT, typename OutT, int B, bool EF, int NT>
+__global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
+  using R = typename Elem<InT>::raw;
+  constexpr int WPT = (B == 32) ? QVPT : QVPT * B / 32;
+  constexpr uint64_t CH = (uint64_t)NT * QVPT;
+  __shared__ float mm[2 * (NT / WAVE)];
+
+  const uint32_t P = a.P;
+  const uint32_t group = blockIdx.x / P, part = blockIdx.x % P;
+  const uint32_t n_groups = gridDim.x / P;
+  uint32_t* bar = nullptr;
+  uint32_t* slots = nullptr;
+  if (P > 1) {
+    bar = a.ws + (uint64_t)group * quant_group_mem_words(P);
+    slots = bar + 64;
+  }
+
+  for (uint64_t grp = group; grp < a.n_grp; grp += n_groups) {
+    const uint64_t c0 = (uint64_t)part * CH + (uint64_t)threadIdx.x * QVPT;
+    const int nv = (int)min((uint64_t)QVPT, sat_sub(a.G, c0));
+    const uint64_t off = grp * a.G + c0;
+    float v[QVPT];
+    {
+      R xr[QVPT];
+      if (nv > 0) load_run_partial<R, QVPT>((const R*)a.x + off, nv, R{}, xr);
+      if constexpr (EF) {
+        float er[QVPT];
+        if (nv > 0) load_run_partial<float, QVPT>(a.e + off, nv, 0.0f, er);
+#pragma unroll
+        for (int i = 0; i < QVPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) + er[i] : 0.0f;
+      } else {
+#pragma unroll
+        for (int i = 0; i < QVPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) : 0.0f;
+      }
+    }
+
+    uint32_t w[WPT];
+    float lo = 0.0f, scale = 0.0f;
+    if constexpr (B == 32) {
+#pragma unroll
+      for (int i = 0; i < QVPT; ++i) w[i] = __float_as_uint(v[i]);
+    } else {
+      // ---- min / max of the group
+      lo = __int_as_float(0x7F800000);    // +inf
+      float hi = __int_as_float(0xFF800000);  // -inf
+#pragma unroll
+      for (int i = 0; i < QVPT; ++i)
+        if (i < nv) { lo = fminf(lo, v[i]); hi = fmaxf(hi, v[i]); }
+      block_minmax<NT>(lo, hi, mm);
+      if (P > 1) {
+        if (threadIdx.x == 0) {
+          st_agent(&slots[2 * part], __float_as_uint(lo));
+          st_agent(&slots[2 * part + 1], __float_as_uint(hi));
+        }
+        group_barrier(bar, P);
+        lo = __uint_as_float(ld_agent(&slots[0]));
+        hi = __uint_as_float(ld_agent(&slots[1]));
+        for (uint32_t j = 1; j < P; ++j) {
+          lo = fminf(lo, __uint_as_float(ld_agent(&slots[2 * j])));
+          hi = fmaxf(hi, __uint_as_float(ld_agent(&slots[2 * j + 1])));
+        }
+        // no workgroup may overwrite its slot for the next group before all
+        // have read this one
+        group_barrier(bar, P);
+      }
+      lo = lo + 0.0f;   // -0 reads as +0
+      hi = hi + 0.0f;
+      constexpr uint32_t LV = (1u << B) - 1u;
+      uint32_t c[QVPT];
+      if (hi == lo) {
+#pragma unroll
+        for (int i = 0; i < QVPT; ++i) c[i] = 0u;
+        scale = 0.0f;
+      } else {
+        const float range = hi - lo;
+        scale = range / (float)LV;
+#pragma unroll
+        for (int i = 0; i < QVPT; ++i) {
+          const float u = (v[i] - lo) / range;
+          const float t = u * (float)LV;
+          const uint32_t q = (uint32_t)rintf(t);
+          c[i] = (i < nv) ? min(q, LV) : 0u;
+        }
+      }
+      pack_codes<B>(c, w);
+      if constexpr (EF) {
+#pragma unroll
+        for (int i = 0; i < QVPT; ++i) {
+          const float prod = (float)c[i] * scale;
+          const float xh = lo + prod;
+          v[i] = v[i] - through<OutT>(xh);      // the residual, in place
+        }
+      }
+    }
+    if constexpr (B == 32 && EF) {
+#pragma unroll
+      for (int i = 0; i < QVPT; ++i) v[i] = v[i] - through<OutT>(v[i]);
+    }
+
+    // ---- outputs
+    const uint64_t wo = (B == 32) ? c0 : (c0 * (uint64_t)B) / 32u;
+    const int nw = (int)min((uint64_t)WPT, sat_sub(a.wpg, wo));
+    if (nw > 0) store_run_partial<uint32_t, WPT>(a.codes + grp * a.wpg + wo, nw, w);
+    if (part == 0 && threadIdx.x == 0) {
+      a.meta[2 * grp] = lo;
+      a.meta[2 * grp + 1] = scale;
+    }
+    if constexpr (EF) {
+      if (nv > 0) store_run_partial<float, QVPT>(a.e + off, nv, v);
+    }
+  }
+  if (P > 1) group_exit<NT>(bar, P, slots, 2ull * P);
+}
+
+template <typename OutT, int B, int NT>
+__global__ __launch_bounds__(NT) void k_quant_unpack(UnpackArgs a) {
+  using R = typename Elem<OutT>::raw;
+  constexpr int WPT = (B == 32) ? QVPT : QVPT * B / 32;
+  constexpr uint64_t CH = (uint64_t)NT * QVPT;
+  const uint64_t nch = (a.G + CH - 1) / CH;
+  for (uint64_t wi = blockIdx.x; wi < a.n_grp * nch; wi += gridDim.x) {
+    const uint64_t grp = wi / nch, ch = wi % nch;
+    const uint64_t c0 = ch * CH + (uint64_t)threadIdx.x * QVPT;
+    const int nv = (int)min((uint64_t)QVPT, sat_sub(a.G, c0));
+    if (nv == 0) continue;
+    const uint64_t wo = (B == 32) ? c0 : (c0 * (uint64_t)B) / 32u;
+    const int nw = (int)min((uint64_t)WPT, sat_sub(a.wpg, wo));
+    uint32_t w[WPT];
+    load_run_partial<uint32_t, WPT>(a.codes + grp * a.wpg + wo, nw, 0u, w);
+    R y[QVPT];
+    if constexpr (B == 32) {
+#pragma unroll
+      for (int i = 0; i < QVPT; ++i) y[i] = Elem<OutT>::down(__uint_as_float(w[i]));
+    } else {
+      const float lo = a.meta[2 * grp], scale = a.meta[2 * grp + 1];
+      uint32_t c[QVPT];
+      unpack_codes<B>(w, c);
+#pragma unroll
+      for (int i = 0; i < QVPT; ++i) {
+        const float prod = (float)c[i] * scale;
+        y[i] = Elem<OutT>::down(lo + prod);
+      }
+    }
+    store_run_partial<R, QVPT>((R*)a.y + grp * a.G + c0, nv, y);
+  }
+}
+
+// ------------------------------------------------------------------ plans
+namespace {
+
+constexpr int BIG_NT = 512;
+constexpr int ROW_NT = 64;
+
+template <typename InT, typename OutT, bool EF, int NT>
+const void* pack_ptr_b(uint32_t b) {
+  switch (b) {
+    case 1: return (const void*)k_quant_pack<InT, OutT, 1, EF, NT>;
+    case 2: return (const void*)k_quant_pack<InT, OutT, 2, EF, NT>;
+    case 3: return (const void*)k_quant_pack<InT, OutT, 3, EF, NT>;
+    case 4: return (const void*)k_quant_pack<InT, OutT, 4, EF, NT>;
+    case 5: return (const void*)k_quant_pack<InT, OutT, 5, EF, NT>;
+    case 6: return (const void*)k_quant_pack<InT, OutT, 6, EF, NT>;
+    case 7: return (const void*)k_quant_pack<InT, OutT, 7, EF, NT>;
+    case 8: return (const void*)k_quant_pack<InT, OutT, 8, EF, NT>;
+    case 32: return (const void*)k_quant_pack<InT, OutT, 32, EF, NT>;
+  }
+  return nullptr;
+}
+
+template <typename InT>
+const void* pack_ptr(uint32_t b, bool ef, int nt) {
+  // the receiver's output dtype is the input dtype
+  if (nt == ROW_NT) return ef ? pack_ptr_b<InT, InT, true, ROW_NT>(b) : pack_ptr_b<InT, InT, false, ROW_NT>(b);
+  return ef ? pack_ptr_b<InT, InT, true, BIG_NT>(b) : pack_ptr_b<InT, InT, false, BIG_NT>(b);
+}
+
+const void* pick_pack(int dt, uint32_t b, bool ef, int nt) {
+  if (dt == DT_F32) return pack_ptr<float>(b, ef, nt);
+  if (dt == DT_BF16) return pack_ptr<bf16_t>(b, ef, nt);
+  return pack_ptr<f16_t>(b, ef, nt);
+}
+
+template <typename OutT>
+const void* unpack_ptr(uint32_t b) {
+  switch (b) {
+    case 1: return (const void*)k_quant_unpack<OutT, 1, 256>;
+    case 2: return (const void*)k_quant_unpack<OutT, 2, 256>;
+    case 3: return (const void*)k_quant_unpack<OutT, 3, 256>;
+    case 4: return (const void*)k_quant_unpack<OutT, 4, 256>;
+    case 5: return (const void*)k_quant_unpack<OutT, 5, 256>;
+    case 6: return (const void*)k_quant_unpack<OutT, 6, 256>;
+    case 7: return (const void*)k_quant_unpack<OutT, 7, 256>;
+    case 8: return (const void*)k_quant_unpack<OutT, 8, 256>;
+    case 32: return (const void*)k_quant_unpack<OutT, 32, 256>;
+  }
+  return nullptr;
+}
+
+}  // namespace
+
+SegPlan plan_quant(int dt, uint32_t bits, bool ef, uint64_t n_grp, uint64_t G) {
+  SegPlan p;
+  const uint32_t cus = (uint32_t)device_cus();
+  p.vpt = QVPT;
+  p.nt = (G <= (uint64_t)ROW_NT * QVPT) ? ROW_NT : BIG_NT;
+  const uint64_t CH = (uint64_t)p.nt * QVPT;
+  p.P = (uint32_t)((G + CH - 1) / CH);
+  int occ = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, pick_pack(dt, bits, ef, p.nt), p.nt, 0) != hipSuccess ||
+      occ < 1)
+    occ = 1;
+  const uint64_t cap = (uint64_t)occ * cus;
+  p.capacity = cap;
+  const uint64_t groups = std::min<uint64_t>(n_grp, std::max<uint64_t>(1, cap / p.P));
+  p.n_groups = (uint32_t)groups;
+  p.grid = (uint32_t)(groups * p.P);
+  const uint64_t ws_groups = std::min<uint64_t>(n_grp, std::max<uint64_t>(1, (uint64_t)cus * 32 / p.P));
+  p.ws_words = (p.P > 1) ? ws_groups * quant_group_mem_words(p.P) : 0;
+  return p;
+}
+
+hipError_t launch_quant(int dt, int out_dt, uint32_t bits, bool ef, const SegPlan& plan, const QuantArgs& args,
+                        hipStream_t st) {
+  if (out_dt != dt) return hipErrorInvalidValue;
+  const void* fn = pick_pack(dt, bits, ef, plan.nt);
+  if (!fn) return hipErrorInvalidValue;
+  QuantArgs a = args;
+  a.P = plan.P;
+  void* params[] = {&a};
+  return hipLaunchKernel(fn, dim3(plan.grid), dim3(plan.nt), params, 0, st);
+}
+
+hipError_t launch_unpack(int out_dt, uint32_t bits, const UnpackArgs& args, hipStream_t st) {
+  const void* fn = (out_dt == DT_F32) ? unpack_ptr<float>(bits)
+                 : (out_dt == DT_BF16) ? unpack_ptr<bf16_t>(bits) : unpack_ptr<f16_t>(bits);
+  if (!fn) return hipErrorInvalidValue;
+  const uint64_t CH = 256ull * QVPT;
+  const uint64_t work = args.n_grp * ((args.G + CH - 1) / CH);
+  const uint64_t grid = std::max<uint64_t>(1, std::min<uint64_t>(work, (uint64_t)device_cus() * 8));
+  UnpackArgs a = args;
+  void* params[] = {&a};
+  return hipLaunchKernel(fn, dim3((uint32_t)grid), dim3(256), params, 0, st);
+}
+
+TC_DEFINE_ERROR_READER(errors_quant)
+
+}  // namespace tc

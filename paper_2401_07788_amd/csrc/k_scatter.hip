@@ -1,0 +1,201 @@
+// k_scatter.hip -- the receiver side of TopK (Sec. 2.3: the dense tensor is
+// zero except at the sent indices) and of AQ-SGD (Sec. 2.5: the receiver adds
+// the sent change into its copy of the per-example buffer and hands on the
+// updated row).
+//
+// Each workgroup owns a chunk [c0, c1) of one segment's dense output.  It
+// finds the payload entries that fall into its chunk with a cooperative
+// search of the ascending index list, builds the chunk in LDS, and writes it
+// out with full-width stores, so the dense output is written exactly once.
+#include <algorithm>
+
+#include "tc_internal.hpp"
+#include "tc_select.hpp"
+
+namespace tc {
+
+constexpr int SC_NT = 256;
+constexpr int SC_VPT = 16;
+constexpr uint64_t SC_CH = (uint64_t)SC_NT * SC_VPT;
+
+// First j in [0, n) with a[j] >= c (n when none), for an ascending a.  Each
+// round probes NT evenly spaced entries in parallel and keeps the gap that
+// must hold the answer, so n entries take about log_{NT+1}(n) rounds.
+template <int NT>
+__device__ uint32_t block_lower_bound(const uint32_t* __restrict__ a, uint32_t n, uint32_t c, uint32_t* scratch) {
+  uint32_t lo = 0, hi = n;
+  while (lo < hi) {
+    const uint64_t len = hi - lo;
+    const uint32_t pt = lo + (uint32_t)(((uint64_t)(threadIdx.x + 1) * len) / (NT + 1));
+    const uint32_t below = (a[pt] < c) ? 1u : 0u;
+    const uint32_t cnt = block_sum<NT>(below, scratch);
+    const uint32_t nlo = cnt ? lo + (uint32_t)(((uint64_t)cnt * len) / (NT + 1)) + 1u : lo;
+    const uint32_t nhi = (cnt < (uint32_t)NT) ? lo + (uint32_t)(((uint64_t)(cnt + 1) * len) / (NT + 1)) : hi;
+    lo = nlo;
+    hi = max(nhi, nlo);   // equal bounds end the search even on unsorted input
+  }
+  return lo;
+}
+
+// the payload range [j0, j1) of the chunk [c0, c1)
+__device__ __forceinline__ void chunk_range(const uint32_t* ix, uint64_t k, uint64_t c0, uint64_t c1,
+                                            uint32_t* scratch, uint32_t& j0, uint32_t& j1) {
+  j0 = block_lower_bound<SC_NT>(ix, (uint32_t)k, (uint32_t)c0, scratch);
+  const uint32_t rest = (uint32_t)min(k - j0, c1 - c0);
+  j1 = j0 + block_lower_bound<SC_NT>(ix + j0, rest, (uint32_t)c1, scratch);
+}
+
+// MODE_VAL: wire values; MODE_CODES: b-bit codes of the kept list (one min-max
+// group per segment)
+enum { MODE_VAL = 0, MODE_CODES = 1 };
+
+template <typename WireT, typename OutT, int MODE, int B>
+__global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
+  using RW = typename Elem<WireT>::raw;
+  using RO = typename Elem<OutT>::raw;
+  __shared__ RO buf[SC_CH];
+  __shared__ uint32_t scratch[SC_NT / WAVE + 2];
+  const uint64_t nch = (a.L + SC_CH - 1) / SC_CH;
+  for (uint64_t wi = blockIdx.x; wi < a.n_seg * nch; wi += gridDim.x) {
+    const uint64_t seg = wi / nch, c0 = (wi % nch) * SC_CH;
+    const uint64_t c1 = min(a.L, c0 + SC_CH);
+    const uint32_t* ix = a.idx + seg * a.k;
+    uint32_t j0, j1;
+    chunk_range(ix, a.k, c0, c1, scratch, j0, j1);
+    // entries past the segment's end belong to no chunk: the last chunk flags them
+    if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
+    for (int i = (int)threadIdx.x; i < (int)SC_CH; i += SC_NT) buf[i] = RO{};
+    __syncthreads();
+    float lo = 0.0f, scale = 0.0f;
+    if constexpr (MODE == MODE_CODES) { lo = a.meta[2 * seg]; scale = a.meta[2 * seg + 1]; }
+    for (uint32_t j = j0 + threadIdx.x; j < j1; j += SC_NT) {
+      const uint32_t i = ix[j];
+      if (i < c0 || i >= c1 || (j > j0 && ix[j - 1] >= i)) { raise_error(KERR_BAD_INDEX); continue; }
+      float x;
+      if constexpr (MODE == MODE_VAL) {
+        x = Elem<WireT>::up(((const RW*)a.val)[seg * a.k + j]);
+      } else if constexpr (B == 32) {
+        x = __uint_as_float(a.codes[seg * a.wpg + j]);
+      } else {
+        const uint64_t bit = (uint64_t)j * B;
+        const uint32_t* w = a.codes + seg * a.wpg + (bit >> 5);
+        uint32_t c = w[0] >> (bit & 31);
+        if ((bit & 31) + B > 32) c |= w[1] << (32 - (bit & 31));
+        c &= (1u << B) - 1u;
+        const float prod = (float)c * scale;
+        x = lo + prod;
+      }
+      buf[i - c0] = Elem<OutT>::down(x);
+    }
+    __syncthreads();
+    const uint64_t t0 = c0 + (uint64_t)threadIdx.x * SC_VPT;
+    const int nv = (int)min((uint64_t)SC_VPT, sat_sub(c1, t0));
+    if (nv > 0) {
+      RO out[SC_VPT];
+      load_run<RO, SC_VPT>(&buf[threadIdx.x * SC_VPT], out);
+      store_run_partial<RO, SC_VPT>((RO*)a.y + seg * a.L + t0, nv, out);
+    }
+    __syncthreads();
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
+  using R = typename Elem<T>::raw;
+  __shared__ R buf[SC_CH];
+  __shared__ uint32_t scratch[SC_NT / WAVE + 2];
+  const uint64_t nch = (a.L + SC_CH - 1) / SC_CH;
+  for (uint64_t wi = blockIdx.x; wi < a.n_seg * nch; wi += gridDim.x) {
+    const uint64_t b = wi / nch, c0 = (wi % nch) * SC_CH;
+    const uint64_t c1 = min(a.L, c0 + SC_CH);
+    const int64_t id = a.ids[b];
+    if (id < 0 || (uint64_t)id >= a.n_samples) {
+      if (threadIdx.x == 0) raise_error(KERR_BAD_ID);
+      continue;
+    }
+    R* row = (R*)a.m + (uint64_t)id * a.L;
+    // the buffer row first: its load overlaps the index search
+    const uint64_t t0 = c0 + (uint64_t)threadIdx.x * SC_VPT;
+    const int nv = (int)min((uint64_t)SC_VPT, sat_sub(c1, t0));
+    R mr[SC_VPT];
+    if (nv > 0) load_run_partial<R, SC_VPT>(row + t0, nv, R{}, mr);
+    const uint32_t* ix = a.idx + b * a.k;
+    uint32_t j0, j1;
+    chunk_range(ix, a.k, c0, c1, scratch, j0, j1);
+    if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
+    if (nv > 0) store_run<R, SC_VPT>(&buf[threadIdx.x * SC_VPT], mr);
+    __syncthreads();
+    for (uint32_t j = j0 + threadIdx.x; j < j1; j += SC_NT) {
+      const uint32_t i = ix[j];
+      if (i < c0 || i >= c1 || (j > j0 && ix[j - 1] >= i)) { raise_error(KERR_BAD_INDEX); continue; }
+      const float add = Elem<T>::up(((const R*)a.val)[b * a.k + j]);
+      buf[i - c0] = Elem<T>::down(Elem<T>::up(buf[i - c0]) + add);
+    }
+    __syncthreads();
+    if (nv > 0) {
+      load_run<R, SC_VPT>(&buf[threadIdx.x * SC_VPT], mr);
+      store_run_partial<R, SC_VPT>(row + t0, nv, mr);
+      store_run_partial<R, SC_VPT>((R*)a.y + b * a.L + t0, nv, mr);
+    }
+    __syncthreads();
+  }
+}
+
+namespace {
+
+uint32_t scatter_grid(uint64_t n_seg, uint64_t L) {
+  const uint64_t work = n_seg * ((L + SC_CH - 1) / SC_CH);
+  return (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(work, (uint64_t)device_cus() * 8));
+}
+
+template <typename WireT>
+const void* val_ptr(int out_dt) {
+  if (out_dt == DT_F32) return (const void*)k_topk_scatter<WireT, float, MODE_VAL, 0>;
+  if (out_dt == DT_BF16) return (const void*)k_topk_scatter<WireT, bf16_t, MODE_VAL, 0>;
+  return (const void*)k_topk_scatter<WireT, f16_t, MODE_VAL, 0>;
+}
+
+template <typename OutT>
+const void* codes_ptr(uint32_t b) {
+  switch (b) {
+    case 1: return (const void*)k_topk_scatter<float, OutT, MODE_CODES, 1>;
+    case 2: return (const void*)k_topk_scatter<float, OutT, MODE_CODES, 2>;
+    case 3: return (const void*)k_topk_scatter<float, OutT, MODE_CODES, 3>;
+    case 4: return (const void*)k_topk_scatter<float, OutT, MODE_CODES, 4>;
+    case 5: return (const void*)k_topk_scatter<float, OutT, MODE_CODES, 5>;
+    case 6: return (const void*)k_topk_scatter<float, OutT, MODE_CODES, 6>;
+    case 7: return (const void*)k_topk_scatter<float, OutT, MODE_CODES, 7>;
+    case 8: return (const void*)k_topk_scatter<float, OutT, MODE_CODES, 8>;
+    case 32: return (const void*)k_topk_scatter<float, OutT, MODE_CODES, 32>;
+  }
+  return nullptr;
+}
+
+}  // namespace
+
+// wire < 0 selects the quantized kept list (bits = -wire)
+hipError_t launch_topk_decompress(int wire, int out_dt, const ScatterArgs& args, hipStream_t st) {
+  const void* fn = nullptr;
+  if (wire >= 0) {
+    fn = (wire == DT_F32) ? val_ptr<float>(out_dt) : (wire == DT_BF16) ? val_ptr<bf16_t>(out_dt) : val_ptr<f16_t>(out_dt);
+  } else {
+    const uint32_t b = (uint32_t)(-wire);
+    fn = (out_dt == DT_F32) ? codes_ptr<float>(b) : (out_dt == DT_BF16) ? codes_ptr<bf16_t>(b) : codes_ptr<f16_t>(b);
+  }
+  if (!fn) return hipErrorInvalidValue;
+  ScatterArgs a = args;
+  void* params[] = {&a};
+  return hipLaunchKernel(fn, dim3(scatter_grid(a.n_seg, a.L)), dim3(SC_NT), params, 0, st);
+}
+
+hipError_t launch_aqsgd_recv(int dt, const ScatterArgs& args, hipStream_t st) {
+  const void* fn = (dt == DT_F32) ? (const void*)k_aqsgd_recv<float>
+                 : (dt == DT_BF16) ? (const void*)k_aqsgd_recv<bf16_t> : (const void*)k_aqsgd_recv<f16_t>;
+  ScatterArgs a = args;
+  void* params[] = {&a};
+  return hipLaunchKernel(fn, dim3(scatter_grid(a.n_seg, a.L)), dim3(SC_NT), params, 0, st);
+}
+
+TC_DEFINE_ERROR_READER(errors_scatter)
+
+}  // namespace tc

@@ -1,0 +1,326 @@
+// tc_api.cpp -- the C ABI declared in include/tc.h: argument validation,
+// launch planning and status reporting.  No device memory is allocated here.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/tc.h"
+#include "tc_internal.hpp"
+
+#define TC_API extern "C" __attribute__((visibility("default")))
+
+namespace tc {
+
+int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+}  // namespace tc
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+tc_status fail(tc_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+tc_status hip_fail(hipError_t e, const char* what) {
+  return fail(TC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool dt_ok(int dt) { return dt == TC_F32 || dt == TC_BF16 || dt == TC_F16; }
+bool bits_ok(uint32_t b) { return (b >= 1 && b <= 8) || b == 32; }
+
+// common codec checks; `need_k` for TopK-based kinds
+tc_status check_codec(const tc_codec* c, int kind_mask) {
+  if (!c) return fail(TC_ERR_NULL, "codec is NULL");
+  if (c->kind < TC_TOPK || c->kind > TC_TOPK_QUANT) return fail(TC_ERR_ARG, "codec.kind %d", c->kind);
+  if (c->reserved != 0) return fail(TC_ERR_ARG, "codec.reserved must be 0");
+  if (!((1 << c->kind) & kind_mask)) return fail(TC_ERR_ARG, "codec.kind %d not valid for this call", c->kind);
+  if (c->seg_len >= (1ull << 32)) return fail(TC_ERR_ARG, "seg_len %llu must be < 2^32", (unsigned long long)c->seg_len);
+  if (c->n_seg != 0 && c->seg_len != 0 && c->n_seg > UINT64_MAX / c->seg_len)
+    return fail(TC_ERR_ARG, "n_seg * seg_len overflows");
+  if (c->kind == TC_TOPK || c->kind == TC_TOPK_QUANT) {
+    if (c->k > c->seg_len) return fail(TC_ERR_ARG, "k %llu > seg_len %llu", (unsigned long long)c->k,
+                                       (unsigned long long)c->seg_len);
+  }
+  if (c->kind == TC_QUANT || c->kind == TC_TOPK_QUANT) {
+    if (!bits_ok(c->bits)) return fail(TC_ERR_ARG, "bits %u not in 1..8 or 32", c->bits);
+  }
+  return TC_OK;
+}
+
+tc_status check_ws(const tc::SegPlan& p, const void* ws, size_t ws_bytes) {
+  const size_t need = (size_t)p.ws_words * 4u;
+  if (need == 0) return TC_OK;
+  if (!ws) return fail(TC_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+  if (ws_bytes < need) return fail(TC_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
+  if (((uintptr_t)ws & 3u) != 0) return fail(TC_ERR_ALIGN, "workspace must be 4-byte aligned");
+  return TC_OK;
+}
+
+// a segment spread over more workgroups than the device holds at once cannot
+// use the register-resident kernels
+tc_status check_resident(const tc::SegPlan& p) {
+  if (p.n_groups == 0 || p.P > p.capacity)
+    return fail(TC_ERR_ARG, "a segment needs %u workgroups at once, the device holds %llu", p.P,
+                (unsigned long long)p.capacity);
+  return TC_OK;
+}
+
+tc_status topk_common(int sel, const tc_codec* c, const void* x, int dt, float* e, void* m, uint64_t n_samples,
+                      const int64_t* ids, const tc_payload* out, void* ws, size_t ws_bytes, void* stream) {
+  if (!dt_ok(dt)) return fail(TC_ERR_DTYPE, "dtype %d", dt);
+  if (c->wire != dt) return fail(TC_ERR_DTYPE, "wire dtype %d must equal the input dtype %d", c->wire, dt);
+  if (!out) return fail(TC_ERR_NULL, "payload is NULL");
+  const uint64_t n = c->n_seg * c->seg_len;
+  if (n == 0) return TC_OK;
+  if (!x) return fail(TC_ERR_NULL, "input is NULL");
+  if (sel == tc::SEL_EF && !e) return fail(TC_ERR_NULL, "error buffer is NULL");
+  if (sel == tc::SEL_AQSGD && (!m || !ids)) return fail(TC_ERR_NULL, "buffer or ids is NULL");
+  if (c->k > 0 && (!out->idx || !out->val)) return fail(TC_ERR_NULL, "payload idx/val is NULL");
+  if (c->k == 0 && sel == tc::SEL_PLAIN) return TC_OK;   // empty payload
+  if (c->k == 0 && sel == tc::SEL_AQSGD) return TC_OK;   // nothing sent, buffer unchanged
+  const tc::SegPlan p = tc::plan_topk(sel, dt, c->n_seg, c->seg_len);
+  tc_status s = check_resident(p);
+  if (s != TC_OK) return s;
+  s = check_ws(p, ws, ws_bytes);
+  if (s != TC_OK) return s;
+  tc::TopkArgs a{};
+  a.x = x;
+  a.e = e;
+  a.m = m;
+  a.ids = ids;
+  a.n_samples = n_samples;
+  a.idx = out->idx;
+  a.val = out->val;
+  a.n_seg = c->n_seg;
+  a.L = c->seg_len;
+  a.k = c->k;
+  a.ws = (uint32_t*)ws;
+  hipError_t he = tc::launch_topk(sel, dt, p, a, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "topk launch");
+  return TC_OK;
+}
+
+tc_status quant_common(bool ef, const tc_codec* c, const void* x, int dt, float* e, const tc_payload* out,
+                       void* ws, size_t ws_bytes, void* stream) {
+  if (!dt_ok(dt)) return fail(TC_ERR_DTYPE, "dtype %d", dt);
+  if (!out) return fail(TC_ERR_NULL, "payload is NULL");
+  const uint64_t n = c->n_seg * c->seg_len;
+  if (n == 0) return TC_OK;
+  if (!x) return fail(TC_ERR_NULL, "input is NULL");
+  if (ef && !e) return fail(TC_ERR_NULL, "error buffer is NULL");
+  if (!out->codes || !out->meta) return fail(TC_ERR_NULL, "payload codes/meta is NULL");
+  if (((uintptr_t)out->codes & 3u) != 0) return fail(TC_ERR_ALIGN, "codes must be 4-byte aligned");
+  const tc::SegPlan p = tc::plan_quant(dt, c->bits, ef, c->n_seg, c->seg_len);
+  tc_status s = check_resident(p);
+  if (s != TC_OK) return s;
+  s = check_ws(p, ws, ws_bytes);
+  if (s != TC_OK) return s;
+  tc::QuantArgs a{};
+  a.x = x;
+  a.e = e;
+  a.codes = (uint32_t*)out->codes;
+  a.meta = out->meta;
+  a.n_grp = c->n_seg;
+  a.G = c->seg_len;
+  a.wpg = tc_quant_group_bytes(c->seg_len, c->bits) / 4u;
+  a.ws = (uint32_t*)ws;
+  hipError_t he = tc::launch_quant(dt, dt, c->bits, ef, p, a, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "quant launch");
+  return TC_OK;
+}
+
+}  // namespace
+
+TC_API uint64_t tc_topk_count(uint64_t seg_len, uint32_t num, uint32_t den) {
+  if (den == 0) return 0;
+  const unsigned __int128 p = (unsigned __int128)seg_len * num + (den - 1u);
+  return (uint64_t)(p / den);
+}
+
+TC_API uint64_t tc_quant_group_bytes(uint64_t grp_len, uint32_t bits) {
+  if (bits == 32) return 4u * grp_len;
+  if (bits < 1 || bits > 8) return 0;
+  return 4u * ((grp_len * bits + 31u) / 32u);
+}
+
+TC_API tc_status tc_workspace_bytes(const tc_codec* c, size_t* bytes) {
+  if (!bytes) return fail(TC_ERR_NULL, "bytes is NULL");
+  *bytes = 0;
+  tc_status s = check_codec(c, (1 << TC_TOPK) | (1 << TC_QUANT) | (1 << TC_TOPK_QUANT));
+  if (s != TC_OK) return s;
+  if (c->n_seg * c->seg_len == 0) return TC_OK;
+  uint64_t words = 0;
+  const int dt = dt_ok(c->wire) ? c->wire : TC_F32;
+  if (c->kind == TC_TOPK) {
+    // one layout serves the plain, EF and AQ-SGD senders of this shape
+    words = tc::plan_topk(tc::SEL_EF, dt, c->n_seg, c->seg_len).ws_words;
+  } else if (c->kind == TC_QUANT) {
+    words = std::max(tc::plan_quant(dt, c->bits, true, c->n_seg, c->seg_len).ws_words,
+                     tc::plan_quant(dt, c->bits, false, c->n_seg, c->seg_len).ws_words);
+  } else {
+    return fail(TC_ERR_ARG, "TC_TOPK_QUANT is not supported by this build");
+  }
+  *bytes = (size_t)words * 4u;
+  return TC_OK;
+}
+
+TC_API const char* tc_status_str(int s) {
+  switch (s) {
+    case TC_OK: return "ok";
+    case TC_ERR_NULL: return "null pointer";
+    case TC_ERR_ARG: return "invalid argument";
+    case TC_ERR_DTYPE: return "unsupported dtype";
+    case TC_ERR_WORKSPACE: return "workspace missing or too small";
+    case TC_ERR_HIP: return "HIP runtime error";
+    case TC_ERR_ALIGN: return "misaligned buffer";
+  }
+  return "unknown status";
+}
+
+TC_API const char* tc_last_error(void) { return g_err; }
+
+TC_API tc_status tc_device_errors(uint32_t* bits, int clear) {
+  if (!bits) return fail(TC_ERR_NULL, "bits is NULL");
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  uint32_t a = 0, b = 0, d = 0;
+  if ((e = tc::errors_topk(&a, clear != 0)) != hipSuccess) return hip_fail(e, "error word (topk)");
+  if ((e = tc::errors_quant(&b, clear != 0)) != hipSuccess) return hip_fail(e, "error word (quant)");
+  if ((e = tc::errors_scatter(&d, clear != 0)) != hipSuccess) return hip_fail(e, "error word (scatter)");
+  *bits = a | b | d;
+  return TC_OK;
+}
+
+TC_API tc_status tc_topk_compress(const tc_codec* c, const void* x, int dt, const tc_payload* out, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  tc_status s = check_codec(c, 1 << TC_TOPK);
+  if (s != TC_OK) return s;
+  return topk_common(tc::SEL_PLAIN, c, x, dt, nullptr, nullptr, 0, nullptr, out, ws, ws_bytes, stream);
+}
+
+TC_API tc_status tc_topk_decompress(const tc_codec* c, const tc_payload* in, void* y, int out_dt, void* stream) {
+  tc_status s = check_codec(c, (1 << TC_TOPK) | (1 << TC_TOPK_QUANT));
+  if (s != TC_OK) return s;
+  if (!dt_ok(out_dt)) return fail(TC_ERR_DTYPE, "out dtype %d", out_dt);
+  if (!in) return fail(TC_ERR_NULL, "payload is NULL");
+  if (c->n_seg * c->seg_len == 0) return TC_OK;
+  if (!y) return fail(TC_ERR_NULL, "output is NULL");
+  if (c->k > 0 && !in->idx) return fail(TC_ERR_NULL, "payload idx is NULL");
+  int wire;
+  if (c->kind == TC_TOPK) {
+    if (!dt_ok(c->wire)) return fail(TC_ERR_DTYPE, "wire dtype %d", c->wire);
+    if (c->k > 0 && !in->val) return fail(TC_ERR_NULL, "payload val is NULL");
+    wire = c->wire;
+  } else {
+    if (c->k > 0 && (!in->codes || !in->meta)) return fail(TC_ERR_NULL, "payload codes/meta is NULL");
+    if (((uintptr_t)in->codes & 3u) != 0) return fail(TC_ERR_ALIGN, "codes must be 4-byte aligned");
+    wire = -(int)c->bits;
+  }
+  tc::ScatterArgs a{};
+  a.idx = in->idx;
+  a.val = in->val;
+  a.codes = (const uint32_t*)in->codes;
+  a.meta = in->meta;
+  a.y = y;
+  a.n_seg = c->n_seg;
+  a.L = c->seg_len;
+  a.k = c->k;
+  a.wpg = (c->kind == TC_TOPK_QUANT) ? tc_quant_group_bytes(c->k, c->bits) / 4u : 0u;
+  hipError_t he = tc::launch_topk_decompress(wire, out_dt, a, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "topk decompress launch");
+  return TC_OK;
+}
+
+TC_API tc_status tc_quant_pack(const tc_codec* c, const void* x, int dt, const tc_payload* out, void* ws,
+                               size_t ws_bytes, void* stream) {
+  tc_status s = check_codec(c, 1 << TC_QUANT);
+  if (s != TC_OK) return s;
+  return quant_common(false, c, x, dt, nullptr, out, ws, ws_bytes, stream);
+}
+
+TC_API tc_status tc_quant_unpack(const tc_codec* c, const tc_payload* in, void* y, int out_dt, void* stream) {
+  tc_status s = check_codec(c, 1 << TC_QUANT);
+  if (s != TC_OK) return s;
+  if (!dt_ok(out_dt)) return fail(TC_ERR_DTYPE, "out dtype %d", out_dt);
+  if (!in) return fail(TC_ERR_NULL, "payload is NULL");
+  if (c->n_seg * c->seg_len == 0) return TC_OK;
+  if (!y || !in->codes || !in->meta) return fail(TC_ERR_NULL, "output, codes or meta is NULL");
+  if (((uintptr_t)in->codes & 3u) != 0) return fail(TC_ERR_ALIGN, "codes must be 4-byte aligned");
+  tc::UnpackArgs a{};
+  a.codes = (const uint32_t*)in->codes;
+  a.meta = in->meta;
+  a.y = y;
+  a.n_grp = c->n_seg;
+  a.G = c->seg_len;
+  a.wpg = tc_quant_group_bytes(c->seg_len, c->bits) / 4u;
+  hipError_t he = tc::launch_unpack(out_dt, c->bits, a, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "quant unpack launch");
+  return TC_OK;
+}
+
+TC_API tc_status tc_ef_step(const tc_codec* c, const void* x, int dt, float* e, const tc_payload* out, void* ws,
+                            size_t ws_bytes, void* stream) {
+  tc_status s = check_codec(c, (1 << TC_TOPK) | (1 << TC_QUANT) | (1 << TC_TOPK_QUANT));
+  if (s != TC_OK) return s;
+  if (c->kind == TC_TOPK) return topk_common(tc::SEL_EF, c, x, dt, e, nullptr, 0, nullptr, out, ws, ws_bytes, stream);
+  if (c->kind == TC_QUANT) return quant_common(true, c, x, dt, e, out, ws, ws_bytes, stream);
+  return fail(TC_ERR_ARG, "TC_TOPK_QUANT is not supported by this build");
+}
+
+TC_API tc_status tc_aqsgd_step(const tc_codec* c, const void* a, int dt, void* m, uint64_t n_samples,
+                               const int64_t* ids, uint32_t n_ids, const tc_payload* out, void* ws,
+                               size_t ws_bytes, void* stream) {
+  tc_status s = check_codec(c, 1 << TC_TOPK);
+  if (s != TC_OK) return s;
+  if (c->n_seg != n_ids) return fail(TC_ERR_ARG, "codec.n_seg %llu != n_ids %u", (unsigned long long)c->n_seg, n_ids);
+  if (n_ids > 0 && n_samples == 0) return fail(TC_ERR_ARG, "n_samples is 0");
+  if (c->seg_len != 0 && n_samples > UINT64_MAX / c->seg_len) return fail(TC_ERR_ARG, "n_samples * seg_len overflows");
+  return topk_common(tc::SEL_AQSGD, c, a, dt, nullptr, m, n_samples, ids, out, ws, ws_bytes, stream);
+}
+
+TC_API tc_status tc_aqsgd_reconstruct(const tc_codec* c, const tc_payload* in, void* m_r, int dt, uint64_t n_samples,
+                                      const int64_t* ids, uint32_t n_ids, void* a_hat, void* stream) {
+  tc_status s = check_codec(c, 1 << TC_TOPK);
+  if (s != TC_OK) return s;
+  if (!dt_ok(dt)) return fail(TC_ERR_DTYPE, "dtype %d", dt);
+  if (c->wire != dt) return fail(TC_ERR_DTYPE, "wire dtype %d must equal the buffer dtype %d", c->wire, dt);
+  if (c->n_seg != n_ids) return fail(TC_ERR_ARG, "codec.n_seg %llu != n_ids %u", (unsigned long long)c->n_seg, n_ids);
+  if (!in) return fail(TC_ERR_NULL, "payload is NULL");
+  if (c->n_seg * c->seg_len == 0) return TC_OK;
+  if (n_samples == 0) return fail(TC_ERR_ARG, "n_samples is 0");
+  if (c->seg_len != 0 && n_samples > UINT64_MAX / c->seg_len) return fail(TC_ERR_ARG, "n_samples * seg_len overflows");
+  if (!m_r || !ids || !a_hat) return fail(TC_ERR_NULL, "buffer, ids or output is NULL");
+  if (c->k > 0 && (!in->idx || !in->val)) return fail(TC_ERR_NULL, "payload idx/val is NULL");
+  tc::ScatterArgs a{};
+  a.idx = in->idx;
+  a.val = in->val;
+  a.y = a_hat;
+  a.m = m_r;
+  a.ids = ids;
+  a.n_samples = n_samples;
+  a.n_seg = c->n_seg;
+  a.L = c->seg_len;
+  a.k = c->k;
+  hipError_t he = tc::launch_aqsgd_recv(dt, a, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "aqsgd reconstruct launch");
+  return TC_OK;
+}

@@ -1,0 +1,343 @@
+// tc_device.hpp -- device-side building blocks for the gfx950 boundary
+// compressors: element formats, vector memory access, wave64 / workgroup
+// reductions and scans, and the bounded cross-workgroup barrier.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tc {
+
+constexpr int WAVE = 64;
+
+// kernel-side error bits, OR-ed into a per-device sticky word
+enum : uint32_t {
+  KERR_TIMEOUT = 1u,     // a cross-workgroup wait gave up (co-residency violated)
+  KERR_BAD_ID = 2u,      // an AQ-SGD sample id outside [0, n_samples)
+  KERR_BAD_INDEX = 4u,   // a payload index outside its segment or chunk
+  KERR_INTERNAL = 8u,    // a selection placed an entry past k (never expected)
+};
+
+// one word per kernel translation unit (internal linkage); the host reads
+// it through hipMemcpyFromSymbol in that same unit
+static __device__ uint32_t g_kernel_errors;
+
+__device__ __forceinline__ void raise_error(uint32_t bits) {
+  __hip_atomic_fetch_or(&g_kernel_errors, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ------------------------------------------------------------------ formats
+// Element types: float, and 16-bit patterns tagged by these wrappers so that
+// templates can tell bfloat16 from binary16.
+struct bf16_t { uint16_t u; };
+struct f16_t { uint16_t u; };
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  using raw = float;
+  static __device__ __forceinline__ float up(float v) { return v; }
+  static __device__ __forceinline__ float down(float v) { return v; }
+};
+template <> struct Elem<bf16_t> {
+  using raw = uint16_t;
+  // exact: bfloat16 is the high half of a binary32
+  static __device__ __forceinline__ float up(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+  // round to nearest even (hardware conversion, default rounding mode)
+  static __device__ __forceinline__ uint16_t down(float v) {
+    return __builtin_bit_cast(uint16_t, (__bf16)v);
+  }
+};
+template <> struct Elem<f16_t> {
+  using raw = uint16_t;
+  static __device__ __forceinline__ float up(uint16_t h) {
+    return (float)__builtin_bit_cast(_Float16, h);
+  }
+  static __device__ __forceinline__ uint16_t down(float v) {
+    return __builtin_bit_cast(uint16_t, (_Float16)v);
+  }
+};
+
+// the value a receiver holds after v went through element type T
+template <typename T>
+__device__ __forceinline__ float through(float v) { return Elem<T>::up(Elem<T>::down(v)); }
+
+// magnitude key: the binary32 pattern without its sign.  For finite values
+// the unsigned order of keys is the order of |v|, and +0 / -0 share key 0.
+__device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
+
+// ------------------------------------------------------------ vector access
+// Load/store N consecutive raw elements starting at p (element units).
+// Uses 16-byte accesses when the run is 16-byte aligned and a multiple of 16
+// bytes, else 8-byte, else scalar accesses.
+template <typename R, int N>
+__device__ __forceinline__ void load_run(const R* __restrict__ p, R (&out)[N]) {
+  constexpr int BYTES = N * (int)sizeof(R);
+  const uintptr_t a = (uintptr_t)p;
+  if constexpr (BYTES % 16 == 0) {
+    if ((a & 15u) == 0) {
+      constexpr int PER = 16 / (int)sizeof(R);
+#pragma unroll
+      for (int i = 0; i < N / PER; ++i) {
+        uint4 w = *reinterpret_cast<const uint4*>(p + i * PER);
+        __builtin_memcpy(&out[i * PER], &w, 16);
+      }
+      return;
+    }
+  }
+  if constexpr (BYTES % 8 == 0) {
+    if ((a & 7u) == 0) {
+      constexpr int PER = 8 / (int)sizeof(R);
+#pragma unroll
+      for (int i = 0; i < N / PER; ++i) {
+        uint2 w = *reinterpret_cast<const uint2*>(p + i * PER);
+        __builtin_memcpy(&out[i * PER], &w, 8);
+      }
+      return;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < N; ++i) out[i] = p[i];
+}
+
+template <typename R, int N>
+__device__ __forceinline__ void store_run(R* __restrict__ p, const R (&in)[N]) {
+  constexpr int BYTES = N * (int)sizeof(R);
+  const uintptr_t a = (uintptr_t)p;
+  if constexpr (BYTES % 16 == 0) {
+    if ((a & 15u) == 0) {
+      constexpr int PER = 16 / (int)sizeof(R);
+#pragma unroll
+      for (int i = 0; i < N / PER; ++i) {
+        uint4 w;
+        __builtin_memcpy(&w, &in[i * PER], 16);
+        *reinterpret_cast<uint4*>(p + i * PER) = w;
+      }
+      return;
+    }
+  }
+  if constexpr (BYTES % 8 == 0) {
+    if ((a & 7u) == 0) {
+      constexpr int PER = 8 / (int)sizeof(R);
+#pragma unroll
+      for (int i = 0; i < N / PER; ++i) {
+        uint2 w;
+        __builtin_memcpy(&w, &in[i * PER], 8);
+        *reinterpret_cast<uint2*>(p + i * PER) = w;
+      }
+      return;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < N; ++i) p[i] = in[i];
+}
+
+// Load a run that may be cut short at `n` valid elements (n <= N); elements
+// past n are left as `fill`.
+template <typename R, int N>
+__device__ __forceinline__ void load_run_partial(const R* __restrict__ p, int n, R fill, R (&out)[N]) {
+  if (n >= N) { load_run<R, N>(p, out); return; }
+#pragma unroll
+  for (int i = 0; i < N; ++i) out[i] = (i < n) ? p[i] : fill;
+}
+
+template <typename R, int N>
+__device__ __forceinline__ void store_run_partial(R* __restrict__ p, int n, const R (&in)[N]) {
+  if (n >= N) { store_run<R, N>(p, in); return; }
+#pragma unroll
+  for (int i = 0; i < N; ++i)
+    if (i < n) p[i] = in[i];
+}
+
+// a - b clamped at 0, written without a guarded subtraction.  The device
+// compiler of this toolchain can turn `b < a ? a - b : 0` into an unguarded
+// no-wrap subtraction and then use the implied a >= b to fold unrelated
+// min() calls away; every clamped difference in this library goes through
+// this form instead.
+template <typename T>
+__device__ __forceinline__ T sat_sub(T a, T b) { return a - min(a, b); }
+
+// --------------------------------------------------------- wave64 helpers
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (WAVE - 1)); }
+
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) {
+    uint32_t y = __shfl_up(x, d, WAVE);
+    if (lane >= d) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
+#pragma unroll
+  for (int d = WAVE / 2; d > 0; d >>= 1) x += __shfl_xor(x, d, WAVE);
+  return x;
+}
+
+__device__ __forceinline__ float wave_min(float x) {
+#pragma unroll
+  for (int d = WAVE / 2; d > 0; d >>= 1) x = fminf(x, __shfl_xor(x, d, WAVE));
+  return x;
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int d = WAVE / 2; d > 0; d >>= 1) x = fmaxf(x, __shfl_xor(x, d, WAVE));
+  return x;
+}
+
+// ------------------------------------------------------- workgroup helpers
+// scratch must hold NT/64 + 1 words of LDS.  All threads of the workgroup
+// must call these (they contain barriers).
+template <int NT>
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratch, uint32_t& total) {
+  constexpr int NW = NT / WAVE;
+  const int w = (int)threadIdx.x / WAVE;
+  uint32_t incl = wave_incl_scan(v);
+  if constexpr (NW == 1) {
+    total = __shfl(incl, WAVE - 1, WAVE);
+    return incl - v;
+  } else {
+    if (lane_id() == WAVE - 1) scratch[w] = incl;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t acc = 0;
+#pragma unroll
+      for (int i = 0; i < NW; ++i) { uint32_t t = scratch[i]; scratch[i] = acc; acc += t; }
+      scratch[NW] = acc;
+    }
+    __syncthreads();
+    uint32_t r = scratch[w] + incl - v;
+    total = scratch[NW];
+    __syncthreads();
+    return r;
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* scratch) {
+  constexpr int NW = NT / WAVE;
+  uint32_t s = wave_sum(v);
+  if constexpr (NW == 1) {
+    return s;
+  } else {
+    const int w = (int)threadIdx.x / WAVE;
+    if (lane_id() == 0) scratch[w] = s;
+    __syncthreads();
+    uint32_t t = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) t += scratch[i];
+    __syncthreads();
+    return t;
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ void block_minmax(float& lo, float& hi, float* scratch /*2*NT/64*/) {
+  constexpr int NW = NT / WAVE;
+  lo = wave_min(lo);
+  hi = wave_max(hi);
+  if constexpr (NW > 1) {
+    const int w = (int)threadIdx.x / WAVE;
+    if (lane_id() == 0) { scratch[w] = lo; scratch[NW + w] = hi; }
+    __syncthreads();
+    lo = scratch[0];
+    hi = scratch[NW];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) { lo = fminf(lo, scratch[i]); hi = fmaxf(hi, scratch[NW + i]); }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------ cross-workgroup barrier
+// A sense-reversing barrier among the P workgroups of one group (state[0..2]:
+// arrival count, sense, exit count; see group_exit).  Data that
+// crosses workgroups is written with device-scope atomics (add_agent /
+// st_agent) and read with device-scope loads (ld_agent).  state[0] is
+// the arrival count (back to 0 after every round), state[1] the sense word,
+// which flips once per round.  The wait is bounded: if the other workgroups
+// do not arrive (they are not co-resident), it gives up, raises KERR_TIMEOUT
+// and lets the kernel run to its end.
+constexpr uint32_t BARRIER_SPIN_LIMIT = 1u << 19;
+
+__device__ __forceinline__ void group_barrier(uint32_t* state, uint32_t P) {
+  // every wave first completes its own global writes and atomics at device
+  // scope; the workgroup barrier then orders them before the arrival below
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t* count = state;
+    uint32_t* sense = state + 1;
+    const uint32_t s0 = __hip_atomic_load(sense, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t prev = __hip_atomic_fetch_add(count, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == P - 1) {
+      __hip_atomic_store(count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(sense, s0 ^ 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      uint32_t spins = 0;
+      while (__hip_atomic_load(sense, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) == s0) {
+        __builtin_amdgcn_s_sleep(1);
+        ++spins;
+        // once any wait on the device has given up, stop waiting at once
+        if ((spins & 1023u) == 0u &&
+            (__hip_atomic_load(&g_kernel_errors, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & KERR_TIMEOUT))
+          break;
+        if (spins > BARRIER_SPIN_LIMIT) { raise_error(KERR_TIMEOUT); break; }
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// Leave a group's workspace zero-filled: every workgroup counts itself out in
+// state[2]; the last one clears `words` (per-workgroup slots, which are
+// rewritten before every read and so never cleared in flight), the sense word
+// and the counter.  Nobody waits here.
+template <int NT>
+__device__ __forceinline__ void group_exit(uint32_t* state, uint32_t P, uint32_t* words, uint64_t n_words) {
+  __shared__ uint32_t last_out;
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t prev = __hip_atomic_fetch_add(state + 2, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    last_out = (prev == P - 1) ? 1u : 0u;
+  }
+  __syncthreads();
+  if (last_out) {
+    for (uint64_t i = threadIdx.x; i < n_words; i += NT)
+      __hip_atomic_store(words + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0) {
+      __hip_atomic_store(state + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(state + 2, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+__device__ __forceinline__ uint32_t ld_agent(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void add_agent(uint32_t* p, uint32_t v) {
+  __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// host side: read (and optionally clear) this translation unit's error word
+#define TC_DEFINE_ERROR_READER(fn)                                                          \
+  hipError_t fn(uint32_t* bits, bool clear) {                                               \
+    uint32_t v = 0;                                                                         \
+    hipError_t st = hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_kernel_errors), sizeof(v), 0,      \
+                                        hipMemcpyDeviceToHost);                             \
+    if (st != hipSuccess) return st;                                                        \
+    *bits = v;                                                                              \
+    if (clear && v) {                                                                       \
+      const uint32_t z = 0;                                                                 \
+      st = hipMemcpyToSymbol(HIP_SYMBOL(g_kernel_errors), &z, sizeof(z), 0,                 \
+                             hipMemcpyHostToDevice);                                        \
+    }                                                                                       \
+    return st;                                                                              \
+  }
+
+}  // namespace tc

@@ -1,0 +1,94 @@
+// tc_internal.hpp -- launch plans and launcher entry points shared by the
+// C-ABI layer (tc_api.cpp) and the kernel translation units.  Not installed.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tc {
+
+enum Dt : int { DT_F32 = 0, DT_BF16 = 1, DT_F16 = 2 };
+
+inline size_t dt_size(int dt) { return dt == DT_F32 ? 4u : 2u; }
+
+// How one segmented kernel is laid out on the device: NT threads per
+// workgroup, VPT consecutive elements per thread, P workgroups per segment
+// (a "group"), n_groups groups resident at once (grid = n_groups * P), each
+// looping over segments group, group + n_groups, ...
+struct SegPlan {
+  int nt = 0;
+  int vpt = 0;
+  uint32_t P = 1;
+  uint32_t n_groups = 0;
+  uint32_t grid = 0;
+  uint64_t capacity = 0;   // workgroups of this kernel the device holds at once
+  uint64_t ws_words = 0;   // 32-bit words of zero-initialised workspace needed
+};
+
+// ------------------------------------------------------------------- TopK
+enum SelKind : int { SEL_PLAIN = 0, SEL_EF = 1, SEL_AQSGD = 2 };
+
+struct TopkArgs {
+  const void* x;         // PLAIN/EF: [n_seg][L] input; AQSGD: activations [n_seg][L]
+  float* e;              // EF: [n_seg][L] residual (in-out)
+  void* m;               // AQSGD: buffer [n_samples][L] (in-out)
+  const int64_t* ids;    // AQSGD: [n_seg] sample ids (device)
+  uint64_t n_samples;
+  uint32_t* idx;         // [n_seg][k]
+  void* val;             // [n_seg][k] in the input dtype
+  uint64_t n_seg, L, k;
+  uint32_t P;
+  uint32_t* ws;
+};
+
+SegPlan plan_topk(int sel, int dt, uint64_t n_seg, uint64_t L);
+hipError_t launch_topk(int sel, int dt, const SegPlan& plan, const TopkArgs& a, hipStream_t st);
+
+// ----------------------------------------------------------- quantization
+struct QuantArgs {
+  const void* x;         // [n_grp][G]
+  float* e;              // EF residual [n_grp][G] or nullptr
+  uint32_t* codes;       // [n_grp][wpg] words
+  float* meta;           // [n_grp][2]
+  uint64_t n_grp, G, wpg;
+  uint32_t P;
+  uint32_t* ws;
+};
+
+SegPlan plan_quant(int dt, uint32_t bits, bool ef, uint64_t n_grp, uint64_t G);
+hipError_t launch_quant(int dt, int out_dt, uint32_t bits, bool ef, const SegPlan& plan,
+                        const QuantArgs& a, hipStream_t st);
+
+struct UnpackArgs {
+  const uint32_t* codes;
+  const float* meta;
+  void* y;
+  uint64_t n_grp, G, wpg;
+};
+hipError_t launch_unpack(int out_dt, uint32_t bits, const UnpackArgs& a, hipStream_t st);
+
+// --------------------------------------------------------- receiver side
+struct ScatterArgs {
+  const uint32_t* idx;   // [n_seg][k]
+  const void* val;       // [n_seg][k] wire values (TopK)
+  const uint32_t* codes; // TopK+quant: [n_seg][wpg] codes of the kept list
+  const float* meta;     // TopK+quant: [n_seg][2]
+  void* y;               // dense output [n_seg][L]
+  void* m;               // AQ-SGD receiver buffer [n_samples][L]
+  const int64_t* ids;
+  uint64_t n_samples;
+  uint64_t n_seg, L, k, wpg;
+};
+hipError_t launch_topk_decompress(int wire, int out_dt, const ScatterArgs& a, hipStream_t st);
+hipError_t launch_aqsgd_recv(int dt, const ScatterArgs& a, hipStream_t st);
+
+// sticky kernel error bits of each kernel translation unit
+hipError_t errors_topk(uint32_t* bits, bool clear);
+hipError_t errors_quant(uint32_t* bits, bool clear);
+hipError_t errors_scatter(uint32_t* bits, bool clear);
+
+// device properties (cached per device)
+int device_cus();
+
+}  // namespace tc

@@ -1,0 +1,289 @@
+"""Python binding of libtc (include/tc.h): argument marshalling only.
+
+Each function takes torch tensors that already live on the GPU, allocates the
+outputs with torch (device memory and the current stream are all torch is used
+for), and calls the C entry point of the same name.  Every step of the
+compression runs in the HIP kernels of libtc.so; there is no fallback: if the
+library is missing or no GPU is present, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import threading
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtc.so")
+
+TC_F32, TC_BF16, TC_F16 = 0, 1, 2
+TC_TOPK, TC_QUANT, TC_TOPK_QUANT = 1, 2, 3
+TC_KERR_TIMEOUT, TC_KERR_BAD_ID, TC_KERR_BAD_INDEX, TC_KERR_INTERNAL = 1, 2, 4, 8
+
+_DT = {torch.float32: TC_F32, torch.bfloat16: TC_BF16, torch.float16: TC_F16}
+_TORCH = {v: k for k, v in _DT.items()}
+
+
+class Codec(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("wire", C.c_int32), ("bits", C.c_uint32), ("reserved", C.c_uint32),
+                ("n_seg", C.c_uint64), ("seg_len", C.c_uint64), ("k", C.c_uint64)]
+
+
+class Payload(C.Structure):
+    _fields_ = [("idx", C.c_void_p), ("val", C.c_void_p), ("codes", C.c_void_p), ("meta", C.c_void_p)]
+
+
+class TCError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: {status_str(status)} ({detail})")
+        self.status = status
+
+
+_lib = None
+_lock = threading.Lock()
+
+EXPORTS = {
+    # name: (restype, argtypes)
+    "tc_topk_count": (C.c_uint64, [C.c_uint64, C.c_uint32, C.c_uint32]),
+    "tc_quant_group_bytes": (C.c_uint64, [C.c_uint64, C.c_uint32]),
+    "tc_workspace_bytes": (C.c_int, [C.POINTER(Codec), C.POINTER(C.c_size_t)]),
+    "tc_status_str": (C.c_char_p, [C.c_int]),
+    "tc_last_error": (C.c_char_p, []),
+    "tc_device_errors": (C.c_int, [C.POINTER(C.c_uint32), C.c_int]),
+    "tc_topk_compress": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.POINTER(Payload), C.c_void_p,
+                                   C.c_size_t, C.c_void_p]),
+    "tc_topk_decompress": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.c_void_p, C.c_int, C.c_void_p]),
+    "tc_quant_pack": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.POINTER(Payload), C.c_void_p,
+                                C.c_size_t, C.c_void_p]),
+    "tc_quant_unpack": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.c_void_p, C.c_int, C.c_void_p]),
+    "tc_ef_step": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.POINTER(C.c_float), C.POINTER(Payload),
+                             C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tc_aqsgd_step": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.c_void_p, C.c_uint64, C.c_void_p,
+                                C.c_uint32, C.POINTER(Payload), C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tc_aqsgd_reconstruct": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.c_void_p, C.c_int, C.c_uint64,
+                                       C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p]),
+}
+
+
+def lib():
+    """load libtc.so (raises if it has not been built)"""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2401_07788_amd.build.build()")
+            L = C.CDLL(LIB_PATH)
+            for name, (res, args) in EXPORTS.items():
+                f = getattr(L, name)
+                f.restype = res
+                f.argtypes = args
+            _lib = L
+    return _lib
+
+
+def status_str(s: int) -> str:
+    return lib().tc_status_str(s).decode()
+
+
+def _check(rc: int, where: str):
+    if rc != 0:
+        raise TCError(rc, where, lib().tc_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return C.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _need_gpu(*ts):
+    for t in ts:
+        if t is not None:
+            if not t.is_cuda:
+                raise ValueError("libtc works on GPU tensors only")
+            if not t.is_contiguous():
+                raise ValueError("libtc needs contiguous tensors")
+
+
+def _dt(t) -> int:
+    try:
+        return _DT[t.dtype]
+    except KeyError:
+        raise TypeError(f"unsupported dtype {t.dtype}") from None
+
+
+def codec(kind: int, n_seg: int, seg_len: int, k: int = 0, bits: int = 0, wire: int = TC_F32) -> Codec:
+    return Codec(kind, wire, bits, 0, n_seg, seg_len, k)
+
+
+# ------------------------------------------------------------------ helpers
+def topk_count(seg_len: int, num: int, den: int) -> int:
+    return int(lib().tc_topk_count(seg_len, num, den))
+
+
+def quant_group_bytes(grp_len: int, bits: int) -> int:
+    return int(lib().tc_quant_group_bytes(grp_len, bits))
+
+
+def workspace_bytes(c: Codec) -> int:
+    n = C.c_size_t(0)
+    _check(lib().tc_workspace_bytes(C.byref(c), C.byref(n)), "tc_workspace_bytes")
+    return int(n.value)
+
+
+_ws_cache = {}
+
+
+def workspace(c: Codec, device=None) -> torch.Tensor | None:
+    """a zero-filled workspace for this codec, reused across calls on one device
+    and stream (every completed call leaves it zero-filled again)"""
+    device = torch.device(device or torch.cuda.current_device())
+    n = workspace_bytes(c)
+    if n == 0:
+        return None
+    key = (device.index, torch.cuda.current_stream(device).cuda_stream)
+    ws = _ws_cache.get(key)
+    if ws is None or ws.numel() < n:
+        ws = torch.zeros(max(n, 1 << 16), dtype=torch.uint8, device=device)
+        _ws_cache[key] = ws
+    return ws
+
+
+def device_errors(clear: bool = True) -> int:
+    """sticky TC_KERR_* bits of the current device (synchronizes it).  After a
+    timed-out cross-workgroup wait the cached workspaces are zero-filled again."""
+    bits = C.c_uint32(0)
+    _check(lib().tc_device_errors(C.byref(bits), int(clear)), "tc_device_errors")
+    if bits.value & TC_KERR_TIMEOUT:
+        for ws in _ws_cache.values():
+            ws.zero_()
+        torch.cuda.synchronize()
+    return int(bits.value)
+
+
+def _ws_args(c, device, ws):
+    if ws is None:
+        ws = workspace(c, device)
+    return (_ptr(ws), 0 if ws is None else ws.numel() * ws.element_size())
+
+
+# --------------------------------------------------------------------- TopK
+def topk_compress(x: torch.Tensor, k: int, n_seg: int, ws=None):
+    """TopK per segment of x viewed as [n_seg, seg_len] -> (idx uint32-as-int32, val)"""
+    _need_gpu(x)
+    L = x.numel() // n_seg
+    c = codec(TC_TOPK, n_seg, L, k, wire=_dt(x))
+    idx = torch.empty((n_seg, k), dtype=torch.int32, device=x.device)
+    val = torch.empty((n_seg, k), dtype=x.dtype, device=x.device)
+    p = Payload(_ptr(idx), _ptr(val), None, None)
+    w, wn = _ws_args(c, x.device, ws)
+    _check(lib().tc_topk_compress(C.byref(c), _ptr(x), _dt(x), C.byref(p), w, wn, _stream(x.device)),
+           "tc_topk_compress")
+    return idx, val
+
+
+def topk_decompress(idx: torch.Tensor, val: torch.Tensor, seg_len: int, out_dtype=None):
+    _need_gpu(idx, val)
+    n_seg, k = idx.shape
+    out_dtype = out_dtype or val.dtype
+    c = codec(TC_TOPK, n_seg, seg_len, k, wire=_dt(val))
+    y = torch.empty((n_seg, seg_len), dtype=out_dtype, device=idx.device)
+    p = Payload(_ptr(idx), _ptr(val), None, None)
+    _check(lib().tc_topk_decompress(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(idx.device)),
+           "tc_topk_decompress")
+    return y
+
+
+# ------------------------------------------------------------- quantization
+def quant_pack(x: torch.Tensor, bits: int, n_grp: int, ws=None):
+    """min-max quantization per group -> (codes uint8 [n_grp, group_bytes], meta f32 [n_grp, 2])"""
+    _need_gpu(x)
+    G = x.numel() // n_grp
+    c = codec(TC_QUANT, n_grp, G, bits=bits, wire=_dt(x))
+    codes = torch.empty((n_grp, quant_group_bytes(G, bits)), dtype=torch.uint8, device=x.device)
+    meta = torch.empty((n_grp, 2), dtype=torch.float32, device=x.device)
+    p = Payload(None, None, _ptr(codes), _ptr(meta))
+    w, wn = _ws_args(c, x.device, ws)
+    _check(lib().tc_quant_pack(C.byref(c), _ptr(x), _dt(x), C.byref(p), w, wn, _stream(x.device)), "tc_quant_pack")
+    return codes, meta
+
+
+def quant_unpack(codes: torch.Tensor, meta: torch.Tensor, grp_len: int, bits: int, out_dtype=torch.float32):
+    _need_gpu(codes, meta)
+    n_grp = meta.shape[0]
+    c = codec(TC_QUANT, n_grp, grp_len, bits=bits, wire=_DT[out_dtype])
+    y = torch.empty((n_grp, grp_len), dtype=out_dtype, device=codes.device)
+    p = Payload(None, None, _ptr(codes), _ptr(meta))
+    _check(lib().tc_quant_unpack(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(codes.device)),
+           "tc_quant_unpack")
+    return y
+
+
+# ----------------------------------------------------------- error feedback
+def ef_step_topk(x: torch.Tensor, e: torch.Tensor, k: int, n_seg: int, ws=None):
+    """X = x + e; send TopK(X); e <- X - received.  e (float32) is updated in place."""
+    _need_gpu(x, e)
+    if e.dtype != torch.float32 or e.numel() != x.numel():
+        raise ValueError("e must be float32 with x's element count")
+    L = x.numel() // n_seg
+    c = codec(TC_TOPK, n_seg, L, k, wire=_dt(x))
+    idx = torch.empty((n_seg, k), dtype=torch.int32, device=x.device)
+    val = torch.empty((n_seg, k), dtype=x.dtype, device=x.device)
+    p = Payload(_ptr(idx), _ptr(val), None, None)
+    w, wn = _ws_args(c, x.device, ws)
+    _check(lib().tc_ef_step(C.byref(c), _ptr(x), _dt(x), C.cast(e.data_ptr(), C.POINTER(C.c_float)), C.byref(p),
+                            w, wn, _stream(x.device)), "tc_ef_step")
+    return idx, val
+
+
+def ef_step_quant(x: torch.Tensor, e: torch.Tensor, bits: int, n_grp: int, ws=None):
+    """X = x + e; send Q(X); e <- X - received.  e (float32) is updated in place."""
+    _need_gpu(x, e)
+    if e.dtype != torch.float32 or e.numel() != x.numel():
+        raise ValueError("e must be float32 with x's element count")
+    G = x.numel() // n_grp
+    c = codec(TC_QUANT, n_grp, G, bits=bits, wire=_dt(x))
+    codes = torch.empty((n_grp, quant_group_bytes(G, bits)), dtype=torch.uint8, device=x.device)
+    meta = torch.empty((n_grp, 2), dtype=torch.float32, device=x.device)
+    p = Payload(None, None, _ptr(codes), _ptr(meta))
+    w, wn = _ws_args(c, x.device, ws)
+    _check(lib().tc_ef_step(C.byref(c), _ptr(x), _dt(x), C.cast(e.data_ptr(), C.POINTER(C.c_float)), C.byref(p),
+                            w, wn, _stream(x.device)), "tc_ef_step")
+    return codes, meta
+
+
+# ------------------------------------------------------------------- AQ-SGD
+def aqsgd_step(a: torch.Tensor, m: torch.Tensor, ids: torch.Tensor, k: int, ws=None, out=None):
+    """sender: d = a - m[ids]; send TopK(d); m[ids] += sent.  m is updated in place."""
+    _need_gpu(a, m, ids)
+    if ids.dtype != torch.int64 or a.dtype != m.dtype:
+        raise TypeError("ids must be int64 and a, m share a dtype")
+    n_ids = ids.numel()
+    L = m.shape[1]
+    c = codec(TC_TOPK, n_ids, L, k, wire=_dt(m))
+    if out is None:
+        idx = torch.empty((n_ids, k), dtype=torch.int32, device=a.device)
+        val = torch.empty((n_ids, k), dtype=a.dtype, device=a.device)
+    else:
+        idx, val = out
+    p = Payload(_ptr(idx), _ptr(val), None, None)
+    w, wn = _ws_args(c, a.device, ws)
+    _check(lib().tc_aqsgd_step(C.byref(c), _ptr(a), _dt(a), _ptr(m), m.shape[0], _ptr(ids), n_ids, C.byref(p),
+                               w, wn, _stream(a.device)), "tc_aqsgd_step")
+    return idx, val
+
+
+def aqsgd_reconstruct(idx: torch.Tensor, val: torch.Tensor, m_r: torch.Tensor, ids: torch.Tensor, out=None):
+    """receiver: m_r[ids] += received; returns a_hat = m_r[ids].  m_r is updated in place."""
+    _need_gpu(idx, val, m_r, ids)
+    n_ids, k = idx.shape
+    L = m_r.shape[1]
+    c = codec(TC_TOPK, n_ids, L, k, wire=_dt(m_r))
+    a_hat = torch.empty((n_ids, L), dtype=m_r.dtype, device=m_r.device) if out is None else out
+    p = Payload(_ptr(idx), _ptr(val), None, None)
+    _check(lib().tc_aqsgd_reconstruct(C.byref(c), C.byref(p), _ptr(m_r), _dt(m_r), m_r.shape[0], _ptr(ids), n_ids,
+                                      _ptr(a_hat), _stream(m_r.device)), "tc_aqsgd_reconstruct")
+    return a_hat

@@ -31,3 +31,18 @@ def orc():
     import oracle
     oracle.lib()
     return oracle
+
+
+def pytest_runtest_setup(item):
+    if item.get_closest_marker("gpu") is not None:
+        import torch
+        if not torch.cuda.is_available():
+            pytest.fail("a gpu-marked test needs an MI355X; run `-m 'not gpu'` on machines without one")
+
+
+@pytest.fixture(scope="session")
+def tc():
+    """the GPU binding; the HIP library must be built and loadable"""
+    from paper_2401_07788_amd import tc as _tc
+    _tc.lib()
+    return _tc

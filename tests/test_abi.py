@@ -1,0 +1,74 @@
+"""The C ABI: libtc.so loads on a machine without a GPU, exports exactly the
+functions include/tc.h declares, and its pure host helpers and argument
+checks behave as documented (no device work is started by these calls)."""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tc.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tc_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def tcmod():
+    from paper_2401_07788_amd import tc
+    if not os.path.exists(tc.LIB_PATH):
+        pytest.fail("libtc.so is not built (run __graft_entry__.build())")
+    tc.lib()
+    return tc
+
+
+def test_exports_match_header(tcmod):
+    declared = _declared()
+    assert "tc_aqsgd_step" in declared and "tc_topk_compress" in declared
+    out = subprocess.run(["nm", "-D", "--defined-only", tcmod.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = sorted({ln.split()[-1] for ln in out.splitlines() if " T " in ln})
+    assert exported == declared
+    assert sorted(tcmod.EXPORTS) == declared
+
+
+def test_host_helpers(tcmod, orc):
+    for L, num, den in [(16384, 1, 10), (393216, 3, 10), (2 ** 27, 1, 10), (100, 7, 100), (5, 0, 3), (7, 1, 0)]:
+        assert tcmod.topk_count(L, num, den) == orc.topk_count(L, num, den)
+    for G, b in [(768, 4), (32768, 2), (5, 6), (33, 3), (1, 1), (100, 8)]:
+        assert tcmod.quant_group_bytes(G, b) == orc.quant_group_bytes(G, b)
+    assert tcmod.quant_group_bytes(10, 32) == 40
+    assert tcmod.quant_group_bytes(10, 9) == 0
+    for s in range(7):
+        assert tcmod.status_str(s)
+
+
+def test_validation_before_any_device_call(tcmod):
+    L = tcmod.lib()
+    p = tcmod.Payload(None, None, None, None)
+    # NULL codec
+    assert L.tc_topk_compress(None, None, 0, C.byref(p), None, 0, None) == 1
+    # bad kind, reserved field, k > seg_len, bad bit width
+    for c, fn in [
+        (tcmod.Codec(7, 0, 0, 0, 1, 10, 1), L.tc_topk_compress),
+        (tcmod.Codec(1, 0, 0, 5, 1, 10, 1), L.tc_topk_compress),
+        (tcmod.Codec(1, 0, 0, 0, 1, 10, 11), L.tc_topk_compress),
+        (tcmod.Codec(2, 0, 9, 0, 1, 10, 0), L.tc_quant_pack),
+        (tcmod.Codec(1, 0, 0, 0, 1, 1 << 32, 1), L.tc_topk_compress),
+    ]:
+        assert fn(C.byref(c), None, 0, C.byref(p), None, 0, None) == 2
+        assert L.tc_last_error()
+    # quantization codec to the TopK entry point
+    c = tcmod.Codec(2, 0, 4, 0, 1, 10, 0)
+    assert L.tc_topk_compress(C.byref(c), None, 0, C.byref(p), None, 0, None) == 2
+    # AQ-SGD: n_seg must equal n_ids
+    c = tcmod.Codec(1, 2, 0, 0, 4, 10, 3)
+    assert L.tc_aqsgd_step(C.byref(c), None, 2, None, 10, None, 3, C.byref(p), None, 0, None) == 2
+    # empty tensors are a no-op that succeeds
+    c = tcmod.Codec(1, 0, 0, 0, 0, 10, 0)
+    assert L.tc_topk_compress(C.byref(c), None, 0, C.byref(p), None, 0, None) == 0

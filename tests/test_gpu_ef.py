@@ -1,0 +1,108 @@
+"""GPU parity: error feedback (Sec. 2.4) around TopK and around min-max
+quantization, over several steps with the residual carried on each side:
+payload bit for bit, and the binary32 residual within 1e-6 relative (it is
+expected, and checked, to be bit for bit as well).  The boundary shapes are
+the CNN (post-ReLU activations, small-sigma gradients, per-sample segments)
+and transformer (bfloat16 hidden states with outlier channels, per-row
+segments) workloads at full size."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import DTN, assert_bits_equal, assert_rel_close, raw
+from paper_2401_07788_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def ef_topk_steps(tc, orc, xs, n_seg, L, k):
+    dt = DTN[xs[0].dtype]
+    e_gpu = torch.zeros(n_seg * L, dtype=torch.float32, device="cuda")
+    e_orc = np.zeros((n_seg, L), np.float32)
+    for t, x in enumerate(xs):
+        idx, val = tc.ef_step_topk(x.cuda(), e_gpu, k, n_seg)
+        torch.cuda.synchronize()
+        assert tc.device_errors() == 0
+        oi, ov, e_orc = orc.ef_topk(raw(x), dt, e_orc, n_seg, L, k, threads=0)
+        assert_bits_equal(raw(idx), oi, f"idx step {t}")
+        assert_bits_equal(raw(val), ov, f"val step {t}")
+        eg = raw(e_gpu).reshape(n_seg, L)
+        assert_rel_close(eg, e_orc, 1e-6, f"e step {t}")
+        assert_bits_equal(eg, e_orc, f"e step {t} (bitwise)")
+
+
+def ef_quant_steps(tc, orc, xs, n_grp, G, b):
+    dt = DTN[xs[0].dtype]
+    e_gpu = torch.zeros(n_grp * G, dtype=torch.float32, device="cuda")
+    e_orc = np.zeros((n_grp, G), np.float32)
+    for t, x in enumerate(xs):
+        codes, meta = tc.ef_step_quant(x.cuda(), e_gpu, b, n_grp)
+        torch.cuda.synchronize()
+        assert tc.device_errors() == 0
+        oc, om, e_orc = orc.ef_quant(raw(x), dt, e_orc, n_grp, G, b)
+        assert_bits_equal(raw(codes), oc, f"codes step {t}")
+        assert_bits_equal(raw(meta), om, f"meta step {t}")
+        eg = raw(e_gpu).reshape(n_grp, G)
+        assert_rel_close(eg, e_orc, 1e-6, f"e step {t}")
+        assert_bits_equal(eg, e_orc, f"e step {t} (bitwise)")
+
+
+def cnn_stream(shape, steps, seed):
+    """activation (fwd) and gradient (bwd) tensors of successive steps"""
+    acts = [W.relu_activation(shape, seed, 2 * t) for t in range(steps)]
+    grads = [W.normal_gradient(shape, 1e-3, seed, 2 * t + 1) for t in range(steps)]
+    return acts, grads
+
+
+def test_ef_topk_cnn_tiny(tc, orc):
+    # 32x256x8x8 fp32, TopK 10% per sample + EF, forward and backward
+    acts, grads = cnn_stream((32, 256, 8, 8), 3, seed=0)
+    L = 256 * 8 * 8
+    k = tc.topk_count(L, 1, 10)
+    ef_topk_steps(tc, orc, acts, 32, L, k)
+    ef_topk_steps(tc, orc, grads, 32, L, k)
+
+
+@pytest.mark.parametrize("num", [1, 3])
+def test_ef_topk_resnet18(tc, orc, num):
+    # 128x128x16x16 fp32, TopK 10% / 30% per sample + EF
+    acts, grads = cnn_stream((128, 128, 16, 16), 2, seed=1)
+    L = 128 * 16 * 16
+    k = tc.topk_count(L, num, 10)
+    ef_topk_steps(tc, orc, acts, 128, L, k)
+    ef_topk_steps(tc, orc, grads, 128, L, k)
+
+
+@pytest.mark.parametrize("b", [2, 4, 8])
+def test_ef_quant_resnet18(tc, orc, b):
+    acts, grads = cnn_stream((128, 128, 16, 16), 2, seed=2)
+    L = 128 * 16 * 16
+    ef_quant_steps(tc, orc, acts, 128, L, b)
+    ef_quant_steps(tc, orc, grads, 128, L, b)
+
+
+def test_ef_transformer_rows(tc, orc):
+    # 8x512x768 bf16 with outlier channels; per-token-row TopK 10% and Q4, EF in fp32
+    hs = [W.transformer_hidden((8, 512, 768), seed=3, tensor_id=2 * t) for t in range(3)]
+    gs = [W.normal_gradient((8, 512, 768), 1e-4, 3, 2 * t + 1, dtype=torch.bfloat16) for t in range(3)]
+    k = tc.topk_count(768, 1, 10)
+    ef_topk_steps(tc, orc, hs, 4096, 768, k)
+    ef_topk_steps(tc, orc, gs, 4096, 768, k)
+    ef_quant_steps(tc, orc, hs, 4096, 768, 4)
+    ef_quant_steps(tc, orc, gs, 4096, 768, 4)
+
+
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16, torch.float16])
+def test_ef_ragged(tc, orc, dt):
+    xs = [W.randn((3, 50001), 4, t).to(dt) for t in range(3)]
+    ef_topk_steps(tc, orc, xs, 3, 50001, tc.topk_count(50001, 1, 10))
+    ef_quant_steps(tc, orc, xs, 3, 50001, 4)
+    ys = [W.randn((5, 999), 5, t).to(dt) for t in range(3)]
+    ef_topk_steps(tc, orc, ys, 5, 999, tc.topk_count(999, 3, 10))
+    ef_quant_steps(tc, orc, ys, 5, 999, 3)
+
+
+def test_ef_k_edges(tc, orc):
+    xs = [W.relu_activation((4, 16384), 6, t) for t in range(2)]
+    for k in (0, 16384):
+        ef_topk_steps(tc, orc, xs, 4, 16384, k)

@@ -1,0 +1,50 @@
+"""GPU parity: min-max quantization sender and receiver (Sec. 2.2) against the
+CPU oracle: packed code bytes and (lo, scale) bit for bit, reconstruction bit
+for bit, for every bit width 1..8 and 32, group lengths with ragged words and
+tails, groups spread over several workgroups, and constant groups."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import DTN, TORCH, assert_bits_equal, raw
+from paper_2401_07788_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def run_case(tc, orc, x, n_grp, G, b):
+    dt = DTN[x.dtype]
+    xd = x.cuda()
+    codes, meta = tc.quant_pack(xd, b, n_grp)
+    y = tc.quant_unpack(codes, meta, G, b, out_dtype=x.dtype)
+    torch.cuda.synchronize()
+    assert tc.device_errors() == 0
+    oc, om = orc.quant_pack(raw(x), dt, n_grp, G, b)
+    assert_bits_equal(raw(codes), oc, "codes")
+    assert_bits_equal(raw(meta), om, "meta")
+    oy = orc.quant_unpack(oc, om, n_grp, G, b, dt)
+    assert_bits_equal(raw(y), oy, "dense")
+
+
+@pytest.mark.parametrize("b", [1, 2, 3, 4, 5, 6, 7, 8, 32])
+@pytest.mark.parametrize("G", [1, 31, 768, 1000, 2048, 2049, 40000])
+def test_quant_parity_f32(tc, orc, b, G):
+    n_grp = 3
+    x = (W.randn((n_grp, G), seed=G, tensor_id=b) * torch.tensor([[1e-3], [1.0], [30.0]])).contiguous()
+    run_case(tc, orc, x, n_grp, G, b)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+@pytest.mark.parametrize("b", [2, 4, 6, 8])
+@pytest.mark.parametrize("G", [768, 32768])
+def test_quant_parity_half(tc, orc, dt, b, G):
+    n_grp = 4
+    x = W.randn((n_grp, G), seed=3, tensor_id=b).to(TORCH[dt])
+    run_case(tc, orc, x, n_grp, G, b)
+
+
+def test_quant_constant_and_relu_groups(tc, orc):
+    x = torch.relu(W.randn((4, 32768), seed=1, tensor_id=2))
+    x[1] = 2.5
+    x[2] = -0.0
+    run_case(tc, orc, x.contiguous(), 4, 32768, 4)

@@ -1,0 +1,100 @@
+"""GPU parity: TopK sender and receiver (Sec. 2.3) against the CPU oracle,
+bit for bit (indices, kept values, dense reconstruction), over both kernel
+layouts (one wavefront per short segment; several workgroups per long
+segment), ragged tails, tie-heavy data and the k = 0 / k = seg_len edges."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import DTN, TORCH, assert_bits_equal, raw
+from paper_2401_07788_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def make_input(kind, n_seg, L, dt, seed):
+    z = W.randn((n_seg, L), seed, 11)
+    if kind == "relu":
+        z = torch.relu(z)
+    elif kind == "ties":
+        z = z.to(torch.bfloat16).to(torch.float32)
+        g = torch.Generator().manual_seed(seed)
+        u = torch.rand((n_seg, L), generator=g)
+        z[u < 0.3] = 0.0
+        z[(u >= 0.3) & (u < 0.4)] = -0.0
+    elif kind == "const":
+        z = torch.full((n_seg, L), 1.5)
+    elif kind == "zeros":
+        z = torch.zeros((n_seg, L))
+        z[:, ::3] = -0.0
+    return z.to(TORCH[dt]).contiguous()
+
+
+def run_case(tc, orc, x, n_seg, L, k):
+    dt = DTN[x.dtype]
+    xd = x.cuda()
+    idx, val = tc.topk_compress(xd, k, n_seg)
+    y = tc.topk_decompress(idx, val, L)
+    torch.cuda.synchronize()
+    assert tc.device_errors() == 0
+    oi, ov = orc.topk_compress(raw(x), dt, n_seg, L, k)
+    assert_bits_equal(raw(idx), oi, "idx")
+    assert_bits_equal(raw(val), ov, "val")
+    oy = orc.topk_decompress(oi, ov, dt, n_seg, L, k)
+    assert_bits_equal(raw(y), oy, "dense")
+
+
+ROW_L = [1, 7, 64, 768, 1000, 2048]
+BIG_L = [2049, 16384, 50001]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("L", ROW_L + BIG_L)
+@pytest.mark.parametrize("kind", ["normal", "ties"])
+def test_topk_parity(tc, orc, dt, L, kind):
+    n_seg = 3 if L > 2048 else 5
+    x = make_input(kind, n_seg, L, dt, seed=L)
+    for num, den in [(1, 10), (3, 10)]:
+        run_case(tc, orc, x, n_seg, L, tc.topk_count(L, num, den))
+
+
+@pytest.mark.parametrize("L", [768, 16384, 50001])
+@pytest.mark.parametrize("kind", ["relu", "ties", "const", "zeros"])
+def test_topk_edges(tc, orc, L, kind):
+    n_seg = 2
+    x = make_input(kind, n_seg, L, "f32", seed=7)
+    for k in sorted({0, 1, 2, L // 2, L - 1, L}):
+        run_case(tc, orc, x, n_seg, L, k)
+
+
+def test_topk_many_segments_row_layout(tc, orc):
+    # 4096 token rows of 768 (the transformer boundary): more segments than
+    # resident wavefronts, so each wavefront loops
+    x = W.transformer_hidden((8, 512, 768), seed=0, tensor_id=0).reshape(4096, 768)
+    run_case(tc, orc, x, 4096, 768, tc.topk_count(768, 1, 10))
+
+
+def test_topk_many_segments_group_layout(tc, orc):
+    # more long segments than resident groups of workgroups
+    x = make_input("relu", 300, 20000, "f32", seed=3)
+    run_case(tc, orc, x, 300, 20000, tc.topk_count(20000, 1, 10))
+
+
+def test_decompress_rejects_bad_index_without_fault(tc):
+    idx = torch.tensor([[0, 5, 1 << 20]], dtype=torch.int32, device="cuda")
+    val = torch.ones((1, 3), dtype=torch.float32, device="cuda")
+    tc.device_errors(clear=True)
+    y = tc.topk_decompress(idx, val, 100)
+    torch.cuda.synchronize()
+    assert tc.device_errors(clear=True) & tc.TC_KERR_BAD_INDEX
+    yy = y.cpu()
+    assert yy[0, 0] == 1 and yy[0, 5] == 1 and yy.sum() == 2
+
+
+def test_decompress_flags_unsorted_payload(tc):
+    idx = torch.tensor([[0, 7, 5, 9]], dtype=torch.int32, device="cuda")
+    val = torch.ones((1, 4), dtype=torch.float32, device="cuda")
+    tc.device_errors(clear=True)
+    tc.topk_decompress(idx, val, 100)
+    torch.cuda.synchronize()
+    assert tc.device_errors(clear=True) & tc.TC_KERR_BAD_INDEX
