@@ -1,0 +1,230 @@
+"""Benchmark: boundary-tensor GB/s through compress + decompress with AQ-SGD
+per-example error feedback (TopK 30%), on one MI355X.
+
+Workload (the AQ-SGD boundary of the paper's Sec. 2.5, at the size of a
+GPT-2-small activation, hidden 768, 512 tokens): 4096 training examples, each
+with a 512x768 binary16 buffer on the sending and on the receiving stage
+(2 x 3.2 GB), micro-batches of 8 example ids drawn as a seeded permutation,
+activations that drift from the buffer by N(0, 0.1).  One step = one
+micro-batch through both sides: the sender (gather m[id], delta, TopK 30% per
+example, payload, buffer update) and the receiver (buffer update from the
+payload, reconstruction).  Every input is resident in HBM before timing.
+
+Reported: value = bytes of the boundary tensor (the activations, fp16) / step
+time; pct_hbm_peak = algorithmic bytes of both sides / step time / 8 TB/s;
+roofline for the dominant kernel (HIP events on the launch stream); the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E, published
+SOURCES_HASHED = ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
+                  "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in SOURCES_HASHED:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel: str):
+    """HBM bytes per launch from a committed counter summary, if it was taken
+    on the current kernel sources (else None)"""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_cores() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(n, int(os.environ.get("OMP_NUM_THREADS", n))))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the boundary compressors run per device and this build has no "
+              f"multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2401_07788_amd import tc
+    from paper_2401_07788_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs the GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    tc.lib()
+
+    n_samples, L, B = W.AQSGD["n_samples"], W.AQSGD["seg_len"], W.AQSGD["batch"]
+    k = tc.topk_count(L, 3, 10)
+    n_mb = n_samples // B
+    steps, warm = args.steps, args.warmup
+    if steps + warm > n_mb:
+        print(f"steps + warmup must be <= {n_mb} micro-batches (one epoch)", file=sys.stderr)
+        sys.exit(2)
+
+    # ---- inputs, resident in HBM
+    t_setup = time.perf_counter()
+    m_s = W.aqsgd_buffer(n_samples, L, seed=args.seed, device=dev)
+    m_r = m_s.clone()
+    ids_all = W.epoch_ids(n_samples, B, seed=args.seed)
+    ids_dev = ids_all.to(dev)
+    acts = torch.empty((steps + warm, B, L), dtype=torch.float16, device=dev)
+    for j in range(steps + warm):
+        acts[j] = W.drifted_activation(m_s, ids_all[j], args.seed, 100 + j)
+    idx = torch.empty((B, k), dtype=torch.int32, device=dev)
+    val = torch.empty((B, k), dtype=torch.float16, device=dev)
+    a_hat = torch.empty((B, L), dtype=torch.float16, device=dev)
+    c = tc.codec(tc.TC_TOPK, B, L, k, wire=tc.TC_F16)
+    ws = tc.workspace(c, dev)
+    # the oracle sample needs the buffer rows of its micro-batches as they are
+    # before the GPU touches them
+    n_cpu_mb = 0 if args.no_cpu else min(64, steps + warm)
+    cpu_rows = [m_s[ids_dev[j]].cpu() for j in range(n_cpu_mb)]
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+
+    def step(j):
+        tc.aqsgd_step(acts[j], m_s, ids_dev[j], k, ws=ws, out=(idx, val))
+        tc.aqsgd_reconstruct(idx, val, m_r, ids_dev[j], out=a_hat)
+
+    for j in range(warm):
+        step(j)
+    torch.cuda.synchronize()
+    errs = tc.device_errors(clear=True)
+    if errs:
+        print(f"kernel error bits {errs:#x} during warm-up", file=sys.stderr)
+        sys.exit(1)
+
+    # ---- timed region: K steps, HIP events around each kernel on the launch stream
+    st = torch.cuda.current_stream(dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        j = warm + i
+        e = ev[i]
+        e[0].record(st)
+        tc.aqsgd_step(acts[j], m_s, ids_dev[j], k, ws=ws, out=(idx, val))
+        e[1].record(st)
+        tc.aqsgd_reconstruct(idx, val, m_r, ids_dev[j], out=a_hat)
+        e[2].record(st)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    errs = tc.device_errors(clear=True)
+    if errs:
+        print(f"kernel error bits {errs:#x} in the timed region", file=sys.stderr)
+        sys.exit(1)
+    send_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    recv_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    ms_per_step = wall * 1e3 / steps
+
+    N = B * L
+    boundary_bytes = N * 2
+    bytes_side = 6 * N + 6 * B * k           # read a, read m, write m, write payload / mirror
+    b_alg = 2 * bytes_side
+    value = boundary_bytes / (ms_per_step * 1e-3) / 1e9
+    dominant = "aqsgd_send" if send_ms >= recv_ms else "aqsgd_recv"
+    dom_ms = max(send_ms, recv_ms)
+    achieved = bytes_side / (dom_ms * 1e-3) / 1e9
+    traffic = read_traffic(dominant)
+
+    # ---- CPU baseline: the oracle on a bounded sample of the same micro-batches
+    cpu = None
+    if n_cpu_mb:
+        import oracle
+        cores = cpu_cores()
+        raw16 = lambda t: t.contiguous().view(torch.int16).numpy().view(np.uint16)
+        done, spent = 0, 0.0
+        local = np.arange(B, dtype=np.int64)
+        while done < n_cpu_mb and (spent < args.cpu_seconds or done < 2):
+            rows = raw16(cpu_rows[done]).copy()
+            rows_r = rows.copy()
+            a_np = raw16(acts[done].cpu())
+            t1 = time.perf_counter()
+            oi, ov = oracle.aqsgd_send(a_np, rows, "f16", local, k, threads=cores)
+            oracle.aqsgd_recv(oi, ov, rows_r, "f16", local, k)
+            spent += time.perf_counter() - t1
+            done += 1
+        cpu = {"value": round(boundary_bytes * done / spent / 1e9, 4), "unit": "GB/s", "cores": cores,
+               "kind": "oracle",
+               "sample": f"{done} micro-batches of the same workload (8 examples x 512x768 fp16, TopK 30%), "
+                         f"sender + receiver, {spent:.1f} s on {platform.processor() or platform.machine()}"}
+
+    out = {
+        "metric": "boundary-tensor GB/s through compress+decompress+EF; % of HBM peak",
+        "value": round(value, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "AQ-SGD boundary: 4096 examples x 512x768 fp16 per-example buffers (sender and "
+                        "receiver), micro-batches of 8 ids, TopK 30% of the per-example change, fp16 wire",
+            "storage_dtype": "f16",
+            "micro_batch": B,
+            "seg_len": L,
+            "k": k,
+        },
+        "pct_hbm_peak": round(100.0 * b_alg / (ms_per_step * 1e-3) / (HBM_PEAK_GBPS * 1e9), 3),
+        "effective_GBps": round(b_alg / (ms_per_step * 1e-3) / 1e9, 2),
+        "algorithmic_bytes_per_step": b_alg,
+        "kernels_ms": {"aqsgd_send": round(send_ms, 5), "aqsgd_recv": round(recv_ms, 5)},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic, "algorithmic_bytes": bytes_side},
+        "cpu_baseline": cpu,
+        "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -262,21 +262,23 @@ __device__ __forceinline__ void block_minmax(float& lo, float& hi, float* scratc
 constexpr uint32_t BARRIER_SPIN_LIMIT = 1u << 19;
 
 __device__ __forceinline__ void group_barrier(uint32_t* state, uint32_t P) {
-  // every wave first completes its own global writes and atomics at device
-  // scope; the workgroup barrier then orders them before the arrival below
-  __threadfence();
+  // each wave waits until its own global writes and atomics are acknowledged
+  // (vector memory counter at zero); the workgroup barrier then orders them
+  // before thread 0's device-scope release below
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
     uint32_t* count = state;
     uint32_t* sense = state + 1;
-    const uint32_t s0 = __hip_atomic_load(sense, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-    const uint32_t prev = __hip_atomic_fetch_add(count, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t s0 = __hip_atomic_load(sense, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t prev = __hip_atomic_fetch_add(count, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     if (prev == P - 1) {
       __hip_atomic_store(count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(sense, s0 ^ 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     } else {
+      // relaxed polling (no cache maintenance per poll), one acquire at the end
       uint32_t spins = 0;
-      while (__hip_atomic_load(sense, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) == s0) {
+      while (__hip_atomic_load(sense, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == s0) {
         __builtin_amdgcn_s_sleep(1);
         ++spins;
         // once any wait on the device has given up, stop waiting at once
@@ -286,6 +288,7 @@ __device__ __forceinline__ void group_barrier(uint32_t* state, uint32_t P) {
         if (spins > BARRIER_SPIN_LIMIT) { raise_error(KERR_TIMEOUT); break; }
       }
     }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
   __syncthreads();
 }
@@ -297,7 +300,7 @@ __device__ __forceinline__ void group_barrier(uint32_t* state, uint32_t P) {
 template <int NT>
 __device__ __forceinline__ void group_exit(uint32_t* state, uint32_t P, uint32_t* words, uint64_t n_words) {
   __shared__ uint32_t last_out;
-  __threadfence();
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
     const uint32_t prev = __hip_atomic_fetch_add(state + 2, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
