@@ -9,6 +9,12 @@ activations that drift from the buffer by N(0, 0.1).  One step = one
 micro-batch through both sides: the sender (gather m[id], delta, TopK 30% per
 example, payload, buffer update) and the receiver (buffer update from the
 payload, reconstruction).  Every input is resident in HBM before timing.
+The timed region is the sequence of K micro-batches (sender then receiver for
+each, on one stream) captured once as a HIP graph and replayed: the launches
+of a stream of micro-batches without per-launch host cost.  Per-kernel
+durations for the roofline come from HIP events around each kernel of an
+eager pass over other micro-batches; the eager step time and a two-stream
+variant (sender of j+1 overlapping the receiver of j) are reported beside.
 
 Reported: value = bytes of the boundary tensor (the activations, fp16) / step
 time; pct_hbm_peak = algorithmic bytes of both sides / step time / 8 TB/s;
@@ -100,69 +106,118 @@ def main():
     k = tc.topk_count(L, 3, 10)
     n_mb = n_samples // B
     steps, warm = args.steps, args.warmup
-    if steps + warm > n_mb:
-        print(f"steps + warmup must be <= {n_mb} micro-batches (one epoch)", file=sys.stderr)
+    n_ref = min(100, steps)
+    # micro-batches of one epoch, each used once: eager warm-up, eager
+    # reference pass with per-kernel events, graph warm-up, timed graph,
+    # two-stream reference
+    need_mb = warm + n_ref + warm + steps + warm + n_ref
+    if need_mb > n_mb:
+        print(f"this many steps need {need_mb} micro-batches, an epoch has {n_mb}", file=sys.stderr)
         sys.exit(2)
 
-    # ---- inputs, resident in HBM
+    # ---- inputs, resident in HBM; every timed micro-batch is a fresh one
     t_setup = time.perf_counter()
     m_s = W.aqsgd_buffer(n_samples, L, seed=args.seed, device=dev)
     m_r = m_s.clone()
     ids_all = W.epoch_ids(n_samples, B, seed=args.seed)
     ids_dev = ids_all.to(dev)
-    acts = torch.empty((steps + warm, B, L), dtype=torch.float16, device=dev)
-    for j in range(steps + warm):
+    acts = torch.empty((need_mb, B, L), dtype=torch.float16, device=dev)
+    for j in range(need_mb):
         acts[j] = W.drifted_activation(m_s, ids_all[j], args.seed, 100 + j)
-    idx = torch.empty((B, k), dtype=torch.int32, device=dev)
-    val = torch.empty((B, k), dtype=torch.float16, device=dev)
-    a_hat = torch.empty((B, L), dtype=torch.float16, device=dev)
+    pays = [tc.empty_topk_payload(B, L, k, torch.float16, dev) for _ in range(2)]
+    ahats = [torch.empty((B, L), dtype=torch.float16, device=dev) for _ in range(2)]
     c = tc.codec(tc.TC_TOPK, B, L, k, wire=tc.TC_F16)
     ws = tc.workspace(c, dev)
     # the oracle sample needs the buffer rows of its micro-batches as they are
     # before the GPU touches them
-    n_cpu_mb = 0 if args.no_cpu else min(64, steps + warm)
+    n_cpu_mb = 0 if args.no_cpu else min(64, need_mb)
     cpu_rows = [m_s[ids_dev[j]].cpu() for j in range(n_cpu_mb)]
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
 
-    def step(j):
-        tc.aqsgd_step(acts[j], m_s, ids_dev[j], k, ws=ws, out=(idx, val))
-        tc.aqsgd_reconstruct(idx, val, m_r, ids_dev[j], out=a_hat)
+    def check(where):
+        errs = tc.device_errors(clear=True)
+        if errs:
+            print(f"kernel error bits {errs:#x} {where}", file=sys.stderr)
+            sys.exit(1)
 
-    for j in range(warm):
-        step(j)
-    torch.cuda.synchronize()
-    errs = tc.device_errors(clear=True)
-    if errs:
-        print(f"kernel error bits {errs:#x} during warm-up", file=sys.stderr)
-        sys.exit(1)
+    def steps_on(stream, j0, n, ev=None):
+        """sender then receiver for micro-batches j0 .. j0+n-1 on one stream"""
+        for i in range(n):
+            j = j0 + i
+            if ev: ev[i][0].record(stream)
+            tc.aqsgd_step(acts[j], m_s, ids_dev[j], k, ws=ws, out=pays[0])
+            if ev: ev[i][1].record(stream)
+            tc.aqsgd_reconstruct(pays[0], m_r, ids_dev[j], out=ahats[0])
+            if ev: ev[i][2].record(stream)
 
-    # ---- timed region: K steps, HIP events around each kernel on the launch stream
+    # ---- eager: warm-up, then a reference pass with HIP events around each
+    # kernel on the launch stream (the per-kernel durations of the roofline)
     st = torch.cuda.current_stream(dev)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    j = 0
+    steps_on(st, j, warm); j += warm
     torch.cuda.synchronize()
+    check("during the warm-up")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_ref)]
     t0 = time.perf_counter()
-    for i in range(steps):
-        j = warm + i
-        e = ev[i]
-        e[0].record(st)
-        tc.aqsgd_step(acts[j], m_s, ids_dev[j], k, ws=ws, out=(idx, val))
-        e[1].record(st)
-        tc.aqsgd_reconstruct(idx, val, m_r, ids_dev[j], out=a_hat)
-        e[2].record(st)
+    steps_on(st, j, n_ref, ev); j += n_ref
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    errs = tc.device_errors(clear=True)
-    if errs:
-        print(f"kernel error bits {errs:#x} in the timed region", file=sys.stderr)
-        sys.exit(1)
+    eager_ms = (time.perf_counter() - t0) * 1e3 / n_ref
+    check("in the eager pass")
     send_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
     recv_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+
+    # ---- timed region: the K micro-batches captured as one HIP graph (the
+    # launches of a stream of micro-batches), replayed once
+    cap = torch.cuda.Stream(dev)
+    gw, gt = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(gw, stream=cap):
+        steps_on(cap, j, warm)
+    j += warm
+    with torch.cuda.graph(gt, stream=cap):
+        steps_on(cap, j, steps)
+    j += steps
+    gw.replay()
+    torch.cuda.synchronize()
+    check("during the graph warm-up")
+    t0 = time.perf_counter()
+    gt.replay()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    check("in the timed region")
     ms_per_step = wall * 1e3 / steps
+
+    # ---- reference: sender of j+1 (stream A) overlapping the receiver of j
+    # (stream B), payloads double-buffered
+    sA, sB = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
+    sent = [torch.cuda.Event() for _ in range(2)]
+    freed = [torch.cuda.Event() for _ in range(2)]
+
+    def overlap_steps(j0, n):
+        for i in range(n):
+            jj, b = j0 + i, (j0 + i) % 2
+            with torch.cuda.stream(sA):
+                sA.wait_event(freed[b])
+                tc.aqsgd_step(acts[jj], m_s, ids_dev[jj], k, ws=ws, out=pays[b])
+                sent[b].record(sA)
+            with torch.cuda.stream(sB):
+                sB.wait_event(sent[b])
+                tc.aqsgd_reconstruct(pays[b], m_r, ids_dev[jj], out=ahats[b])
+                freed[b].record(sB)
+
+    overlap_steps(j, warm); j += warm
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    overlap_steps(j, n_ref); j += n_ref
+    torch.cuda.synchronize()
+    overlap_ms = (time.perf_counter() - t0) * 1e3 / n_ref
+    check("in the overlapped reference pass")
 
     N = B * L
     boundary_bytes = N * 2
-    bytes_side = 6 * N + 6 * B * k           # read a, read m, write m, write payload / mirror
+    blk_bytes = B * (tc.n_blocks(L) + 1) * 4
+    bytes_side = 6 * N + 6 * B * k + blk_bytes   # read a, read m, write m, write payload / mirror
     b_alg = 2 * bytes_side
     value = boundary_bytes / (ms_per_step * 1e-3) / 1e9
     dominant = "aqsgd_send" if send_ms >= recv_ms else "aqsgd_recv"
@@ -217,6 +272,8 @@ def main():
         "effective_GBps": round(b_alg / (ms_per_step * 1e-3) / 1e9, 2),
         "algorithmic_bytes_per_step": b_alg,
         "kernels_ms": {"aqsgd_send": round(send_ms, 5), "aqsgd_recv": round(recv_ms, 5)},
+        "eager_ms_per_step": round(eager_ms, 5),
+        "two_stream_overlap_ms_per_step": round(overlap_ms, 5),
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": bytes_side},

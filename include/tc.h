@@ -33,7 +33,7 @@
  *             exact; every narrowing rounds to nearest, ties to even.  All
  *             arithmetic is IEEE binary32 without contraction into FMA.
  *   Workspace Kernels that spread one segment over several workgroups keep
- *             small counters in a caller-owned workspace of
+ *             small counters in a caller-owned, 8-byte aligned workspace of
  *             tc_workspace_bytes() bytes.  It must be zero-filled before its
  *             first use; every completed call leaves it zero-filled again.
  *             After tc_device_errors() reports TC_KERR_TIMEOUT it must be
@@ -62,7 +62,7 @@ typedef enum {
   TC_ERR_DTYPE = 3,      /* dtype not supported for this operation */
   TC_ERR_WORKSPACE = 4,  /* workspace missing or smaller than tc_workspace_bytes() */
   TC_ERR_HIP = 5,        /* the HIP runtime refused the launch (see tc_last_error) */
-  TC_ERR_ALIGN = 6       /* a code buffer is not 4-byte aligned */
+  TC_ERR_ALIGN = 6       /* a code buffer or the workspace is misaligned */
 } tc_status;
 
 typedef enum { TC_F32 = 0, TC_BF16 = 1, TC_F16 = 2 } tc_dtype;
@@ -98,6 +98,9 @@ typedef struct {
   uint64_t k;
 } tc_codec;
 
+/* Length of the index blocks of a TopK payload's block table (see blk). */
+#define TC_BLOCK_LEN 4096u
+
 /* The message a sender produces.  Unused members may be NULL.
  *   idx    TC_TOPK, TC_TOPK_QUANT: [n_seg][k] uint32 indices within the
  *          segment, strictly ascending
@@ -106,12 +109,19 @@ typedef struct {
  *          TC_TOPK_QUANT: [n_seg][tc_quant_group_bytes(k, bits)]; codes are
  *          packed LSB-first into little-endian 32-bit words (4-byte aligned)
  *   meta   TC_QUANT, TC_TOPK_QUANT: [n_seg][2] binary32 (lo, scale); the
- *          receiver reconstructs lo + code * scale                          */
+ *          receiver reconstructs lo + code * scale
+ *   blk    TC_TOPK, TC_TOPK_QUANT, optional: [n_seg][ceil(seg_len /
+ *          TC_BLOCK_LEN) + 1] uint32; blk[s][b] = number of kept entries of
+ *          segment s with index < b * TC_BLOCK_LEN (so blk[s][0] = 0 and the
+ *          last entry is k).  A sender writes it when non-NULL; a receiver
+ *          given it reads each block's entries directly instead of searching
+ *          idx.  4 bytes per 4096 elements.                                  */
 typedef struct {
   uint32_t* idx;
   void* val;
   uint8_t* codes;
   float* meta;
+  uint32_t* blk;
 } tc_payload;
 
 /* ---------------------------------------------------------------- helpers */

@@ -69,10 +69,10 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
     float v[QVPT];
     {
       R xr[QVPT];
-      if (nv > 0) load_run_partial<R, QVPT>((const R*)a.x + off, nv, R{}, xr);
+      if (nv > 0) load_run_partial<R, QVPT, true>((const R*)a.x + off, nv, R{}, xr);
       if constexpr (EF) {
         float er[QVPT];
-        if (nv > 0) load_run_partial<float, QVPT>(a.e + off, nv, 0.0f, er);
+        if (nv > 0) load_run_partial<float, QVPT, true>(a.e + off, nv, 0.0f, er);
 #pragma unroll
         for (int i = 0; i < QVPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) + er[i] : 0.0f;
       } else {
@@ -147,13 +147,13 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
     // ---- outputs
     const uint64_t wo = (B == 32) ? c0 : (c0 * (uint64_t)B) / 32u;
     const int nw = (int)min((uint64_t)WPT, sat_sub(a.wpg, wo));
-    if (nw > 0) store_run_partial<uint32_t, WPT>(a.codes + grp * a.wpg + wo, nw, w);
+    if (nw > 0) store_run_partial<uint32_t, WPT, true>(a.codes + grp * a.wpg + wo, nw, w);
     if (part == 0 && threadIdx.x == 0) {
       a.meta[2 * grp] = lo;
       a.meta[2 * grp + 1] = scale;
     }
     if constexpr (EF) {
-      if (nv > 0) store_run_partial<float, QVPT>(a.e + off, nv, v);
+      if (nv > 0) store_run_partial<float, QVPT, true>(a.e + off, nv, v);
     }
   }
   if (P > 1) group_exit<NT>(bar, P, slots, 2ull * P);
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(NT) void k_quant_unpack(UnpackArgs a) {
     const uint64_t wo = (B == 32) ? c0 : (c0 * (uint64_t)B) / 32u;
     const int nw = (int)min((uint64_t)WPT, sat_sub(a.wpg, wo));
     uint32_t w[WPT];
-    load_run_partial<uint32_t, WPT>(a.codes + grp * a.wpg + wo, nw, 0u, w);
+    load_run_partial<uint32_t, WPT, true>(a.codes + grp * a.wpg + wo, nw, 0u, w);
     R y[QVPT];
     if constexpr (B == 32) {
 #pragma unroll
@@ -188,7 +188,7 @@ __global__ __launch_bounds__(NT) void k_quant_unpack(UnpackArgs a) {
         y[i] = Elem<OutT>::down(lo + prod);
       }
     }
-    store_run_partial<R, QVPT>((R*)a.y + grp * a.G + c0, nv, y);
+    store_run_partial<R, QVPT, true>((R*)a.y + grp * a.G + c0, nv, y);
   }
 }
 

@@ -37,9 +37,23 @@ __device__ uint32_t block_lower_bound(const uint32_t* __restrict__ a, uint32_t n
   return lo;
 }
 
-// the payload range [j0, j1) of the chunk [c0, c1)
-__device__ __forceinline__ void chunk_range(const uint32_t* ix, uint64_t k, uint64_t c0, uint64_t c1,
-                                            uint32_t* scratch, uint32_t& j0, uint32_t& j1) {
+static_assert(SC_CH == BLOCK_LEN, "a receiver chunk is one block of the payload's block table");
+
+// the payload range [j0, j1) of the chunk [c0, c1): from the block table
+// when the payload carries one (checked against what a valid payload allows),
+// else by searching the index list
+__device__ __forceinline__ void chunk_range(const uint32_t* ix, const uint32_t* bt, uint64_t k, uint64_t c0,
+                                            uint64_t c1, uint32_t* scratch, uint32_t& j0, uint32_t& j1) {
+  if (bt) {
+    const uint64_t c = c0 / SC_CH;
+    j0 = bt[c];
+    j1 = bt[c + 1];
+    if (j0 > j1 || j1 > k || j1 - j0 > c1 - c0) {
+      if (threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
+      j0 = j1 = 0;
+    }
+    return;
+  }
   j0 = block_lower_bound<SC_NT>(ix, (uint32_t)k, (uint32_t)c0, scratch);
   const uint32_t rest = (uint32_t)min(k - j0, c1 - c0);
   j1 = j0 + block_lower_bound<SC_NT>(ix + j0, rest, (uint32_t)c1, scratch);
@@ -60,8 +74,9 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
     const uint64_t seg = wi / nch, c0 = (wi % nch) * SC_CH;
     const uint64_t c1 = min(a.L, c0 + SC_CH);
     const uint32_t* ix = a.idx + seg * a.k;
+    const uint32_t* bt = a.blk ? a.blk + seg * (n_blocks(a.L) + 1) : nullptr;
     uint32_t j0, j1;
-    chunk_range(ix, a.k, c0, c1, scratch, j0, j1);
+    chunk_range(ix, bt, a.k, c0, c1, scratch, j0, j1);
     // entries past the segment's end belong to no chunk: the last chunk flags them
     if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
     for (int i = (int)threadIdx.x; i < (int)SC_CH; i += SC_NT) buf[i] = RO{};
@@ -93,7 +108,7 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
     if (nv > 0) {
       RO out[SC_VPT];
       load_run<RO, SC_VPT>(&buf[threadIdx.x * SC_VPT], out);
-      store_run_partial<RO, SC_VPT>((RO*)a.y + seg * a.L + t0, nv, out);
+      store_run_partial<RO, SC_VPT, true>((RO*)a.y + seg * a.L + t0, nv, out);
     }
     __syncthreads();
   }
@@ -118,10 +133,11 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
     const uint64_t t0 = c0 + (uint64_t)threadIdx.x * SC_VPT;
     const int nv = (int)min((uint64_t)SC_VPT, sat_sub(c1, t0));
     R mr[SC_VPT];
-    if (nv > 0) load_run_partial<R, SC_VPT>(row + t0, nv, R{}, mr);
+    if (nv > 0) load_run_partial<R, SC_VPT, true>(row + t0, nv, R{}, mr);
     const uint32_t* ix = a.idx + b * a.k;
+    const uint32_t* bt = a.blk ? a.blk + b * (n_blocks(a.L) + 1) : nullptr;
     uint32_t j0, j1;
-    chunk_range(ix, a.k, c0, c1, scratch, j0, j1);
+    chunk_range(ix, bt, a.k, c0, c1, scratch, j0, j1);
     if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
     if (nv > 0) store_run<R, SC_VPT>(&buf[threadIdx.x * SC_VPT], mr);
     __syncthreads();
@@ -134,8 +150,8 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
     __syncthreads();
     if (nv > 0) {
       load_run<R, SC_VPT>(&buf[threadIdx.x * SC_VPT], mr);
-      store_run_partial<R, SC_VPT>(row + t0, nv, mr);
-      store_run_partial<R, SC_VPT>((R*)a.y + b * a.L + t0, nv, mr);
+      store_run_partial<R, SC_VPT, true>(row + t0, nv, mr);
+      store_run_partial<R, SC_VPT, true>((R*)a.y + b * a.L + t0, nv, mr);
     }
     __syncthreads();
   }

@@ -36,10 +36,23 @@ struct RowShared {
   uint32_t scratch[2];
 };
 
+// LDS of the several-workgroup layout: the selection histogram, and after
+// the selection the workgroup's payload entries, staged so that they leave
+// in index order with coalesced stores
+template <int NT, int VPT, typename R>
+union BigShared {
+  SelShared<NT> sel;
+  struct {
+    uint32_t idx[NT * VPT];
+    R val[NT * VPT];
+  } st;
+};
+
 template <typename InT, int SEL, int VPT, int NT>
 __global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
   using R = typename Elem<InT>::raw;
-  using Sh = std::conditional_t<(NT > WAVE), SelShared<NT>, RowShared>;
+  constexpr bool BIG = NT > WAVE;
+  using Sh = std::conditional_t<BIG, BigShared<NT, VPT, R>, RowShared>;
   __shared__ Sh sh;
   constexpr uint64_t CH = (uint64_t)NT * VPT;
 
@@ -48,9 +61,10 @@ __global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
   map_wg(blockIdx.x, gridDim.x, P, group, part);
   const uint32_t n_groups = gridDim.x / P;
   GroupMem gm{};
-  if constexpr (NT > WAVE) {
+  if constexpr (BIG) {
     if (P > 1) gm = group_mem(a.ws, group, P);
   }
+  bool exited = false;
 
   for (uint64_t seg = group; seg < a.n_seg; seg += n_groups) {
     const uint64_t c0 = (uint64_t)part * CH + (uint64_t)threadIdx.x * VPT;
@@ -71,14 +85,14 @@ __global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
     {
       R xr[VPT];
       const uint64_t off = seg * a.L + c0;
-      if (nv > 0) load_run_partial<R, VPT>((const R*)a.x + off, nv, R{}, xr);
+      if (nv > 0) load_run_partial<R, VPT, true>((const R*)a.x + off, nv, R{}, xr);
       if constexpr (SEL == SEL_EF) {
         float er[VPT];
-        if (nv > 0) load_run_partial<float, VPT>(a.e + off, nv, 0.0f, er);
+        if (nv > 0) load_run_partial<float, VPT, true>(a.e + off, nv, 0.0f, er);
 #pragma unroll
         for (int i = 0; i < VPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) + er[i] : 0.0f;
       } else if constexpr (SEL == SEL_AQSGD) {
-        if (nv > 0) load_run_partial<R, VPT>((const R*)a.m + mrow + c0, nv, R{}, mr);
+        if (nv > 0) load_run_partial<R, VPT, true>((const R*)a.m + mrow + c0, nv, R{}, mr);
 #pragma unroll
         for (int i = 0; i < VPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) - Elem<InT>::up(mr[i]) : 0.0f;
       } else {
@@ -86,19 +100,28 @@ __global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
         for (int i = 0; i < VPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) : 0.0f;
       }
     }
+
     uint32_t key[VPT];
 #pragma unroll
     for (int i = 0; i < VPT; ++i) key[i] = mag_key(v[i]);
 
     // ---- selection
     SelResult sr;
-    if (a.k == 0) {
-      sr.T = 0xFFFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0;
+    Placement pl;
+    if constexpr (BIG) {
+      if (a.k == 0) { sr.T = 0xFFFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
+      else sr = radix_select<NT, VPT>(key, nv, (uint32_t)a.k, P, part, gm, sh.sel);
+      pl = place<NT, VPT>(key, nv, sr, sh.sel.scratch);
+      // the group's slots have been read: count out now, before the writes
+      if (P > 1 && seg + n_groups >= a.n_seg) {
+        group_exit<NT>(gm.bar, P, gm.slots, slot_words(P));
+        exited = true;
+      }
     } else {
-      if constexpr (NT > WAVE) sr = radix_select<NT, VPT>(key, nv, (uint32_t)a.k, P, part, gm, sh);
+      if (a.k == 0) { sr.T = 0xFFFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
       else sr = bitwise_select<VPT>(key, nv, (uint32_t)a.k);
+      pl = place<NT, VPT>(key, nv, sr, sh.scratch);
     }
-    const Placement pl = place<NT, VPT>(key, nv, sr, sh.scratch);
 
     // ---- payload + epilogue
     uint32_t* idx = a.idx + seg * a.k;
@@ -109,14 +132,18 @@ __global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
     for (int i = 0; i < VPT; ++i) {
       bool kept = false;
       if (i < nv) {
-        kept = key[i] > sr.T || (key[i] == sr.T && ties++ < pl.tie_keep);
+        const bool tie = key[i] == sr.T;
+        kept = key[i] > sr.T || (tie && ties < pl.tie_keep);
+        ties += tie ? 1u : 0u;
         if (kept) {
           const R w = Elem<InT>::down(v[i]);
-          if (pos < a.k) {
-            idx[pos] = (uint32_t)(c0 + i);
-            val[pos] = w;
+          if constexpr (BIG) {
+            const uint32_t li = pos - pl.wg_first;     // slot inside the workgroup's run
+            if (li < CH) { sh.st.idx[li] = (uint32_t)(c0 + i); sh.st.val[li] = w; }
+            else raise_error(KERR_INTERNAL);
           } else {
-            raise_error(KERR_INTERNAL);
+            if (pos < a.k) { idx[pos] = (uint32_t)(c0 + i); val[pos] = w; }
+            else raise_error(KERR_INTERNAL);
           }
           ++pos;
           if constexpr (SEL == SEL_AQSGD) mr[i] = Elem<InT>::down(Elem<InT>::up(mr[i]) + Elem<InT>::up(w));
@@ -125,14 +152,48 @@ __global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
       if constexpr (SEL == SEL_EF) eo[i] = v[i] - (kept ? through<InT>(v[i]) : 0.0f);
     }
     if constexpr (SEL == SEL_EF) {
-      if (nv > 0) store_run_partial<float, VPT>(a.e + seg * a.L + c0, nv, eo);
+      if (nv > 0) store_run_partial<float, VPT, true>(a.e + seg * a.L + c0, nv, eo);
     }
     if constexpr (SEL == SEL_AQSGD) {
-      if (nv > 0 && a.k > 0) store_run_partial<R, VPT>((R*)a.m + mrow + c0, nv, mr);
+      if (nv > 0 && a.k > 0) store_run_partial<R, VPT, true>((R*)a.m + mrow + c0, nv, mr);
+    }
+    if constexpr (BIG) {
+      // the workgroup's run of the payload, in index order, coalesced
+      __syncthreads();
+      const uint32_t cnt = min(pl.wg_count, (uint32_t)CH);
+      if (pl.wg_first + cnt > a.k) { if (threadIdx.x == 0) raise_error(KERR_INTERNAL); }
+      else {
+        copy_lds_to_global<NT>(idx + pl.wg_first, sh.st.idx, cnt);
+        copy_lds_to_global<NT>(val + pl.wg_first, sh.st.val, cnt);
+      }
+      // block table: kept entries below each block boundary this workgroup covers,
+      // found by a lower bound in the staged (ascending) run
+      if (a.blk) {
+        uint32_t* bt = a.blk + seg * (n_blocks(a.L) + 1);
+        const uint64_t w0 = (uint64_t)part * CH, w1 = min(a.L, w0 + CH);
+        for (uint64_t b = (w0 + BLOCK_LEN - 1) / BLOCK_LEN + threadIdx.x; b * BLOCK_LEN < w1; b += NT) {
+          const uint64_t B = b * BLOCK_LEN;
+          uint32_t lo = 0, hi = cnt;
+          while (lo < hi) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (sh.st.idx[mid] < B) lo = mid + 1; else hi = mid;
+          }
+          bt[b] = pl.wg_first + lo;
+        }
+        if (part == 0 && threadIdx.x == 0) bt[n_blocks(a.L)] = (uint32_t)a.k;
+      }
+      __syncthreads();
+    } else {
+      if (a.blk && threadIdx.x == 0) {
+        // a wavefront segment is shorter than one block
+        uint32_t* bt = a.blk + seg * (n_blocks(a.L) + 1);
+        bt[0] = 0;
+        bt[n_blocks(a.L)] = (uint32_t)a.k;
+      }
     }
   }
-  if constexpr (NT > WAVE) {
-    if (P > 1) group_exit<NT>(gm.bar, P, gm.slots, (uint64_t)P * SLOT_WORDS);
+  if constexpr (BIG) {
+    if (P > 1 && !exited) group_exit<NT>(gm.bar, P, gm.slots, slot_words(P));
   }
 }
 
@@ -142,6 +203,7 @@ namespace {
 constexpr int BIG_NT = 512;
 constexpr int ROW_NT = 64;
 constexpr uint64_t ROW_MAX = (uint64_t)ROW_NT * 32;   // longest segment one wavefront holds
+static_assert(ROW_MAX <= BLOCK_LEN, "a wavefront segment fits in one block of the block table");
 
 template <typename InT, int SEL>
 const void* kernel_ptr(int nt, int vpt) {
@@ -160,7 +222,6 @@ const void* kernel_ptr(int nt, int vpt) {
       case 8: return (const void*)k_topk_seg<InT, SEL, 8, BIG_NT>;
       case 16: return (const void*)k_topk_seg<InT, SEL, 16, BIG_NT>;
       case 24: return (const void*)k_topk_seg<InT, SEL, 24, BIG_NT>;
-      case 32: return (const void*)k_topk_seg<InT, SEL, 32, BIG_NT>;
     }
   }
   return nullptr;
@@ -205,7 +266,7 @@ SegPlan plan_topk(int sel, int dt, uint64_t n_seg, uint64_t L) {
   }
   // several workgroups per segment: the longest run per thread that still
   // gives every compute unit a workgroup, else the shortest run
-  static const int vpts[] = {32, 24, 16, 8, 4};
+  static const int vpts[] = {24, 16, 8, 4};
   p.nt = BIG_NT;
   p.vpt = 4;
   for (int v : vpts) {

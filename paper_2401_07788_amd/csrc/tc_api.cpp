@@ -71,7 +71,7 @@ tc_status check_ws(const tc::SegPlan& p, const void* ws, size_t ws_bytes) {
   if (need == 0) return TC_OK;
   if (!ws) return fail(TC_ERR_WORKSPACE, "workspace of %zu bytes required", need);
   if (ws_bytes < need) return fail(TC_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
-  if (((uintptr_t)ws & 3u) != 0) return fail(TC_ERR_ALIGN, "workspace must be 4-byte aligned");
+  if (((uintptr_t)ws & 7u) != 0) return fail(TC_ERR_ALIGN, "workspace must be 8-byte aligned");
   return TC_OK;
 }
 
@@ -95,8 +95,9 @@ tc_status topk_common(int sel, const tc_codec* c, const void* x, int dt, float* 
   if (sel == tc::SEL_EF && !e) return fail(TC_ERR_NULL, "error buffer is NULL");
   if (sel == tc::SEL_AQSGD && (!m || !ids)) return fail(TC_ERR_NULL, "buffer or ids is NULL");
   if (c->k > 0 && (!out->idx || !out->val)) return fail(TC_ERR_NULL, "payload idx/val is NULL");
-  if (c->k == 0 && sel == tc::SEL_PLAIN) return TC_OK;   // empty payload
-  if (c->k == 0 && sel == tc::SEL_AQSGD) return TC_OK;   // nothing sent, buffer unchanged
+  // k == 0: an empty payload (and, for AQ-SGD, an unchanged buffer); only a
+  // requested block table still has to be written
+  if (c->k == 0 && !out->blk && (sel == tc::SEL_PLAIN || sel == tc::SEL_AQSGD)) return TC_OK;
   const tc::SegPlan p = tc::plan_topk(sel, dt, c->n_seg, c->seg_len);
   tc_status s = check_resident(p);
   if (s != TC_OK) return s;
@@ -110,6 +111,7 @@ tc_status topk_common(int sel, const tc_codec* c, const void* x, int dt, float* 
   a.n_samples = n_samples;
   a.idx = out->idx;
   a.val = out->val;
+  a.blk = out->blk;
   a.n_seg = c->n_seg;
   a.L = c->seg_len;
   a.k = c->k;
@@ -237,6 +239,7 @@ TC_API tc_status tc_topk_decompress(const tc_codec* c, const tc_payload* in, voi
   }
   tc::ScatterArgs a{};
   a.idx = in->idx;
+  a.blk = in->blk;
   a.val = in->val;
   a.codes = (const uint32_t*)in->codes;
   a.meta = in->meta;
@@ -312,6 +315,7 @@ TC_API tc_status tc_aqsgd_reconstruct(const tc_codec* c, const tc_payload* in, v
   if (c->k > 0 && (!in->idx || !in->val)) return fail(TC_ERR_NULL, "payload idx/val is NULL");
   tc::ScatterArgs a{};
   a.idx = in->idx;
+  a.blk = in->blk;
   a.val = in->val;
   a.y = a_hat;
   a.m = m_r;

@@ -68,8 +68,25 @@ __device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v)
 // ------------------------------------------------------------ vector access
 // Load/store N consecutive raw elements starting at p (element units).
 // Uses 16-byte accesses when the run is 16-byte aligned and a multiple of 16
-// bytes, else 8-byte, else scalar accesses.
-template <typename R, int N>
+// bytes, else 8-byte, else scalar accesses.  STREAM marks data touched once
+// per launch (the boundary tensors): those accesses carry the non-temporal
+// hint so that they do not displace reused lines or pile up as dirty L2
+// lines at the end of the kernel.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <bool STREAM, typename V>
+__device__ __forceinline__ V vload(const V* p) {
+  if constexpr (STREAM) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+template <bool STREAM, typename V>
+__device__ __forceinline__ void vstore(V* p, V v) {
+  if constexpr (STREAM) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
+template <typename R, int N, bool STREAM = false>
 __device__ __forceinline__ void load_run(const R* __restrict__ p, R (&out)[N]) {
   constexpr int BYTES = N * (int)sizeof(R);
   const uintptr_t a = (uintptr_t)p;
@@ -78,7 +95,7 @@ __device__ __forceinline__ void load_run(const R* __restrict__ p, R (&out)[N]) {
       constexpr int PER = 16 / (int)sizeof(R);
 #pragma unroll
       for (int i = 0; i < N / PER; ++i) {
-        uint4 w = *reinterpret_cast<const uint4*>(p + i * PER);
+        const u32x4 w = vload<STREAM>(reinterpret_cast<const u32x4*>(p + i * PER));
         __builtin_memcpy(&out[i * PER], &w, 16);
       }
       return;
@@ -89,7 +106,7 @@ __device__ __forceinline__ void load_run(const R* __restrict__ p, R (&out)[N]) {
       constexpr int PER = 8 / (int)sizeof(R);
 #pragma unroll
       for (int i = 0; i < N / PER; ++i) {
-        uint2 w = *reinterpret_cast<const uint2*>(p + i * PER);
+        const u32x2 w = vload<STREAM>(reinterpret_cast<const u32x2*>(p + i * PER));
         __builtin_memcpy(&out[i * PER], &w, 8);
       }
       return;
@@ -99,7 +116,7 @@ __device__ __forceinline__ void load_run(const R* __restrict__ p, R (&out)[N]) {
   for (int i = 0; i < N; ++i) out[i] = p[i];
 }
 
-template <typename R, int N>
+template <typename R, int N, bool STREAM = false>
 __device__ __forceinline__ void store_run(R* __restrict__ p, const R (&in)[N]) {
   constexpr int BYTES = N * (int)sizeof(R);
   const uintptr_t a = (uintptr_t)p;
@@ -108,9 +125,9 @@ __device__ __forceinline__ void store_run(R* __restrict__ p, const R (&in)[N]) {
       constexpr int PER = 16 / (int)sizeof(R);
 #pragma unroll
       for (int i = 0; i < N / PER; ++i) {
-        uint4 w;
+        u32x4 w;
         __builtin_memcpy(&w, &in[i * PER], 16);
-        *reinterpret_cast<uint4*>(p + i * PER) = w;
+        vstore<STREAM>(reinterpret_cast<u32x4*>(p + i * PER), w);
       }
       return;
     }
@@ -120,9 +137,9 @@ __device__ __forceinline__ void store_run(R* __restrict__ p, const R (&in)[N]) {
       constexpr int PER = 8 / (int)sizeof(R);
 #pragma unroll
       for (int i = 0; i < N / PER; ++i) {
-        uint2 w;
+        u32x2 w;
         __builtin_memcpy(&w, &in[i * PER], 8);
-        *reinterpret_cast<uint2*>(p + i * PER) = w;
+        vstore<STREAM>(reinterpret_cast<u32x2*>(p + i * PER), w);
       }
       return;
     }
@@ -133,19 +150,42 @@ __device__ __forceinline__ void store_run(R* __restrict__ p, const R (&in)[N]) {
 
 // Load a run that may be cut short at `n` valid elements (n <= N); elements
 // past n are left as `fill`.
-template <typename R, int N>
+template <typename R, int N, bool STREAM = false>
 __device__ __forceinline__ void load_run_partial(const R* __restrict__ p, int n, R fill, R (&out)[N]) {
-  if (n >= N) { load_run<R, N>(p, out); return; }
+  if (n >= N) { load_run<R, N, STREAM>(p, out); return; }
 #pragma unroll
   for (int i = 0; i < N; ++i) out[i] = (i < n) ? p[i] : fill;
 }
 
-template <typename R, int N>
+template <typename R, int N, bool STREAM = false>
 __device__ __forceinline__ void store_run_partial(R* __restrict__ p, int n, const R (&in)[N]) {
-  if (n >= N) { store_run<R, N>(p, in); return; }
+  if (n >= N) { store_run<R, N, STREAM>(p, in); return; }
 #pragma unroll
   for (int i = 0; i < N; ++i)
     if (i < n) p[i] = in[i];
+}
+
+// Copy n consecutive elements from LDS to device memory, all threads of the
+// workgroup together: unaligned head and tail element by element, the body
+// in 16-byte stores at 16-byte aligned addresses.
+template <int NT, typename R>
+__device__ __forceinline__ void copy_lds_to_global(R* __restrict__ dst, const R* src, uint32_t n) {
+  constexpr uint32_t PER = 16 / sizeof(R);
+  const uint32_t mis = (uint32_t)(((uintptr_t)dst / sizeof(R)) % PER);
+  const uint32_t head = min(n, (PER - mis) % PER);
+  const uint32_t body = (n - head) / PER;
+  const int t = (int)threadIdx.x;
+  if ((uint32_t)t < head) dst[t] = src[t];
+  for (uint32_t q = (uint32_t)t; q < body; q += NT) {
+    R tmp[PER];
+#pragma unroll
+    for (uint32_t i = 0; i < PER; ++i) tmp[i] = src[head + q * PER + i];
+    u32x4 w;
+    __builtin_memcpy(&w, tmp, 16);
+    vstore<true>(reinterpret_cast<u32x4*>(dst + head + q * PER), w);
+  }
+  const uint32_t done = head + body * PER;
+  if ((uint32_t)t < n - done) dst[done + t] = src[done + t];
 }
 
 // a - b clamped at 0, written without a guarded subtraction.  The device
@@ -159,33 +199,48 @@ __device__ __forceinline__ T sat_sub(T a, T b) { return a - min(a, b); }
 // --------------------------------------------------------- wave64 helpers
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (WAVE - 1)); }
 
+// Cross-lane steps use DPP (data-parallel primitives: lane shifts inside a
+// 16-lane row, then row broadcasts), which run on the VALU without an LDS
+// round trip.  Lanes without a source lane read `old`.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, CTRL, ROW_MASK, 0xF, false);
+}
+constexpr int DPP_ROW_SHR1 = 0x111, DPP_ROW_SHR2 = 0x112, DPP_ROW_SHR4 = 0x114, DPP_ROW_SHR8 = 0x118;
+constexpr int DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143;
+
+// inclusive prefix sum over the 64 lanes (all lanes must be active)
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int d = 1; d < WAVE; d <<= 1) {
-    uint32_t y = __shfl_up(x, d, WAVE);
-    if (lane >= d) x += y;
-  }
+  x += dpp_u32<DPP_ROW_SHR1, 0xF>(0u, x);
+  x += dpp_u32<DPP_ROW_SHR2, 0xF>(0u, x);
+  x += dpp_u32<DPP_ROW_SHR4, 0xF>(0u, x);
+  x += dpp_u32<DPP_ROW_SHR8, 0xF>(0u, x);
+  x += dpp_u32<DPP_ROW_BCAST15, 0xA>(0u, x);   // rows 1, 3 add the end of rows 0, 2
+  x += dpp_u32<DPP_ROW_BCAST31, 0xC>(0u, x);   // rows 2, 3 add the end of row 1
   return x;
 }
 
 __device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
-#pragma unroll
-  for (int d = WAVE / 2; d > 0; d >>= 1) x += __shfl_xor(x, d, WAVE);
-  return x;
+  return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(x), WAVE - 1);
 }
 
-__device__ __forceinline__ float wave_min(float x) {
-#pragma unroll
-  for (int d = WAVE / 2; d > 0; d >>= 1) x = fminf(x, __shfl_xor(x, d, WAVE));
-  return x;
+// running min / max in the same lane pattern; lane 63 ends with the result
+template <bool MAX>
+__device__ __forceinline__ float wave_minmax(float x) {
+  const uint32_t id = __float_as_uint(MAX ? -__builtin_inff() : __builtin_inff());
+  auto op = [](float a, float b) { return MAX ? fmaxf(a, b) : fminf(a, b); };
+  uint32_t u = __float_as_uint(x);
+  u = __float_as_uint(op(__uint_as_float(u), __uint_as_float(dpp_u32<DPP_ROW_SHR1, 0xF>(id, u))));
+  u = __float_as_uint(op(__uint_as_float(u), __uint_as_float(dpp_u32<DPP_ROW_SHR2, 0xF>(id, u))));
+  u = __float_as_uint(op(__uint_as_float(u), __uint_as_float(dpp_u32<DPP_ROW_SHR4, 0xF>(id, u))));
+  u = __float_as_uint(op(__uint_as_float(u), __uint_as_float(dpp_u32<DPP_ROW_SHR8, 0xF>(id, u))));
+  u = __float_as_uint(op(__uint_as_float(u), __uint_as_float(dpp_u32<DPP_ROW_BCAST15, 0xA>(id, u))));
+  u = __float_as_uint(op(__uint_as_float(u), __uint_as_float(dpp_u32<DPP_ROW_BCAST31, 0xC>(id, u))));
+  return __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)u, WAVE - 1));
 }
 
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int d = WAVE / 2; d > 0; d >>= 1) x = fmaxf(x, __shfl_xor(x, d, WAVE));
-  return x;
-}
+__device__ __forceinline__ float wave_min(float x) { return wave_minmax<false>(x); }
+__device__ __forceinline__ float wave_max(float x) { return wave_minmax<true>(x); }
 
 // ------------------------------------------------------- workgroup helpers
 // scratch must hold NT/64 + 1 words of LDS.  All threads of the workgroup
@@ -196,7 +251,7 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratc
   const int w = (int)threadIdx.x / WAVE;
   uint32_t incl = wave_incl_scan(v);
   if constexpr (NW == 1) {
-    total = __shfl(incl, WAVE - 1, WAVE);
+    total = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1);
     return incl - v;
   } else {
     if (lane_id() == WAVE - 1) scratch[w] = incl;
@@ -252,31 +307,33 @@ __device__ __forceinline__ void block_minmax(float& lo, float& hi, float* scratc
 
 // ------------------------------------------------ cross-workgroup barrier
 // A sense-reversing barrier among the P workgroups of one group (state[0..2]:
-// arrival count, sense, exit count; see group_exit).  Data that
-// crosses workgroups is written with device-scope atomics (add_agent /
-// st_agent) and read with device-scope loads (ld_agent).  state[0] is
-// the arrival count (back to 0 after every round), state[1] the sense word,
-// which flips once per round.  The wait is bounded: if the other workgroups
-// do not arrive (they are not co-resident), it gives up, raises KERR_TIMEOUT
-// and lets the kernel run to its end.
+// arrival count, sense, exit count; see group_exit).
+//
+// Everything one workgroup hands to another inside a launch (histograms,
+// slots, these counters) is written and read with device-scope atomics
+// (add_agent / st_agent / ld_agent), which are coherent at device scope by
+// themselves.  The barrier therefore only has to order them: each wave
+// waits until its own memory operations have completed before the
+// workgroup arrives, and every later read is issued after the wait has seen
+// the flip.  No cache write-back or invalidate is needed (those would only
+// matter for plain loads and stores, which never cross workgroups here).
+// The wait is bounded: if the other workgroups do not arrive (they are not
+// co-resident), it gives up, raises KERR_TIMEOUT and lets the kernel finish.
 constexpr uint32_t BARRIER_SPIN_LIMIT = 1u << 19;
 
 __device__ __forceinline__ void group_barrier(uint32_t* state, uint32_t P) {
-  // each wave waits until its own global writes and atomics are acknowledged
-  // (vector memory counter at zero); the workgroup barrier then orders them
-  // before thread 0's device-scope release below
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
     uint32_t* count = state;
     uint32_t* sense = state + 1;
     const uint32_t s0 = __hip_atomic_load(sense, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint32_t prev = __hip_atomic_fetch_add(count, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t prev = __hip_atomic_fetch_add(count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (prev == P - 1) {
       __hip_atomic_store(count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(sense, s0 ^ 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      __builtin_amdgcn_s_waitcnt(0);
+      __hip_atomic_store(sense, s0 ^ 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     } else {
-      // relaxed polling (no cache maintenance per poll), one acquire at the end
       uint32_t spins = 0;
       while (__hip_atomic_load(sense, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == s0) {
         __builtin_amdgcn_s_sleep(1);
@@ -288,7 +345,6 @@ __device__ __forceinline__ void group_barrier(uint32_t* state, uint32_t P) {
         if (spins > BARRIER_SPIN_LIMIT) { raise_error(KERR_TIMEOUT); break; }
       }
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
   __syncthreads();
 }
@@ -303,7 +359,7 @@ __device__ __forceinline__ void group_exit(uint32_t* state, uint32_t P, uint32_t
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(state + 2, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t prev = __hip_atomic_fetch_add(state + 2, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     last_out = (prev == P - 1) ? 1u : 0u;
   }
   __syncthreads();
@@ -325,6 +381,9 @@ __device__ __forceinline__ void st_agent(uint32_t* p, uint32_t v) {
 }
 __device__ __forceinline__ void add_agent(uint32_t* p, uint32_t v) {
   __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_agent64(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // host side: read (and optionally clear) this translation unit's error word

@@ -37,10 +37,14 @@ struct TopkArgs {
   uint64_t n_samples;
   uint32_t* idx;         // [n_seg][k]
   void* val;             // [n_seg][k] in the input dtype
+  uint32_t* blk;         // optional [n_seg][nblk + 1] block table
   uint64_t n_seg, L, k;
   uint32_t P;
   uint32_t* ws;
 };
+
+constexpr uint64_t BLOCK_LEN = 4096;   // TC_BLOCK_LEN
+__host__ __device__ constexpr uint64_t n_blocks(uint64_t L) { return (L + BLOCK_LEN - 1) / BLOCK_LEN; }
 
 SegPlan plan_topk(int sel, int dt, uint64_t n_seg, uint64_t L);
 hipError_t launch_topk(int sel, int dt, const SegPlan& plan, const TopkArgs& a, hipStream_t st);
@@ -71,6 +75,7 @@ hipError_t launch_unpack(int out_dt, uint32_t bits, const UnpackArgs& a, hipStre
 // --------------------------------------------------------- receiver side
 struct ScatterArgs {
   const uint32_t* idx;   // [n_seg][k]
+  const uint32_t* blk;   // optional [n_seg][nblk + 1] block table
   const void* val;       // [n_seg][k] wire values (TopK)
   const uint32_t* codes; // TopK+quant: [n_seg][wpg] codes of the kept list
   const float* meta;     // TopK+quant: [n_seg][2]

@@ -11,6 +11,7 @@ from __future__ import annotations
 import ctypes as C
 import os
 import threading
+from typing import NamedTuple, Optional
 
 import torch
 
@@ -31,7 +32,29 @@ class Codec(C.Structure):
 
 
 class Payload(C.Structure):
-    _fields_ = [("idx", C.c_void_p), ("val", C.c_void_p), ("codes", C.c_void_p), ("meta", C.c_void_p)]
+    _fields_ = [("idx", C.c_void_p), ("val", C.c_void_p), ("codes", C.c_void_p), ("meta", C.c_void_p),
+                ("blk", C.c_void_p)]
+
+
+BLOCK_LEN = 4096   # TC_BLOCK_LEN
+
+
+def n_blocks(seg_len: int) -> int:
+    return (seg_len + BLOCK_LEN - 1) // BLOCK_LEN
+
+
+class TopkPayload(NamedTuple):
+    """a TopK message: indices (uint32 patterns in an int32 tensor), values,
+    and the block table ([n_seg, n_blocks + 1] int32, or None)"""
+    idx: torch.Tensor
+    val: torch.Tensor
+    blk: Optional[torch.Tensor]
+
+
+def empty_topk_payload(n_seg: int, seg_len: int, k: int, dtype, device, blk: bool = True) -> TopkPayload:
+    return TopkPayload(torch.empty((n_seg, k), dtype=torch.int32, device=device),
+                       torch.empty((n_seg, k), dtype=dtype, device=device),
+                       torch.empty((n_seg, n_blocks(seg_len) + 1), dtype=torch.int32, device=device) if blk else None)
 
 
 class TCError(RuntimeError):
@@ -171,28 +194,28 @@ def _ws_args(c, device, ws):
 
 
 # --------------------------------------------------------------------- TopK
-def topk_compress(x: torch.Tensor, k: int, n_seg: int, ws=None):
-    """TopK per segment of x viewed as [n_seg, seg_len] -> (idx uint32-as-int32, val)"""
+def topk_compress(x: torch.Tensor, k: int, n_seg: int, ws=None, out: TopkPayload = None, blk: bool = True):
+    """TopK per segment of x viewed as [n_seg, seg_len] -> TopkPayload"""
     _need_gpu(x)
     L = x.numel() // n_seg
     c = codec(TC_TOPK, n_seg, L, k, wire=_dt(x))
-    idx = torch.empty((n_seg, k), dtype=torch.int32, device=x.device)
-    val = torch.empty((n_seg, k), dtype=x.dtype, device=x.device)
-    p = Payload(_ptr(idx), _ptr(val), None, None)
+    out = out or empty_topk_payload(n_seg, L, k, x.dtype, x.device, blk)
+    p = Payload(_ptr(out.idx), _ptr(out.val), None, None, _ptr(out.blk))
     w, wn = _ws_args(c, x.device, ws)
     _check(lib().tc_topk_compress(C.byref(c), _ptr(x), _dt(x), C.byref(p), w, wn, _stream(x.device)),
            "tc_topk_compress")
-    return idx, val
+    return out
 
 
-def topk_decompress(idx: torch.Tensor, val: torch.Tensor, seg_len: int, out_dtype=None):
-    _need_gpu(idx, val)
-    n_seg, k = idx.shape
-    out_dtype = out_dtype or val.dtype
-    c = codec(TC_TOPK, n_seg, seg_len, k, wire=_dt(val))
-    y = torch.empty((n_seg, seg_len), dtype=out_dtype, device=idx.device)
-    p = Payload(_ptr(idx), _ptr(val), None, None)
-    _check(lib().tc_topk_decompress(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(idx.device)),
+def topk_decompress(pl: TopkPayload, seg_len: int, out_dtype=None, use_blk: bool = True):
+    """dense [n_seg, seg_len] tensor: the sent values at their indices, +0 elsewhere"""
+    _need_gpu(pl.idx, pl.val, pl.blk)
+    n_seg, k = pl.idx.shape
+    out_dtype = out_dtype or pl.val.dtype
+    c = codec(TC_TOPK, n_seg, seg_len, k, wire=_dt(pl.val))
+    y = torch.empty((n_seg, seg_len), dtype=out_dtype, device=pl.idx.device)
+    p = Payload(_ptr(pl.idx), _ptr(pl.val), None, None, _ptr(pl.blk) if use_blk else None)
+    _check(lib().tc_topk_decompress(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(pl.idx.device)),
            "tc_topk_decompress")
     return y
 
@@ -205,7 +228,7 @@ def quant_pack(x: torch.Tensor, bits: int, n_grp: int, ws=None):
     c = codec(TC_QUANT, n_grp, G, bits=bits, wire=_dt(x))
     codes = torch.empty((n_grp, quant_group_bytes(G, bits)), dtype=torch.uint8, device=x.device)
     meta = torch.empty((n_grp, 2), dtype=torch.float32, device=x.device)
-    p = Payload(None, None, _ptr(codes), _ptr(meta))
+    p = Payload(None, None, _ptr(codes), _ptr(meta), None)
     w, wn = _ws_args(c, x.device, ws)
     _check(lib().tc_quant_pack(C.byref(c), _ptr(x), _dt(x), C.byref(p), w, wn, _stream(x.device)), "tc_quant_pack")
     return codes, meta
@@ -216,27 +239,27 @@ def quant_unpack(codes: torch.Tensor, meta: torch.Tensor, grp_len: int, bits: in
     n_grp = meta.shape[0]
     c = codec(TC_QUANT, n_grp, grp_len, bits=bits, wire=_DT[out_dtype])
     y = torch.empty((n_grp, grp_len), dtype=out_dtype, device=codes.device)
-    p = Payload(None, None, _ptr(codes), _ptr(meta))
+    p = Payload(None, None, _ptr(codes), _ptr(meta), None)
     _check(lib().tc_quant_unpack(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(codes.device)),
            "tc_quant_unpack")
     return y
 
 
 # ----------------------------------------------------------- error feedback
-def ef_step_topk(x: torch.Tensor, e: torch.Tensor, k: int, n_seg: int, ws=None):
+def ef_step_topk(x: torch.Tensor, e: torch.Tensor, k: int, n_seg: int, ws=None, out: TopkPayload = None,
+                 blk: bool = True):
     """X = x + e; send TopK(X); e <- X - received.  e (float32) is updated in place."""
     _need_gpu(x, e)
     if e.dtype != torch.float32 or e.numel() != x.numel():
         raise ValueError("e must be float32 with x's element count")
     L = x.numel() // n_seg
     c = codec(TC_TOPK, n_seg, L, k, wire=_dt(x))
-    idx = torch.empty((n_seg, k), dtype=torch.int32, device=x.device)
-    val = torch.empty((n_seg, k), dtype=x.dtype, device=x.device)
-    p = Payload(_ptr(idx), _ptr(val), None, None)
+    out = out or empty_topk_payload(n_seg, L, k, x.dtype, x.device, blk)
+    p = Payload(_ptr(out.idx), _ptr(out.val), None, None, _ptr(out.blk))
     w, wn = _ws_args(c, x.device, ws)
     _check(lib().tc_ef_step(C.byref(c), _ptr(x), _dt(x), C.cast(e.data_ptr(), C.POINTER(C.c_float)), C.byref(p),
                             w, wn, _stream(x.device)), "tc_ef_step")
-    return idx, val
+    return out
 
 
 def ef_step_quant(x: torch.Tensor, e: torch.Tensor, bits: int, n_grp: int, ws=None):
@@ -248,7 +271,7 @@ def ef_step_quant(x: torch.Tensor, e: torch.Tensor, bits: int, n_grp: int, ws=No
     c = codec(TC_QUANT, n_grp, G, bits=bits, wire=_dt(x))
     codes = torch.empty((n_grp, quant_group_bytes(G, bits)), dtype=torch.uint8, device=x.device)
     meta = torch.empty((n_grp, 2), dtype=torch.float32, device=x.device)
-    p = Payload(None, None, _ptr(codes), _ptr(meta))
+    p = Payload(None, None, _ptr(codes), _ptr(meta), None)
     w, wn = _ws_args(c, x.device, ws)
     _check(lib().tc_ef_step(C.byref(c), _ptr(x), _dt(x), C.cast(e.data_ptr(), C.POINTER(C.c_float)), C.byref(p),
                             w, wn, _stream(x.device)), "tc_ef_step")
@@ -256,7 +279,8 @@ def ef_step_quant(x: torch.Tensor, e: torch.Tensor, bits: int, n_grp: int, ws=No
 
 
 # ------------------------------------------------------------------- AQ-SGD
-def aqsgd_step(a: torch.Tensor, m: torch.Tensor, ids: torch.Tensor, k: int, ws=None, out=None):
+def aqsgd_step(a: torch.Tensor, m: torch.Tensor, ids: torch.Tensor, k: int, ws=None, out: TopkPayload = None,
+               blk: bool = True):
     """sender: d = a - m[ids]; send TopK(d); m[ids] += sent.  m is updated in place."""
     _need_gpu(a, m, ids)
     if ids.dtype != torch.int64 or a.dtype != m.dtype:
@@ -264,26 +288,22 @@ def aqsgd_step(a: torch.Tensor, m: torch.Tensor, ids: torch.Tensor, k: int, ws=N
     n_ids = ids.numel()
     L = m.shape[1]
     c = codec(TC_TOPK, n_ids, L, k, wire=_dt(m))
-    if out is None:
-        idx = torch.empty((n_ids, k), dtype=torch.int32, device=a.device)
-        val = torch.empty((n_ids, k), dtype=a.dtype, device=a.device)
-    else:
-        idx, val = out
-    p = Payload(_ptr(idx), _ptr(val), None, None)
+    out = out or empty_topk_payload(n_ids, L, k, a.dtype, a.device, blk)
+    p = Payload(_ptr(out.idx), _ptr(out.val), None, None, _ptr(out.blk))
     w, wn = _ws_args(c, a.device, ws)
     _check(lib().tc_aqsgd_step(C.byref(c), _ptr(a), _dt(a), _ptr(m), m.shape[0], _ptr(ids), n_ids, C.byref(p),
                                w, wn, _stream(a.device)), "tc_aqsgd_step")
-    return idx, val
+    return out
 
 
-def aqsgd_reconstruct(idx: torch.Tensor, val: torch.Tensor, m_r: torch.Tensor, ids: torch.Tensor, out=None):
+def aqsgd_reconstruct(pl: TopkPayload, m_r: torch.Tensor, ids: torch.Tensor, out=None, use_blk: bool = True):
     """receiver: m_r[ids] += received; returns a_hat = m_r[ids].  m_r is updated in place."""
-    _need_gpu(idx, val, m_r, ids)
-    n_ids, k = idx.shape
+    _need_gpu(pl.idx, pl.val, pl.blk, m_r, ids)
+    n_ids, k = pl.idx.shape
     L = m_r.shape[1]
     c = codec(TC_TOPK, n_ids, L, k, wire=_dt(m_r))
     a_hat = torch.empty((n_ids, L), dtype=m_r.dtype, device=m_r.device) if out is None else out
-    p = Payload(_ptr(idx), _ptr(val), None, None)
+    p = Payload(_ptr(pl.idx), _ptr(pl.val), None, None, _ptr(pl.blk) if use_blk else None)
     _check(lib().tc_aqsgd_reconstruct(C.byref(c), C.byref(p), _ptr(m_r), _dt(m_r), m_r.shape[0], _ptr(ids), n_ids,
                                       _ptr(a_hat), _stream(m_r.device)), "tc_aqsgd_reconstruct")
     return a_hat

@@ -48,3 +48,16 @@ def assert_rel_close(got, want, rel, what):
     lim = rel * np.abs(w)
     bad = np.flatnonzero(err > lim)
     assert bad.size == 0, f"{what}: {bad.size} entries beyond {rel} relative; first {bad[:5].tolist()}"
+
+
+def check_block_table(blk, oracle_idx, L, what="blk"):
+    """blk[s][b] must count the kept indices below b * 4096 (and end with k)"""
+    g = raw(blk).astype(np.int64)
+    n_seg, k = oracle_idx.shape
+    nb = (L + 4095) // 4096
+    assert g.shape == (n_seg, nb + 1), f"{what}: shape {g.shape}"
+    bounds = np.arange(nb + 1, dtype=np.int64) * 4096
+    for s in range(n_seg):
+        want = np.searchsorted(oracle_idx[s].astype(np.int64), bounds, side="left")
+        want[-1] = k
+        assert np.array_equal(g[s], want), f"{what}: segment {s}: got {g[s][:8]} want {want[:8]}"

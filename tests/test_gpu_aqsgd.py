@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import DTN, TORCH, assert_bits_equal, raw
+from gpu_helpers import DTN, TORCH, assert_bits_equal, check_block_table, raw
 from paper_2401_07788_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -23,14 +23,16 @@ def aq_steps(tc, orc, m0, ids_list, acts, k, check_rows=None):
     mo_r = mo.copy()
     for t, (ids, a) in enumerate(zip(ids_list, acts)):
         idsd = ids.cuda()
-        idx, val = tc.aqsgd_step(a.cuda(), m_s, idsd, k)
-        a_hat = tc.aqsgd_reconstruct(idx, val, m_r, idsd)
+        p = tc.aqsgd_step(a.cuda(), m_s, idsd, k)
+        # alternate the receiver between the block table and the index search
+        a_hat = tc.aqsgd_reconstruct(p, m_r, idsd, use_blk=(t % 2 == 0))
         torch.cuda.synchronize()
         assert tc.device_errors() == 0
         oi, ov = orc.aqsgd_send(raw(a), mo, dt, ids.numpy(), k)
         oa = orc.aqsgd_recv(oi, ov, mo_r, dt, ids.numpy(), k)
-        assert_bits_equal(raw(idx), oi, f"idx step {t}")
-        assert_bits_equal(raw(val), ov, f"val step {t}")
+        assert_bits_equal(raw(p.idx), oi, f"idx step {t}")
+        assert_bits_equal(raw(p.val), ov, f"val step {t}")
+        check_block_table(p.blk, oi, m0.shape[1], f"blk step {t}")
         assert_bits_equal(raw(a_hat), oa, f"a_hat step {t}")
         rows = ids.numpy() if check_rows is None else np.union1d(ids.numpy(), check_rows)
         assert_bits_equal(raw(m_s[torch.from_numpy(rows).cuda()]), mo[rows], f"m_s rows step {t}")
@@ -85,8 +87,9 @@ def test_aqsgd_full_size(tc, orc):
         ids = ids_all[t]
         rows0 = raw(m_s[ids.cuda()])                     # the oracle's copy of the touched rows
         a = W.drifted_activation(m_s, ids, 0, 100 + t)
-        idx, val = tc.aqsgd_step(a, m_s, ids.cuda(), k)
-        a_hat = tc.aqsgd_reconstruct(idx, val, m_r, ids.cuda())
+        p = tc.aqsgd_step(a, m_s, ids.cuda(), k)
+        a_hat = tc.aqsgd_reconstruct(p, m_r, ids.cuda(), use_blk=(t == 0))
+        idx, val = p.idx, p.val
         torch.cuda.synchronize()
         assert tc.device_errors() == 0
         mo = rows0.copy()
@@ -96,6 +99,7 @@ def test_aqsgd_full_size(tc, orc):
         oa = orc.aqsgd_recv(oi, ov, mo_r, "f16", local, k)
         assert_bits_equal(raw(idx), oi, f"idx mb {t}")
         assert_bits_equal(raw(val), ov, f"val mb {t}")
+        check_block_table(p.blk, oi, L, f"blk mb {t}")
         assert_bits_equal(raw(a_hat), oa, f"a_hat mb {t}")
         assert_bits_equal(raw(m_s[ids.cuda()]), mo, f"m_s rows mb {t}")
         assert_bits_equal(raw(m_r[ids.cuda()]), mo_r, f"m_r rows mb {t}")

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import DTN, assert_bits_equal, assert_rel_close, raw
+from gpu_helpers import DTN, assert_bits_equal, assert_rel_close, check_block_table, raw
 from paper_2401_07788_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -20,12 +20,15 @@ def ef_topk_steps(tc, orc, xs, n_seg, L, k):
     e_gpu = torch.zeros(n_seg * L, dtype=torch.float32, device="cuda")
     e_orc = np.zeros((n_seg, L), np.float32)
     for t, x in enumerate(xs):
-        idx, val = tc.ef_step_topk(x.cuda(), e_gpu, k, n_seg)
+        p = tc.ef_step_topk(x.cuda(), e_gpu, k, n_seg)
+        y = tc.topk_decompress(p, L)
         torch.cuda.synchronize()
         assert tc.device_errors() == 0
         oi, ov, e_orc = orc.ef_topk(raw(x), dt, e_orc, n_seg, L, k, threads=0)
-        assert_bits_equal(raw(idx), oi, f"idx step {t}")
-        assert_bits_equal(raw(val), ov, f"val step {t}")
+        assert_bits_equal(raw(p.idx), oi, f"idx step {t}")
+        assert_bits_equal(raw(p.val), ov, f"val step {t}")
+        check_block_table(p.blk, oi, L, f"blk step {t}")
+        assert_bits_equal(raw(y), orc.topk_decompress(oi, ov, dt, n_seg, L, k), f"received step {t}")
         eg = raw(e_gpu).reshape(n_seg, L)
         assert_rel_close(eg, e_orc, 1e-6, f"e step {t}")
         assert_bits_equal(eg, e_orc, f"e step {t} (bitwise)")

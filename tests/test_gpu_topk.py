@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import DTN, TORCH, assert_bits_equal, raw
+from gpu_helpers import DTN, TORCH, assert_bits_equal, check_block_table, raw
 from paper_2401_07788_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -33,15 +33,18 @@ def make_input(kind, n_seg, L, dt, seed):
 def run_case(tc, orc, x, n_seg, L, k):
     dt = DTN[x.dtype]
     xd = x.cuda()
-    idx, val = tc.topk_compress(xd, k, n_seg)
-    y = tc.topk_decompress(idx, val, L)
+    p = tc.topk_compress(xd, k, n_seg)
+    y = tc.topk_decompress(p, L)
+    y_search = tc.topk_decompress(p, L, use_blk=False)
     torch.cuda.synchronize()
     assert tc.device_errors() == 0
     oi, ov = orc.topk_compress(raw(x), dt, n_seg, L, k)
-    assert_bits_equal(raw(idx), oi, "idx")
-    assert_bits_equal(raw(val), ov, "val")
+    assert_bits_equal(raw(p.idx), oi, "idx")
+    assert_bits_equal(raw(p.val), ov, "val")
+    check_block_table(p.blk, oi, L)
     oy = orc.topk_decompress(oi, ov, dt, n_seg, L, k)
     assert_bits_equal(raw(y), oy, "dense")
+    assert_bits_equal(raw(y_search), oy, "dense (index search)")
 
 
 ROW_L = [1, 7, 64, 768, 1000, 2048]
@@ -84,7 +87,7 @@ def test_decompress_rejects_bad_index_without_fault(tc):
     idx = torch.tensor([[0, 5, 1 << 20]], dtype=torch.int32, device="cuda")
     val = torch.ones((1, 3), dtype=torch.float32, device="cuda")
     tc.device_errors(clear=True)
-    y = tc.topk_decompress(idx, val, 100)
+    y = tc.topk_decompress(tc.TopkPayload(idx, val, None), 100)
     torch.cuda.synchronize()
     assert tc.device_errors(clear=True) & tc.TC_KERR_BAD_INDEX
     yy = y.cpu()
@@ -95,6 +98,16 @@ def test_decompress_flags_unsorted_payload(tc):
     idx = torch.tensor([[0, 7, 5, 9]], dtype=torch.int32, device="cuda")
     val = torch.ones((1, 4), dtype=torch.float32, device="cuda")
     tc.device_errors(clear=True)
-    tc.topk_decompress(idx, val, 100)
+    tc.topk_decompress(tc.TopkPayload(idx, val, None), 100)
+    torch.cuda.synchronize()
+    assert tc.device_errors(clear=True) & tc.TC_KERR_BAD_INDEX
+
+
+def test_decompress_flags_bad_block_table(tc):
+    idx = torch.tensor([[0, 5, 9]], dtype=torch.int32, device="cuda")
+    val = torch.ones((1, 3), dtype=torch.float32, device="cuda")
+    blk = torch.tensor([[0, 7]], dtype=torch.int32, device="cuda")     # claims 7 entries, k is 3
+    tc.device_errors(clear=True)
+    tc.topk_decompress(tc.TopkPayload(idx, val, blk), 100)
     torch.cuda.synchronize()
     assert tc.device_errors(clear=True) & tc.TC_KERR_BAD_INDEX
