@@ -182,8 +182,12 @@ tc_status tc_quant_unpack(const tc_codec* c, const tc_payload* in, void* y, int 
 /* Sec. 2.4 sender with error feedback: X = x + e (binary32), send C(X), then
  * e <- X - r where r is exactly what the receiver's dense tensor will hold
  * (read back as binary32).  C is the codec's compressor (TopK, quantization,
- * or TopK whose kept list is quantized).  e: [n_seg][seg_len] binary32,
- * in-out, one buffer per compression operator, zero at the first step. */
+ * or TopK whose kept list is quantized as one min-max group per segment,
+ * TC_TOPK_QUANT).  e: [n_seg][seg_len] binary32, in-out, one buffer per
+ * compression operator, zero at the first step.  Segments longer than one
+ * resident group of workgroups holds (TC_TOPK) and every TC_TOPK_QUANT
+ * segment run through a chain of kernels over the whole segment; they need
+ * seg_len < 2^31. */
 tc_status tc_ef_step(const tc_codec* c, const void* x, int dt, float* e, const tc_payload* out,
                      void* ws, size_t ws_bytes, void* stream);
 

@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libtc.so")
-SOURCES = ["k_topk.hip", "k_quant.hip", "k_scatter.hip", "tc_api.cpp"]
+SOURCES = ["k_topk.hip", "k_quant.hip", "k_scatter.hip", "k_global.hip", "tc_api.cpp"]
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fvisibility=hidden", "-Wall",

@@ -63,6 +63,12 @@ __device__ __forceinline__ void chunk_range(const uint32_t* ix, const uint32_t* 
 // group per segment)
 enum { MODE_VAL = 0, MODE_CODES = 1 };
 
+// Entries a chunk can hold (sorted, distinct indices inside SC_CH elements)
+// spread over the threads: at most SC_VPT per thread.  Each thread loads all
+// of its entries before applying any, so the loads overlap instead of paying
+// one memory round trip per entry.
+constexpr int SC_EPT = (int)(SC_CH / SC_NT);
+
 template <typename WireT, typename OutT, int MODE, int B>
 __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
   using RW = typename Elem<WireT>::raw;
@@ -79,28 +85,46 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
     chunk_range(ix, bt, a.k, c0, c1, scratch, j0, j1);
     // entries past the segment's end belong to no chunk: the last chunk flags them
     if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
-    for (int i = (int)threadIdx.x; i < (int)SC_CH; i += SC_NT) buf[i] = RO{};
-    __syncthreads();
     float lo = 0.0f, scale = 0.0f;
     if constexpr (MODE == MODE_CODES) { lo = a.meta[2 * seg]; scale = a.meta[2 * seg + 1]; }
-    for (uint32_t j = j0 + threadIdx.x; j < j1; j += SC_NT) {
-      const uint32_t i = ix[j];
-      if (i < c0 || i >= c1 || (j > j0 && ix[j - 1] >= i)) { raise_error(KERR_BAD_INDEX); continue; }
-      float x;
-      if constexpr (MODE == MODE_VAL) {
-        x = Elem<WireT>::up(((const RW*)a.val)[seg * a.k + j]);
-      } else if constexpr (B == 32) {
-        x = __uint_as_float(a.codes[seg * a.wpg + j]);
-      } else {
-        const uint64_t bit = (uint64_t)j * B;
-        const uint32_t* w = a.codes + seg * a.wpg + (bit >> 5);
-        uint32_t c = w[0] >> (bit & 31);
-        if ((bit & 31) + B > 32) c |= w[1] << (32 - (bit & 31));
-        c &= (1u << B) - 1u;
-        const float prod = (float)c * scale;
-        x = lo + prod;
+    // this thread's entries j0 + t + r*SC_NT, all loaded first
+    uint32_t ei[SC_EPT];
+    float ex[SC_EPT];
+#pragma unroll
+    for (int r = 0; r < SC_EPT; ++r) {
+      const uint32_t j = j0 + threadIdx.x + (uint32_t)r * SC_NT;
+      ei[r] = 0xFFFFFFFFu;
+      ex[r] = 0.0f;
+      if (j < j1) {
+        ei[r] = ix[j];
+        // without a block table the ranges come from a search that needs
+        // ascending indices: check them
+        if (!bt && j > j0 && ix[j - 1] >= ei[r]) raise_error(KERR_BAD_INDEX);
+        if constexpr (MODE == MODE_VAL) {
+          ex[r] = Elem<WireT>::up(((const RW*)a.val)[seg * a.k + j]);
+        } else if constexpr (B == 32) {
+          ex[r] = __uint_as_float(a.codes[seg * a.wpg + j]);
+        } else {
+          const uint64_t bit = (uint64_t)j * B;
+          const uint32_t* w = a.codes + seg * a.wpg + (bit >> 5);
+          uint32_t c = w[0] >> (bit & 31);
+          if ((bit & 31) + B > 32) c |= w[1] << (32 - (bit & 31));
+          c &= (1u << B) - 1u;
+          const float prod = (float)c * scale;
+          ex[r] = lo + prod;
+        }
       }
-      buf[i - c0] = Elem<OutT>::down(x);
+    }
+    for (int i = (int)threadIdx.x; i < (int)SC_CH; i += SC_NT) buf[i] = RO{};
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < SC_EPT; ++r) {
+      const uint32_t j = j0 + threadIdx.x + (uint32_t)r * SC_NT;
+      if (j < j1) {
+        const uint32_t i = ei[r];
+        if (i < c0 || i >= c1) raise_error(KERR_BAD_INDEX);
+        else buf[i - c0] = Elem<OutT>::down(ex[r]);
+      }
     }
     __syncthreads();
     const uint64_t t0 = c0 + (uint64_t)threadIdx.x * SC_VPT;
@@ -129,7 +153,7 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
       continue;
     }
     R* row = (R*)a.m + (uint64_t)id * a.L;
-    // the buffer row first: its load overlaps the index search
+    // the buffer row first: its load overlaps the payload range and entries
     const uint64_t t0 = c0 + (uint64_t)threadIdx.x * SC_VPT;
     const int nv = (int)min((uint64_t)SC_VPT, sat_sub(c1, t0));
     R mr[SC_VPT];
@@ -139,13 +163,29 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
     uint32_t j0, j1;
     chunk_range(ix, bt, a.k, c0, c1, scratch, j0, j1);
     if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
+    uint32_t ei[SC_EPT];
+    float ex[SC_EPT];
+#pragma unroll
+    for (int r = 0; r < SC_EPT; ++r) {
+      const uint32_t j = j0 + threadIdx.x + (uint32_t)r * SC_NT;
+      ei[r] = 0xFFFFFFFFu;
+      ex[r] = 0.0f;
+      if (j < j1) {
+        ei[r] = ix[j];
+        if (!bt && j > j0 && ix[j - 1] >= ei[r]) raise_error(KERR_BAD_INDEX);
+        ex[r] = Elem<T>::up(((const R*)a.val)[b * a.k + j]);
+      }
+    }
     if (nv > 0) store_run<R, SC_VPT>(&buf[threadIdx.x * SC_VPT], mr);
     __syncthreads();
-    for (uint32_t j = j0 + threadIdx.x; j < j1; j += SC_NT) {
-      const uint32_t i = ix[j];
-      if (i < c0 || i >= c1 || (j > j0 && ix[j - 1] >= i)) { raise_error(KERR_BAD_INDEX); continue; }
-      const float add = Elem<T>::up(((const R*)a.val)[b * a.k + j]);
-      buf[i - c0] = Elem<T>::down(Elem<T>::up(buf[i - c0]) + add);
+#pragma unroll
+    for (int r = 0; r < SC_EPT; ++r) {
+      const uint32_t j = j0 + threadIdx.x + (uint32_t)r * SC_NT;
+      if (j < j1) {
+        const uint32_t i = ei[r];
+        if (i < c0 || i >= c1) raise_error(KERR_BAD_INDEX);
+        else buf[i - c0] = Elem<T>::down(Elem<T>::up(buf[i - c0]) + ex[r]);
+      }
     }
     __syncthreads();
     if (nv > 0) {

@@ -84,6 +84,38 @@ tc_status check_resident(const tc::SegPlan& p) {
   return TC_OK;
 }
 
+// TopK of segments too long to keep on chip, one segment after the other
+// (see k_global.hip); qbits != 0 quantizes the kept list (needs e)
+tc_status global_topk(uint32_t qbits, const tc_codec* c, const void* x, int dt, float* e, const tc_payload* out,
+                      void* ws, size_t ws_bytes, void* stream) {
+  const uint64_t L = c->seg_len, k = c->k;
+  if (L >= (1ull << 31)) return fail(TC_ERR_ARG, "seg_len %llu must be < 2^31 for a segment this long",
+                                     (unsigned long long)L);
+  const size_t need = (size_t)tc::global_ws_words(L) * 4u;
+  if (!ws) return fail(TC_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+  if (ws_bytes < need) return fail(TC_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
+  if (((uintptr_t)ws & 7u) != 0) return fail(TC_ERR_ALIGN, "workspace must be 8-byte aligned");
+  const uint64_t gb = qbits ? tc_quant_group_bytes(k, qbits) : 0;
+  const uint64_t nb = tc::n_blocks(L) + 1;
+  for (uint64_t s = 0; s < c->n_seg; ++s) {
+    tc::GlobalArgs a{};
+    a.x = (const char*)x + s * L * tc::dt_size(dt);
+    a.e = e ? e + s * L : nullptr;
+    a.idx = out->idx ? out->idx + s * k : nullptr;
+    a.val = (!qbits && out->val) ? (char*)out->val + s * k * tc::dt_size(dt) : nullptr;
+    a.codes = qbits ? (uint32_t*)(out->codes + s * gb) : nullptr;
+    a.meta = qbits ? out->meta + 2 * s : nullptr;
+    a.blk = out->blk ? out->blk + s * nb : nullptr;
+    a.L = L;
+    a.k = k;
+    a.wpg = gb / 4u;
+    tc::global_ws_carve((uint32_t*)ws, L, a);
+    hipError_t he = tc::launch_global(dt, e != nullptr, qbits, a, (hipStream_t)stream);
+    if (he != hipSuccess) return hip_fail(he, "global topk launch");
+  }
+  return TC_OK;
+}
+
 tc_status topk_common(int sel, const tc_codec* c, const void* x, int dt, float* e, void* m, uint64_t n_samples,
                       const int64_t* ids, const tc_payload* out, void* ws, size_t ws_bytes, void* stream) {
   if (!dt_ok(dt)) return fail(TC_ERR_DTYPE, "dtype %d", dt);
@@ -100,7 +132,11 @@ tc_status topk_common(int sel, const tc_codec* c, const void* x, int dt, float* 
   if (c->k == 0 && !out->blk && (sel == tc::SEL_PLAIN || sel == tc::SEL_AQSGD)) return TC_OK;
   const tc::SegPlan p = tc::plan_topk(sel, dt, c->n_seg, c->seg_len);
   tc_status s = check_resident(p);
-  if (s != TC_OK) return s;
+  if (s != TC_OK) {
+    if (sel == tc::SEL_AQSGD) return s;
+    g_err[0] = 0;
+    return global_topk(0, c, x, dt, e, out, ws, ws_bytes, stream);   // too long for one resident group
+  }
   s = check_ws(p, ws, ws_bytes);
   if (s != TC_OK) return s;
   tc::TopkArgs a{};
@@ -173,13 +209,15 @@ TC_API tc_status tc_workspace_bytes(const tc_codec* c, size_t* bytes) {
   uint64_t words = 0;
   const int dt = dt_ok(c->wire) ? c->wire : TC_F32;
   if (c->kind == TC_TOPK) {
-    // one layout serves the plain, EF and AQ-SGD senders of this shape
-    words = tc::plan_topk(tc::SEL_EF, dt, c->n_seg, c->seg_len).ws_words;
+    // one layout serves the plain, EF and AQ-SGD senders of this shape; a
+    // segment too long for it takes the global chain
+    const tc::SegPlan p = tc::plan_topk(tc::SEL_EF, dt, c->n_seg, c->seg_len);
+    words = (p.n_groups == 0 || p.P > p.capacity) ? tc::global_ws_words(c->seg_len) : p.ws_words;
   } else if (c->kind == TC_QUANT) {
     words = std::max(tc::plan_quant(dt, c->bits, true, c->n_seg, c->seg_len).ws_words,
                      tc::plan_quant(dt, c->bits, false, c->n_seg, c->seg_len).ws_words);
   } else {
-    return fail(TC_ERR_ARG, "TC_TOPK_QUANT is not supported by this build");
+    words = tc::global_ws_words(c->seg_len);
   }
   *bytes = (size_t)words * 4u;
   return TC_OK;
@@ -208,7 +246,9 @@ TC_API tc_status tc_device_errors(uint32_t* bits, int clear) {
   if ((e = tc::errors_topk(&a, clear != 0)) != hipSuccess) return hip_fail(e, "error word (topk)");
   if ((e = tc::errors_quant(&b, clear != 0)) != hipSuccess) return hip_fail(e, "error word (quant)");
   if ((e = tc::errors_scatter(&d, clear != 0)) != hipSuccess) return hip_fail(e, "error word (scatter)");
-  *bits = a | b | d;
+  uint32_t g = 0;
+  if ((e = tc::errors_global(&g, clear != 0)) != hipSuccess) return hip_fail(e, "error word (global)");
+  *bits = a | b | d | g;
   return TC_OK;
 }
 
@@ -286,7 +326,16 @@ TC_API tc_status tc_ef_step(const tc_codec* c, const void* x, int dt, float* e, 
   if (s != TC_OK) return s;
   if (c->kind == TC_TOPK) return topk_common(tc::SEL_EF, c, x, dt, e, nullptr, 0, nullptr, out, ws, ws_bytes, stream);
   if (c->kind == TC_QUANT) return quant_common(true, c, x, dt, e, out, ws, ws_bytes, stream);
-  return fail(TC_ERR_ARG, "TC_TOPK_QUANT is not supported by this build");
+  // TopK, then the kept list quantized as one min-max group per segment
+  if (!dt_ok(dt)) return fail(TC_ERR_DTYPE, "dtype %d", dt);
+  if (c->wire != dt) return fail(TC_ERR_DTYPE, "wire (receiver) dtype %d must equal the input dtype %d", c->wire, dt);
+  if (!out) return fail(TC_ERR_NULL, "payload is NULL");
+  if (c->n_seg * c->seg_len == 0) return TC_OK;
+  if (!x || !e) return fail(TC_ERR_NULL, "input or error buffer is NULL");
+  if (c->k > 0 && (!out->idx || !out->codes || !out->meta)) return fail(TC_ERR_NULL, "payload idx/codes/meta is NULL");
+  if (!out->meta) return fail(TC_ERR_NULL, "payload meta is NULL");
+  if (((uintptr_t)out->codes & 3u) != 0) return fail(TC_ERR_ALIGN, "codes must be 4-byte aligned");
+  return global_topk(c->bits, c, x, dt, e, out, ws, ws_bytes, stream);
 }
 
 TC_API tc_status tc_aqsgd_step(const tc_codec* c, const void* a, int dt, void* m, uint64_t n_samples,

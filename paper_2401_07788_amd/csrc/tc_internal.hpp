@@ -88,10 +88,31 @@ struct ScatterArgs {
 hipError_t launch_topk_decompress(int wire, int out_dt, const ScatterArgs& a, hipStream_t st);
 hipError_t launch_aqsgd_recv(int dt, const ScatterArgs& a, hipStream_t st);
 
+// ------------------------------------------------ segments too long to hold
+// TopK over one segment with a chain of kernels (histogram passes, picks,
+// an ordered emit with decoupled look-back, the kept-list quantizer)
+struct GlobalArgs {
+  const void* x;         // [L] input
+  float* e;              // [L] residual (in-out) or nullptr
+  uint32_t* idx;         // [k]
+  void* val;             // [k] wire values (plain TopK) or nullptr
+  uint32_t* codes;       // quantized kept list: [wpg] words
+  float* meta;           // quantized kept list: [2]
+  uint32_t* blk;         // optional [n_blocks(L) + 1]
+  uint64_t L, k, wpg, n_tiles;
+  uint32_t* state;       // workspace pieces (global_ws_carve)
+  uint32_t* hist;
+  uint32_t* tiles;
+};
+uint64_t global_ws_words(uint64_t L);
+void global_ws_carve(uint32_t* ws, uint64_t L, GlobalArgs& a);
+hipError_t launch_global(int dt, bool ef, uint32_t qbits, const GlobalArgs& a, hipStream_t st);
+
 // sticky kernel error bits of each kernel translation unit
 hipError_t errors_topk(uint32_t* bits, bool clear);
 hipError_t errors_quant(uint32_t* bits, bool clear);
 hipError_t errors_scatter(uint32_t* bits, bool clear);
+hipError_t errors_global(uint32_t* bits, bool clear);
 
 // device properties (cached per device)
 int device_cus();

@@ -278,6 +278,51 @@ def ef_step_quant(x: torch.Tensor, e: torch.Tensor, bits: int, n_grp: int, ws=No
     return codes, meta
 
 
+class TopkQuantPayload(NamedTuple):
+    """a TopK message whose kept values travel as b-bit min-max codes (one
+    group per segment): indices, codes (uint8 [n_seg, group_bytes]), meta
+    (float32 [n_seg, 2] = lo, scale) and the block table (or None)"""
+    idx: torch.Tensor
+    codes: torch.Tensor
+    meta: torch.Tensor
+    blk: Optional[torch.Tensor]
+    bits: int
+
+
+def ef_step_topk_quant(x: torch.Tensor, e: torch.Tensor, k: int, bits: int, n_seg: int = 1, ws=None,
+                       blk: bool = True) -> TopkQuantPayload:
+    """X = x + e; send TopK(X) with the kept values quantized; e <- X - received
+    (the receiver rounds to x's dtype).  e (float32) is updated in place."""
+    _need_gpu(x, e)
+    if e.dtype != torch.float32 or e.numel() != x.numel():
+        raise ValueError("e must be float32 with x's element count")
+    L = x.numel() // n_seg
+    c = codec(TC_TOPK_QUANT, n_seg, L, k, bits=bits, wire=_dt(x))
+    dev = x.device
+    out = TopkQuantPayload(torch.empty((n_seg, k), dtype=torch.int32, device=dev),
+                           torch.empty((n_seg, quant_group_bytes(k, bits)), dtype=torch.uint8, device=dev),
+                           torch.empty((n_seg, 2), dtype=torch.float32, device=dev),
+                           torch.empty((n_seg, n_blocks(L) + 1), dtype=torch.int32, device=dev) if blk else None,
+                           bits)
+    p = Payload(_ptr(out.idx), None, _ptr(out.codes), _ptr(out.meta), _ptr(out.blk))
+    w, wn = _ws_args(c, dev, ws)
+    _check(lib().tc_ef_step(C.byref(c), _ptr(x), _dt(x), C.cast(e.data_ptr(), C.POINTER(C.c_float)), C.byref(p),
+                            w, wn, _stream(dev)), "tc_ef_step")
+    return out
+
+
+def topk_quant_decompress(pl: TopkQuantPayload, seg_len: int, out_dtype=torch.float32, use_blk: bool = True):
+    """dense [n_seg, seg_len]: lo + code * scale at the indices, +0 elsewhere"""
+    _need_gpu(pl.idx, pl.codes, pl.meta, pl.blk)
+    n_seg, k = pl.idx.shape
+    c = codec(TC_TOPK_QUANT, n_seg, seg_len, k, bits=pl.bits, wire=_DT[out_dtype])
+    y = torch.empty((n_seg, seg_len), dtype=out_dtype, device=pl.idx.device)
+    p = Payload(_ptr(pl.idx), None, _ptr(pl.codes), _ptr(pl.meta), _ptr(pl.blk) if use_blk else None)
+    _check(lib().tc_topk_decompress(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(pl.idx.device)),
+           "tc_topk_decompress")
+    return y
+
+
 # ------------------------------------------------------------------- AQ-SGD
 def aqsgd_step(a: torch.Tensor, m: torch.Tensor, ids: torch.Tensor, k: int, ws=None, out: TopkPayload = None,
                blk: bool = True):
