@@ -20,6 +20,13 @@ Reported: value = bytes of the boundary tensor (the activations, fp16) / step
 time; pct_hbm_peak = algorithmic bytes of both sides / step time / 8 TB/s;
 roofline for the dominant kernel (HIP events on the launch stream); the CPU
 oracle timed on a bounded sample of the same workload.
+
+--workload lm: the large language model boundary (Sec. 3.2 scale): eight
+bfloat16 micro-batches of 16 x 2048 x 4096 activations, each one segment of
+2^27 elements, TopK 10 % with error feedback and the kept list quantized to 4
+bits as one min-max group; the residual is carried from one micro-batch to
+the next.  One step = one micro-batch; compress(j+1) runs on one stream while
+decompress(j) runs on another, payloads double-buffered.
 """
 from __future__ import annotations
 
@@ -35,19 +42,23 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E, published
-SOURCES_HASHED = ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
-                  "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"]
+SOURCES_HASHED = {
+    "aqsgd": ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
+              "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
+    "lm": ["paper_2401_07788_amd/csrc/k_global.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
+           "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
+}
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(workload: str) -> str:
     h = hashlib.sha256()
-    for p in SOURCES_HASHED:
+    for p in SOURCES_HASHED[workload]:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def read_traffic(kernel: str):
+def read_traffic(kernel: str, workload: str):
     """HBM bytes per launch from a committed counter summary, if it was taken
     on the current kernel sources (else None)"""
     path = os.path.join(ROOT, "profiles", f"{kernel}_traffic.txt")
@@ -59,7 +70,7 @@ def read_traffic(kernel: str):
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("source_hash") != kernel_source_hash():
+    if vals.get("source_hash") != kernel_source_hash(workload):
         return None
     try:
         return float(vals["hbm_bytes_per_launch"])
@@ -85,17 +96,17 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run 5 device copies of 256 MiB (the reference for HBM byte counters)")
+    ap.add_argument("--workload", choices=["aqsgd", "lm"], default="aqsgd",
+                    help="aqsgd: the AQ-SGD boundary (default); lm: the large language model micro-batch stream")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the boundary compressors run per device and this build has no "
               f"multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     from paper_2401_07788_amd import tc
-    from paper_2401_07788_amd import workloads as W
 
     if not torch.cuda.is_available():
         print("bench.py needs the GPU", file=sys.stderr)
@@ -112,6 +123,24 @@ def main():
         print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n, "launches": 5}))
         return
     tc.lib()
+    out = run_lm(args, dev) if args.workload == "lm" else run_aqsgd(args, dev)
+    print(json.dumps(out), flush=True)
+
+
+def check_errors(where):
+    from paper_2401_07788_amd import tc
+    errs = tc.device_errors(clear=True)
+    if errs:
+        print(f"kernel error bits {errs:#x} {where}", file=sys.stderr)
+        sys.exit(1)
+
+
+def run_aqsgd(args, dev):
+    import numpy as np
+    import torch
+
+    from paper_2401_07788_amd import tc
+    from paper_2401_07788_amd import workloads as W
 
     n_samples, L, B = W.AQSGD["n_samples"], W.AQSGD["seg_len"], W.AQSGD["batch"]
     k = tc.topk_count(L, 3, 10)
@@ -146,11 +175,7 @@ def main():
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
 
-    def check(where):
-        errs = tc.device_errors(clear=True)
-        if errs:
-            print(f"kernel error bits {errs:#x} {where}", file=sys.stderr)
-            sys.exit(1)
+    check = check_errors
 
     def steps_on(stream, j0, n, ev=None):
         """sender then receiver for micro-batches j0 .. j0+n-1 on one stream"""
@@ -234,7 +259,7 @@ def main():
     dominant = "aqsgd_send" if send_ms >= recv_ms else "aqsgd_recv"
     dom_ms = max(send_ms, recv_ms)
     achieved = bytes_side / (dom_ms * 1e-3) / 1e9
-    traffic = read_traffic(dominant)
+    traffic = read_traffic(dominant, "aqsgd")
 
     # ---- CPU baseline: the oracle on a bounded sample of the same micro-batches
     cpu = None
@@ -291,7 +316,155 @@ def main():
         "cpu_baseline": cpu,
         "setup_s": round(setup_s, 1),
     }
-    print(json.dumps(out), flush=True)
+    return out
+
+
+def run_lm(args, dev):
+    """EF TopK 10 % with a 4-bit kept list over a stream of 2^27-element bf16
+    micro-batches; compress(j+1) overlaps decompress(j)"""
+    import numpy as np
+    import torch
+
+    from paper_2401_07788_amd import tc
+    from paper_2401_07788_amd import workloads as W
+
+    shape, L, n_mb = W.LM_STREAM["shape"], W.LM_STREAM["seg_len"], W.LM_STREAM["n_micro"]
+    k = tc.topk_count(L, 1, 10)
+    bits = 4
+    steps, warm = args.steps, args.warmup
+    n_ref = min(16, steps)
+
+    t_setup = time.perf_counter()
+    xs = [W.sparse_outlier_stream(shape, args.seed, j, device=dev).reshape(-1) for j in range(n_mb)]
+    e = torch.zeros(L, dtype=torch.float32, device=dev)
+    x_cpu0 = xs[0].cpu() if not args.no_cpu else None
+    c = tc.codec(tc.TC_TOPK_QUANT, 1, L, k, bits=bits, wire=tc.TC_BF16)
+    sA, sB = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
+    with torch.cuda.stream(sA):
+        ws = tc.workspace(c, dev)
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+
+    # payload and received tensor double-buffered: the sender of j+1 writes
+    # one pair while the receiver of j reads the other
+    gb = tc.quant_group_bytes(k, bits)
+    pays = [tc.empty_topk_quant_payload(1, L, k, bits, dev) for _ in range(2)]
+    ys = [torch.empty((1, L), dtype=torch.bfloat16, device=dev) for _ in range(2)]
+    sent = [torch.cuda.Event() for _ in range(2)]
+    freed = [torch.cuda.Event() for _ in range(2)]
+
+    def send(j, b):
+        tc.ef_step_topk_quant(xs[j % n_mb], e, k, bits, ws=ws, out=pays[b])
+
+    def stream_steps(j0, n):
+        for i in range(n):
+            j, b = j0 + i, (j0 + i) % 2
+            with torch.cuda.stream(sA):
+                sA.wait_event(freed[b])
+                send(j, b)
+                sent[b].record(sA)
+            with torch.cuda.stream(sB):
+                sB.wait_event(sent[b])
+                tc.topk_quant_decompress(pays[b], L, out=ys[b])
+                freed[b].record(sB)
+
+    # ---- serial reference pass with HIP events on each launch stream: the
+    # sender chain and the receiver kernel of each micro-batch
+    j = 0
+    stream_steps(j, warm); j += warm
+    torch.cuda.synchronize()
+    check_errors("during the warm-up")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n_ref)]
+    for i in range(n_ref):
+        with torch.cuda.stream(sA):
+            ev[i][0].record(sA)
+            send(j + i, 0)
+            ev[i][1].record(sA)
+        with torch.cuda.stream(sB):
+            sB.wait_event(ev[i][1])
+            ev[i][2].record(sB)
+            tc.topk_quant_decompress(pays[0], L, out=ys[0])
+            ev[i][3].record(sB)
+        sA.wait_stream(sB)
+    j += n_ref
+    torch.cuda.synchronize()
+    check_errors("in the reference pass")
+    send_ms = float(np.mean([a[0].elapsed_time(a[1]) for a in ev]))
+    recv_ms = float(np.mean([a[2].elapsed_time(a[3]) for a in ev]))
+
+    # ---- timed region: K micro-batches, compress(j+1) || decompress(j)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    stream_steps(j, steps); j += steps
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    check_errors("in the timed region")
+    ms_per_step = wall * 1e3 / steps
+
+    N = L
+    boundary_bytes = 2 * N
+    payload = 4 * k + gb + 8 + 4 * (tc.n_blocks(L) + 1)
+    send_bytes = 2 * N + 4 * N + 4 * N + payload      # read x, read e, write e, write payload
+    recv_bytes = payload + 2 * N                      # read payload, write y
+    b_alg = send_bytes + recv_bytes
+    value = boundary_bytes / (ms_per_step * 1e-3) / 1e9
+    achieved = send_bytes / (send_ms * 1e-3) / 1e9
+
+    cpu = None
+    if x_cpu0 is not None:
+        # the oracle on one micro-batch sliced to 2^24 elements (one eighth),
+        # TopK 10 % of the slice: its sort is the dominant cost, so the rate
+        # is a slight overestimate of the full-length one
+        import oracle
+        cores = cpu_cores()
+        n_s = 1 << 24
+        xr = x_cpu0[:n_s].contiguous().view(torch.int16).numpy().view(np.uint16)
+        k_s = tc.topk_count(n_s, 1, 10)
+        t1 = time.perf_counter()
+        done = 0
+        e_s = np.zeros((1, n_s), np.float32)
+        while done < 1 or (time.perf_counter() - t1 < args.cpu_seconds and done < 4):
+            oi, oc, om, e_s = oracle.ef_topk_quant(xr, "bf16", e_s, 1, n_s, k_s, bits)
+            oracle.topk_quant_decompress(oi, oc, om, 1, n_s, k_s, bits, "bf16")
+            done += 1
+        spent = time.perf_counter() - t1
+        cpu = {"value": round(2 * n_s * done / spent / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "sample": f"{done} x one eighth of a micro-batch (2^24 bf16, TopK 10 %, 4-bit kept list, EF), "
+                         f"sender + receiver, {spent:.1f} s on {platform.processor() or platform.machine()}; "
+                         f"one segment, so the oracle runs on one thread"}
+
+    return {
+        "metric": "boundary-tensor GB/s through compress+decompress+EF; % of HBM peak",
+        "value": round(value, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "large-LM micro-batch stream: 8 x [16, 2048, 4096] bf16 activations (N(0,1), 0.1 % "
+                        "outliers x50), global TopK 10 % + EF fp32, kept list 4-bit min-max (one group), "
+                        "compress(j+1) || decompress(j) on two streams",
+            "storage_dtype": "bf16",
+            "seg_len": L,
+            "k": k,
+            "bits": bits,
+        },
+        "pct_hbm_peak": round(100.0 * b_alg / (ms_per_step * 1e-3) / (HBM_PEAK_GBPS * 1e9), 3),
+        "effective_GBps": round(b_alg / (ms_per_step * 1e-3) / 1e9, 2),
+        "algorithmic_bytes_per_step": b_alg,
+        "kernels_ms": {"lm_send_chain": round(send_ms, 5), "lm_recv": round(recv_ms, 5)},
+        "roofline": {"bound": "hbm", "kernel": "lm_send_chain", "achieved": round(achieved, 2),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": read_traffic("lm_send_chain", "lm"), "algorithmic_bytes": send_bytes},
+        "cpu_baseline": cpu,
+        "setup_s": round(setup_s, 1),
+    }
 
 
 if __name__ == "__main__":

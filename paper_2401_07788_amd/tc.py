@@ -289,8 +289,18 @@ class TopkQuantPayload(NamedTuple):
     bits: int
 
 
+def empty_topk_quant_payload(n_seg: int, seg_len: int, k: int, bits: int, device,
+                             blk: bool = True) -> TopkQuantPayload:
+    return TopkQuantPayload(torch.empty((n_seg, k), dtype=torch.int32, device=device),
+                            torch.empty((n_seg, quant_group_bytes(k, bits)), dtype=torch.uint8, device=device),
+                            torch.empty((n_seg, 2), dtype=torch.float32, device=device),
+                            torch.empty((n_seg, n_blocks(seg_len) + 1), dtype=torch.int32, device=device)
+                            if blk else None,
+                            bits)
+
+
 def ef_step_topk_quant(x: torch.Tensor, e: torch.Tensor, k: int, bits: int, n_seg: int = 1, ws=None,
-                       blk: bool = True) -> TopkQuantPayload:
+                       out: TopkQuantPayload = None, blk: bool = True) -> TopkQuantPayload:
     """X = x + e; send TopK(X) with the kept values quantized; e <- X - received
     (the receiver rounds to x's dtype).  e (float32) is updated in place."""
     _need_gpu(x, e)
@@ -299,11 +309,10 @@ def ef_step_topk_quant(x: torch.Tensor, e: torch.Tensor, k: int, bits: int, n_se
     L = x.numel() // n_seg
     c = codec(TC_TOPK_QUANT, n_seg, L, k, bits=bits, wire=_dt(x))
     dev = x.device
-    out = TopkQuantPayload(torch.empty((n_seg, k), dtype=torch.int32, device=dev),
-                           torch.empty((n_seg, quant_group_bytes(k, bits)), dtype=torch.uint8, device=dev),
-                           torch.empty((n_seg, 2), dtype=torch.float32, device=dev),
-                           torch.empty((n_seg, n_blocks(L) + 1), dtype=torch.int32, device=dev) if blk else None,
-                           bits)
+    if out is None:
+        out = empty_topk_quant_payload(n_seg, L, k, bits, dev, blk)
+    elif out.bits != bits or out.idx.shape != (n_seg, k):
+        raise ValueError("payload shape or bits do not match")
     p = Payload(_ptr(out.idx), None, _ptr(out.codes), _ptr(out.meta), _ptr(out.blk))
     w, wn = _ws_args(c, dev, ws)
     _check(lib().tc_ef_step(C.byref(c), _ptr(x), _dt(x), C.cast(e.data_ptr(), C.POINTER(C.c_float)), C.byref(p),
@@ -311,12 +320,17 @@ def ef_step_topk_quant(x: torch.Tensor, e: torch.Tensor, k: int, bits: int, n_se
     return out
 
 
-def topk_quant_decompress(pl: TopkQuantPayload, seg_len: int, out_dtype=torch.float32, use_blk: bool = True):
+def topk_quant_decompress(pl: TopkQuantPayload, seg_len: int, out_dtype=torch.float32, use_blk: bool = True,
+                          out: torch.Tensor = None):
     """dense [n_seg, seg_len]: lo + code * scale at the indices, +0 elsewhere"""
-    _need_gpu(pl.idx, pl.codes, pl.meta, pl.blk)
+    _need_gpu(pl.idx, pl.codes, pl.meta, pl.blk, out)
     n_seg, k = pl.idx.shape
+    if out is not None:
+        if out.numel() != n_seg * seg_len:
+            raise ValueError("out has the wrong element count")
+        out_dtype = out.dtype
     c = codec(TC_TOPK_QUANT, n_seg, seg_len, k, bits=pl.bits, wire=_DT[out_dtype])
-    y = torch.empty((n_seg, seg_len), dtype=out_dtype, device=pl.idx.device)
+    y = out if out is not None else torch.empty((n_seg, seg_len), dtype=out_dtype, device=pl.idx.device)
     p = Payload(_ptr(pl.idx), None, _ptr(pl.codes), _ptr(pl.meta), _ptr(pl.blk) if use_blk else None)
     _check(lib().tc_topk_decompress(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(pl.idx.device)),
            "tc_topk_decompress")
