@@ -3,20 +3,36 @@
 // error feedback (Sec. 2.4) and, optionally, the kept list quantized as one
 // min-max group (Sec. 2.2).
 //
-// A chain of kernels on one stream; kernel boundaries are the global syncs:
-//   hist<1>, pick<1>   12-bit digit of all keys        -> bin b1
-//   hist<2>, pick<2>   next 12 bits of keys in b1       -> bin b2
-//   hist<3>, pick<3>   last 7 bits of keys in (b1, b2)  -> threshold T, ties r
-//   emit               one ordered pass over 4096-element tiles: counts,
-//                      decoupled look-back for the tile's payload offset,
-//                      compaction of idx (and values), the dense residual,
-//                      the block table, min / max of the kept values
-//   qpack (quantized kept list only)  codes of the kept list, meta, and the
-//                      residual at the kept entries (X read back from e,
-//                      where emit left it)
-//   clean              tile states and counters back to zero
-// The input is read four times (three histogram passes and the emit pass).
+// A chain of kernels on one stream; kernel boundaries are the global syncs,
+// and the last workgroup to finish a kernel takes the decision that kernel
+// feeds:
+//   sample   histogram of the top 12 key bits over about 512 evenly spaced
+//            4096-element tiles -> a band of digits that holds the k-th
+//            largest key with high probability
+//   band     one pass over all keys: count the keys above the band, write
+//            the values inside it to a candidate list (exact check that the
+//            band holds the k-th key)
+//   pass 1-3 the three radix digits (12/12/7 bits) -> threshold T and the tie
+//            quota r, over the candidate list when the band held the k-th
+//            key, else over the whole segment
+//   keptmm   (quantized kept list) min / max of the kept values from the
+//            candidate list and the band pass, so that emit can quantize
+//   emit     one ordered pass over tiles: counts, decoupled look-back for
+//            the tile's payload offset, payload staged in LDS and written
+//            coalesced, the dense residual, the block table
+//   qpack    (quantized kept list, only when keptmm could not fix min / max)
+//            codes, meta and the residual at the kept entries
+//   clean    tile words, candidate list and state back to zero
+// The input is read twice on the candidate path (band, emit), plus the
+// sample.
+//
+// Device-scope atomics on one address serialize at the memory side, so
+// every counter that all workgroups touch is spread over 8 slots 128 bytes
+// apart (workgroup w uses slot w % 8): kernel completion counts, the
+// candidate sub-lists and the band's sums.
 #include <algorithm>
+#include <cmath>
+#include <type_traits>
 
 #include "tc_internal.hpp"
 #include "tc_select.hpp"
@@ -27,20 +43,94 @@ constexpr int G_NT = 256;
 constexpr int G_VPT = 16;
 constexpr uint64_t G_TILE = (uint64_t)G_NT * G_VPT;   // == BLOCK_LEN
 static_assert(G_TILE == BLOCK_LEN, "one emit tile per block of the block table");
+constexpr uint32_t SAMPLE_TILES = 512;      // tiles in the sample (every stride-th tile; all if fewer)
+constexpr uint32_t SAMPLE_GRID = 256;
+constexpr uint32_t CAND_GRID = 256;         // workgroups that read the candidate list
+constexpr uint32_t NSLOT = 8;               // slots of a spread counter
+constexpr uint32_t SLOT_WORDS = 32;         // 128 bytes between slots
+constexpr uint32_t CBUF = (uint32_t)G_TILE; // band: candidates buffered in LDS
 
-// state words (workspace)
+// state words (workspace); every word is zero at rest
 enum : int {
   ST_B1 = 0, ST_NEED2, ST_B2, ST_NEED3, ST_T, ST_R,
-  ST_TICKET, ST_EXIT, ST_MIN, ST_MAX,     // emit bookkeeping; ST_MIN/MAX hold ordered keys
-  ST_WORDS = 64
+  ST_MIN, ST_MAX,       // emit: min (as ~order key) / max (order key) of the kept values
+  ST_BLO, ST_BHI,       // band of top digits
+  ST_ABOVE,             // keys above the band
+  ST_FAST,              // 1: the band held the k-th key, passes run on candidates
+  ST_NEED1,
+  ST_AMIN, ST_AMAX,     // values with key > T (as ST_MIN / ST_MAX)
+  ST_TPOS, ST_TNEG,     // candidates with key == T, by sign
+  ST_PRE,               // 1: lo / hi / scale known before emit
+  ST_LO, ST_HI, ST_SCALE,
+  ST_SPREAD = 64,       // spread counters: NSLOT slots + a top word, SLOT_WORDS apart
+  SP_WORDS = (NSLOT + 1) * SLOT_WORDS,
+  SP_DONE = ST_SPREAD,                  // kernel completion (top word: slots done)
+  SP_NCAND = SP_DONE + SP_WORDS,        // candidates per sub-list
+  SP_ABOVE = SP_NCAND + SP_WORDS,       // band: keys above the band
+  SP_AMIN = SP_ABOVE + SP_WORDS,        // band: values above the band
+  SP_AMAX = SP_AMIN + SP_WORDS,
+  ST_WORDS = 2048
 };
+static_assert(SP_AMAX + SP_WORDS <= ST_WORDS, "state words");
 
+__device__ __forceinline__ uint32_t* slot(uint32_t* st, int sp, uint32_t c) { return st + sp + SLOT_WORDS * c; }
+
+// order-preserving map of floats to unsigned (finite values map into
+// [0x007FFFFF, 0xFF800000]); the minimum is kept as the maximum of the
+// complement, so that 0 means "none" for both
 __device__ __forceinline__ uint32_t order_key(float f) {
   const uint32_t u = __float_as_uint(f);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 __device__ __forceinline__ float from_order_key(uint32_t o) {
   return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
+}
+__device__ __forceinline__ void push_minmax(uint32_t* st, int wmin, int wmax, float lo, float hi) {
+  if (lo <= hi) {
+    __hip_atomic_fetch_max(&st[wmin], ~order_key(lo), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_max(&st[wmax], order_key(hi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// true in every thread of the workgroup that finishes last; it sees every
+// device-scope update the other workgroups made before finishing.  Each
+// workgroup counts in slot (blockIdx % 8); the last of a slot counts in the
+// top word.
+__device__ __forceinline__ bool last_block(uint32_t* st) {
+  __shared__ uint32_t s_last;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t G = gridDim.x, c = blockIdx.x % NSLOT;
+    const uint32_t n_c = (G - 1 - c) / NSLOT + 1;   // workgroups of this slot
+    const uint32_t n_slots = min(G, NSLOT);
+    uint32_t* sc = slot(st, SP_DONE, c);
+    uint32_t* top = slot(st, SP_DONE, NSLOT);
+    bool last = false;
+    if (__hip_atomic_fetch_add(sc, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == n_c - 1) {
+      __hip_atomic_store(sc, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __builtin_amdgcn_s_waitcnt(0);
+      if (__hip_atomic_fetch_add(top, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == n_slots - 1) {
+        __hip_atomic_store(top, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        last = true;
+      }
+    }
+    s_last = last ? 1u : 0u;
+  }
+  __syncthreads();
+  return s_last != 0u;
+}
+
+// sum / min / max over the slots of a spread counter
+__device__ __forceinline__ uint64_t slot_sum(uint32_t* st, int sp) {
+  uint64_t t = 0;
+  for (uint32_t c = 0; c < NSLOT; ++c) t += ld_agent(slot(st, sp, c));
+  return t;
+}
+__device__ __forceinline__ uint32_t slot_max(uint32_t* st, int sp) {
+  uint32_t t = 0;
+  for (uint32_t c = 0; c < NSLOT; ++c) t = max(t, ld_agent(slot(st, sp, c)));
+  return t;
 }
 
 template <typename InT, bool EF>
@@ -59,19 +149,39 @@ __device__ __forceinline__ void load_tile_values(const GlobalArgs& a, uint64_t t
   }
 }
 
-// ------------------------------------------------------------- histograms
-template <typename InT, bool EF, int PASS>
-__global__ __launch_bounds__(G_NT) void k_g_hist(GlobalArgs a) {
-  constexpr int NB = (PASS == 3) ? LAST_BINS : HIST_BINS;
-  __shared__ uint32_t hist[NB];
-  for (int b = threadIdx.x; b < NB; b += G_NT) hist[b] = 0u;
+__device__ __forceinline__ void zero_lds_bins(uint32_t* h, int nb) {
+  for (int b = threadIdx.x; b < nb; b += G_NT) h[b] = 0u;
+}
+
+// LDS histogram -> the device histogram (non-zero bins only)
+__device__ __forceinline__ void merge_bins(const uint32_t* h, uint32_t* gh, int nb) {
+  for (int b = threadIdx.x; b < nb; b += G_NT)
+    if (h[b]) add_agent(&gh[b], h[b]);
+}
+
+// the last workgroup: copy a device histogram into LDS and zero it
+__device__ __forceinline__ void take_bins(uint32_t* h, uint32_t* gh, int nb) {
+  for (int b = threadIdx.x; b < nb; b += G_NT) {
+    h[b] = ld_agent(&gh[b]);
+    st_agent(&gh[b], 0u);
+  }
   __syncthreads();
-  const uint32_t* st = a.state;
-  const uint32_t b1 = (PASS >= 2) ? st[ST_B1] : 0u;
-  const uint32_t p24 = (PASS == 3) ? ((st[ST_B1] << 12) | st[ST_B2]) : 0u;
+}
+
+// ---------------------------------------------------------------- sample
+template <typename InT, bool EF>
+__global__ __launch_bounds__(G_NT) void k_g_sample(GlobalArgs a) {
+  __shared__ uint32_t hist[HIST_BINS];
+  __shared__ uint32_t scratch[G_NT / WAVE + 2];
+  __shared__ uint32_t found[2];
+  zero_lds_bins(hist, HIST_BINS);
+  __syncthreads();
+  uint32_t* st = a.state;
+  const uint64_t stride = a.sample_stride;
+  const uint64_t n_s = (a.n_tiles + stride - 1) / stride;
   uint32_t zc = 0;
-  for (uint64_t tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
-    const uint64_t t0 = tile * G_TILE + (uint64_t)threadIdx.x * G_VPT;
+  for (uint64_t q = blockIdx.x; q < n_s; q += gridDim.x) {
+    const uint64_t t0 = q * stride * G_TILE + (uint64_t)threadIdx.x * G_VPT;
     const int nv = (int)min((uint64_t)G_VPT, sat_sub(a.L, t0));
     float v[G_VPT];
     load_tile_values<InT, EF>(a, t0, nv, v);
@@ -79,307 +189,694 @@ __global__ __launch_bounds__(G_NT) void k_g_hist(GlobalArgs a) {
     for (int i = 0; i < G_VPT; ++i) {
       if (i < nv) {
         const uint32_t kk = mag_key(v[i]);
-        bool in;
-        uint32_t d;
-        if constexpr (PASS == 1) { in = true; d = kk >> 19; }
-        else if constexpr (PASS == 2) { in = (kk >> 19) == b1; d = (kk >> 7) & 0xFFFu; }
-        else { in = (kk >> 7) == p24; d = kk & 0x7Fu; }
-        if (in) {
-          if (kk == 0u) ++zc;
-          else atomicAdd(&hist[d], 1u);
-        }
+        if (kk == 0u) ++zc;
+        else atomicAdd(&hist[kk >> 19], 1u);
       }
     }
   }
   const uint32_t zs = wave_sum(zc);
   if (lane_id() == 0 && zs) atomicAdd(&hist[0], zs);
   __syncthreads();
-  uint32_t* gh = a.hist + (PASS - 1) * HIST_BINS;
-  for (int b = threadIdx.x; b < NB; b += G_NT)
-    if (hist[b]) add_agent(&gh[b], hist[b]);
+  uint32_t* gh = a.hist;   // histogram 0
+  merge_bins(hist, gh, HIST_BINS);
+  if (!last_block(st)) return;
+  take_bins(hist, gh, HIST_BINS);
+  uint32_t part = 0;
+  for (int b = threadIdx.x; b < HIST_BINS; b += G_NT) part += hist[b];
+  const uint32_t ns = block_sum<G_NT>(part, scratch);
+  // ranks of the sample that bracket the k-th key of the whole segment:
+  // the expected rank +- 4 binomial standard deviations (+16)
+  const double p = (double)a.k / (double)a.L;
+  const double ks = p * (double)ns;
+  const double d = 4.0 * sqrt(ks * (1.0 - p)) + 16.0;
+  const double lo_r = fmin(fmax(floor(ks - d), 1.0), (double)ns);
+  const double hi_r = fmin(fmax(ceil(ks + d), 1.0), (double)ns);
+  find_bin<G_NT, HIST_BINS>(hist, (uint32_t)lo_r, scratch, found);
+  const uint32_t bhi = found[0];
+  __syncthreads();
+  find_bin<G_NT, HIST_BINS>(hist, (uint32_t)hi_r, scratch, found);
+  if (threadIdx.x == 0) {
+    st[ST_BHI] = bhi;
+    st[ST_BLO] = found[0];
+  }
 }
 
-// one workgroup: find the bin of this pass, advance the state, clear the
-// histogram for the next call
-template <int PASS>
-__global__ __launch_bounds__(512) void k_g_pick(GlobalArgs a) {
-  constexpr int NB = (PASS == 3) ? LAST_BINS : HIST_BINS;
-  __shared__ uint32_t h[NB];
-  __shared__ uint32_t scratch[512 / WAVE + 2];
-  __shared__ uint32_t found[2];
-  uint32_t* gh = a.hist + (PASS - 1) * HIST_BINS;
-  for (int b = threadIdx.x; b < NB; b += 512) { h[b] = ld_agent(&gh[b]); st_agent(&gh[b], 0u); }
-  __syncthreads();
+// ------------------------------------------------------------------- band
+// candidate sub-list c holds a.cand_cap / a.n_sub values at a.cand + c * that
+__device__ __forceinline__ uint64_t sub_cap(const GlobalArgs& a) { return a.cand_cap / a.n_sub; }
+
+// Tile records (4 words per tile).  band writes [0] keys above the band,
+// [1] where the tile's candidates start in the candidate array, [2] how many;
+// tcount overwrites [0] keys > T, [1] keys == T, [2] / [3] the exclusive
+// prefix of those over the tiles of its workgroup.
+constexpr uint32_t TL_MAX = 64;   // band: tiles with buffered candidates before a flush
+
+template <typename InT, bool EF>
+__global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
+  __shared__ uint32_t s_cand[CBUF];
+  __shared__ uint32_t s_tl_tile[TL_MAX], s_tl_pos[TL_MAX];
+  __shared__ uint32_t scratch[G_NT / WAVE + 2];
+  __shared__ uint32_t s_base;
+  __shared__ float s_mm[2 * (G_NT / WAVE)];
   uint32_t* st = a.state;
-  const uint32_t need = (PASS == 1) ? (uint32_t)a.k : (PASS == 2) ? st[ST_NEED2] : st[ST_NEED3];
-  find_bin<512, NB>(h, need, scratch, found);
+  // the quantized kept list's emit ORs codes into the words it shares with
+  // neighbouring tiles: they start at zero
+  if (a.codes) {
+    const uint64_t gsz = (uint64_t)gridDim.x * G_NT;
+    for (uint64_t i = (uint64_t)blockIdx.x * G_NT + threadIdx.x; i < a.wpg; i += gsz) a.codes[i] = 0u;
+  }
+  const uint32_t blo = st[ST_BLO], bhi = st[ST_BHI];
+  const uint32_t c = blockIdx.x % a.n_sub;
+  const uint64_t capc = sub_cap(a);
+  uint32_t nbuf = 0, ntl = 0;   // workgroup-uniform
+  // buffered candidates -> the workgroup's sub-list (one reservation), and
+  // the buffered tiles' record word [1]
+  auto flush = [&]() {
+    __syncthreads();
+    if (threadIdx.x == 0)
+      s_base = __hip_atomic_fetch_add(slot(st, SP_NCAND, c), nbuf, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    const uint64_t base = s_base;
+    uint32_t* list = a.cand + c * capc;
+    for (uint32_t j = threadIdx.x; j < nbuf; j += G_NT)
+      if (base + j < capc) list[base + j] = s_cand[j];
+    for (uint32_t j = threadIdx.x; j < ntl; j += G_NT)
+      a.tiles[4 * (uint64_t)s_tl_tile[j] + 1] = (uint32_t)min(c * capc + base + s_tl_pos[j], a.cand_cap);
+    __syncthreads();
+    nbuf = 0;
+    ntl = 0;
+  };
+  float amin = __builtin_inff(), amax = -__builtin_inff();
+  uint32_t above_all = 0;   // workgroup-uniform
+  for (uint64_t tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
+    const uint64_t t0 = tile * G_TILE + (uint64_t)threadIdx.x * G_VPT;
+    const int nv = (int)min((uint64_t)G_VPT, sat_sub(a.L, t0));
+    float v[G_VPT];
+    load_tile_values<InT, EF>(a, t0, nv, v);
+    uint32_t inb = 0, above = 0;
+#pragma unroll
+    for (int i = 0; i < G_VPT; ++i) {
+      if (i < nv) {
+        const uint32_t dg = mag_key(v[i]) >> 19;
+        if (dg > bhi) { ++above; amin = fminf(amin, v[i]); amax = fmaxf(amax, v[i]); }
+        else if (dg >= blo) ++inb;
+      }
+    }
+    uint32_t tot;
+    uint32_t off = block_excl_scan<G_NT>(inb | (above << 16), scratch, tot) & 0xFFFFu;
+    const uint32_t n_t = tot & 0xFFFFu, ab_t = tot >> 16;
+    above_all += ab_t;
+    if (n_t && (nbuf + n_t > CBUF || ntl == TL_MAX)) flush();
+    if (threadIdx.x == 0) {
+      a.tiles[4 * tile + 0] = ab_t;
+      a.tiles[4 * tile + 1] = 0u;
+      a.tiles[4 * tile + 2] = n_t;
+      if (n_t) { s_tl_tile[ntl] = (uint32_t)tile; s_tl_pos[ntl] = nbuf; }
+    }
+    if (n_t) {
+      off += nbuf;
+#pragma unroll
+      for (int i = 0; i < G_VPT; ++i) {
+        if (i < nv) {
+          const uint32_t dg = mag_key(v[i]) >> 19;
+          if (dg <= bhi && dg >= blo) s_cand[off++] = __float_as_uint(v[i]);
+        }
+      }
+      nbuf += n_t;
+      ++ntl;
+    }
+  }
+  if (nbuf) flush();
+  block_minmax<G_NT>(amin, amax, s_mm);
+  const uint32_t cs = blockIdx.x % NSLOT;
+  if (threadIdx.x == 0) {
+    if (above_all) add_agent(slot(st, SP_ABOVE, cs), above_all);
+    if (amin <= amax) {
+      __hip_atomic_fetch_max(slot(st, SP_AMIN, cs), ~order_key(amin), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_max(slot(st, SP_AMAX, cs), order_key(amax), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  if (!last_block(st)) return;
+  if (threadIdx.x != 0) return;
+  const uint64_t ab = slot_sum(st, SP_ABOVE);
+  uint64_t nc = 0;
+  bool fits = true;
+  for (uint32_t q = 0; q < a.n_sub; ++q) {
+    const uint32_t n = ld_agent(slot(st, SP_NCAND, q));
+    nc += n;
+    fits = fits && n <= capc;
+  }
+  const bool fast = fits && ab < a.k && a.k <= ab + nc;
+  st[ST_ABOVE] = (uint32_t)ab;
+  st[ST_FAST] = fast ? 1u : 0u;
+  st[ST_NEED1] = fast ? (uint32_t)(a.k - ab) : (uint32_t)a.k;
+  // values above the band, for the kept list's min / max
+  st[ST_AMIN] = slot_max(st, SP_AMIN);
+  st[ST_AMAX] = slot_max(st, SP_AMAX);
+}
+
+// f(value bits) over every candidate, on the first CAND_GRID workgroups
+template <typename F>
+__device__ __forceinline__ void for_candidates(const GlobalArgs& a, F&& f) {
+  const uint32_t G = min(gridDim.x, CAND_GRID);
+  if (blockIdx.x >= G) return;
+  const uint64_t capc = sub_cap(a);
+  for (uint32_t c = 0; c < a.n_sub; ++c) {
+    const uint64_t n = min((uint64_t)a.state[SP_NCAND + SLOT_WORDS * c], capc);
+    const uint32_t* list = a.cand + c * capc;
+    for (uint64_t j = (uint64_t)blockIdx.x * G_NT + threadIdx.x; j < n; j += (uint64_t)G * G_NT) f(list[j]);
+  }
+}
+
+// ------------------------------------------------------------- passes 1-3
+template <typename InT, bool EF, int PASS>
+__global__ __launch_bounds__(G_NT) void k_g_pass(GlobalArgs a) {
+  constexpr int NB = (PASS == 3) ? LAST_BINS : HIST_BINS;
+  __shared__ uint32_t hist[NB];
+  __shared__ uint32_t scratch[G_NT / WAVE + 2];
+  __shared__ uint32_t found[2];
+  uint32_t* st = a.state;
+  const bool fast = st[ST_FAST] != 0u;
+  zero_lds_bins(hist, NB);
+  __syncthreads();
+  const uint32_t b1 = (PASS >= 2) ? st[ST_B1] : 0u;
+  const uint32_t p24 = (PASS == 3) ? ((st[ST_B1] << 12) | st[ST_B2]) : 0u;
+  uint32_t zc = 0;
+  auto count = [&](uint32_t kk) {
+    bool in;
+    uint32_t d;
+    if constexpr (PASS == 1) { in = true; d = kk >> 19; }
+    else if constexpr (PASS == 2) { in = (kk >> 19) == b1; d = (kk >> 7) & 0xFFFu; }
+    else { in = (kk >> 7) == p24; d = kk & 0x7Fu; }
+    if (in) {
+      if (kk == 0u) ++zc;
+      else atomicAdd(&hist[d], 1u);
+    }
+  };
+  if (fast) {
+    for_candidates(a, [&](uint32_t bits) { count(bits & 0x7FFFFFFFu); });
+  } else {
+    for (uint64_t tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
+      const uint64_t t0 = tile * G_TILE + (uint64_t)threadIdx.x * G_VPT;
+      const int nv = (int)min((uint64_t)G_VPT, sat_sub(a.L, t0));
+      float v[G_VPT];
+      load_tile_values<InT, EF>(a, t0, nv, v);
+#pragma unroll
+      for (int i = 0; i < G_VPT; ++i)
+        if (i < nv) count(mag_key(v[i]));
+    }
+  }
+  const uint32_t zs = wave_sum(zc);
+  if (lane_id() == 0 && zs) atomicAdd(&hist[0], zs);
+  __syncthreads();
+  uint32_t* gh = a.hist + (uint64_t)PASS * HIST_BINS;   // histograms 1..3
+  merge_bins(hist, gh, NB);
+  if (!last_block(st)) return;
+  take_bins(hist, gh, NB);
+  const uint32_t need = (PASS == 1) ? st[ST_NEED1] : (PASS == 2) ? st[ST_NEED2] : st[ST_NEED3];
+  find_bin<G_NT, NB>(hist, need, scratch, found);
   if (threadIdx.x == 0) {
     if constexpr (PASS == 1) { st[ST_B1] = found[0]; st[ST_NEED2] = need - found[1]; }
     else if constexpr (PASS == 2) { st[ST_B2] = found[0]; st[ST_NEED3] = need - found[1]; }
     else {
-      st[ST_T] = (((st[ST_B1] << 12) | st[ST_B2]) << 7) | found[0];
+      st[ST_T] = (p24 << 7) | found[0];
       st[ST_R] = need - found[1];
     }
   }
 }
 
-// ------------------------------------------------------------------- emit
-// Tile state word: bit 63..62 flag (1 = own counts, 2 = inclusive prefix),
-// bits 61..31 keys > T, bits 30..0 keys == T.
-constexpr uint64_t TF_AGG = 1ull << 62, TF_INC = 2ull << 62, TF_MASK = 3ull << 62;
-__device__ __forceinline__ uint64_t tile_word(uint64_t flag, uint32_t gt, uint32_t eq) {
-  return flag | ((uint64_t)gt << 31) | (uint64_t)eq;
+// ------------------------------------------------------------------ keptmm
+// min / max of the kept values, from the candidate list (keys == T are the
+// ties; keys > T in the list are kept) and the values above the band.  The r
+// kept ties are the lowest-indexed ones; the list does not keep indices, so
+// when ties of both signs exist and only some are kept, the tie values can
+// decide lo or hi only if no kept value lies beyond +-|T| on that side; then
+// the quantization is left to qpack.
+__global__ __launch_bounds__(G_NT) void k_g_keptmm(GlobalArgs a) {
+  __shared__ uint32_t scratch[G_NT / WAVE + 2];
+  __shared__ float s_mm[2 * (G_NT / WAVE)];
+  uint32_t* st = a.state;
+  if (st[ST_FAST] == 0u) return;
+  const uint32_t T = st[ST_T];
+  float mn = __builtin_inff(), mx = -__builtin_inff();
+  uint32_t tp = 0, tn = 0;
+  for_candidates(a, [&](uint32_t bits) {
+    const uint32_t kk = bits & 0x7FFFFFFFu;
+    if (kk > T) { const float v = __uint_as_float(bits); mn = fminf(mn, v); mx = fmaxf(mx, v); }
+    else if (kk == T) { if (bits >> 31) ++tn; else ++tp; }
+  });
+  block_minmax<G_NT>(mn, mx, s_mm);
+  const uint32_t tps = block_sum<G_NT>(tp, scratch);
+  const uint32_t tns = block_sum<G_NT>(tn, scratch);
+  if (threadIdx.x == 0) {
+    push_minmax(st, ST_AMIN, ST_AMAX, mn, mx);
+    if (tps) add_agent(&st[ST_TPOS], tps);
+    if (tns) add_agent(&st[ST_TNEG], tns);
+  }
+  if (!last_block(st)) return;
+  if (threadIdx.x != 0) return;
+  const uint32_t wmin = ld_agent(&st[ST_AMIN]), wmax = ld_agent(&st[ST_AMAX]);
+  float lo = wmax ? from_order_key(~wmin) : __builtin_inff();
+  float hi = wmax ? from_order_key(wmax) : -__builtin_inff();
+  const uint32_t r = st[ST_R];
+  const uint32_t np = ld_agent(&st[ST_TPOS]), nn = ld_agent(&st[ST_TNEG]);
+  const float tf = __uint_as_float(T);
+  bool pos_in = false, neg_in = false, ok = true;
+  if (r == 0u) {
+  } else if (r >= np + nn || T == 0u) {
+    // every tie kept, or the ties are zeros (whose sign lo / hi lose anyway)
+    pos_in = np > 0;
+    neg_in = nn > 0;
+  } else if (np > 0 && nn > 0) {
+    // which sign the kept ties have is unknown here: harmless only if kept
+    // values lie beyond both +|T| and -|T|
+    ok = hi >= tf && lo <= -tf;
+  } else {
+    pos_in = np > 0;
+    neg_in = nn > 0;
+  }
+  if (!ok) return;   // ST_PRE stays 0: qpack quantizes
+  if (pos_in) { lo = fminf(lo, tf); hi = fmaxf(hi, tf); }
+  if (neg_in) { lo = fminf(lo, -tf); hi = fmaxf(hi, -tf); }
+  lo = lo + 0.0f;
+  hi = hi + 0.0f;
+  const uint32_t LV = (1u << a.bits) - 1u;
+  const float scale = (hi != lo) ? (hi - lo) / (float)LV : 0.0f;
+  st[ST_LO] = __float_as_uint(lo);
+  st[ST_HI] = __float_as_uint(hi);
+  st[ST_SCALE] = __float_as_uint(scale);
+  st[ST_PRE] = 1u;
+  a.meta[0] = lo;
+  a.meta[1] = scale;
 }
-constexpr uint32_t LOOKBACK_SPIN_LIMIT = 1u << 22;
 
-template <typename InT, bool EF, bool QKEPT>
+// ------------------------------------------------------------------ tcount
+// Keys > T and == T per tile (from the candidate list and the band's counts
+// on the fast path, else from the data), their exclusive prefix over each
+// workgroup's contiguous range of tiles, and -- in the last workgroup -- the
+// exclusive prefix of the workgroup totals.  emit then knows every tile's
+// payload offset without waiting on other tiles.
+constexpr uint32_t TC_GRID = 1024;   // tcount workgroups at most
+constexpr uint32_t TPW_MAX = 512;    // tiles per tcount workgroup (segments < 2^31)
+static_assert((uint64_t)TC_GRID * TPW_MAX * G_TILE >= (1ull << 31), "tile ranges cover 2^31 elements");
+static_assert(TPW_MAX == 2 * G_NT, "two tiles per thread in the workgroup scan");
+
+template <typename InT, bool EF>
+__global__ __launch_bounds__(G_NT) void k_g_tcount(GlobalArgs a) {
+  __shared__ uint32_t s_gt[TPW_MAX], s_eq[TPW_MAX];
+  __shared__ uint32_t scratch[G_NT / WAVE + 2];
+  uint32_t* st = a.state;
+  const bool fast = st[ST_FAST] != 0u;
+  const uint32_t T = st[ST_T];
+  const uint64_t t_lo = (uint64_t)blockIdx.x * a.tpw;
+  const uint32_t nt = (uint32_t)min((uint64_t)a.tpw, sat_sub(a.n_tiles, t_lo));
+  if (fast) {
+    // one wavefront per tile
+    const uint32_t w = threadIdx.x / WAVE, lane = (uint32_t)lane_id();
+    for (uint32_t i = w; i < nt; i += G_NT / WAVE) {
+      const uint32_t* rec = a.tiles + 4 * (t_lo + i);
+      const uint32_t ab = rec[0], off = rec[1], n = rec[2];
+      uint32_t gt = 0, eq = 0;
+      if ((uint64_t)off + n <= a.cand_cap) {
+        for (uint32_t j = lane; j < n; j += WAVE) {
+          const uint32_t kk = a.cand[off + j] & 0x7FFFFFFFu;
+          gt += kk > T;
+          eq += kk == T;
+        }
+      } else if (lane == 0) {
+        raise_error(KERR_INTERNAL);
+      }
+      gt = wave_sum(gt);
+      eq = wave_sum(eq);
+      if (lane == 0) { s_gt[i] = ab + gt; s_eq[i] = eq; }
+    }
+  } else {
+    for (uint32_t i = 0; i < nt; ++i) {
+      const uint64_t t0 = (t_lo + i) * G_TILE + (uint64_t)threadIdx.x * G_VPT;
+      const int nv = (int)min((uint64_t)G_VPT, sat_sub(a.L, t0));
+      float v[G_VPT];
+      load_tile_values<InT, EF>(a, t0, nv, v);
+      uint32_t gt = 0, eq = 0;
+#pragma unroll
+      for (int q = 0; q < G_VPT; ++q) {
+        if (q < nv) {
+          const uint32_t kk = mag_key(v[q]);
+          gt += kk > T;
+          eq += kk == T;
+        }
+      }
+      const uint32_t tot = block_sum<G_NT>(gt | (eq << 16), scratch);
+      if (threadIdx.x == 0) { s_gt[i] = tot & 0xFFFFu; s_eq[i] = tot >> 16; }
+    }
+  }
+  __syncthreads();
+  // exclusive prefix over the workgroup's tiles, two per thread
+  const uint32_t i0 = 2 * threadIdx.x, i1 = i0 + 1;
+  const uint32_t g0 = (i0 < nt) ? s_gt[i0] : 0u, g1 = (i1 < nt) ? s_gt[i1] : 0u;
+  const uint32_t e0 = (i0 < nt) ? s_eq[i0] : 0u, e1 = (i1 < nt) ? s_eq[i1] : 0u;
+  uint32_t gtot, etot;
+  const uint32_t gx = block_excl_scan<G_NT>(g0 + g1, scratch, gtot);
+  const uint32_t ex = block_excl_scan<G_NT>(e0 + e1, scratch, etot);
+  if (i0 < nt) {
+    uint32_t* rec = a.tiles + 4 * (t_lo + i0);
+    rec[0] = g0; rec[1] = e0; rec[2] = gx; rec[3] = ex;
+  }
+  if (i1 < nt) {
+    uint32_t* rec = a.tiles + 4 * (t_lo + i1);
+    rec[0] = g1; rec[1] = e1; rec[2] = gx + g0; rec[3] = ex + e0;
+  }
+  if (threadIdx.x == 0) {
+    st_agent(&a.wgs[2 * blockIdx.x], gtot);
+    st_agent(&a.wgs[2 * blockIdx.x + 1], etot);
+  }
+  if (!last_block(st)) return;
+  // exclusive prefix of the workgroup totals, four per thread
+  constexpr int PER = (int)(TC_GRID / G_NT);
+  uint32_t gw[PER], ew[PER], gs = 0, es = 0;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const uint32_t wi = threadIdx.x * PER + q;
+    gw[q] = (wi < gridDim.x) ? ld_agent(&a.wgs[2 * wi]) : 0u;
+    ew[q] = (wi < gridDim.x) ? ld_agent(&a.wgs[2 * wi + 1]) : 0u;
+    gs += gw[q];
+    es += ew[q];
+  }
+  uint32_t dummy;
+  uint32_t gp = block_excl_scan<G_NT>(gs, scratch, dummy);
+  uint32_t ep = block_excl_scan<G_NT>(es, scratch, dummy);
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const uint32_t wi = threadIdx.x * PER + q;
+    if (wi < gridDim.x) {
+      a.wgs[2 * wi] = gp;
+      a.wgs[2 * wi + 1] = ep;
+    }
+    gp += gw[q];
+    ep += ew[q];
+  }
+}
+
+// ------------------------------------------------------------------- emit
+template <uint32_t B>
+__device__ __forceinline__ uint32_t quant_code(float x, float lo, float range) {
+  constexpr uint32_t LV = (1u << B) - 1u;
+  if (!(range > 0.0f)) return 0u;
+  const float u = (x - lo) / range;
+  const float t = u * (float)LV;
+  return min((uint32_t)rintf(t), LV);
+}
+
+// codes of entries [f, f + n) of the payload (c[j - f], B bits each), into
+// the words they cover; a word not wholly inside the range is OR-ed in (the
+// words start at zero), the rest are stored
+template <uint32_t B, typename CT>
+__device__ __forceinline__ void write_codes(uint32_t* codes, uint64_t wpg, uint64_t f, uint32_t n, const CT* c,
+                                            bool shared_edges) {
+  if (n == 0) return;
+  const uint64_t b0 = f * B, b1 = (f + n) * B;   // bit range
+  const uint64_t w0 = b0 / 32, w1 = (b1 - 1) / 32;
+  for (uint64_t w = w0 + threadIdx.x; w <= w1; w += G_NT) {
+    const uint64_t wb = w * 32;
+    const uint64_t j0 = max(wb / B, f), j1 = min((wb + 31) / B, f + n - 1);
+    uint32_t word = 0;
+    for (uint64_t j = j0; j <= j1; ++j) {
+      const int64_t o = (int64_t)(j * B) - (int64_t)wb;
+      const uint32_t code = (uint32_t)c[j - f];
+      word |= (o >= 0) ? (code << (uint32_t)o) : (code >> (uint32_t)(-o));
+    }
+    if (w >= wpg) { raise_error(KERR_INTERNAL); continue; }
+    const bool inside = wb >= b0 && wb + 32 <= b1;
+    if (inside || !shared_edges) codes[w] = word;
+    else if (word) __hip_atomic_fetch_or(&codes[w], word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Q = 0: TopK values in the input dtype; Q = b: the kept list quantized
+template <typename InT, bool EF, uint32_t Q>
 __global__ __launch_bounds__(G_NT) void k_g_emit(GlobalArgs a) {
   using R = typename Elem<InT>::raw;
-  __shared__ uint32_t s_tile;
+  constexpr bool QK = Q != 0;
+  // staged payload of one tile: offsets in the tile, and the wire value, the
+  // b-bit code, or the binary32 bits (b = 32); small, so that many tiles are
+  // in flight per compute unit
+  using SV = std::conditional_t<Q == 0, R, std::conditional_t<Q == 32, uint32_t, uint8_t>>;
+  __shared__ uint16_t s_off[G_TILE];
+  __shared__ SV s_val[G_TILE];
   __shared__ uint32_t scratch[G_NT / WAVE + 2];
-  __shared__ uint32_t s_prefix[2];
   __shared__ float s_mm[2 * (G_NT / WAVE)];
-  uint64_t* tiles = reinterpret_cast<uint64_t*>(a.tiles);
   uint32_t* st = a.state;
   const uint32_t T = (a.k == 0) ? 0xFFFFFFFFu : st[ST_T];
   const uint32_t r = (a.k == 0) ? 0u : st[ST_R];
+  // quantize here when lo / hi are known (always for b = 32)
+  const bool pre = QK && (Q == 32 || st[ST_PRE] != 0u);
+  float lo = 0.0f, range = 0.0f, scale = 0.0f;
+  if (QK && Q != 32 && pre) {
+    lo = __uint_as_float(st[ST_LO]);
+    range = __uint_as_float(st[ST_HI]) - lo;
+    scale = __uint_as_float(st[ST_SCALE]);
+  }
   float kmin = __builtin_inff(), kmax = -__builtin_inff();
-  for (;;) {
-    if (threadIdx.x == 0) s_tile = __hip_atomic_fetch_add(&st[ST_TICKET], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __syncthreads();
-    const uint64_t tile = s_tile;
-    __syncthreads();
-    if (tile >= a.n_tiles) break;
+  for (uint64_t tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
+    // the tile's offset (from tcount), loaded together with its data
+    uint32_t gt_before = 0, eq_before = 0, rec_gt = 0, rec_eq = 0;
+    if (a.k > 0) {
+      // 8-byte loads: the workspace is 8-byte aligned
+      const u32x2 cnt2 = *reinterpret_cast<const u32x2*>(a.tiles + 4 * tile);
+      const u32x2 pre2 = *reinterpret_cast<const u32x2*>(a.tiles + 4 * tile + 2);
+      const u32x2 wg2 = *reinterpret_cast<const u32x2*>(a.wgs + 2 * (tile / a.tpw));
+      rec_gt = cnt2.x;
+      rec_eq = cnt2.y;
+      gt_before = wg2.x + pre2.x;
+      eq_before = wg2.y + pre2.y;
+    }
     const uint64_t t0 = tile * G_TILE + (uint64_t)threadIdx.x * G_VPT;
     const int nv = (int)min((uint64_t)G_VPT, sat_sub(a.L, t0));
     float v[G_VPT];
     load_tile_values<InT, EF>(a, t0, nv, v);
-    uint32_t key[G_VPT];
-#pragma unroll
-    for (int i = 0; i < G_VPT; ++i) key[i] = mag_key(v[i]);
     uint32_t gt = 0, eq = 0;
 #pragma unroll
-    for (int i = 0; i < G_VPT; ++i)
-      if (i < nv) { gt += key[i] > T; eq += key[i] == T; }
+    for (int i = 0; i < G_VPT; ++i) {
+      if (i < nv) {
+        const uint32_t kk = mag_key(v[i]);
+        gt += kk > T;
+        eq += kk == T;
+      }
+    }
     uint32_t tot;
     const uint32_t ex = block_excl_scan<G_NT>(gt | (eq << 16), scratch, tot);
     const uint32_t gt_t = tot & 0xFFFFu, eq_t = tot >> 16;
-    // ---- the tile's offset: publish own counts, look back over predecessors
-    if (threadIdx.x == 0) {
-      uint32_t pg = 0, pe = 0;
-      if (tile == 0) {
-        __hip_atomic_store(&tiles[0], tile_word(TF_INC, gt_t, eq_t), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      } else {
-        __hip_atomic_store(&tiles[tile], tile_word(TF_AGG, gt_t, eq_t), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        uint64_t j = tile - 1;
-        uint32_t spins = 0;
-        for (;;) {
-          const uint64_t w = __hip_atomic_load(&tiles[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          const uint64_t f = w & TF_MASK;
-          if (f == 0) {
-            __builtin_amdgcn_s_sleep(1);
-            if (++spins > LOOKBACK_SPIN_LIMIT) { raise_error(KERR_TIMEOUT); break; }
-            continue;
-          }
-          pg += (uint32_t)((w >> 31) & 0x7FFFFFFFu);
-          pe += (uint32_t)(w & 0x7FFFFFFFu);
-          if (f == TF_INC || j == 0) break;
-          --j;
-        }
-        __builtin_amdgcn_s_waitcnt(0);
-        __hip_atomic_store(&tiles[tile], tile_word(TF_INC, pg + gt_t, pe + eq_t), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-      }
-      s_prefix[0] = pg;
-      s_prefix[1] = pe;
-    }
-    __syncthreads();
-    const uint32_t gt_before = s_prefix[0], eq_before = s_prefix[1];
+    if (a.k > 0 && threadIdx.x == 0 && (rec_gt != gt_t || rec_eq != eq_t)) raise_error(KERR_INTERNAL);
     // ---- placement inside the tile (ties: the lowest indices overall)
     const uint32_t quota_t = min(sat_sub(r, eq_before), eq_t);
     const uint32_t gt_ex = ex & 0xFFFFu, eq_ex = ex >> 16;
     const uint32_t tile_first = gt_before + min(eq_before, r);
-    uint32_t pos = tile_first + gt_ex + min(eq_ex, quota_t);
+    const uint32_t cnt = gt_t + quota_t;
+    uint32_t lp = gt_ex + min(eq_ex, quota_t);   // position in the tile's part of the payload
     const uint32_t tie_keep = min(sat_sub(quota_t, eq_ex), (uint32_t)G_VPT);
     uint32_t ties = 0;
-    float eo[G_VPT];
 #pragma unroll
     for (int i = 0; i < G_VPT; ++i) {
       bool kept = false;
       if (i < nv) {
-        const bool tie = key[i] == T;
-        kept = key[i] > T || (tie && ties < tie_keep);
+        const uint32_t kk = mag_key(v[i]);
+        const bool tie = kk == T;
+        kept = kk > T || (tie && ties < tie_keep);
         ties += tie ? 1u : 0u;
-        if (kept) {
-          if (pos < a.k) {
-            a.idx[pos] = (uint32_t)(t0 + i);
-            if constexpr (!QKEPT) ((R*)a.val)[pos] = Elem<InT>::down(v[i]);
+      }
+      float rec = 0.0f;   // what the receiver holds here (binary32 before its rounding)
+      if (kept) {
+        if (lp < G_TILE) {
+          s_off[lp] = (uint16_t)(threadIdx.x * G_VPT + i);
+          if constexpr (!QK) {
+            s_val[lp] = Elem<InT>::down(v[i]);
+            rec = v[i];
+          } else if constexpr (Q == 32) {
+            s_val[lp] = __float_as_uint(v[i]);
+            rec = v[i];
           } else {
-            raise_error(KERR_INTERNAL);
+            if (pre) {
+              const uint32_t c = quant_code<Q>(v[i], lo, range);
+              s_val[lp] = (uint8_t)c;
+              const float prod = (float)c * scale;
+              rec = lo + prod;
+            }
           }
-          ++pos;
-          if constexpr (QKEPT) { kmin = fminf(kmin, v[i]); kmax = fmaxf(kmax, v[i]); }
+        } else {
+          raise_error(KERR_INTERNAL);
         }
+        ++lp;
+        if constexpr (QK && Q != 32) { kmin = fminf(kmin, v[i]); kmax = fmaxf(kmax, v[i]); }
       }
       if constexpr (EF) {
-        // the quantized case corrects the kept entries later (qpack reads X back from here)
-        eo[i] = (kept && !QKEPT) ? v[i] - through<InT>(v[i]) : v[i] - 0.0f;
+        // the residual, in place; without lo / hi the kept entries keep X
+        // here and qpack corrects them
+        v[i] = (kept && (!QK || pre)) ? v[i] - through<InT>(rec) : v[i] - 0.0f;
       }
     }
     if constexpr (EF) {
-      if (nv > 0) store_run_partial<float, G_VPT, true>(a.e + t0, nv, eo);
+      // write-back stores: the four 16-byte stores of a thread fill each
+      // 128-byte line only together, which the L2 merges before writing it
+      if (nv > 0) store_run_partial<float, G_VPT, false>(a.e + t0, nv, v);
     }
     if (a.blk && threadIdx.x == 0) a.blk[tile] = tile_first;
+    __syncthreads();
+    // ---- the tile's payload entries, coalesced
+    const uint32_t n_ok = (uint32_t)min((uint64_t)cnt, sat_sub(a.k, (uint64_t)tile_first));
+    if (n_ok < cnt && threadIdx.x == 0) raise_error(KERR_INTERNAL);
+    for (uint32_t j = threadIdx.x; j < n_ok; j += G_NT) {
+      const uint64_t g = (uint64_t)tile_first + j;
+      a.idx[g] = (uint32_t)(tile * G_TILE + s_off[j]);
+      if constexpr (!QK) ((R*)a.val)[g] = s_val[j];
+      if constexpr (Q == 32) a.codes[g] = s_val[j];
+    }
+    if constexpr (QK && Q != 32) {
+      if (pre) write_codes<Q>(a.codes, a.wpg, tile_first, n_ok, s_val, true);
+    }
+    __syncthreads();
   }
-  if (a.blk && blockIdx.x == 0 && threadIdx.x == 0) a.blk[a.n_tiles] = (uint32_t)a.k;
-  if constexpr (QKEPT) {
-    block_minmax<G_NT>(kmin, kmax, s_mm);
-    if (threadIdx.x == 0 && kmin <= kmax) {
-      __hip_atomic_fetch_min(&st[ST_MIN], order_key(kmin), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_fetch_max(&st[ST_MAX], order_key(kmax), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    if (a.blk) a.blk[a.n_tiles] = (uint32_t)a.k;
+    if constexpr (Q == 32) { a.meta[0] = 0.0f; a.meta[1] = 0.0f; }
+  }
+  if constexpr (QK && Q != 32) {
+    if (!pre) {
+      block_minmax<G_NT>(kmin, kmax, s_mm);
+      if (threadIdx.x == 0) push_minmax(st, ST_MIN, ST_MAX, kmin, kmax);
     }
   }
 }
 
 // ------------------------------------------------------------------ qpack
-// codes of the kept list (one min-max group), meta, and with error feedback
-// the residual at the kept entries: e[idx_j] holds X there (emit left it)
+// Only when emit could not quantize: codes of the kept list (one min-max
+// group), meta, and the residual at the kept entries, where emit left X.
+// Chunks of 8192 entries start on word boundaries for every b.
 constexpr int QP_VPT = 32;
+constexpr uint32_t QP_CH = (uint32_t)G_NT * QP_VPT;
 
-template <int B, typename OutT, bool EF>
+template <uint32_t B, typename OutT>
 __global__ __launch_bounds__(G_NT) void k_g_qpack(GlobalArgs a) {
-  constexpr int WPT = (B == 32) ? QP_VPT : QP_VPT * B / 32;
+  static_assert((QP_CH * B) % 32 == 0, "chunks on word boundaries");
+  __shared__ uint8_t s_code[QP_CH];
   const uint32_t* st = a.state;
-  float lo = 0.0f, scale = 0.0f, hi = 0.0f;
-  const bool any = a.k > 0;
-  if (any) {
-    lo = from_order_key(st[ST_MIN]) + 0.0f;
+  if (st[ST_PRE]) return;
+  constexpr uint32_t LV = (1u << B) - 1u;
+  float lo = 0.0f, hi = 0.0f, scale = 0.0f;
+  if (a.k > 0) {
+    lo = from_order_key(~st[ST_MIN]) + 0.0f;
     hi = from_order_key(st[ST_MAX]) + 0.0f;
   }
-  constexpr uint32_t LV = (B == 32) ? 0u : (1u << B) - 1u;
-  if (B != 32 && any && hi != lo) scale = (hi - lo) / (float)LV;
+  if (hi != lo) scale = (hi - lo) / (float)LV;
+  const float range = hi - lo;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
-    a.meta[0] = (B == 32) ? 0.0f : lo;
+    a.meta[0] = lo;
     a.meta[1] = scale;
   }
-  for (uint64_t j0 = ((uint64_t)blockIdx.x * G_NT + threadIdx.x) * QP_VPT; j0 < a.k;
-       j0 += (uint64_t)gridDim.x * G_NT * QP_VPT) {
-    const int n = (int)min((uint64_t)QP_VPT, a.k - j0);
-    uint32_t ix[QP_VPT];
-    float x[QP_VPT];
-#pragma unroll
+  for (uint64_t c0 = (uint64_t)blockIdx.x * QP_CH; c0 < a.k; c0 += (uint64_t)gridDim.x * QP_CH) {
+    const uint32_t n = (uint32_t)min((uint64_t)QP_CH, a.k - c0);
+#pragma unroll 4
     for (int i = 0; i < QP_VPT; ++i) {
-      ix[i] = (i < n) ? a.idx[j0 + i] : 0u;
-      x[i] = (i < n && ix[i] < a.L) ? a.e[ix[i]] : 0.0f;
-    }
-    uint32_t w[WPT];
-    uint32_t c[QP_VPT];
-    if constexpr (B == 32) {
-#pragma unroll
-      for (int i = 0; i < QP_VPT; ++i) w[i] = __float_as_uint(x[i]);
-    } else {
-      const float range = hi - lo;
-#pragma unroll
-      for (int i = 0; i < QP_VPT; ++i) {
-        uint32_t q = 0;
-        if (hi != lo) {
-          const float u = (x[i] - lo) / range;
-          const float t = u * (float)LV;
-          q = min((uint32_t)rintf(t), LV);
+      const uint32_t jl = (uint32_t)i * G_NT + threadIdx.x;
+      if (jl < n) {
+        const uint32_t ix = a.idx[c0 + jl];
+        uint32_t c = 0;
+        if (ix < a.L) {
+          const float x = a.e[ix];
+          c = quant_code<B>(x, lo, range);
+          const float prod = (float)c * scale;
+          const float rec = lo + prod;
+          a.e[ix] = x - through<OutT>(rec);
+        } else {
+          raise_error(KERR_INTERNAL);
         }
-        c[i] = (i < n) ? q : 0u;
-      }
-#pragma unroll
-      for (int q = 0; q < WPT; ++q) w[q] = 0u;
-#pragma unroll
-      for (int i = 0; i < QP_VPT; ++i) {
-        const int bit = i * B;
-        w[bit >> 5] |= c[i] << (bit & 31);
-        if ((bit & 31) + B > 32) w[(bit >> 5) + 1] |= c[i] >> (32 - (bit & 31));
+        s_code[jl] = (uint8_t)c;
       }
     }
-    const uint64_t wo = (B == 32) ? j0 : (j0 * (uint64_t)B) / 32u;
-    const int nw = (int)min((uint64_t)WPT, sat_sub(a.wpg, wo));
-    if (nw > 0) store_run_partial<uint32_t, WPT, true>(a.codes + wo, nw, w);
-    if constexpr (EF) {
-#pragma unroll
-      for (int i = 0; i < QP_VPT; ++i) {
-        if (i < n) {
-          if (ix[i] >= a.L) { raise_error(KERR_INTERNAL); continue; }
-          float rec;
-          if constexpr (B == 32) rec = x[i];
-          else { const float prod = (float)c[i] * scale; rec = lo + prod; }
-          a.e[ix[i]] = x[i] - through<OutT>(rec);
-        }
-      }
-    }
+    __syncthreads();
+    write_codes<B>(a.codes, a.wpg, c0, n, s_code, false);
+    __syncthreads();
   }
 }
 
-// back to the zero-filled workspace: tile states, counters and the state words
+// back to the zero-filled workspace: tile words, the used part of the
+// candidate list (its offset depends on the segment length, so a later call
+// may find tile words there), then the state words (the last workgroup, once
+// every workgroup has read the candidate counts)
 __global__ __launch_bounds__(G_NT) void k_g_clean(GlobalArgs a) {
-  for (uint64_t i = (uint64_t)blockIdx.x * G_NT + threadIdx.x; i < 2 * a.n_tiles; i += (uint64_t)gridDim.x * G_NT)
-    st_agent(&a.tiles[i], 0u);
-  if (blockIdx.x == 0)
-    for (int i = threadIdx.x; i < ST_WORDS; i += G_NT) st_agent(&a.state[i], 0u);
-}
-
-// min/max start values before emit
-__global__ void k_g_minmax_init(GlobalArgs a) {
-  if (threadIdx.x == 0) {
-    a.state[ST_MIN] = 0xFFFFFFFFu;
-    a.state[ST_MAX] = 0u;
-    a.state[ST_TICKET] = 0u;
+  uint32_t* st = a.state;
+  const uint64_t gsz = (uint64_t)gridDim.x * G_NT, t = (uint64_t)blockIdx.x * G_NT + threadIdx.x;
+  for (uint64_t i = t; i < 4 * a.n_tiles; i += gsz) st_agent(&a.tiles[i], 0u);
+  for (uint64_t i = t; i < 2 * TC_GRID; i += gsz) st_agent(&a.wgs[i], 0u);
+  const uint64_t capc = sub_cap(a);
+  for (uint32_t c = 0; c < a.n_sub; ++c) {
+    const uint64_t n = min((uint64_t)st[SP_NCAND + SLOT_WORDS * c], capc);
+    for (uint64_t i = t; i < n; i += gsz) st_agent(&a.cand[c * capc + i], 0u);
   }
+  if (!last_block(st)) return;
+  for (int i = threadIdx.x; i < ST_WORDS; i += G_NT) st_agent(&st[i], 0u);
 }
 
 // ------------------------------------------------------------------ plans
 namespace {
 
 template <typename InT, bool EF>
-const void* hist_ptr(int pass) {
-  if (pass == 1) return (const void*)k_g_hist<InT, EF, 1>;
-  if (pass == 2) return (const void*)k_g_hist<InT, EF, 2>;
-  return (const void*)k_g_hist<InT, EF, 3>;
-}
-template <typename InT>
-const void* hist_ptr_ef(bool ef, int pass) { return ef ? hist_ptr<InT, true>(pass) : hist_ptr<InT, false>(pass); }
-const void* pick_hist(int dt, bool ef, int pass) {
-  if (dt == DT_F32) return hist_ptr_ef<float>(ef, pass);
-  if (dt == DT_BF16) return hist_ptr_ef<bf16_t>(ef, pass);
-  return hist_ptr_ef<f16_t>(ef, pass);
-}
-
-template <typename InT>
-const void* emit_ptr(bool ef, bool qkept) {
-  if (ef) return qkept ? (const void*)k_g_emit<InT, true, true> : (const void*)k_g_emit<InT, true, false>;
-  return qkept ? (const void*)k_g_emit<InT, false, true> : (const void*)k_g_emit<InT, false, false>;
-}
-const void* pick_emit(int dt, bool ef, bool qkept) {
-  if (dt == DT_F32) return emit_ptr<float>(ef, qkept);
-  if (dt == DT_BF16) return emit_ptr<bf16_t>(ef, qkept);
-  return emit_ptr<f16_t>(ef, qkept);
-}
-
-template <typename OutT, bool EF>
-const void* qpack_ptr_b(uint32_t b) {
-  switch (b) {
-    case 1: return (const void*)k_g_qpack<1, OutT, EF>;
-    case 2: return (const void*)k_g_qpack<2, OutT, EF>;
-    case 3: return (const void*)k_g_qpack<3, OutT, EF>;
-    case 4: return (const void*)k_g_qpack<4, OutT, EF>;
-    case 5: return (const void*)k_g_qpack<5, OutT, EF>;
-    case 6: return (const void*)k_g_qpack<6, OutT, EF>;
-    case 7: return (const void*)k_g_qpack<7, OutT, EF>;
-    case 8: return (const void*)k_g_qpack<8, OutT, EF>;
-    case 32: return (const void*)k_g_qpack<32, OutT, EF>;
+const void* chain_ptr(int which) {
+  switch (which) {
+    case 0: return (const void*)k_g_sample<InT, EF>;
+    case 1: return (const void*)k_g_band<InT, EF>;
+    case 2: return (const void*)k_g_pass<InT, EF, 1>;
+    case 3: return (const void*)k_g_pass<InT, EF, 2>;
+    case 4: return (const void*)k_g_pass<InT, EF, 3>;
+    case 5: return (const void*)k_g_tcount<InT, EF>;
   }
   return nullptr;
 }
-const void* pick_qpack(int out_dt, bool ef, uint32_t b) {
-  if (out_dt == DT_F32) return ef ? qpack_ptr_b<float, true>(b) : qpack_ptr_b<float, false>(b);
-  if (out_dt == DT_BF16) return ef ? qpack_ptr_b<bf16_t, true>(b) : qpack_ptr_b<bf16_t, false>(b);
-  return ef ? qpack_ptr_b<f16_t, true>(b) : qpack_ptr_b<f16_t, false>(b);
+const void* pick_chain(int dt, bool ef, int which) {
+  if (dt == DT_F32) return ef ? chain_ptr<float, true>(which) : chain_ptr<float, false>(which);
+  if (dt == DT_BF16) return ef ? chain_ptr<bf16_t, true>(which) : chain_ptr<bf16_t, false>(which);
+  return ef ? chain_ptr<f16_t, true>(which) : chain_ptr<f16_t, false>(which);
+}
+
+template <typename InT>
+const void* emit_ptr(bool ef, uint32_t q) {
+  if (q == 0) return ef ? (const void*)k_g_emit<InT, true, 0> : (const void*)k_g_emit<InT, false, 0>;
+  if (!ef) return nullptr;
+  switch (q) {
+    case 1: return (const void*)k_g_emit<InT, true, 1>;
+    case 2: return (const void*)k_g_emit<InT, true, 2>;
+    case 3: return (const void*)k_g_emit<InT, true, 3>;
+    case 4: return (const void*)k_g_emit<InT, true, 4>;
+    case 5: return (const void*)k_g_emit<InT, true, 5>;
+    case 6: return (const void*)k_g_emit<InT, true, 6>;
+    case 7: return (const void*)k_g_emit<InT, true, 7>;
+    case 8: return (const void*)k_g_emit<InT, true, 8>;
+    case 32: return (const void*)k_g_emit<InT, true, 32>;
+  }
+  return nullptr;
+}
+const void* pick_emit(int dt, bool ef, uint32_t q) {
+  if (dt == DT_F32) return emit_ptr<float>(ef, q);
+  if (dt == DT_BF16) return emit_ptr<bf16_t>(ef, q);
+  return emit_ptr<f16_t>(ef, q);
+}
+
+template <typename OutT>
+const void* qpack_ptr(uint32_t b) {
+  switch (b) {
+    case 1: return (const void*)k_g_qpack<1, OutT>;
+    case 2: return (const void*)k_g_qpack<2, OutT>;
+    case 3: return (const void*)k_g_qpack<3, OutT>;
+    case 4: return (const void*)k_g_qpack<4, OutT>;
+    case 5: return (const void*)k_g_qpack<5, OutT>;
+    case 6: return (const void*)k_g_qpack<6, OutT>;
+    case 7: return (const void*)k_g_qpack<7, OutT>;
+    case 8: return (const void*)k_g_qpack<8, OutT>;
+  }
+  return nullptr;
+}
+const void* pick_qpack(int out_dt, uint32_t b) {
+  if (out_dt == DT_F32) return qpack_ptr<float>(b);
+  if (out_dt == DT_BF16) return qpack_ptr<bf16_t>(b);
+  return qpack_ptr<f16_t>(b);
 }
 
 hipError_t launch(const void* fn, uint32_t grid, uint32_t nt, const GlobalArgs& args, hipStream_t st) {
@@ -389,45 +886,64 @@ hipError_t launch(const void* fn, uint32_t grid, uint32_t nt, const GlobalArgs& 
   return hipLaunchKernel(fn, dim3(grid), dim3(nt), params, 0, st);
 }
 
+uint64_t cand_capacity(uint64_t L) { return L / 4 + 4096; }
+
 }  // namespace
 
 uint64_t global_ws_words(uint64_t L) {
-  // state, three histograms, and two words per tile
-  return (uint64_t)ST_WORDS + 3ull * HIST_BINS + 2ull * n_blocks(L);
+  // state, four histograms, a record per tile, tcount's workgroup totals,
+  // the candidate sub-lists
+  return (uint64_t)ST_WORDS + 4ull * HIST_BINS + 4ull * n_blocks(L) + 2ull * TC_GRID + cand_capacity(L);
+}
+
+static uint32_t chain_grid(uint64_t n_tiles) {
+  // eight workgroups per compute unit, each over many tiles
+  return (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(n_tiles, (uint64_t)device_cus() * 8));
 }
 
 void global_ws_carve(uint32_t* ws, uint64_t L, GlobalArgs& a) {
   a.state = ws;
   a.hist = ws + ST_WORDS;
-  a.tiles = ws + ST_WORDS + 3 * HIST_BINS;
+  a.tiles = ws + ST_WORDS + 4 * HIST_BINS;
   a.n_tiles = n_blocks(L);
+  a.wgs = a.tiles + 4 * a.n_tiles;
+  a.cand = a.wgs + 2 * TC_GRID;
+  a.cand_cap = cand_capacity(L);
+  a.sample_stride = (uint32_t)((a.n_tiles + SAMPLE_TILES - 1) / SAMPLE_TILES);
+  a.n_sub = std::min<uint32_t>(chain_grid(a.n_tiles), NSLOT);
+  const uint64_t tc_grid = std::max<uint64_t>(1, std::min<uint64_t>(a.n_tiles, TC_GRID));
+  a.tpw = (uint32_t)((a.n_tiles + tc_grid - 1) / tc_grid);
 }
 
 hipError_t launch_global(int dt, bool ef, uint32_t qbits, const GlobalArgs& args, hipStream_t st) {
-  // the quantized kept list reads X back from the residual buffer
+  // the quantized kept list needs the residual buffer (qpack reads X there)
   if (qbits != 0 && !ef) return hipErrorInvalidValue;
   const uint32_t cus = (uint32_t)device_cus();
-  const uint32_t grid = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(args.n_tiles, (uint64_t)cus * 8));
-  const bool qkept = qbits != 0;
+  const uint32_t grid = chain_grid(args.n_tiles);
+  GlobalArgs a = args;
+  if (a.n_sub < 1 || a.n_sub > NSLOT || a.n_sub > grid || a.tpw < 1 || a.tpw > TPW_MAX ||
+      (a.n_tiles + a.tpw - 1) / a.tpw > TC_GRID)
+    return hipErrorInvalidValue;
+  a.bits = qbits;
   hipError_t e = hipSuccess;
-  if (args.k > 0) {
-    for (int pass = 1; pass <= 3 && e == hipSuccess; ++pass) {
-      e = launch(pick_hist(dt, ef, pass), grid, G_NT, args, st);
-      if (e == hipSuccess) {
-        const void* pk = (pass == 1) ? (const void*)k_g_pick<1> : (pass == 2) ? (const void*)k_g_pick<2>
-                                                                                : (const void*)k_g_pick<3>;
-        e = launch(pk, 1, 512, args, st);
-      }
+  if (a.k > 0) {
+    const uint64_t n_s = (a.n_tiles + a.sample_stride - 1) / a.sample_stride;
+    const uint32_t sgrid = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(n_s, SAMPLE_GRID));
+    e = launch(pick_chain(dt, ef, 0), sgrid, G_NT, a, st);
+    for (int which = 1; which <= 4 && e == hipSuccess; ++which) e = launch(pick_chain(dt, ef, which), grid, G_NT, a, st);
+    if (e == hipSuccess && qbits != 0 && qbits != 32) e = launch((const void*)k_g_keptmm, CAND_GRID, G_NT, a, st);
+    if (e == hipSuccess) {
+      const uint32_t tgrid = (uint32_t)((a.n_tiles + a.tpw - 1) / a.tpw);
+      e = launch(pick_chain(dt, ef, 5), tgrid, G_NT, a, st);
     }
   }
-  if (e == hipSuccess) e = launch((const void*)k_g_minmax_init, 1, 64, args, st);
-  if (e == hipSuccess) e = launch(pick_emit(dt, ef, qkept), grid, G_NT, args, st);
-  if (e == hipSuccess && qkept) {
-    const uint64_t work = (args.k + (uint64_t)G_NT * QP_VPT - 1) / ((uint64_t)G_NT * QP_VPT);
+  if (e == hipSuccess) e = launch(pick_emit(dt, ef, qbits), grid, G_NT, a, st);
+  if (e == hipSuccess && qbits != 0 && qbits != 32) {
+    const uint64_t work = (a.k + QP_CH - 1) / QP_CH;
     const uint32_t qgrid = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(work, (uint64_t)cus * 8));
-    e = launch(pick_qpack(dt, ef, qbits), qgrid, G_NT, args, st);
+    e = launch(pick_qpack(dt, qbits), qgrid, G_NT, a, st);
   }
-  if (e == hipSuccess) e = launch((const void*)k_g_clean, std::min<uint32_t>(grid, 256), G_NT, args, st);
+  if (e == hipSuccess) e = launch((const void*)k_g_clean, std::min<uint32_t>(grid, 1024), G_NT, a, st);
   return e;
 }
 

@@ -147,13 +147,13 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
     // ---- outputs
     const uint64_t wo = (B == 32) ? c0 : (c0 * (uint64_t)B) / 32u;
     const int nw = (int)min((uint64_t)WPT, sat_sub(a.wpg, wo));
-    if (nw > 0) store_run_partial<uint32_t, WPT, true>(a.codes + grp * a.wpg + wo, nw, w);
+    if (nw > 0) store_run_partial<uint32_t, WPT, false>(a.codes + grp * a.wpg + wo, nw, w);
     if (part == 0 && threadIdx.x == 0) {
       a.meta[2 * grp] = lo;
       a.meta[2 * grp + 1] = scale;
     }
     if constexpr (EF) {
-      if (nv > 0) store_run_partial<float, QVPT, true>(a.e + off, nv, v);
+      if (nv > 0) store_run_partial<float, QVPT, false>(a.e + off, nv, v);
     }
   }
   if (P > 1) group_exit<NT>(bar, P, slots, 2ull * P);
@@ -188,7 +188,7 @@ __global__ __launch_bounds__(NT) void k_quant_unpack(UnpackArgs a) {
         y[i] = Elem<OutT>::down(lo + prod);
       }
     }
-    store_run_partial<R, QVPT, true>((R*)a.y + grp * a.G + c0, nv, y);
+    store_run_partial<R, QVPT, false>((R*)a.y + grp * a.G + c0, nv, y);
   }
 }
 

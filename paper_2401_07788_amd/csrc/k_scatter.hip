@@ -127,13 +127,8 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
       }
     }
     __syncthreads();
-    const uint64_t t0 = c0 + (uint64_t)threadIdx.x * SC_VPT;
-    const int nv = (int)min((uint64_t)SC_VPT, sat_sub(c1, t0));
-    if (nv > 0) {
-      RO out[SC_VPT];
-      load_run<RO, SC_VPT>(&buf[threadIdx.x * SC_VPT], out);
-      store_run_partial<RO, SC_VPT, true>((RO*)a.y + seg * a.L + t0, nv, out);
-    }
+    // the dense chunk, each store instruction covering whole lines
+    copy_lds_to_global<SC_NT, RO>((RO*)a.y + seg * a.L + c0, buf, (uint32_t)(c1 - c0));
     __syncthreads();
   }
 }
@@ -188,11 +183,10 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
       }
     }
     __syncthreads();
-    if (nv > 0) {
-      load_run<R, SC_VPT>(&buf[threadIdx.x * SC_VPT], mr);
-      store_run_partial<R, SC_VPT, true>(row + t0, nv, mr);
-      store_run_partial<R, SC_VPT, true>((R*)a.y + b * a.L + t0, nv, mr);
-    }
+    // the updated row chunk to the buffer and to a_hat, each store
+    // instruction covering whole lines
+    copy_lds_to_global<SC_NT, R>(row + c0, buf, (uint32_t)(c1 - c0));
+    copy_lds_to_global<SC_NT, R>((R*)a.y + b * a.L + c0, buf, (uint32_t)(c1 - c0));
     __syncthreads();
   }
 }

@@ -70,8 +70,12 @@ __device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v)
 // Uses 16-byte accesses when the run is 16-byte aligned and a multiple of 16
 // bytes, else 8-byte, else scalar accesses.  STREAM marks data touched once
 // per launch (the boundary tensors): those accesses carry the non-temporal
-// hint so that they do not displace reused lines or pile up as dirty L2
-// lines at the end of the kernel.
+// hint so that they do not displace reused lines.  Stores take the hint only
+// where one instruction of a wavefront covers whole 128-byte lines (lane-
+// contiguous 16-byte stores, copy_lds_to_global): a thread's run of several
+// 16-byte stores fills each line only across instructions, which non-
+// temporal stores write out piecewise (measured: up to 1.8x the bytes);
+// write-back stores let the L2 merge them first.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 

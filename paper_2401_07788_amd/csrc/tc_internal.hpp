@@ -89,8 +89,9 @@ hipError_t launch_topk_decompress(int wire, int out_dt, const ScatterArgs& a, hi
 hipError_t launch_aqsgd_recv(int dt, const ScatterArgs& a, hipStream_t st);
 
 // ------------------------------------------------ segments too long to hold
-// TopK over one segment with a chain of kernels (histogram passes, picks,
-// an ordered emit with decoupled look-back, the kept-list quantizer)
+// TopK over one segment with a chain of kernels (a sampled band, candidate
+// or whole-segment radix passes, an ordered emit with decoupled look-back,
+// the kept-list quantizer)
 struct GlobalArgs {
   const void* x;         // [L] input
   float* e;              // [L] residual (in-out) or nullptr
@@ -102,7 +103,14 @@ struct GlobalArgs {
   uint64_t L, k, wpg, n_tiles;
   uint32_t* state;       // workspace pieces (global_ws_carve)
   uint32_t* hist;
-  uint32_t* tiles;
+  uint32_t* tiles;       // 4 words per tile
+  uint32_t* wgs;         // tile-count workgroup totals / prefixes
+  uint32_t* cand;        // candidate sub-lists: binary32 bits of the values in the band
+  uint64_t cand_cap;     // all sub-lists together
+  uint32_t bits;         // quantized kept list: b (0: values)
+  uint32_t sample_stride;
+  uint32_t n_sub;        // candidate sub-lists (<= 8, <= the chain's grid)
+  uint32_t tpw;          // tiles per tile-count workgroup
 };
 uint64_t global_ws_words(uint64_t L);
 void global_ws_carve(uint32_t* ws, uint64_t L, GlobalArgs& a);

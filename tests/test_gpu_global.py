@@ -95,6 +95,48 @@ def test_topk_quant_constant_group(tc, orc):
     tq_steps(tc, orc, xs, 1, 100, 4)
 
 
+def tie_sign_inputs():
+    """ties of both signs at the threshold (1000 values of +-1), 300 of them
+    kept; 200 larger values: +-5 (kept values beyond +|T| and -|T|), or all
+    +5 (then which ties are kept decides the minimum of the kept list)"""
+    L = 20000
+    rng = np.random.default_rng(5)
+    base = ((rng.random(L) - 0.5) * 0.9).astype(np.float32)
+    pos = rng.permutation(L)
+    both = base.copy()
+    both[pos[:100]] = 5.0
+    both[pos[100:200]] = -5.0
+    both[pos[200:1200]] = np.where(np.arange(1000) % 2 == 0, 1.0, -1.0).astype(np.float32)
+    one = both.copy()
+    one[pos[100:200]] = 5.0
+    return both, one
+
+
+@pytest.mark.parametrize("case", [0, 1])
+def test_topk_quant_tie_signs(tc, orc, case):
+    x = tie_sign_inputs()[case]
+    tq_steps(tc, orc, [torch.from_numpy(x), torch.from_numpy(x[::-1].copy())], 1, 500, 4)
+
+
+def test_workspace_left_zero_across_lengths(tc, orc):
+    """every call leaves the shared workspace zero-filled: a short segment
+    with a long candidate list, then a longer one whose tile words lie
+    where that list was, then a register-resident TopK on the same
+    workspace"""
+    short = [torch.full((4096 + 17,), -2.5, dtype=torch.float32)]
+    tq_steps(tc, orc, short, 1, 100, 4)
+    longer = [W.randn((6 * 4096 + 5,), 17, t) for t in range(2)]
+    tq_steps(tc, orc, longer, 1, 2000, 4)
+    x = W.randn((32, 16384), 17, 9)
+    k = tc.topk_count(16384, 1, 10)
+    p = tc.topk_compress(x.cuda(), k, 32)
+    torch.cuda.synchronize()
+    assert tc.device_errors() == 0
+    oi, ov = orc.topk_compress(raw(x), "f32", 32, 16384, k, "f32")
+    assert_bits_equal(raw(p.idx), oi, "resident idx")
+    assert_bits_equal(raw(p.val), ov, "resident val")
+
+
 # ------------------------------------------- plain and EF TopK, long segments
 LONG = (1 << 24) + 777    # more workgroups than can be resident at once
 
