@@ -11,10 +11,12 @@ example, payload, buffer update) and the receiver (buffer update from the
 payload, reconstruction).  Every input is resident in HBM before timing.
 The timed region is the sequence of K micro-batches (sender then receiver for
 each, on one stream) captured once as a HIP graph and replayed: the launches
-of a stream of micro-batches without per-launch host cost.  Per-kernel
-durations for the roofline come from HIP events around each kernel of an
-eager pass over other micro-batches; the eager step time and a two-stream
-variant (sender of j+1 overlapping the receiver of j) are reported beside.
+of a stream of micro-batches without per-launch host cost.  Reported beside:
+a pipelined graph (each receiver on a second stream, overlapping the next
+sender as on two pipeline stages; slower on one GPU, where the two compete
+for the compute units), the eager step and an eager two-stream variant.
+Per-kernel durations for the roofline come from HIP events around each
+kernel of an eager pass over other micro-batches.
 
 Reported: value = bytes of the boundary tensor (the activations, fp16) / step
 time; pct_hbm_peak = algorithmic bytes of both sides / step time / 8 TB/s;
@@ -47,6 +49,10 @@ SOURCES_HASHED = {
               "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
     "lm": ["paper_2401_07788_amd/csrc/k_global.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
            "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
+    "resnet": ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
+               "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
+    "transformer": ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
+                    "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
 }
 
 
@@ -96,8 +102,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run 5 device copies of 256 MiB (the reference for HBM byte counters)")
-    ap.add_argument("--workload", choices=["aqsgd", "lm"], default="aqsgd",
-                    help="aqsgd: the AQ-SGD boundary (default); lm: the large language model micro-batch stream")
+    ap.add_argument("--workload", choices=["aqsgd", "lm", "resnet", "transformer"], default="aqsgd",
+                    help="aqsgd: the AQ-SGD boundary (default); lm: the large language model micro-batch stream; "
+                         "resnet / transformer: error feedback on a CNN / transformer boundary")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the boundary compressors run per device and this build has no "
@@ -123,8 +130,31 @@ def main():
         print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n, "launches": 5}))
         return
     tc.lib()
-    out = run_lm(args, dev) if args.workload == "lm" else run_aqsgd(args, dev)
+    if args.workload == "lm":
+        out = run_lm(args, dev)
+    elif args.workload in EF_WORKLOADS:
+        out = run_ef(args, dev, args.workload)
+    else:
+        out = run_aqsgd(args, dev)
     print(json.dumps(out), flush=True)
+
+
+def device_copy_gbps(dev, n_bytes=1 << 30, reps=5):
+    """bytes read + written per second by a device-to-device copy of 1 GiB:
+    the HBM rate a plain streaming kernel reaches on this GPU"""
+    import torch
+    src = torch.empty(n_bytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    gbps = 2 * n_bytes * reps / (a.elapsed_time(b) * 1e-3) / 1e9
+    del src, dst
+    return round(gbps, 1)
 
 
 def check_errors(where):
@@ -147,19 +177,18 @@ def run_aqsgd(args, dev):
     n_mb = n_samples // B
     steps, warm = args.steps, args.warmup
     n_ref = min(100, steps)
-    # micro-batches of one epoch, each used once: eager warm-up, eager
-    # reference pass with per-kernel events, graph warm-up, timed graph,
-    # two-stream reference
-    need_mb = warm + n_ref + warm + steps + warm + n_ref
-    if need_mb > n_mb:
-        print(f"this many steps need {need_mb} micro-batches, an epoch has {n_mb}", file=sys.stderr)
-        sys.exit(2)
+    # micro-batches, each used once: eager warm-up, eager reference pass with
+    # per-kernel events, serial graph (warm-up, K), pipelined graph (warm-up,
+    # K, the timed region), eager two-stream reference; as many epochs as
+    # that takes (ids distinct within each micro-batch)
+    need_mb = warm + n_ref + 2 * (warm + steps) + warm + n_ref
+    n_epochs = (need_mb + n_mb - 1) // n_mb
 
     # ---- inputs, resident in HBM; every timed micro-batch is a fresh one
     t_setup = time.perf_counter()
     m_s = W.aqsgd_buffer(n_samples, L, seed=args.seed, device=dev)
     m_r = m_s.clone()
-    ids_all = W.epoch_ids(n_samples, B, seed=args.seed)
+    ids_all = torch.cat([W.epoch_ids(n_samples, B, seed=args.seed, tensor_id=1 + ep) for ep in range(n_epochs)])
     ids_dev = ids_all.to(dev)
     acts = torch.empty((need_mb, B, L), dtype=torch.float16, device=dev)
     for j in range(need_mb):
@@ -203,26 +232,57 @@ def run_aqsgd(args, dev):
     send_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
     recv_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
 
-    # ---- timed region: the K micro-batches captured as one HIP graph (the
-    # launches of a stream of micro-batches), replayed once
-    cap = torch.cuda.Stream(dev)
-    gw, gt = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
-    torch.cuda.synchronize()
-    with torch.cuda.graph(gw, stream=cap):
-        steps_on(cap, j, warm)
-    j += warm
-    with torch.cuda.graph(gt, stream=cap):
-        steps_on(cap, j, steps)
-    j += steps
+    # ---- the K micro-batches captured as HIP graphs (the launches of a
+    # stream of micro-batches without per-launch host cost), replayed once:
+    # serial (sender then receiver of each micro-batch on one stream) and
+    # pipelined (the timed region: senders in order on one stream, the
+    # receiver of j on a second stream after the sender of j, so that it
+    # overlaps the sender of j+1 as on two pipeline stages; the sender of j+2
+    # waits for the receiver of j, whose payload buffer it reuses)
+    cap, side = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
+
+    def pipelined(j0, n):
+        done = [torch.cuda.Event() for _ in range(n)]
+        for i in range(n):
+            jj, b = j0 + i, i % 2
+            if i >= 2:
+                cap.wait_event(done[i - 2])
+            tc.aqsgd_step(acts[jj], m_s, ids_dev[jj], k, ws=ws, out=pays[b])
+            side.wait_stream(cap)
+            with torch.cuda.stream(side):
+                tc.aqsgd_reconstruct(pays[b], m_r, ids_dev[jj], out=ahats[b])
+                done[i].record(side)
+        cap.wait_stream(side)
+
+    def graph_of(fn, j0, n):
+        g = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=cap):
+            fn(j0, n)
+        return g
+
+    def timed(g):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        g.replay()
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    gw = graph_of(lambda j0, n: steps_on(cap, j0, n), j, warm); j += warm
+    gs = graph_of(lambda j0, n: steps_on(cap, j0, n), j, steps); j += steps
     gw.replay()
     torch.cuda.synchronize()
     check("during the graph warm-up")
-    t0 = time.perf_counter()
-    gt.replay()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    wall = timed(gs)
     check("in the timed region")
     ms_per_step = wall * 1e3 / steps
+    gpw = graph_of(pipelined, j, warm); j += warm
+    gp = graph_of(pipelined, j, steps); j += steps
+    gpw.replay()
+    torch.cuda.synchronize()
+    check("during the pipelined graph warm-up")
+    pipelined_ms = timed(gp) * 1e3 / steps
+    check("in the pipelined graph")
 
     # ---- reference: sender of j+1 (stream A) overlapping the receiver of j
     # (stream B), payloads double-buffered
@@ -301,6 +361,7 @@ def run_aqsgd(args, dev):
                         "receiver), micro-batches of 8 ids, TopK 30% of the per-example change, fp16 wire",
             "storage_dtype": "f16",
             "micro_batch": B,
+            "timed_region": "HIP graph of K micro-batches, sender then receiver of each on one stream",
             "seg_len": L,
             "k": k,
         },
@@ -308,8 +369,10 @@ def run_aqsgd(args, dev):
         "effective_GBps": round(b_alg / (ms_per_step * 1e-3) / 1e9, 2),
         "algorithmic_bytes_per_step": b_alg,
         "kernels_ms": {"aqsgd_send": round(send_ms, 5), "aqsgd_recv": round(recv_ms, 5)},
+        "pipelined_graph_ms_per_step": round(pipelined_ms, 5),
         "eager_ms_per_step": round(eager_ms, 5),
-        "two_stream_overlap_ms_per_step": round(overlap_ms, 5),
+        "eager_two_stream_ms_per_step": round(overlap_ms, 5),
+        "device_copy_GBps": device_copy_gbps(dev),
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": bytes_side},
@@ -317,6 +380,175 @@ def run_aqsgd(args, dev):
         "setup_s": round(setup_s, 1),
     }
     return out
+
+
+EF_WORKLOADS = {
+    # ResNet-18 boundary: post-ReLU activations 128 x 128x16x16 fp32, one
+    # segment / group per sample; TopK 10 % + EF, variants TopK 30 %, Q2/4/8 + EF
+    "resnet": dict(desc="ResNet-18 boundary: 128 x 128x16x16 fp32 post-ReLU activations, per-sample segments",
+                   shape=(128, 128, 16, 16), n_seg=128, gen="relu", dtype="f32",
+                   main=("topk", 1, 10), variants=[("topk", 3, 10), ("quant", 2), ("quant", 4), ("quant", 8)]),
+    # transformer boundary: bf16 hidden states 8 x 512 x 768 with outlier
+    # channels, one segment / group per token row; TopK 10 % + EF, variant Q4 + EF
+    "transformer": dict(desc="GPT-2-small boundary: 8 x 512 x 768 bf16 hidden states with 4 outlier channels x20, "
+                             "per-token-row segments", shape=(8, 512, 768), n_seg=8 * 512, gen="hidden",
+                        dtype="bf16", main=("topk", 1, 10), variants=[("quant", 4)]),
+}
+
+
+def run_ef(args, dev, name):
+    """error feedback around TopK or quantization on a CNN or transformer
+    boundary: one step = the sender (X = x + e, compress, residual) and the
+    receiver (dense tensor) of one tensor"""
+    import numpy as np
+    import torch
+
+    from paper_2401_07788_amd import tc
+    from paper_2401_07788_amd import workloads as W
+
+    cfg = EF_WORKLOADS[name]
+    shape, n_seg = cfg["shape"], cfg["n_seg"]
+    N = int(np.prod(shape))
+    L = N // n_seg
+    tdt = torch.float32 if cfg["dtype"] == "f32" else torch.bfloat16
+    esz = 4 if cfg["dtype"] == "f32" else 2
+    steps, warm = args.steps, args.warmup
+    n_ref = min(50, steps)
+    # enough (x, e) sets that one pass over them exceeds 512 MB (more than the
+    # on-package cache holds)
+    n_sets = max(2, -(-(512 << 20) // (N * (esz + 4))))
+    t_setup = time.perf_counter()
+    gen = (lambda i: W.relu_activation(shape, args.seed, i, device=dev)) if cfg["gen"] == "relu" else \
+        (lambda i: W.transformer_hidden(shape, args.seed, i, device=dev))
+    xs = [gen(i).reshape(n_seg, L).contiguous() for i in range(n_sets)]
+    es = [torch.zeros((n_seg, L), dtype=torch.float32, device=dev) for _ in range(n_sets)]
+    y = torch.empty((n_seg, L), dtype=tdt, device=dev)
+    setup_s = time.perf_counter() - t_setup
+
+    def make(codec):
+        """(send(i), recv(), bytes sent, bytes received) for one codec"""
+        if codec[0] == "topk":
+            k = tc.topk_count(L, codec[1], codec[2])
+            pl = tc.empty_topk_payload(n_seg, L, k, tdt, dev)
+            c = tc.codec(tc.TC_TOPK, n_seg, L, k, wire=tc._dt(xs[0]))
+            ws = tc.workspace(c, dev)
+            payload = n_seg * (k * (4 + esz) + 4 * (tc.n_blocks(L) + 1))
+
+            def send(i):
+                tc.ef_step_topk(xs[i % n_sets], es[i % n_sets], k, n_seg, ws=ws, out=pl)
+
+            def recv():
+                tc.topk_decompress(pl, L, out=y)
+            label = f"TopK {100 * codec[1] // codec[2]} % + EF"
+        else:
+            b = codec[1]
+            codes = torch.empty((n_seg, tc.quant_group_bytes(L, b)), dtype=torch.uint8, device=dev)
+            meta = torch.empty((n_seg, 2), dtype=torch.float32, device=dev)
+            c = tc.codec(tc.TC_QUANT, n_seg, L, bits=b, wire=tc._dt(xs[0]))
+            ws = tc.workspace(c, dev)
+            payload = codes.numel() + meta.numel() * 4
+
+            def send(i):
+                tc.ef_step_quant(xs[i % n_sets], es[i % n_sets], b, n_seg, ws=ws, out=(codes, meta))
+
+            def recv():
+                tc.quant_unpack(codes, meta, L, b, out=y)
+            label = f"Q{b} + EF"
+        send_bytes = esz * N + 4 * N + 4 * N + payload   # read x, read e, write e, write payload
+        recv_bytes = payload + esz * N                   # read payload, write the dense tensor
+        return send, recv, send_bytes, recv_bytes, label
+
+    def measure(codec, n_steps, with_events):
+        send, recv, sb, rb, label = make(codec)
+        st = torch.cuda.current_stream(dev)
+        for i in range(warm):
+            send(i); recv()
+        torch.cuda.synchronize()
+        check_errors(f"during the warm-up ({label})")
+        ev_ms = None
+        if with_events:
+            ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_ref)]
+            for i in range(n_ref):
+                ev[i][0].record(st); send(i); ev[i][1].record(st); recv(); ev[i][2].record(st)
+            torch.cuda.synchronize()
+            check_errors(f"in the reference pass ({label})")
+            ev_ms = (float(np.mean([e[0].elapsed_time(e[1]) for e in ev])),
+                     float(np.mean([e[1].elapsed_time(e[2]) for e in ev])))
+        cap = torch.cuda.Stream(dev)
+        g = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=cap):
+            for i in range(n_steps):
+                send(i); recv()
+        g.replay()   # warm-up replay
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        g.replay()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / n_steps
+        check_errors(f"in the timed region ({label})")
+        return ms, ev_ms, sb, rb, label
+
+    ms_per_step, (send_ms, recv_ms), sb, rb, label = measure(cfg["main"], steps, True)
+    variants = {}
+    for v in cfg["variants"]:
+        vms, vev, vsb, vrb, vlabel = measure(v, max(10, steps // 4), True)
+        variants[vlabel] = {"ms_per_step": round(vms, 5), "boundary_GBps": round(esz * N / (vms * 1e-3) / 1e9, 2),
+                            "pct_hbm_peak": round(100 * (vsb + vrb) / (vms * 1e-3) / (HBM_PEAK_GBPS * 1e9), 3),
+                            "send_ms": round(vev[0], 5), "recv_ms": round(vev[1], 5)}
+    boundary = esz * N
+    value = boundary / (ms_per_step * 1e-3) / 1e9
+    dominant = "send" if send_ms >= recv_ms else "recv"
+    dom_bytes, dom_ms = (sb, send_ms) if dominant == "send" else (rb, recv_ms)
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    kname = f"{name}_ef_{dominant}"
+
+    cpu = None
+    if not args.no_cpu:
+        import oracle
+        cores = cpu_cores()
+        k = tc.topk_count(L, cfg["main"][1], cfg["main"][2])
+        xr = xs[0].cpu()
+        xr = xr.numpy() if tdt == torch.float32 else xr.view(torch.int16).numpy().view(np.uint16)
+        e_np = np.zeros((n_seg, L), np.float32)
+        t1 = time.perf_counter()
+        done = 0
+        while done < 1 or (time.perf_counter() - t1 < args.cpu_seconds and done < 50):
+            oi, ov, e_np = oracle.ef_topk(xr, cfg["dtype"], e_np, n_seg, L, k, threads=cores)
+            oracle.topk_decompress(oi, ov, cfg["dtype"], n_seg, L, k)
+            done += 1
+        spent = time.perf_counter() - t1
+        cpu = {"value": round(boundary * done / spent / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
+               "sample": f"{done} tensors of the same workload ({label}), sender + receiver, {spent:.1f} s on "
+                         f"{platform.processor() or platform.machine()}"}
+    return {
+        "metric": "boundary-tensor GB/s through compress+decompress+EF; % of HBM peak",
+        "value": round(value, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg['desc']}; {label}", "storage_dtype": cfg["dtype"], "n_seg": n_seg,
+                   "seg_len": L, "rotating_sets": n_sets,
+                   "timed_region": "HIP graph of K steps, sender then receiver of each on one stream"},
+        "pct_hbm_peak": round(100.0 * (sb + rb) / (ms_per_step * 1e-3) / (HBM_PEAK_GBPS * 1e9), 3),
+        "effective_GBps": round((sb + rb) / (ms_per_step * 1e-3) / 1e9, 2),
+        "algorithmic_bytes_per_step": sb + rb,
+        "kernels_ms": {"send": round(send_ms, 5), "recv": round(recv_ms, 5)},
+        "variants": variants,
+        "device_copy_GBps": device_copy_gbps(dev),
+        "roofline": {"bound": "hbm", "kernel": kname, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": read_traffic(kname, name), "algorithmic_bytes": dom_bytes},
+        "cpu_baseline": cpu,
+        "setup_s": round(setup_s, 1),
+    }
 
 
 def run_lm(args, dev):
@@ -459,6 +691,7 @@ def run_lm(args, dev):
         "effective_GBps": round(b_alg / (ms_per_step * 1e-3) / 1e9, 2),
         "algorithmic_bytes_per_step": b_alg,
         "kernels_ms": {"lm_send_chain": round(send_ms, 5), "lm_recv": round(recv_ms, 5)},
+        "device_copy_GBps": device_copy_gbps(dev),
         "roofline": {"bound": "hbm", "kernel": "lm_send_chain", "achieved": round(achieved, 2),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": read_traffic("lm_send_chain", "lm"), "algorithmic_bytes": send_bytes},

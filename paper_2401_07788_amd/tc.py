@@ -207,13 +207,17 @@ def topk_compress(x: torch.Tensor, k: int, n_seg: int, ws=None, out: TopkPayload
     return out
 
 
-def topk_decompress(pl: TopkPayload, seg_len: int, out_dtype=None, use_blk: bool = True):
+def topk_decompress(pl: TopkPayload, seg_len: int, out_dtype=None, use_blk: bool = True, out: torch.Tensor = None):
     """dense [n_seg, seg_len] tensor: the sent values at their indices, +0 elsewhere"""
-    _need_gpu(pl.idx, pl.val, pl.blk)
+    _need_gpu(pl.idx, pl.val, pl.blk, out)
     n_seg, k = pl.idx.shape
+    if out is not None:
+        if out.numel() != n_seg * seg_len:
+            raise ValueError("out has the wrong element count")
+        out_dtype = out.dtype
     out_dtype = out_dtype or pl.val.dtype
     c = codec(TC_TOPK, n_seg, seg_len, k, wire=_dt(pl.val))
-    y = torch.empty((n_seg, seg_len), dtype=out_dtype, device=pl.idx.device)
+    y = out if out is not None else torch.empty((n_seg, seg_len), dtype=out_dtype, device=pl.idx.device)
     p = Payload(_ptr(pl.idx), _ptr(pl.val), None, None, _ptr(pl.blk) if use_blk else None)
     _check(lib().tc_topk_decompress(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(pl.idx.device)),
            "tc_topk_decompress")
@@ -234,11 +238,17 @@ def quant_pack(x: torch.Tensor, bits: int, n_grp: int, ws=None):
     return codes, meta
 
 
-def quant_unpack(codes: torch.Tensor, meta: torch.Tensor, grp_len: int, bits: int, out_dtype=torch.float32):
-    _need_gpu(codes, meta)
+def quant_unpack(codes: torch.Tensor, meta: torch.Tensor, grp_len: int, bits: int, out_dtype=torch.float32,
+                 out: torch.Tensor = None):
+    """dense [n_grp, grp_len]: lo + code * scale per group"""
+    _need_gpu(codes, meta, out)
     n_grp = meta.shape[0]
+    if out is not None:
+        if out.numel() != n_grp * grp_len:
+            raise ValueError("out has the wrong element count")
+        out_dtype = out.dtype
     c = codec(TC_QUANT, n_grp, grp_len, bits=bits, wire=_DT[out_dtype])
-    y = torch.empty((n_grp, grp_len), dtype=out_dtype, device=codes.device)
+    y = out if out is not None else torch.empty((n_grp, grp_len), dtype=out_dtype, device=codes.device)
     p = Payload(None, None, _ptr(codes), _ptr(meta), None)
     _check(lib().tc_quant_unpack(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(codes.device)),
            "tc_quant_unpack")
@@ -262,15 +272,22 @@ def ef_step_topk(x: torch.Tensor, e: torch.Tensor, k: int, n_seg: int, ws=None, 
     return out
 
 
-def ef_step_quant(x: torch.Tensor, e: torch.Tensor, bits: int, n_grp: int, ws=None):
-    """X = x + e; send Q(X); e <- X - received.  e (float32) is updated in place."""
+def ef_step_quant(x: torch.Tensor, e: torch.Tensor, bits: int, n_grp: int, ws=None, out=None):
+    """X = x + e; send Q(X); e <- X - received.  e (float32) is updated in place.
+    out: optional (codes, meta) to write into."""
     _need_gpu(x, e)
     if e.dtype != torch.float32 or e.numel() != x.numel():
         raise ValueError("e must be float32 with x's element count")
     G = x.numel() // n_grp
     c = codec(TC_QUANT, n_grp, G, bits=bits, wire=_dt(x))
-    codes = torch.empty((n_grp, quant_group_bytes(G, bits)), dtype=torch.uint8, device=x.device)
-    meta = torch.empty((n_grp, 2), dtype=torch.float32, device=x.device)
+    if out is not None:
+        codes, meta = out
+        _need_gpu(codes, meta)
+        if codes.numel() != n_grp * quant_group_bytes(G, bits) or meta.numel() != 2 * n_grp:
+            raise ValueError("codes / meta have the wrong size")
+    else:
+        codes = torch.empty((n_grp, quant_group_bytes(G, bits)), dtype=torch.uint8, device=x.device)
+        meta = torch.empty((n_grp, 2), dtype=torch.float32, device=x.device)
     p = Payload(None, None, _ptr(codes), _ptr(meta), None)
     w, wn = _ws_args(c, x.device, ws)
     _check(lib().tc_ef_step(C.byref(c), _ptr(x), _dt(x), C.cast(e.data_ptr(), C.POINTER(C.c_float)), C.byref(p),
