@@ -1,19 +1,27 @@
 // k_topk.hip -- the sender side of TopK (Sec. 2.3), with error feedback
 // (Sec. 2.4) or AQ-SGD (Sec. 2.5) fused around it.
 //
-// One kernel body, three producers / epilogues:
+// One selection, three producers / epilogues:
 //   PLAIN : v = x                                  -> payload
 //   EF    : v = x + e                              -> payload, e <- v - r
 //           r = what the receiver gets: wire(v) at kept entries, +0 elsewhere
 //   AQSGD : v = a - m[id]                          -> payload, m[id][kept] += wire(v)
-// The segment (a sample, a token row, a whole tensor) stays in registers for
-// the whole kernel: inputs are read once, the selection passes work on
-// registers and LDS, and the outputs are written once.
+// The segment (a sample, a token row, a whole example) stays in registers for
+// the whole kernel: inputs are read once, the selection works on registers
+// and LDS, and the outputs are written once.
+//
+// Two engines:
+//   k_topk_row : one wavefront per segment of up to 2048 elements (token
+//                rows); bitwise select with ballots, no LDS, no barriers.
+//   k_topk_grp : P workgroups of 512 threads per segment (samples,
+//                examples); striped register layout, two cross-workgroup
+//                exchanges (tc_group.hpp), payload staged in LDS and written
+//                in index order with full-line stores.
 #include <algorithm>
 #include <type_traits>
 
+#include "tc_group.hpp"
 #include "tc_internal.hpp"
-#include "tc_select.hpp"
 
 namespace tc {
 
@@ -32,42 +40,13 @@ __device__ __forceinline__ void map_wg(uint32_t wg, uint32_t grid, uint32_t P, u
   }
 }
 
-struct RowShared {
-  uint32_t scratch[2];
-};
-
-// LDS of the several-workgroup layout: the selection histogram, and after
-// the selection the workgroup's payload entries, staged so that they leave
-// in index order with coalesced stores
-template <int NT, int VPT, typename R>
-union BigShared {
-  SelShared<NT> sel;
-  struct {
-    uint32_t idx[NT * VPT];
-    R val[NT * VPT];
-  } st;
-};
-
-template <typename InT, int SEL, int VPT, int NT>
-__global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
+// ------------------------------------------------------------- row engine
+template <typename InT, int SEL, int VPT>
+__global__ __launch_bounds__(WAVE) void k_topk_row(TopkArgs a) {
   using R = typename Elem<InT>::raw;
-  constexpr bool BIG = NT > WAVE;
-  using Sh = std::conditional_t<BIG, BigShared<NT, VPT, R>, RowShared>;
-  __shared__ Sh sh;
-  constexpr uint64_t CH = (uint64_t)NT * VPT;
-
-  const uint32_t P = a.P;
-  uint32_t group, part;
-  map_wg(blockIdx.x, gridDim.x, P, group, part);
-  const uint32_t n_groups = gridDim.x / P;
-  GroupMem gm{};
-  if constexpr (BIG) {
-    if (P > 1) gm = group_mem(a.ws, group, P);
-  }
-  bool exited = false;
-
-  for (uint64_t seg = group; seg < a.n_seg; seg += n_groups) {
-    const uint64_t c0 = (uint64_t)part * CH + (uint64_t)threadIdx.x * VPT;
+  __shared__ uint32_t scratch[2];
+  for (uint64_t seg = blockIdx.x; seg < a.n_seg; seg += gridDim.x) {
+    const uint64_t c0 = (uint64_t)threadIdx.x * VPT;
     const int nv = (int)min((uint64_t)VPT, sat_sub(a.L, c0));
 
     // ---- producer: the vector to compress, in binary32
@@ -77,8 +56,8 @@ __global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
     if constexpr (SEL == SEL_AQSGD) {
       const int64_t id = a.ids[seg];
       if (id < 0 || (uint64_t)id >= a.n_samples) {
-        if (threadIdx.x == 0 && part == 0) raise_error(KERR_BAD_ID);
-        continue;              // every workgroup of the group skips alike
+        if (threadIdx.x == 0) raise_error(KERR_BAD_ID);
+        continue;
       }
       mrow = (uint64_t)id * a.L;
     }
@@ -100,30 +79,15 @@ __global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
         for (int i = 0; i < VPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) : 0.0f;
       }
     }
-
     uint32_t key[VPT];
 #pragma unroll
     for (int i = 0; i < VPT; ++i) key[i] = mag_key(v[i]);
 
-    // ---- selection
     SelResult sr;
-    Placement pl;
-    if constexpr (BIG) {
-      if (a.k == 0) { sr.T = 0xFFFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
-      else sr = radix_select<NT, VPT>(key, nv, (uint32_t)a.k, P, part, gm, sh.sel);
-      pl = place<NT, VPT>(key, nv, sr, sh.sel.scratch);
-      // the group's slots have been read: count out now, before the writes
-      if (P > 1 && seg + n_groups >= a.n_seg) {
-        group_exit<NT>(gm.bar, P, gm.slots, slot_words(P));
-        exited = true;
-      }
-    } else {
-      if (a.k == 0) { sr.T = 0xFFFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
-      else sr = bitwise_select<VPT>(key, nv, (uint32_t)a.k);
-      pl = place<NT, VPT>(key, nv, sr, sh.scratch);
-    }
+    if (a.k == 0) { sr.T = 0xFFFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
+    else sr = bitwise_select<VPT>(key, nv, (uint32_t)a.k);
+    const Placement pl = place<WAVE, VPT>(key, nv, sr, scratch);
 
-    // ---- payload + epilogue
     uint32_t* idx = a.idx + seg * a.k;
     R* val = (R*)a.val + seg * a.k;
     uint32_t pos = pl.pos, ties = 0;
@@ -137,14 +101,8 @@ __global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
         ties += tie ? 1u : 0u;
         if (kept) {
           const R w = Elem<InT>::down(v[i]);
-          if constexpr (BIG) {
-            const uint32_t li = pos - pl.wg_first;     // slot inside the workgroup's run
-            if (li < CH) { sh.st.idx[li] = (uint32_t)(c0 + i); sh.st.val[li] = w; }
-            else raise_error(KERR_INTERNAL);
-          } else {
-            if (pos < a.k) { idx[pos] = (uint32_t)(c0 + i); val[pos] = w; }
-            else raise_error(KERR_INTERNAL);
-          }
+          if (pos < a.k) { idx[pos] = (uint32_t)(c0 + i); val[pos] = w; }
+          else raise_error(KERR_INTERNAL);
           ++pos;
           if constexpr (SEL == SEL_AQSGD) mr[i] = Elem<InT>::down(Elem<InT>::up(mr[i]) + Elem<InT>::up(w));
         }
@@ -157,87 +115,320 @@ __global__ __launch_bounds__(NT) void k_topk_seg(TopkArgs a) {
     if constexpr (SEL == SEL_AQSGD) {
       if (nv > 0 && a.k > 0) store_run_partial<R, VPT, false>((R*)a.m + mrow + c0, nv, mr);
     }
-    if constexpr (BIG) {
-      // the workgroup's run of the payload, in index order, coalesced
-      __syncthreads();
-      const uint32_t cnt = min(pl.wg_count, (uint32_t)CH);
-      if (pl.wg_first + cnt > a.k) { if (threadIdx.x == 0) raise_error(KERR_INTERNAL); }
-      else {
-        copy_lds_to_global<NT>(idx + pl.wg_first, sh.st.idx, cnt);
-        copy_lds_to_global<NT>(val + pl.wg_first, sh.st.val, cnt);
-      }
-      // block table: kept entries below each block boundary this workgroup covers,
-      // found by a lower bound in the staged (ascending) run
-      if (a.blk) {
-        uint32_t* bt = a.blk + seg * (n_blocks(a.L) + 1);
-        const uint64_t w0 = (uint64_t)part * CH, w1 = min(a.L, w0 + CH);
-        for (uint64_t b = (w0 + BLOCK_LEN - 1) / BLOCK_LEN + threadIdx.x; b * BLOCK_LEN < w1; b += NT) {
-          const uint64_t B = b * BLOCK_LEN;
-          uint32_t lo = 0, hi = cnt;
-          while (lo < hi) {
-            const uint32_t mid = (lo + hi) >> 1;
-            if (sh.st.idx[mid] < B) lo = mid + 1; else hi = mid;
-          }
-          bt[b] = pl.wg_first + lo;
+    if (a.blk && threadIdx.x == 0) {
+      // a wavefront segment is shorter than one block
+      uint32_t* bt = a.blk + seg * (n_blocks(a.L) + 1);
+      bt[0] = 0;
+      bt[n_blocks(a.L)] = (uint32_t)a.k;
+    }
+  }
+}
+
+// ----------------------------------------------------------- group engine
+// LDS: the selection's histogram and candidate list, then (after the
+// selection) the workgroup's payload entries, staged so that they leave in
+// index order with full-line stores; WAVE extra entries are per-lane dummy
+// slots for the entries a lane does not keep.
+template <uint32_t CH, typename Raw>
+union GrpShared {
+  GrpSelShared<grp_local_cap(CH)> sel;
+  struct {
+    uint32_t idx[CH + WAVE];
+    Raw val[CH + WAVE];
+  } st;
+};
+
+// one 16-byte run of E elements (full, 16-byte aligned)
+template <typename Raw, int E, bool STREAM>
+__device__ __forceinline__ void load16(const Raw* p, Raw (&out)[E]) {
+  static_assert(E * sizeof(Raw) == 16, "one 16-byte access");
+  const u32x4 w = vload<STREAM>(reinterpret_cast<const u32x4*>(p));
+  __builtin_memcpy(out, &w, 16);
+}
+template <typename Raw, int E, bool STREAM>
+__device__ __forceinline__ void store16(Raw* p, const Raw (&in)[E]) {
+  static_assert(E * sizeof(Raw) == 16, "one 16-byte access");
+  u32x4 w;
+  __builtin_memcpy(&w, in, 16);
+  vstore<STREAM>(reinterpret_cast<u32x4*>(p), w);
+}
+
+// One segment on one workgroup of its group.  FULL: the workgroup's chunk
+// lies inside the segment and every buffer is 16-byte aligned, so that all
+// runs are whole 16-byte accesses and no element needs a bounds check.
+template <typename InT, int SEL, int R, bool FULL>
+__device__ __forceinline__ void grp_segment(const TopkArgs& a, uint64_t seg, uint32_t P,
+                                            uint32_t part, const GrpMem& gm,
+                                            GrpShared<(uint32_t)GRP_NT * R * (16 / sizeof(typename Elem<InT>::raw)),
+                                                      typename Elem<InT>::raw>& sh,
+                                            GrpSmall& sm, GrpState& gs, bool last_seg, bool& exited) {
+  using Raw = typename Elem<InT>::raw;
+  constexpr int NT = GRP_NT;
+  constexpr int E = 16 / (int)sizeof(Raw);
+  constexpr uint32_t CH = (uint32_t)NT * R * E;
+  const int t = (int)threadIdx.x;
+  const uint32_t dummy = (uint32_t)lane_id();
+  const uint64_t c0 = (uint64_t)part * CH;
+  const Raw* xs = (const Raw*)a.x + seg * a.L + c0;
+  float* es = (SEL == SEL_EF) ? a.e + seg * a.L + c0 : nullptr;
+
+  // ---- producer: run j of this thread starts at chunk offset (j*NT + t)*E;
+  // all loads are issued before any is used, the input's before the buffer
+  // row's address (AQSGD: the example id) is waited for
+  int n[R];
+  Raw xr[R][E];
+  Raw mr[R][E];               // AQSGD: the buffer row, kept for the update
+  float er[R][E];             // EF: the residual
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const uint32_t off = (uint32_t)(j * NT + t) * E;
+    n[j] = FULL ? E : (int)min((uint64_t)E, sat_sub(a.L, c0 + off));
+    if constexpr (FULL) load16<Raw, E, true>(xs + off, xr[j]);
+    else if (n[j] > 0) load_run_partial<Raw, E, true>(xs + off, n[j], Raw{}, xr[j]);
+  }
+  Raw* ms = nullptr;
+  if constexpr (SEL == SEL_AQSGD) {
+    const int64_t id = a.ids[seg];
+    if (id < 0 || (uint64_t)id >= a.n_samples) {
+      if (t == 0 && part == 0) raise_error(KERR_BAD_ID);
+      return;                  // every workgroup of the group skips alike
+    }
+    ms = (Raw*)a.m + (uint64_t)id * a.L + c0;
+  }
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const uint32_t off = (uint32_t)(j * NT + t) * E;
+    if constexpr (FULL) {
+      if constexpr (SEL == SEL_AQSGD) load16<Raw, E, true>(ms + off, mr[j]);
+      if constexpr (SEL == SEL_EF) {
+        if constexpr (E == 4) {
+          load16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&er[j][0]));
+        } else {
+          load16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&er[j][0]));
+          load16<float, 4, true>(es + off + 4, *reinterpret_cast<float(*)[4]>(&er[j][4]));
         }
-        if (part == 0 && threadIdx.x == 0) bt[n_blocks(a.L)] = (uint32_t)a.k;
       }
-      __syncthreads();
     } else {
-      if (a.blk && threadIdx.x == 0) {
-        // a wavefront segment is shorter than one block
-        uint32_t* bt = a.blk + seg * (n_blocks(a.L) + 1);
-        bt[0] = 0;
-        bt[n_blocks(a.L)] = (uint32_t)a.k;
+      if (n[j] > 0) {
+        if constexpr (SEL == SEL_AQSGD) load_run_partial<Raw, E, true>(ms + off, n[j], Raw{}, mr[j]);
+        if constexpr (SEL == SEL_EF) load_run_partial<float, E, true>(es + off, n[j], 0.0f, er[j]);
       }
     }
   }
-  if constexpr (BIG) {
-    if (P > 1 && !exited) group_exit<NT>(gm.bar, P, gm.slots, slot_words(P));
+  float v[R][E];
+#pragma unroll
+  for (int j = 0; j < R; ++j)
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      float x = Elem<InT>::up(xr[j][i]);
+      if constexpr (SEL == SEL_EF) x = x + er[j][i];
+      if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(mr[j][i]);
+      v[j][i] = (FULL || i < n[j]) ? x : 0.0f;
+    }
+
+  // ---- selection
+  SelResult sr;
+  if (a.k == 0) { sr.T = 0xFFFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
+  else {
+    const uint32_t n_wg = FULL ? CH : (uint32_t)min((uint64_t)CH, a.L - c0);
+    sr = grp_select<NT, R, E, CH, FULL>(v, n, (uint32_t)a.k, n_wg, a.L, P, part, gm, sh.sel, sm, gs);
   }
+  // the group's exchange words have all been read: count out now, before the writes
+  if (P > 1 && last_seg) {
+    grp_exit<NT>(gm, P, gs);
+    exited = true;
+  }
+
+  // ---- placement: keys > T and == T per run, scanned over the workgroup
+  // in index order (run-major, then thread); both counts stay below 2^16
+  uint32_t pk[R], ex[R], tot[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    uint32_t gt = 0, eq = 0;
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      const uint32_t kk = mag_key(v[j][i]);
+      const bool ok = FULL || i < n[j];
+      gt += (ok && kk > sr.T) ? 1u : 0u;
+      eq += (ok && kk == sr.T) ? 1u : 0u;
+    }
+    pk[j] = gt | (eq << 16);
+  }
+  block_excl_scan_multi<NT, R>(pk, ex, tot, sm.scratch);
+  uint32_t eq_wg = 0;
+#pragma unroll
+  for (int j = 0; j < R; ++j) eq_wg += tot[j] >> 16;
+  const uint32_t quota_wg = min(sat_sub(sr.r, sr.eq_before), eq_wg);   // ties this workgroup keeps
+  const uint32_t wg_first = sr.gt_before + min(sr.eq_before, sr.r);
+  uint32_t pos0[R], tie_keep[R];
+  uint32_t eq_run = 0, kept_run = 0;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const uint32_t gtt = tot[j] & 0xFFFFu, eqt = tot[j] >> 16;
+    const uint32_t gx = ex[j] & 0xFFFFu, qx = ex[j] >> 16;
+    const uint32_t quota_j = min(sat_sub(quota_wg, eq_run), eqt);    // ties kept in run j
+    pos0[j] = kept_run + gx + min(qx, quota_j);
+    tie_keep[j] = min(pk[j] >> 16, sat_sub(quota_j, qx));
+    eq_run += eqt;
+    kept_run += gtt + quota_j;
+  }
+  const uint32_t wg_count = kept_run;
+
+  // ---- payload into LDS + epilogue (entries not kept write to the lane's
+  // dummy slot)
+  bool overflow = false;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const uint32_t off = (uint32_t)(j * NT + t) * E;
+    uint32_t pos = pos0[j], ties = 0;
+    float eo[E];
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      const uint32_t kk = mag_key(v[j][i]);
+      const bool ok = FULL || i < n[j];
+      const bool tie = ok && kk == sr.T;
+      const bool kept = ok && (kk > sr.T || (tie && ties < tie_keep[j]));
+      ties += tie ? 1u : 0u;
+      const Raw w = Elem<InT>::down(v[j][i]);
+      overflow |= kept && pos >= CH;
+      const uint32_t slot = (kept && pos < CH) ? pos : CH + dummy;
+      sh.st.idx[slot] = (uint32_t)c0 + off + (uint32_t)i;
+      sh.st.val[slot] = w;
+      pos += kept ? 1u : 0u;
+      if constexpr (SEL == SEL_AQSGD) {
+        const Raw upd = Elem<InT>::down(Elem<InT>::up(mr[j][i]) + Elem<InT>::up(w));
+        mr[j][i] = kept ? upd : mr[j][i];
+      }
+      if constexpr (SEL == SEL_EF) eo[i] = v[j][i] - (kept ? through<InT>(v[j][i]) : 0.0f);
+    }
+    // one store instruction of a wavefront covers 1 KiB here: non-temporal
+    // stores write whole lines
+    if constexpr (FULL) {
+      if constexpr (SEL == SEL_EF) {
+        if constexpr (E == 4) {
+          store16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&eo[0]));
+        } else {
+          store16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&eo[0]));
+          store16<float, 4, true>(es + off + 4, *reinterpret_cast<float(*)[4]>(&eo[4]));
+        }
+      }
+      if constexpr (SEL == SEL_AQSGD) store16<Raw, E, true>(ms + off, mr[j]);
+    } else if (n[j] > 0) {
+      if constexpr (SEL == SEL_EF) store_run_partial<float, E, true>(es + off, n[j], eo);
+      if constexpr (SEL == SEL_AQSGD) store_run_partial<Raw, E, true>(ms + off, n[j], mr[j]);
+    }
+  }
+  if (overflow) raise_error(KERR_INTERNAL);
+  __syncthreads();
+  // the workgroup's run of the payload, in index order, coalesced
+  uint32_t* idx = a.idx + seg * a.k;
+  Raw* val = (Raw*)a.val + seg * a.k;
+  const uint32_t cnt = min(wg_count, CH);
+  if (wg_first + cnt > a.k) {
+    if (t == 0) raise_error(KERR_INTERNAL);
+  } else {
+    copy_lds_to_global<NT>(idx + wg_first, sh.st.idx, cnt);
+    copy_lds_to_global<NT>(val + wg_first, sh.st.val, cnt);
+  }
+  // block table: kept entries below each block boundary this workgroup
+  // covers, by a lower bound in the staged (ascending) run
+  if (a.blk) {
+    uint32_t* bt = a.blk + seg * (n_blocks(a.L) + 1);
+    const uint64_t w1 = min(a.L, c0 + CH);
+    for (uint64_t b = (c0 + BLOCK_LEN - 1) / BLOCK_LEN + t; b * BLOCK_LEN < w1; b += NT) {
+      const uint64_t B = b * BLOCK_LEN;
+      uint32_t lo = 0, hi = cnt;
+      while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (sh.st.idx[mid] < B) lo = mid + 1; else hi = mid;
+      }
+      bt[b] = wg_first + lo;
+    }
+    if (part == 0 && t == 0) bt[n_blocks(a.L)] = (uint32_t)a.k;
+  }
+  __syncthreads();
+}
+
+template <typename InT, int SEL, int R>
+__global__ __launch_bounds__(GRP_NT) void k_topk_grp(TopkArgs a) {
+  using Raw = typename Elem<InT>::raw;
+  constexpr int E = 16 / (int)sizeof(Raw);            // elements per 16-byte run
+  constexpr uint32_t CH = (uint32_t)GRP_NT * R * E;    // elements per workgroup
+  __shared__ GrpShared<CH, Raw> sh;
+  __shared__ GrpSmall sm;
+
+  const uint32_t P = a.P;
+  uint32_t group, part;
+  map_wg(blockIdx.x, gridDim.x, P, group, part);
+  const uint32_t n_groups = gridDim.x / P;
+  GrpMem gm{};
+  if (P > 1) gm = grp_mem(a.ws, group, P);
+  GrpState gs;
+  bool exited = false;
+  // whole 16-byte runs everywhere: every buffer 16-byte aligned, segment
+  // starts too (L a multiple of the run length), and this chunk inside the segment
+  const uintptr_t al = (uintptr_t)a.x | (uintptr_t)a.e | (uintptr_t)a.m;
+  const bool full = (al & 15u) == 0 && (a.L % E) == 0 && (uint64_t)(part + 1) * CH <= a.L;
+
+  for (uint64_t seg = group; seg < a.n_seg; seg += n_groups, ++gs.iter) {
+    const bool last_seg = seg + n_groups >= a.n_seg;
+    if (full) grp_segment<InT, SEL, R, true>(a, seg, P, part, gm, sh, sm, gs, last_seg, exited);
+    else grp_segment<InT, SEL, R, false>(a, seg, P, part, gm, sh, sm, gs, last_seg, exited);
+  }
+  if (P > 1 && !exited) grp_exit<GRP_NT>(gm, P, gs);
 }
 
 // ------------------------------------------------------------------ plans
 namespace {
 
-constexpr int BIG_NT = 512;
-constexpr int ROW_NT = 64;
-constexpr uint64_t ROW_MAX = (uint64_t)ROW_NT * 32;   // longest segment one wavefront holds
+constexpr uint64_t ROW_MAX = (uint64_t)WAVE * 32;   // longest segment one wavefront holds
 static_assert(ROW_MAX <= BLOCK_LEN, "a wavefront segment fits in one block of the block table");
 
 template <typename InT, int SEL>
-const void* kernel_ptr(int nt, int vpt) {
-  if (nt == ROW_NT) {
-    switch (vpt) {
-      case 4: return (const void*)k_topk_seg<InT, SEL, 4, ROW_NT>;
-      case 8: return (const void*)k_topk_seg<InT, SEL, 8, ROW_NT>;
-      case 12: return (const void*)k_topk_seg<InT, SEL, 12, ROW_NT>;
-      case 16: return (const void*)k_topk_seg<InT, SEL, 16, ROW_NT>;
-      case 24: return (const void*)k_topk_seg<InT, SEL, 24, ROW_NT>;
-      case 32: return (const void*)k_topk_seg<InT, SEL, 32, ROW_NT>;
+const void* row_ptr(int vpt) {
+  switch (vpt) {
+    case 4: return (const void*)k_topk_row<InT, SEL, 4>;
+    case 8: return (const void*)k_topk_row<InT, SEL, 8>;
+    case 12: return (const void*)k_topk_row<InT, SEL, 12>;
+    case 16: return (const void*)k_topk_row<InT, SEL, 16>;
+    case 24: return (const void*)k_topk_row<InT, SEL, 24>;
+    case 32: return (const void*)k_topk_row<InT, SEL, 32>;
+  }
+  return nullptr;
+}
+
+// group engine: R runs of 16 bytes per thread (VPT = R * elements per run)
+template <typename InT, int SEL>
+const void* grp_ptr(int r) {
+  if constexpr (sizeof(typename Elem<InT>::raw) == 4) {
+    switch (r) {
+      case 1: return (const void*)k_topk_grp<InT, SEL, 1>;
+      case 2: return (const void*)k_topk_grp<InT, SEL, 2>;
+      case 4: return (const void*)k_topk_grp<InT, SEL, 4>;
+      case 6: return (const void*)k_topk_grp<InT, SEL, 6>;
     }
   } else {
-    switch (vpt) {
-      case 4: return (const void*)k_topk_seg<InT, SEL, 4, BIG_NT>;
-      case 8: return (const void*)k_topk_seg<InT, SEL, 8, BIG_NT>;
-      case 16: return (const void*)k_topk_seg<InT, SEL, 16, BIG_NT>;
-      case 24: return (const void*)k_topk_seg<InT, SEL, 24, BIG_NT>;
+    switch (r) {
+      case 1: return (const void*)k_topk_grp<InT, SEL, 1>;
+      case 2: return (const void*)k_topk_grp<InT, SEL, 2>;
+      case 3: return (const void*)k_topk_grp<InT, SEL, 3>;
     }
   }
   return nullptr;
 }
 
 template <int SEL>
-const void* kernel_ptr_dt(int dt, int nt, int vpt) {
-  if (dt == DT_F32) return kernel_ptr<float, SEL>(nt, vpt);
-  if (dt == DT_BF16) return kernel_ptr<bf16_t, SEL>(nt, vpt);
-  return kernel_ptr<f16_t, SEL>(nt, vpt);
+const void* pick_sel(int dt, bool row, int v) {
+  if (dt == DT_F32) return row ? row_ptr<float, SEL>(v) : grp_ptr<float, SEL>(v);
+  if (dt == DT_BF16) return row ? row_ptr<bf16_t, SEL>(v) : grp_ptr<bf16_t, SEL>(v);
+  return row ? row_ptr<f16_t, SEL>(v) : grp_ptr<f16_t, SEL>(v);
 }
 
-const void* pick(int sel, int dt, int nt, int vpt) {
-  if (sel == SEL_PLAIN) return kernel_ptr_dt<SEL_PLAIN>(dt, nt, vpt);
-  if (sel == SEL_EF) return kernel_ptr_dt<SEL_EF>(dt, nt, vpt);
-  return kernel_ptr_dt<SEL_AQSGD>(dt, nt, vpt);
+// v: the row engine's elements per thread, or the group engine's runs per thread
+const void* pick(int sel, int dt, bool row, int v) {
+  if (sel == SEL_PLAIN) return pick_sel<SEL_PLAIN>(dt, row, v);
+  if (sel == SEL_EF) return pick_sel<SEL_EF>(dt, row, v);
+  return pick_sel<SEL_AQSGD>(dt, row, v);
 }
 
 int occupancy(const void* fn, int nt) {
@@ -254,43 +445,54 @@ SegPlan plan_topk(int sel, int dt, uint64_t n_seg, uint64_t L) {
   if (L <= ROW_MAX) {
     // one wavefront per segment: the smallest run length that covers L
     static const int vpts[] = {4, 8, 12, 16, 24, 32};
-    p.nt = ROW_NT;
-    for (int v : vpts) { p.vpt = v; if ((uint64_t)ROW_NT * v >= L) break; }
+    p.nt = WAVE;
+    for (int v : vpts) { p.vpt = v; if ((uint64_t)WAVE * v >= L) break; }
     p.P = 1;
-    const uint64_t cap = (uint64_t)occupancy(pick(sel, dt, p.nt, p.vpt), p.nt) * cus;
+    const uint64_t cap = (uint64_t)occupancy(pick(sel, dt, true, p.vpt), p.nt) * cus;
     p.capacity = cap;
     p.n_groups = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(n_seg, cap));
     p.grid = p.n_groups;
     p.ws_words = 0;
     return p;
   }
-  // several workgroups per segment: the longest run per thread that still
-  // gives every compute unit a workgroup, else the shortest run
-  static const int vpts[] = {24, 16, 8, 4};
-  p.nt = BIG_NT;
-  p.vpt = 4;
-  for (int v : vpts) {
-    const uint64_t P = (L + (uint64_t)BIG_NT * v - 1) / ((uint64_t)BIG_NT * v);
-    if (n_seg * P >= cus) { p.vpt = v; break; }
+  // several workgroups per segment: the most 16-byte runs per thread that
+  // still give every compute unit a workgroup, else the fewest
+  const int E = (dt == DT_F32) ? 4 : 8;
+  static const int runs32[] = {6, 4, 2, 1};
+  static const int runs16[] = {3, 2, 1};
+  const int* runs = (dt == DT_F32) ? runs32 : runs16;
+  const int n_runs = (dt == DT_F32) ? 4 : 3;
+  p.nt = GRP_NT;
+  p.vpt = runs[n_runs - 1];   // runs per thread
+  for (int i = 0; i < n_runs; ++i) {
+    const uint64_t ch = (uint64_t)GRP_NT * runs[i] * E;
+    const uint64_t P = (L + ch - 1) / ch;
+    if (n_seg * P >= cus) { p.vpt = runs[i]; break; }
   }
-  const uint64_t CH = (uint64_t)BIG_NT * p.vpt;
-  p.P = (uint32_t)((L + CH - 1) / CH);
-  const uint64_t cap = (uint64_t)occupancy(pick(sel, dt, p.nt, p.vpt), p.nt) * cus;
+  const uint64_t CH = (uint64_t)GRP_NT * p.vpt * E;
+  const uint64_t P = (L + CH - 1) / CH;
+  const uint64_t cap = (uint64_t)occupancy(pick(sel, dt, false, p.vpt), p.nt) * cus;
   p.capacity = cap;
+  if (P > GRP_MAX_P) {       // too long for one resident group: the caller takes the global chain
+    p.P = (uint32_t)std::min<uint64_t>(P, UINT32_MAX);
+    p.n_groups = 0;
+    return p;
+  }
+  p.P = (uint32_t)P;
   uint64_t groups = std::min<uint64_t>(n_seg, std::max<uint64_t>(1, cap / p.P));
   if (p.P > 1 && groups >= 8) groups -= groups % 8;
   p.n_groups = (uint32_t)groups;
   p.grid = (uint32_t)(groups * p.P);
   // the workspace is sized for the most groups any instance could keep
-  // resident (4 workgroups of 512 threads per compute unit), so that one size
-  // serves every selection kind of the same layout
+  // resident (4 workgroups per compute unit), so that one size serves every
+  // selection kind of the same layout
   const uint64_t ws_groups = std::min<uint64_t>(n_seg, std::max<uint64_t>(1, (uint64_t)cus * 4 / p.P));
-  p.ws_words = (p.P > 1) ? ws_groups * group_mem_words(p.P) : 0;
+  p.ws_words = (p.P > 1) ? ws_groups * grp_mem_words(p.P) : 0;
   return p;
 }
 
 hipError_t launch_topk(int sel, int dt, const SegPlan& plan, const TopkArgs& args, hipStream_t st) {
-  const void* fn = pick(sel, dt, plan.nt, plan.vpt);
+  const void* fn = pick(sel, dt, plan.nt == WAVE, plan.vpt);
   if (!fn) return hipErrorInvalidValue;
   TopkArgs a = args;
   a.P = plan.P;

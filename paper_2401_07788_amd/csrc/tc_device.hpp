@@ -248,7 +248,9 @@ __device__ __forceinline__ float wave_max(float x) { return wave_minmax<true>(x)
 
 // ------------------------------------------------------- workgroup helpers
 // scratch must hold NT/64 + 1 words of LDS.  All threads of the workgroup
-// must call these (they contain barriers).
+// must call these (they contain barriers).  Wave totals go through LDS once;
+// every wave then adds the totals of the waves before it itself, so there is
+// one LDS round trip between the two barriers and no serial chain.
 template <int NT>
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratch, uint32_t& total) {
   constexpr int NW = NT / WAVE;
@@ -260,17 +262,16 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratc
   } else {
     if (lane_id() == WAVE - 1) scratch[w] = incl;
     __syncthreads();
-    if (threadIdx.x == 0) {
-      uint32_t acc = 0;
+    uint32_t pre = 0, tot = 0;
 #pragma unroll
-      for (int i = 0; i < NW; ++i) { uint32_t t = scratch[i]; scratch[i] = acc; acc += t; }
-      scratch[NW] = acc;
+    for (int i = 0; i < NW; ++i) {
+      const uint32_t x = scratch[i];
+      pre += (i < w) ? x : 0u;
+      tot += x;
     }
+    total = tot;
     __syncthreads();
-    uint32_t r = scratch[w] + incl - v;
-    total = scratch[NW];
-    __syncthreads();
-    return r;
+    return pre + incl - v;
   }
 }
 

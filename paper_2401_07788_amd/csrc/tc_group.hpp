@@ -1,0 +1,551 @@
+// tc_group.hpp -- exact TopK threshold for a segment spread over P
+// workgroups whose values stay in registers (the group engine).
+//
+// TopK (Sec. 2.3 of the paper) keeps the k entries of largest magnitude.  The
+// magnitude is the 31-bit key of mag_key(); the k-th largest key T and the
+// tie quota r = k - #(key > T) define the kept set: key > T, or key == T and
+// the entry is among the r lowest-index ties.
+//
+// Layout: workgroup `part` of a group owns the chunk [part*CH, part*CH + CH)
+// of its segment; thread t holds R runs of E consecutive elements, run j at
+// offset (j*NT + t)*E of the chunk (striped, so that every load and store
+// instruction of a wavefront covers 1 KiB of contiguous memory).
+//
+// Two cross-workgroup exchanges per segment in the common case:
+//   A. every workgroup adds its 4096-bin histogram of key bits 30..19 into
+//      the group's histogram.  It also guesses, from its own keys, the bin
+//      that holds the k-th largest key and adds 16 finer counts (bits 18..15)
+//      for that bin and its two neighbours.  After the barrier, one read of
+//      the merged counts gives the bin b1 and, when every workgroup's guess
+//      covered b1, the 16-bit prefix of T.
+//   B. every workgroup publishes a record: its count of keys above that
+//      prefix and the keys that share it (a few per workgroup, carried
+//      inline).  After the barrier each workgroup reads all records in one
+//      round trip and finds T, the tie quota and what precedes it by itself.
+// Otherwise (a guess missed, or too many keys share the prefix) the group
+// goes on with 8-bit digit passes, each merged through device memory, and a
+// last pass that publishes per-workgroup counts: exact for any input.
+#pragma once
+
+#include "tc_select.hpp"
+
+namespace tc {
+
+constexpr int GRP_NT = 512;
+constexpr uint32_t GRP_MAX_P = 1024;      // workgroups per segment the engine supports
+constexpr uint32_t REC_W = 64;            // words per record: above, count, inline keys
+constexpr uint32_t REC_KEYS = REC_W - 2;
+constexpr uint32_t FINE_SLOTS = 256;      // fine counts kept for bins b1 mod 256
+constexpr uint32_t DIG_BINS = 256;        // 8-bit digits of the fallback passes
+constexpr uint32_t DIG_ROWS = DIG_BINS + 1;   // per-workgroup slot: bins + larger-prefix count
+constexpr uint32_t REC_P_MAX = 64;        // records of at most this many workgroups are read at once
+
+// candidate keys the LDS list holds (records of up to 64 workgroups)
+__host__ __device__ constexpr uint32_t grp_local_cap(uint32_t CH) { return CH > 4096u ? CH : 4096u; }
+
+// Device memory owned by one group (inside the caller's workspace; zero on
+// entry and left zero on exit):
+//   ctl[64]               [0] barrier arrivals (monotone during a launch), [1] exits
+//   hist1[2][4096]        first-digit histograms, by segment parity
+//   fine[2][256][16]      bits 18..15 of the keys in guessed bins, by bin mod 256
+//   cov[2][256]           guesses per bin mod 256: count + (bin >> 8) << 16
+//   hist2[2][256]         8-bit digit passes (fallback)
+//   rec[P][64]            exchange B records
+//   slots[257][pitch]     last digit per workgroup + larger-prefix counts (fallback)
+struct GrpMem {
+  uint32_t* ctl;
+  uint32_t* hist1;
+  uint32_t* fine;
+  uint32_t* cov;
+  uint32_t* hist2;
+  uint32_t* rec;
+  uint32_t* slots;
+};
+
+__host__ __device__ constexpr uint64_t grp_mem_words(uint32_t P) {
+  return 64u + 2u * HIST_BINS + 2u * FINE_SLOTS * 16u + 2u * FINE_SLOTS + 2u * DIG_BINS + (uint64_t)P * REC_W +
+         (uint64_t)DIG_ROWS * slot_pitch(P);
+}
+
+__device__ __forceinline__ GrpMem grp_mem(uint32_t* ws, uint32_t group, uint32_t P) {
+  uint32_t* b = ws + (uint64_t)group * grp_mem_words(P);
+  GrpMem g;
+  g.ctl = b;
+  g.hist1 = b + 64;
+  g.fine = g.hist1 + 2 * HIST_BINS;
+  g.cov = g.fine + 2 * FINE_SLOTS * 16;
+  g.hist2 = g.cov + 2 * FINE_SLOTS;
+  g.rec = g.hist2 + 2 * DIG_BINS;                 // 16-byte aligned: ws is, and every piece above is
+  g.slots = g.rec + (uint64_t)P * REC_W;
+  return g;
+}
+
+// Barrier among the P workgroups of a group: arrivals are counted in one
+// word that only grows during a launch, so the n-th barrier waits for n*P
+// arrivals and nobody has to reset anything in flight.  Each wave's device-
+// scope stores and atomics complete before its workgroup arrives.  The wait
+// is bounded (co-residency violated): it then raises KERR_TIMEOUT and
+// returns.
+__device__ __forceinline__ void group_sync(uint32_t* ctr, uint32_t target) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t spins = 0;
+    while (ld_agent(ctr) < target) {
+      __builtin_amdgcn_s_sleep(1);
+      ++spins;
+      if ((spins & 1023u) == 0u &&
+          (__hip_atomic_load(&g_kernel_errors, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & KERR_TIMEOUT))
+        break;
+      if (spins > BARRIER_SPIN_LIMIT) { raise_error(KERR_TIMEOUT); break; }
+    }
+  }
+  __syncthreads();
+}
+
+// Exclusive scans of R values per thread across the workgroup in one pass;
+// tot[j] = workgroup total of value j.  scratch: R * NT/64 words.
+template <int NT, int R>
+__device__ __forceinline__ void block_excl_scan_multi(const uint32_t (&v)[R], uint32_t (&ex)[R],
+                                                      uint32_t (&tot)[R], uint32_t* scratch) {
+  constexpr int NW = NT / WAVE;
+  const int w = (int)threadIdx.x / WAVE;
+  uint32_t incl[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) incl[j] = wave_incl_scan(v[j]);
+  if (lane_id() == WAVE - 1) {
+#pragma unroll
+    for (int j = 0; j < R; ++j) scratch[j * NW + w] = incl[j];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    uint32_t pre = 0, t = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const uint32_t x = scratch[j * NW + i];
+      pre += (i < w) ? x : 0u;
+      t += x;
+    }
+    ex[j] = pre + incl[j] - v[j];
+    tot[j] = t;
+  }
+  __syncthreads();
+}
+
+// LDS of the group engine's selection
+template <uint32_t CLOC>
+struct GrpSelShared {
+  uint32_t hist[HIST_BINS + WAVE];   // histograms (the last WAVE words: per-lane dummies)
+  uint32_t cand[CLOC];               // exchange B records of all workgroups
+};
+
+struct GrpSmall {
+  uint32_t scratch[8 * (GRP_NT / WAVE)];
+  uint32_t found[2];
+  uint32_t red[DIG_BINS];            // one digit's counts, copies summed
+  uint32_t fwin[3 * 16 + WAVE];      // this workgroup's fine counts, then the merged ones
+  uint32_t misc[8];
+};
+
+// Per-workgroup state carried across the segments a group handles.
+struct GrpState {
+  uint32_t nbar = 0;       // barriers passed (equal in all workgroups of the group)
+  uint32_t iter = 0;       // segments handled
+  bool used_slots = false; // the fallback ran (its words must be cleared on exit)
+};
+
+// Histogram copies for digit counts: values that repeat (differences of
+// 16-bit numbers often do) would make the lanes of one wave hit one LDS
+// address; with a copy per lane group (lane mod CP), spaced by an odd stride
+// so that one bin's copies sit in distinct banks, at most 64/CP lanes meet.
+// Word HS-1 of each copy absorbs lanes with nothing to count.
+constexpr int DIG_CP = 16, DIG_HS = 257;
+static_assert(DIG_CP * DIG_HS <= HIST_BINS + WAVE, "histogram copies fit the selection histogram");
+
+template <int NT>
+__device__ __forceinline__ void dig_zero(uint32_t* hist) {
+  for (int i = (int)threadIdx.x; i < DIG_CP * DIG_HS; i += NT) hist[i] = 0u;
+}
+__device__ __forceinline__ void dig_add(uint32_t* hist, bool m, uint32_t digit) {
+  const uint32_t base = (uint32_t)(lane_id() & (DIG_CP - 1)) * DIG_HS;
+  atomicAdd(&hist[base + (m ? digit : (uint32_t)(DIG_HS - 1))], 1u);
+}
+// copies summed into red[0..NB); call after a barrier that follows the adds
+template <int NT, int NB>
+__device__ __forceinline__ void dig_reduce(const uint32_t* hist, uint32_t* red) {
+  const int t = (int)threadIdx.x;
+  if (t < NB) {
+    uint32_t s = 0;
+#pragma unroll
+    for (int c = 0; c < DIG_CP; ++c) s += hist[c * DIG_HS + t];
+    red[t] = s;
+  }
+}
+
+// After the second barrier of a segment every workgroup has read the
+// exchange A words of its parity: each clears a slice of them.
+__device__ __forceinline__ void grp_clear_a(const GrpMem& g, uint32_t par, uint32_t P, uint32_t part) {
+  const uint32_t n1 = HIST_BINS, n2 = FINE_SLOTS * 16, n3 = FINE_SLOTS;
+  uint32_t* h1 = g.hist1 + par * n1;
+  uint32_t* f1 = g.fine + par * n2;
+  uint32_t* c1 = g.cov + par * n3;
+  const uint32_t step = P * GRP_NT;
+  for (uint32_t i = part * GRP_NT + threadIdx.x; i < n1 + n2 + n3; i += step) {
+    uint32_t* p = (i < n1) ? h1 + i : (i < n1 + n2) ? f1 + (i - n1) : c1 + (i - n1 - n2);
+    st_agent(p, 0u);
+  }
+}
+
+// Exact threshold of one segment held by the P workgroups of a group (this
+// one is `part`), k >= 1.  v[j][i] is element i of this thread's run j; with
+// FULL every element is valid, else run j holds n[j] valid elements.  n_wg:
+// valid elements of this workgroup; L: of the segment.
+template <int NT, int R, int E, uint32_t CH, bool FULL>
+__device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const int (&n)[R], uint32_t k, uint32_t n_wg,
+                                                uint64_t L, uint32_t P, uint32_t part, const GrpMem& g,
+                                                GrpSelShared<grp_local_cap(CH)>& sh, GrpSmall& sm, GrpState& gs) {
+  constexpr uint32_t CLOC = grp_local_cap(CH);
+  const int t = (int)threadIdx.x;
+  const uint32_t dummy = HIST_BINS + (uint32_t)lane_id();
+  auto ok = [&](int j, int i) { return FULL || i < n[j]; };
+  auto key = [&](int j, int i) { return mag_key(v[j][i]); };
+  SelResult res;
+  const uint32_t par = gs.iter & 1u;
+
+  // ---- A: bits 30..19 of every key; exact zeros (common after a ReLU) are
+  // counted in registers and added once per wave, off one hot bin
+  zero_lds<NT>(sh.hist, HIST_BINS);
+  __syncthreads();
+  uint32_t zc = 0;
+#pragma unroll
+  for (int j = 0; j < R; ++j)
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      const uint32_t kk = key(j, i);
+      const bool live = ok(j, i) && kk != 0u;
+      zc += (ok(j, i) && kk == 0u) ? 1u : 0u;
+      atomicAdd(&sh.hist[live ? (kk >> 19) : dummy], 1u);
+    }
+  {
+    const uint32_t zs = wave_sum(zc);
+    if (lane_id() == 0 && zs) atomicAdd(&sh.hist[0], zs);
+  }
+  __syncthreads();
+
+  uint32_t prefix, pbits, need;          // known leading bits of T, keys still to place
+  bool fine = false;
+  if (P > 1) {
+    // this workgroup's guess: its own bin at the same rank fraction
+    const uint32_t need_loc = (uint32_t)min<uint64_t>(max<uint64_t>(((uint64_t)k * n_wg + L - 1) / L, 1), n_wg);
+    find_bin<NT, HIST_BINS>(sh.hist, need_loc, sm.scratch, sm.found);
+    const uint32_t bh = sm.found[0];
+    const uint32_t lo = bh > 0u ? bh - 1u : 0u, hi = min(bh + 1u, (uint32_t)HIST_BINS - 1u);
+    // bits 18..15 of the (non-zero) keys in bins lo..hi
+    if (t < 3 * 16) sm.fwin[t] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < R; ++j)
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        const uint32_t kk = key(j, i), b = kk >> 19;
+        const bool in = ok(j, i) && kk != 0u && b >= lo && b <= hi;
+        atomicAdd(&sm.fwin[in ? (b - lo) * 16u + ((kk >> 15) & 15u) : 3u * 16u + (uint32_t)lane_id()], 1u);
+      }
+    __syncthreads();
+    if (t == 0 && lo == 0u) {
+      // bin 0 also holds the exact zeros, whose bits 18..15 are 0
+      uint32_t nz = 0;
+      for (int q = 0; q < 16; ++q) nz += sm.fwin[q];
+      sm.fwin[0] += sh.hist[0] - nz;
+    }
+    __syncthreads();
+    // merge into the group's counts
+    uint32_t* h1 = g.hist1 + par * HIST_BINS;
+    uint32_t* f1 = g.fine + par * FINE_SLOTS * 16;
+    uint32_t* c1 = g.cov + par * FINE_SLOTS;
+    for (int b = t; b < HIST_BINS; b += NT)
+      if (sh.hist[b]) add_agent(&h1[b], sh.hist[b]);
+    if (t < 3 * 16) {
+      const uint32_t b = lo + (uint32_t)t / 16u;
+      if (b <= hi && sm.fwin[t]) add_agent(&f1[(b & (FINE_SLOTS - 1)) * 16u + (uint32_t)t % 16u], sm.fwin[t]);
+    } else if (t < 3 * 16 + 3) {
+      const uint32_t b = lo + (uint32_t)(t - 3 * 16);
+      if (b <= hi) add_agent(&c1[b & (FINE_SLOTS - 1)], 1u + ((b >> 8) << 16));
+    }
+    group_sync(g.ctl, P * ++gs.nbar);
+    // one round trip: the merged histogram, the fine counts and coverage of this window
+    uint32_t fw = 0;
+    if (t < 3 * 16 + 3) {
+      const uint32_t b = lo + (uint32_t)(t < 48 ? t / 16 : t - 48);
+      if (b <= hi) fw = ld_agent(t < 48 ? &f1[(b & (FINE_SLOTS - 1)) * 16u + (uint32_t)t % 16u] : &c1[b & (FINE_SLOTS - 1)]);
+    }
+    find_bin_global<NT>(h1, k, sm.scratch, sm.found);   // its barriers also publish nothing else
+    const uint32_t b1 = sm.found[0];
+    need = k - sm.found[1];
+    if (t < 3 * 16 + 3) sm.fwin[t] = fw;
+    __syncthreads();
+    fine = b1 >= lo && b1 <= hi && sm.fwin[48 + (b1 - lo)] == P + ((P * (b1 >> 8)) << 16);
+    prefix = b1;
+    pbits = 12;
+    if (fine) {
+      // bits 18..15 of T from the merged fine counts of b1 (every thread alike)
+      const uint32_t* f = &sm.fwin[(b1 - lo) * 16u];
+      uint32_t acc = 0, f1v = 16;
+      for (int s = 15; s >= 0; --s) {
+        const uint32_t c = f[s];
+        if (acc < need && need <= acc + c) { f1v = (uint32_t)s; break; }
+        acc += c;
+      }
+      if (f1v < 16) {
+        prefix = (b1 << 4) | f1v;
+        pbits = 16;
+        need -= acc;
+      } else {
+        fine = false;   // inconsistent counts: never expected; take the exact passes
+      }
+    }
+    __syncthreads();
+  } else {
+    find_bin<NT, HIST_BINS>(sh.hist, k, sm.scratch, sm.found);
+    prefix = sm.found[0];
+    pbits = 12;
+    need = k - sm.found[1];
+    __syncthreads();
+  }
+
+  // ---- B: records (fine mode): keys above the 16-bit prefix, and the keys
+  // that share it, inline
+  const uint32_t rshift = 31u - pbits;               // key bits below the prefix
+  bool done = false, cleared = false;
+  static_assert(REC_P_MAX * REC_W <= CLOC, "the records of a group fit the LDS list");
+  if (fine && P <= REC_P_MAX) {
+    uint32_t abv = 0, cnt = 0;
+#pragma unroll
+    for (int j = 0; j < R; ++j)
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        const uint32_t kp = key(j, i) >> rshift;
+        abv += (ok(j, i) && kp > prefix) ? 1u : 0u;
+        cnt += (ok(j, i) && kp == prefix) ? 1u : 0u;
+      }
+    uint32_t cv[2] = {cnt, abv}, cx[2], ct[2];
+    block_excl_scan_multi<NT, 2>(cv, cx, ct, sm.scratch);
+    uint32_t* my = g.rec + (uint64_t)part * REC_W;
+    if (cnt) {
+      uint32_t q = cx[0];
+#pragma unroll
+      for (int j = 0; j < R; ++j)
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+          const uint32_t kk = key(j, i);
+          if (ok(j, i) && (kk >> rshift) == prefix) {
+            if (q < REC_KEYS) st_agent(&my[2 + q], kk);
+            ++q;
+          }
+        }
+    }
+    if (t == 0) { st_agent(&my[0], ct[1]); st_agent(&my[1], ct[0]); }
+    group_sync(g.ctl, P * ++gs.nbar);
+    grp_clear_a(g, par, P, part);
+    cleared = true;
+    // all records, one 16-byte load per thread and pass
+    for (uint32_t q = (uint32_t)t; q < P * (REC_W / 4); q += NT) {
+      const uint64_t* src = reinterpret_cast<const uint64_t*>(g.rec) + 2ull * q;
+      const uint64_t w0 = ld_agent64(src), w1 = ld_agent64(src + 1);
+      sh.cand[4 * q] = (uint32_t)w0;
+      sh.cand[4 * q + 1] = (uint32_t)(w0 >> 32);
+      sh.cand[4 * q + 2] = (uint32_t)w1;
+      sh.cand[4 * q + 3] = (uint32_t)(w1 >> 32);
+    }
+    __syncthreads();
+    // totals: keys above the prefix before this workgroup and overall,
+    // records that did not fit
+    uint32_t abv_before = 0, abv_all = 0, bad = 0;
+    for (uint32_t w0 = 0; w0 < P; w0 += NT) {
+      const uint32_t w = w0 + (uint32_t)t;
+      const uint32_t aw = (w < P) ? sh.cand[w * REC_W] : 0u, cw = (w < P) ? sh.cand[w * REC_W + 1] : 0u;
+      uint32_t rv[3] = {(w < part) ? aw : 0u, aw, (cw > REC_KEYS) ? 1u : 0u}, rx[3], rt[3];
+      block_excl_scan_multi<NT, 3>(rv, rx, rt, sm.scratch);
+      abv_before += rt[0];
+      abv_all += rt[1];
+      bad += rt[2];
+    }
+    if (bad == 0) {
+      // local select over the inline keys: the remaining 15 bits as digits
+      // of 8 and 7 bits; slot s of the records is key s%64 - 2 of workgroup s/64
+      const uint32_t need_b = k - abv_all;
+      constexpr int SPT = (int)(REC_P_MAX * REC_W / NT);
+      uint32_t c[SPT];
+      bool lower[SPT];
+#pragma unroll
+      for (int u = 0; u < SPT; ++u) {
+        const uint32_t sl = (uint32_t)(u * NT + t), w = sl / REC_W, i = sl % REC_W;
+        const bool valid = w < P && i >= 2u && i - 2u < sh.cand[w * REC_W + 1];
+        c[u] = valid ? sh.cand[sl] : ~0u;           // ~0u matches no prefix
+        lower[u] = valid && w < part;
+      }
+      dig_zero<NT>(sh.hist);
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < SPT; ++u) dig_add(sh.hist, (c[u] >> 15) == prefix, (c[u] >> 7) & 0xFFu);
+      __syncthreads();
+      dig_reduce<NT, 256>(sh.hist, sm.red);
+      __syncthreads();
+      find_bin<NT, 256>(sm.red, need_b, sm.scratch, sm.found);
+      const uint32_t p24 = (prefix << 8) | sm.found[0];
+      const uint32_t need_c = need_b - sm.found[1];
+      dig_zero<NT>(sh.hist);
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < SPT; ++u) dig_add(sh.hist, (c[u] >> 7) == p24, c[u] & 0x7Fu);
+      __syncthreads();
+      dig_reduce<NT, 128>(sh.hist, sm.red);
+      __syncthreads();
+      find_bin<NT, 128>(sm.red, need_c, sm.scratch, sm.found);
+      res.T = (p24 << 7) | sm.found[0];
+      res.r = need_c - sm.found[1];
+      // larger keys and ties in lower workgroups' records; both below 2^16
+      uint32_t ge = 0;
+#pragma unroll
+      for (int u = 0; u < SPT; ++u)
+        ge += (lower[u] && c[u] > res.T) ? 1u : ((lower[u] && c[u] == res.T) ? 0x10000u : 0u);
+      const uint32_t sge = block_sum<NT>(ge, sm.scratch);
+      res.gt_before = abv_before + (sge & 0xFFFFu);
+      res.eq_before = sge >> 16;
+      done = true;
+    }
+  }
+  if (done) return res;
+
+  // ---- fallback: 8-bit digit passes merged through device memory, then a
+  // last digit of at most 8 bits counted per workgroup
+  gs.used_slots = gs.used_slots || P > 1;
+  for (int pass = 0; 31u - pbits > 8u; ++pass) {
+    const uint32_t sh8 = 31u - pbits - 8u;         // the digit's lowest bit
+    dig_zero<NT>(sh.hist);
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < R; ++j)
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        const uint32_t kk = key(j, i);
+        dig_add(sh.hist, ok(j, i) && (kk >> (sh8 + 8u)) == prefix, (kk >> sh8) & 0xFFu);
+      }
+    __syncthreads();
+    dig_reduce<NT, 256>(sh.hist, sm.red);
+    __syncthreads();
+    if (P > 1) {
+      uint32_t* h2 = g.hist2 + (pass & 1) * DIG_BINS;
+      if (t < (int)DIG_BINS && sm.red[t]) add_agent(&h2[t], sm.red[t]);
+      group_sync(g.ctl, P * ++gs.nbar);
+      if (t < (int)DIG_BINS) sm.red[t] = ld_agent(&h2[t]);
+      if (!cleared) { grp_clear_a(g, par, P, part); cleared = true; }
+      __syncthreads();
+    }
+    find_bin<NT, 256>(sm.red, need, sm.scratch, sm.found);
+    prefix = (prefix << 8) | sm.found[0];
+    pbits += 8;
+    need -= sm.found[1];
+    __syncthreads();
+  }
+  // last digit: per-workgroup counts, published as transposed slots
+  const uint32_t lb = 31u - pbits;                  // 1..8 bits
+  const uint32_t nbl = 1u << lb;
+  dig_zero<NT>(sh.hist);
+  __syncthreads();
+  uint32_t gtp = 0;   // keys with a larger prefix
+#pragma unroll
+  for (int j = 0; j < R; ++j)
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      const uint32_t kk = key(j, i);
+      dig_add(sh.hist, ok(j, i) && (kk >> lb) == prefix, kk & (nbl - 1u));
+      gtp += (ok(j, i) && (kk >> lb) > prefix) ? 1u : 0u;
+    }
+  const uint32_t gtp_wg = block_sum<NT>(gtp, sm.scratch);   // contains barriers
+  dig_reduce<NT, 256>(sh.hist, sm.red);
+  __syncthreads();
+  uint32_t* hall = sh.cand;                 // [256] whole segment
+  uint32_t* hbef = sh.cand + DIG_BINS;      // [256] lower workgroups
+  uint32_t gtpb = 0;
+  if (P > 1) {
+    const uint32_t pitch = slot_pitch(P);
+    if (t < (int)DIG_BINS) st_agent(&g.slots[(uint64_t)t * pitch + part], sm.red[t]);
+    if (t == 0) st_agent(&g.slots[(uint64_t)DIG_BINS * pitch + part], gtp_wg);
+    group_sync(g.ctl, P * ++gs.nbar);
+    // every digit pass has been read: clear this workgroup's share of them
+    for (int b = (int)(part * NT) + t; b < (int)(2 * DIG_BINS); b += (int)(P * NT)) st_agent(&g.hist2[b], 0u);
+    // row `bin` of the slots holds that bin's count in every workgroup; two
+    // thread sets split each row and read it in 8-byte pairs
+    constexpr int SETS = NT / (int)DIG_BINS;
+    const int bin = t % (int)DIG_BINS, set = t / (int)DIG_BINS;
+    const uint32_t per = pitch / SETS;          // even: pitch is a multiple of 8
+    const uint64_t* row = reinterpret_cast<const uint64_t*>(g.slots + (uint64_t)bin * pitch + set * per);
+    uint32_t a_all = 0, a_bef = 0;
+    for (uint32_t q = 0; q < per / 2; ++q) {
+      const uint64_t pr = ld_agent64(row + q);
+      const uint32_t jw = set * per + 2 * q;
+      const uint32_t lo = (uint32_t)pr, hi = (uint32_t)(pr >> 32);
+      a_all += lo + hi;
+      a_bef += (jw < part ? lo : 0u) + (jw + 1 < part ? hi : 0u);
+    }
+    uint32_t g_own = 0;
+    for (uint32_t q = (uint32_t)t; q < part; q += NT) g_own += ld_agent(g.slots + (uint64_t)DIG_BINS * pitch + q);
+    uint32_t* red = sh.hist;   // [SETS][2][256] partial sums (free now)
+    red[(set * 2) * DIG_BINS + bin] = a_all;
+    red[(set * 2 + 1) * DIG_BINS + bin] = a_bef;
+    __syncthreads();
+    if (t < (int)DIG_BINS) {
+      uint32_t s_all = 0, s_bef = 0;
+#pragma unroll
+      for (int q = 0; q < SETS; ++q) { s_all += red[(q * 2) * DIG_BINS + t]; s_bef += red[(q * 2 + 1) * DIG_BINS + t]; }
+      hall[t] = s_all;
+      hbef[t] = s_bef;
+    }
+    gtpb = block_sum<NT>(g_own, sm.scratch);
+  } else {
+    if (t < (int)DIG_BINS) { hall[t] = sm.red[t]; hbef[t] = 0u; }
+  }
+  __syncthreads();
+  find_bin<NT, 256>(hall, need, sm.scratch, sm.found);
+  const uint32_t d = sm.found[0];
+  res.T = (prefix << lb) | d;
+  res.r = need - sm.found[1];
+  const uint32_t gt_digit = (t < (int)DIG_BINS && (uint32_t)t > d) ? hbef[t] : 0u;
+  res.gt_before = gtpb + block_sum<NT>(gt_digit, sm.scratch);
+  res.eq_before = hbef[d];
+  __syncthreads();
+  return res;
+}
+
+// Leave the group's workspace zero: every workgroup counts itself out; the
+// last one (all others have finished reading) clears the barrier words, the
+// records and, if the fallback ran, the slots (everything else is cleared in
+// flight).  Nobody waits here.
+template <int NT>
+__device__ __forceinline__ void grp_exit(const GrpMem& g, uint32_t P, const GrpState& gs) {
+  __shared__ uint32_t last_out;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t prev = __hip_atomic_fetch_add(g.ctl + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    last_out = (prev == P - 1) ? 1u : 0u;
+  }
+  __syncthreads();
+  if (!last_out) return;
+  const uint64_t nrec = (uint64_t)P * REC_W;
+  for (uint64_t i = threadIdx.x; i < nrec; i += NT) st_agent(&g.rec[i], 0u);
+  if (gs.used_slots) {
+    const uint64_t n = (uint64_t)DIG_ROWS * slot_pitch(P);
+    for (uint64_t i = threadIdx.x; i < n; i += NT) st_agent(&g.slots[i], 0u);
+  }
+  if (threadIdx.x == 0) {
+    st_agent(g.ctl, 0u);
+    st_agent(g.ctl + 1, 0u);
+  }
+  __syncthreads();
+}
+
+}  // namespace tc

@@ -5,15 +5,10 @@
 // key T and the tie quota r = k - #(key > T) define the kept set:
 //   key > T, or key == T and the entry is among the r lowest-index ties.
 //
-// Two strategies, both exact:
-//  * radix_select: three digit passes over the keys (bits 30..19, 18..7,
-//    6..0) with LDS histograms.  A segment may be spread over P workgroups;
-//    the first two passes merge their histograms with device-scope atomics,
-//    the last pass publishes per-workgroup histograms ("slots") so that every
-//    workgroup also learns how many larger keys and ties precede it.  Three
-//    cross-workgroup barriers per segment.
-//  * bitwise_select: one wavefront owns a whole short segment (a token row)
-//    and fixes T bit by bit, counting with ballots; no LDS, no barriers.
+// Shared pieces: bin search over histograms (in LDS or merged in device
+// memory), and the one-wavefront strategy for short segments (a token row),
+// which fixes T bit by bit counting with ballots: no LDS, no barriers.  The
+// several-workgroup strategy is in tc_group.hpp.
 #pragma once
 
 #include "tc_device.hpp"
@@ -23,44 +18,10 @@ namespace tc {
 constexpr int HIST_BINS = 4096;   // 12-bit digits for the first two passes
 constexpr int LAST_BINS = 128;    // 7-bit digit for the last pass
 constexpr int SLOT_ROWS = LAST_BINS + 1;   // per-workgroup slot: 128 bins + larger-prefix count
-constexpr int CAND_CAP = 256;     // per-wave list of the keys inside the first-pass bin
 
 // slot rows are laid out transposed, [row][workgroup], each row padded to a
 // multiple of 8 workgroups so that readers can take them in 8-byte pairs
 __host__ __device__ constexpr uint32_t slot_pitch(uint32_t P) { return (P + 7u) & ~7u; }
-
-// device memory owned by one group of P workgroups (inside the caller's
-// workspace, zero-filled before first use and left zero-filled on exit)
-struct GroupMem {
-  uint32_t* bar;     // [3] barrier count / sense / exit count
-  uint32_t* hist1;   // [HIST_BINS]
-  uint32_t* hist2;   // [HIST_BINS]
-  uint32_t* slots;   // [SLOT_ROWS][slot_pitch(P)]
-};
-
-// words of workspace per group (barrier padded to 64 words)
-__host__ __device__ constexpr uint64_t group_mem_words(uint32_t P) {
-  return 64u + 2u * HIST_BINS + (uint64_t)SLOT_ROWS * slot_pitch(P);
-}
-__host__ __device__ constexpr uint64_t slot_words(uint32_t P) { return (uint64_t)SLOT_ROWS * slot_pitch(P); }
-
-__device__ __forceinline__ GroupMem group_mem(uint32_t* ws, uint32_t group, uint32_t P) {
-  uint32_t* base = ws + (uint64_t)group * group_mem_words(P);
-  GroupMem g;
-  g.bar = base;
-  g.hist1 = base + 64;
-  g.hist2 = base + 64 + HIST_BINS;
-  g.slots = base + 64 + 2 * HIST_BINS;
-  return g;
-}
-
-template <int NT>
-struct SelShared {
-  uint32_t hist[HIST_BINS];
-  uint32_t cand[(NT / WAVE) * CAND_CAP];
-  uint32_t scratch[NT / WAVE + 2];
-  uint32_t found[2];          // bin, count above it
-};
 
 __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
@@ -128,186 +89,9 @@ __device__ __forceinline__ void find_bin_global(const uint32_t* gh, uint32_t nee
   find_bin_loc<NT, BPT>(loc, need, scratch, found);
 }
 
-// Count this workgroup's keys that match `prefix` under `pmask` into LDS bins
-// by `digit = (key >> shift) & dmask`.  Zero keys (exact zeros are common in
-// ReLU outputs) are counted in registers and added once per wave, which keeps
-// them off a single hot LDS address.
-template <int NT, int VPT>
-__device__ __forceinline__ void count_digits(const uint32_t (&key)[VPT], int nv, uint32_t pshift,
-                                             uint32_t prefix, uint32_t shift, uint32_t dmask,
-                                             uint32_t* hist) {
-  uint32_t zc = 0;
-#pragma unroll
-  for (int v = 0; v < VPT; ++v) {
-    if (v < nv) {
-      const uint32_t kk = key[v];
-      if ((kk >> pshift) == prefix) {
-        if (kk == 0u) ++zc;
-        else atomicAdd(&hist[(kk >> shift) & dmask], 1u);
-      }
-    }
-  }
-  const uint32_t zs = wave_sum(zc);
-  if (lane_id() == 0 && zs) atomicAdd(&hist[0], zs);
-}
-
 template <int NT>
 __device__ __forceinline__ void zero_lds(uint32_t* h, int n) {
   for (int b = (int)threadIdx.x; b < n; b += NT) h[b] = 0u;
-}
-
-// Exact threshold for one segment spread over P workgroups (this one is
-// `part`), with k >= 1 entries to keep out of the segment's valid keys.
-template <int NT, int VPT>
-__device__ SelResult radix_select(const uint32_t (&key)[VPT], int nv, uint32_t k, uint32_t P,
-                                  uint32_t part, const GroupMem& g, SelShared<NT>& sh) {
-  static_assert(NT >= 2 * LAST_BINS, "the slot gather splits the workgroup over the last-digit bins");
-  SelResult res;
-  const int t = (int)threadIdx.x;
-  // ---- pass 1: bits 30..19 of all keys
-  zero_lds<NT>(sh.hist, HIST_BINS);
-  __syncthreads();
-  count_digits<NT, VPT>(key, nv, 31, 0u, 19, 0xFFFu, sh.hist);
-  __syncthreads();
-  if (P > 1) {
-    for (int b = t; b < HIST_BINS; b += NT)
-      if (sh.hist[b]) add_agent(&g.hist1[b], sh.hist[b]);
-    group_barrier(g.bar, P);
-    find_bin_global<NT>(g.hist1, k, sh.scratch, sh.found);
-  } else {
-    find_bin<NT, HIST_BINS>(sh.hist, k, sh.scratch, sh.found);
-  }
-  const uint32_t b1 = sh.found[0];
-  const uint32_t need2 = k - sh.found[1];
-  __syncthreads();
-
-  // ---- the keys inside bin b1 go to a per-wave list in LDS (ballot
-  // compaction), so that the next two passes touch only them
-  const int w = t / WAVE;
-  uint32_t* cand = sh.cand + w * CAND_CAP;
-  uint32_t ccount = 0;   // wave-uniform
-  uint32_t gt1 = 0;      // keys above bin b1
-#pragma unroll
-  for (int v = 0; v < VPT; ++v) {
-    const bool valid = v < nv;
-    const uint32_t kk = key[v];
-    const bool in = valid && (kk >> 19) == b1;
-    gt1 += (valid && (kk >> 19) > b1) ? 1u : 0u;
-    const uint64_t bal = __ballot(in);
-    if (in) {
-      const uint32_t slot = ccount + lanes_below(bal);
-      if (slot < (uint32_t)CAND_CAP) cand[slot] = kk;
-    }
-    ccount += (uint32_t)__popcll(bal);
-  }
-  const bool listed = ccount <= (uint32_t)CAND_CAP;   // else this wave counts from registers
-
-  // ---- pass 2: bits 18..7 of keys whose bits 30..19 equal b1
-  zero_lds<NT>(sh.hist, HIST_BINS);
-  __syncthreads();
-  if (listed) {
-    for (uint32_t i = (uint32_t)lane_id(); i < ccount; i += WAVE) atomicAdd(&sh.hist[(cand[i] >> 7) & 0xFFFu], 1u);
-  } else {
-    count_digits<NT, VPT>(key, nv, 19, b1, 7, 0xFFFu, sh.hist);
-  }
-  __syncthreads();
-  if (P > 1) {
-    for (int b = t; b < HIST_BINS; b += NT)
-      if (sh.hist[b]) add_agent(&g.hist2[b], sh.hist[b]);
-    group_barrier(g.bar, P);
-    // every workgroup has read hist1 before arriving here: clear its share
-    for (int b = (int)(part * NT) + t; b < HIST_BINS; b += (int)(P * NT)) st_agent(&g.hist1[b], 0u);
-    find_bin_global<NT>(g.hist2, need2, sh.scratch, sh.found);
-  } else {
-    find_bin<NT, HIST_BINS>(sh.hist, need2, sh.scratch, sh.found);
-  }
-  const uint32_t b2 = sh.found[0];
-  const uint32_t need3 = need2 - sh.found[1];
-  const uint32_t p24 = (b1 << 12) | b2;
-  __syncthreads();
-
-  // ---- pass 3: bits 6..0 of keys whose bits 30..7 equal p24, and the count
-  // of keys with a larger 24-bit prefix
-  zero_lds<NT>(sh.hist, LAST_BINS);
-  __syncthreads();
-  uint32_t gtp = 0;
-  if (listed) {
-    for (uint32_t i = (uint32_t)lane_id(); i < ccount; i += WAVE) {
-      const uint32_t kk = cand[i];
-      if ((kk >> 7) == p24) atomicAdd(&sh.hist[kk & 0x7Fu], 1u);
-      gtp += ((kk >> 7) > p24) ? 1u : 0u;
-    }
-    gtp += gt1;
-  } else {
-    count_digits<NT, VPT>(key, nv, 7, p24, 0, 0x7Fu, sh.hist);
-#pragma unroll
-    for (int v = 0; v < VPT; ++v)
-      if (v < nv && (key[v] >> 7) > p24) ++gtp;
-  }
-  const uint32_t gtp_wg = block_sum<NT>(gtp, sh.scratch);   // contains barriers
-  uint32_t* hall = sh.hist + HIST_BINS - 2 * LAST_BINS;     // [LAST_BINS] whole segment
-  uint32_t* hbef = sh.hist + HIST_BINS - LAST_BINS;         // [LAST_BINS] lower workgroups
-  uint32_t gtpb = 0;     // larger-prefix keys in lower workgroups
-  if (P > 1) {
-    const uint32_t pitch = slot_pitch(P);
-    for (int b = t; b < LAST_BINS; b += NT) st_agent(&g.slots[(uint64_t)b * pitch + part], sh.hist[b]);
-    if (t == 0) st_agent(&g.slots[(uint64_t)LAST_BINS * pitch + part], gtp_wg);
-    group_barrier(g.bar, P);
-    for (int b = (int)(part * NT) + t; b < HIST_BINS; b += (int)(P * NT)) st_agent(&g.hist2[b], 0u);
-    // gather: row `bin` holds the bin's count of every workgroup; NT/128
-    // thread sets split each row, reading it in 8-byte pairs (padding reads 0)
-    constexpr int SETS = NT / LAST_BINS;
-    const int bin = t % LAST_BINS, set = t / LAST_BINS;
-    const uint32_t per = pitch / SETS;          // even: pitch is a multiple of 8
-    const uint64_t* row = reinterpret_cast<const uint64_t*>(g.slots + (uint64_t)bin * pitch + set * per);
-    uint32_t a_all = 0, a_bef = 0;
-    for (uint32_t q = 0; q < per / 2; ++q) {
-      const uint64_t pr = ld_agent64(row + q);
-      const uint32_t j = set * per + 2 * q;
-      const uint32_t lo = (uint32_t)pr, hi = (uint32_t)(pr >> 32);
-      a_all += lo + hi;
-      a_bef += (j < part ? lo : 0u) + (j + 1 < part ? hi : 0u);
-    }
-    // larger-prefix counts of the lower workgroups, in pairs as well
-    uint32_t g_own = 0;
-    {
-      const uint64_t* grow = reinterpret_cast<const uint64_t*>(g.slots + (uint64_t)LAST_BINS * pitch);
-      for (uint32_t q = (uint32_t)t; 2 * q < part; q += NT) {
-        const uint64_t pr = ld_agent64(grow + q);
-        g_own += (uint32_t)pr + ((2 * q + 1 < part) ? (uint32_t)(pr >> 32) : 0u);
-      }
-    }
-    __syncthreads();
-    uint32_t* red = sh.hist;   // [SETS][2][LAST_BINS] partial sums (bins 0..1023, free now)
-    red[(set * 2) * LAST_BINS + bin] = a_all;
-    red[(set * 2 + 1) * LAST_BINS + bin] = a_bef;
-    __syncthreads();
-    if (t < LAST_BINS) {
-      uint32_t s_all = 0, s_bef = 0;
-#pragma unroll
-      for (int q = 0; q < SETS; ++q) { s_all += red[(q * 2) * LAST_BINS + t]; s_bef += red[(q * 2 + 1) * LAST_BINS + t]; }
-      hall[t] = s_all;
-      hbef[t] = s_bef;
-    }
-    gtpb = block_sum<NT>(g_own, sh.scratch);
-  } else {
-    if (t < LAST_BINS) { hall[t] = sh.hist[t]; hbef[t] = 0u; }
-  }
-  __syncthreads();
-  find_bin<NT, LAST_BINS>(hall, need3, sh.scratch, sh.found);
-  const uint32_t d3 = sh.found[0];
-  res.T = (p24 << 7) | d3;
-  res.r = need3 - sh.found[1];
-  if (P > 1) {
-    // keys > T before us: larger prefix, or same prefix with a larger last digit
-    const uint32_t gt_digit = (t < LAST_BINS && (uint32_t)t > d3) ? hbef[t] : 0u;
-    res.gt_before = gtpb + block_sum<NT>(gt_digit, sh.scratch);
-    res.eq_before = hbef[d3 & (LAST_BINS - 1)];
-  } else {
-    res.gt_before = 0u;
-    res.eq_before = 0u;
-  }
-  return res;
 }
 
 // Exact threshold for a segment held entirely by one wavefront (NT == 64).
