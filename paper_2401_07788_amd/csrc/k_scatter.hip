@@ -133,12 +133,67 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
   }
 }
 
+// The payload entries of a chunk, [j0, j1) of segment `seg`, loaded eight at
+// a time with 16-byte accesses aligned in the whole payload array (rows of
+// k entries need not be aligned), then applied to the chunk held in LDS:
+// buf[i - c0] = out(in(buf[i - c0]) + in(val)).  Entries outside [j0, j1) in
+// the aligned groups are skipped; an index outside the chunk is flagged.
+template <typename T, int NT>
+__device__ __forceinline__ void apply_entries(const ScatterArgs& a, uint64_t seg, uint64_t c0, uint64_t c1,
+                                              uint32_t j0, uint32_t j1, typename Elem<T>::raw* buf) {
+  using R = typename Elem<T>::raw;
+  static_assert(sizeof(R) == 2, "eight 16-bit values per 16-byte access");
+  const uint64_t J0 = seg * a.k + j0, J1 = seg * a.k + j1, total = a.n_seg * a.k;
+  const uint64_t A0 = J0 & ~7ull;
+  const uint32_t ng = (uint32_t)((J1 - A0 + 7) / 8);
+  for (uint32_t gq = threadIdx.x; gq < ng; gq += NT) {
+    const uint64_t Jg = A0 + 8ull * gq;
+    uint32_t ii[8];
+    R vr[8];
+    if (Jg + 8 <= total) {
+      const u32x4 i0 = *reinterpret_cast<const u32x4*>(a.idx + Jg);
+      const u32x4 i1 = *reinterpret_cast<const u32x4*>(a.idx + Jg + 4);
+      const u32x4 vv = *reinterpret_cast<const u32x4*>((const R*)a.val + Jg);
+      __builtin_memcpy(ii, &i0, 16);
+      __builtin_memcpy(ii + 4, &i1, 16);
+      __builtin_memcpy(vr, &vv, 16);
+    } else {
+      // the group runs past the end of the payload arrays: element by element
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint64_t J = Jg + e;
+        ii[e] = (J < total) ? a.idx[J] : 0u;
+        vr[e] = (J < total) ? ((const R*)a.val)[J] : R{};
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint64_t J = Jg + e;
+      if (J >= J0 && J < J1) {
+        const uint32_t i = ii[e];
+        if (i < c0 || i >= c1) raise_error(KERR_BAD_INDEX);
+        else buf[i - c0] = Elem<T>::down(Elem<T>::up(buf[i - c0]) + Elem<T>::up(vr[e]));
+      }
+    }
+  }
+}
+
+// AQ-SGD receiver.  Workgroup = one 4096-element chunk of one example's row:
+// the row chunk (m_r) is loaded into registers while the chunk's payload range
+// is read from the block table, written to LDS, updated there with the sent
+// change, and written back to m_r and to a_hat with full-line stores.
 template <typename T>
 __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
   using R = typename Elem<T>::raw;
+  constexpr int PER = 16 / (int)sizeof(R);            // elements per 16-byte access
+  constexpr int VPT = (int)(SC_CH / SC_NT);           // elements per thread
+  static_assert(VPT % PER == 0, "whole 16-byte runs per thread");
   __shared__ R buf[SC_CH];
   __shared__ uint32_t scratch[SC_NT / WAVE + 2];
   const uint64_t nch = (a.L + SC_CH - 1) / SC_CH;
+  // 16-byte paths: 16-bit data, 16-byte aligned rows and payload arrays
+  const bool vec = sizeof(R) == 2 && (a.L % 8) == 0 &&
+                   (((uintptr_t)a.m | (uintptr_t)a.y | (uintptr_t)a.idx | (uintptr_t)a.val) & 15u) == 0;
   for (uint64_t wi = blockIdx.x; wi < a.n_seg * nch; wi += gridDim.x) {
     const uint64_t b = wi / nch, c0 = (wi % nch) * SC_CH;
     const uint64_t c1 = min(a.L, c0 + SC_CH);
@@ -148,45 +203,57 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
       continue;
     }
     R* row = (R*)a.m + (uint64_t)id * a.L;
-    // the buffer row first: its load overlaps the payload range and entries
-    const uint64_t t0 = c0 + (uint64_t)threadIdx.x * SC_VPT;
-    const int nv = (int)min((uint64_t)SC_VPT, sat_sub(c1, t0));
-    R mr[SC_VPT];
-    if (nv > 0) load_run_partial<R, SC_VPT, true>(row + t0, nv, R{}, mr);
+    R* out = (R*)a.y + b * a.L;
+    const bool full = vec && c1 - c0 == SC_CH;
+    // the buffer row's chunk first: its loads overlap the payload range lookup
+    const uint64_t t0 = c0 + (uint64_t)threadIdx.x * VPT;
+    R mr[VPT];
+    const int nv = (int)min((uint64_t)VPT, sat_sub(c1, t0));
+    if (full) {
+#pragma unroll
+      for (int q = 0; q < VPT / PER; ++q) {
+        const u32x4 w = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(row + t0) + q);
+        __builtin_memcpy(&mr[q * PER], &w, 16);
+      }
+    } else if (nv > 0) {
+      load_run_partial<R, VPT, true>(row + t0, nv, R{}, mr);
+    }
     const uint32_t* ix = a.idx + b * a.k;
     const uint32_t* bt = a.blk ? a.blk + b * (n_blocks(a.L) + 1) : nullptr;
     uint32_t j0, j1;
     chunk_range(ix, bt, a.k, c0, c1, scratch, j0, j1);
     if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
-    uint32_t ei[SC_EPT];
-    float ex[SC_EPT];
-#pragma unroll
-    for (int r = 0; r < SC_EPT; ++r) {
-      const uint32_t j = j0 + threadIdx.x + (uint32_t)r * SC_NT;
-      ei[r] = 0xFFFFFFFFu;
-      ex[r] = 0.0f;
-      if (j < j1) {
-        ei[r] = ix[j];
-        if (!bt && j > j0 && ix[j - 1] >= ei[r]) raise_error(KERR_BAD_INDEX);
-        ex[r] = Elem<T>::up(((const R*)a.val)[b * a.k + j]);
+    if (nv > 0) store_run<R, VPT>(&buf[threadIdx.x * VPT], mr);
+    __syncthreads();
+    bool done = false;
+    if constexpr (sizeof(R) == 2) {
+      if (vec && bt) {
+        apply_entries<T, SC_NT>(a, b, c0, c1, j0, j1, buf);
+        done = true;
       }
     }
-    if (nv > 0) store_run<R, SC_VPT>(&buf[threadIdx.x * SC_VPT], mr);
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < SC_EPT; ++r) {
-      const uint32_t j = j0 + threadIdx.x + (uint32_t)r * SC_NT;
-      if (j < j1) {
-        const uint32_t i = ei[r];
+    if (!done) {
+      for (uint32_t j = j0 + threadIdx.x; j < j1; j += SC_NT) {
+        const uint32_t i = ix[j];
+        if (!bt && j > j0 && ix[j - 1] >= i) raise_error(KERR_BAD_INDEX);
         if (i < c0 || i >= c1) raise_error(KERR_BAD_INDEX);
-        else buf[i - c0] = Elem<T>::down(Elem<T>::up(buf[i - c0]) + ex[r]);
+        else buf[i - c0] = Elem<T>::down(Elem<T>::up(buf[i - c0]) + Elem<T>::up(((const R*)a.val)[b * a.k + j]));
       }
     }
     __syncthreads();
-    // the updated row chunk to the buffer and to a_hat, each store
-    // instruction covering whole lines
-    copy_lds_to_global<SC_NT, R>(row + c0, buf, (uint32_t)(c1 - c0));
-    copy_lds_to_global<SC_NT, R>((R*)a.y + b * a.L + c0, buf, (uint32_t)(c1 - c0));
+    // the updated row chunk to the buffer and to a_hat: thread-contiguous
+    // runs, so that each store instruction of a wavefront covers whole lines
+    if (full) {
+#pragma unroll
+      for (int q = 0; q < VPT / PER; ++q) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(&buf[threadIdx.x * VPT + q * PER]);
+        __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(row + t0) + q);
+        __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(out + t0) + q);
+      }
+    } else {
+      copy_lds_to_global<SC_NT, R>(row + c0, buf, (uint32_t)(c1 - c0));
+      copy_lds_to_global<SC_NT, R>(out + c0, buf, (uint32_t)(c1 - c0));
+    }
     __syncthreads();
   }
 }

@@ -153,11 +153,12 @@ __device__ __forceinline__ void store16(Raw* p, const Raw (&in)[E]) {
   vstore<STREAM>(reinterpret_cast<u32x4*>(p), w);
 }
 
-// One segment on one workgroup of its group.  FULL: the workgroup's chunk
-// lies inside the segment and every buffer is 16-byte aligned, so that all
-// runs are whole 16-byte accesses and no element needs a bounds check.
-template <typename InT, int SEL, int R, bool FULL>
-__device__ __forceinline__ void grp_segment(const TopkArgs& a, uint64_t seg, uint32_t P,
+// One segment on one workgroup of its group.  `vec`: every buffer is 16-byte
+// aligned and segments start on 16-byte boundaries, so that whole runs move
+// as single 16-byte accesses; a run cut by the segment's end (or any run
+// without `vec`) goes element by element.
+template <typename InT, int SEL, int R>
+__device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_t seg, uint32_t P,
                                             uint32_t part, const GrpMem& gm,
                                             GrpShared<(uint32_t)GRP_NT * R * (16 / sizeof(typename Elem<InT>::raw)),
                                                       typename Elem<InT>::raw>& sh,
@@ -182,9 +183,13 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, uint64_t seg, uin
 #pragma unroll
   for (int j = 0; j < R; ++j) {
     const uint32_t off = (uint32_t)(j * NT + t) * E;
-    n[j] = FULL ? E : (int)min((uint64_t)E, sat_sub(a.L, c0 + off));
-    if constexpr (FULL) load16<Raw, E, true>(xs + off, xr[j]);
+    n[j] = (int)min((uint64_t)E, sat_sub(a.L, c0 + off));
+    if (vec && n[j] == E) load16<Raw, E, true>(xs + off, xr[j]);
     else if (n[j] > 0) load_run_partial<Raw, E, true>(xs + off, n[j], Raw{}, xr[j]);
+    else {
+#pragma unroll
+      for (int i = 0; i < E; ++i) xr[j][i] = Raw{};
+    }
   }
   Raw* ms = nullptr;
   if constexpr (SEL == SEL_AQSGD) {
@@ -198,7 +203,7 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, uint64_t seg, uin
 #pragma unroll
   for (int j = 0; j < R; ++j) {
     const uint32_t off = (uint32_t)(j * NT + t) * E;
-    if constexpr (FULL) {
+    if (vec && n[j] == E) {
       if constexpr (SEL == SEL_AQSGD) load16<Raw, E, true>(ms + off, mr[j]);
       if constexpr (SEL == SEL_EF) {
         if constexpr (E == 4) {
@@ -223,21 +228,18 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, uint64_t seg, uin
       float x = Elem<InT>::up(xr[j][i]);
       if constexpr (SEL == SEL_EF) x = x + er[j][i];
       if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(mr[j][i]);
-      v[j][i] = (FULL || i < n[j]) ? x : 0.0f;
+      v[j][i] = (i < n[j]) ? x : 0.0f;     // past the segment's end: +0
     }
 
-  // ---- selection
+  // ---- selection (elements past the segment's end hold +0: see grp_select)
   SelResult sr;
   if (a.k == 0) { sr.T = 0xFFFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
-  else {
-    const uint32_t n_wg = FULL ? CH : (uint32_t)min((uint64_t)CH, a.L - c0);
-    sr = grp_select<NT, R, E, CH, FULL>(v, n, (uint32_t)a.k, n_wg, a.L, P, part, gm, sh.sel, sm, gs);
-  }
-  // the group's exchange words have all been read: count out now, before the writes
-  if (P > 1 && last_seg) {
-    grp_exit<NT>(gm, P, gs);
-    exited = true;
-  }
+  else sr = grp_select<NT, R, E, CH>(v, (uint32_t)a.k, a.L, P, part, gm, sh.sel, sm, gs);
+  // the group's exchange words have all been read: draw the exit ticket now
+  // (its answer is needed only at the end)
+  uint32_t ticket = 0;
+  const bool exiting = P > 1 && last_seg;
+  if (exiting) ticket = grp_exit_ticket(gm);
 
   // ---- placement: keys > T and == T per run, scanned over the workgroup
   // in index order (run-major, then thread); both counts stay below 2^16
@@ -247,10 +249,10 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, uint64_t seg, uin
     uint32_t gt = 0, eq = 0;
 #pragma unroll
     for (int i = 0; i < E; ++i) {
+      // padding (+0 past the end) is never kept: it ranks after every element
       const uint32_t kk = mag_key(v[j][i]);
-      const bool ok = FULL || i < n[j];
-      gt += (ok && kk > sr.T) ? 1u : 0u;
-      eq += (ok && kk == sr.T) ? 1u : 0u;
+      gt += (kk > sr.T) ? 1u : 0u;
+      eq += (kk == sr.T) ? 1u : 0u;
     }
     pk[j] = gt | (eq << 16);
   }
@@ -260,13 +262,14 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, uint64_t seg, uin
   for (int j = 0; j < R; ++j) eq_wg += tot[j] >> 16;
   const uint32_t quota_wg = min(sat_sub(sr.r, sr.eq_before), eq_wg);   // ties this workgroup keeps
   const uint32_t wg_first = sr.gt_before + min(sr.eq_before, sr.r);
-  uint32_t pos0[R], tie_keep[R];
+  uint32_t pos0[R], tie_keep[R], kept_before[R];
   uint32_t eq_run = 0, kept_run = 0;
 #pragma unroll
   for (int j = 0; j < R; ++j) {
     const uint32_t gtt = tot[j] & 0xFFFFu, eqt = tot[j] >> 16;
     const uint32_t gx = ex[j] & 0xFFFFu, qx = ex[j] >> 16;
     const uint32_t quota_j = min(sat_sub(quota_wg, eq_run), eqt);    // ties kept in run j
+    kept_before[j] = kept_run;
     pos0[j] = kept_run + gx + min(qx, quota_j);
     tie_keep[j] = min(pk[j] >> 16, sat_sub(quota_j, qx));
     eq_run += eqt;
@@ -285,9 +288,8 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, uint64_t seg, uin
 #pragma unroll
     for (int i = 0; i < E; ++i) {
       const uint32_t kk = mag_key(v[j][i]);
-      const bool ok = FULL || i < n[j];
-      const bool tie = ok && kk == sr.T;
-      const bool kept = ok && (kk > sr.T || (tie && ties < tie_keep[j]));
+      const bool tie = kk == sr.T;
+      const bool kept = kk > sr.T || (tie && ties < tie_keep[j]);
       ties += tie ? 1u : 0u;
       const Raw w = Elem<InT>::down(v[j][i]);
       overflow |= kept && pos >= CH;
@@ -303,7 +305,7 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, uint64_t seg, uin
     }
     // one store instruction of a wavefront covers 1 KiB here: non-temporal
     // stores write whole lines
-    if constexpr (FULL) {
+    if (vec && n[j] == E) {
       if constexpr (SEL == SEL_EF) {
         if constexpr (E == 4) {
           store16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&eo[0]));
@@ -331,20 +333,22 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, uint64_t seg, uin
     copy_lds_to_global<NT>(val + wg_first, sh.st.val, cnt);
   }
   // block table: kept entries below each block boundary this workgroup
-  // covers, by a lower bound in the staged (ascending) run
-  if (a.blk) {
+  // covers.  Block boundaries are multiples of 4096 elements and runs span
+  // NT*E (4096 or 2048) elements, so each boundary starts a run: the count
+  // is the workgroup's first slot plus the runs before it.
+  static_assert(BLOCK_LEN % ((uint64_t)NT * E) == 0 && CH % ((uint64_t)NT * E) == 0, "block boundaries start runs");
+  if (a.blk && t == 0) {
     uint32_t* bt = a.blk + seg * (n_blocks(a.L) + 1);
-    const uint64_t w1 = min(a.L, c0 + CH);
-    for (uint64_t b = (c0 + BLOCK_LEN - 1) / BLOCK_LEN + t; b * BLOCK_LEN < w1; b += NT) {
-      const uint64_t B = b * BLOCK_LEN;
-      uint32_t lo = 0, hi = cnt;
-      while (lo < hi) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (sh.st.idx[mid] < B) lo = mid + 1; else hi = mid;
-      }
-      bt[b] = wg_first + lo;
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const uint64_t B = c0 + (uint64_t)j * NT * E;
+      if (B % BLOCK_LEN == 0 && B < a.L) bt[B / BLOCK_LEN] = wg_first + kept_before[j];
     }
-    if (part == 0 && t == 0) bt[n_blocks(a.L)] = (uint32_t)a.k;
+    if (part == 0) bt[n_blocks(a.L)] = (uint32_t)a.k;
+  }
+  if (exiting) {
+    grp_exit_finish<NT>(gm, P, gs, ticket, &sm.misc[0]);
+    exited = true;
   }
   __syncthreads();
 }
@@ -368,14 +372,16 @@ __global__ __launch_bounds__(GRP_NT) void k_topk_grp(TopkArgs a) {
   // whole 16-byte runs everywhere: every buffer 16-byte aligned, segment
   // starts too (L a multiple of the run length), and this chunk inside the segment
   const uintptr_t al = (uintptr_t)a.x | (uintptr_t)a.e | (uintptr_t)a.m;
-  const bool full = (al & 15u) == 0 && (a.L % E) == 0 && (uint64_t)(part + 1) * CH <= a.L;
+  const bool vec = (al & 15u) == 0 && (a.L % E) == 0;
 
   for (uint64_t seg = group; seg < a.n_seg; seg += n_groups, ++gs.iter) {
     const bool last_seg = seg + n_groups >= a.n_seg;
-    if (full) grp_segment<InT, SEL, R, true>(a, seg, P, part, gm, sh, sm, gs, last_seg, exited);
-    else grp_segment<InT, SEL, R, false>(a, seg, P, part, gm, sh, sm, gs, last_seg, exited);
+    grp_segment<InT, SEL, R>(a, vec, seg, P, part, gm, sh, sm, gs, last_seg, exited);
   }
-  if (P > 1 && !exited) grp_exit<GRP_NT>(gm, P, gs);
+  if (P > 1 && !exited) {
+    const uint32_t ticket = grp_exit_ticket(gm);
+    grp_exit_finish<GRP_NT>(gm, P, gs, ticket, &sm.misc[0]);
+  }
 }
 
 // ------------------------------------------------------------------ plans

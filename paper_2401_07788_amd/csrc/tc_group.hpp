@@ -44,39 +44,42 @@ constexpr uint32_t REC_P_MAX = 64;        // records of at most this many workgr
 __host__ __device__ constexpr uint32_t grp_local_cap(uint32_t CH) { return CH > 4096u ? CH : 4096u; }
 
 // Device memory owned by one group (inside the caller's workspace; zero on
-// entry and left zero on exit):
+// entry and left zero on exit), as word offsets from the group's base:
 //   ctl[64]               [0] barrier arrivals (monotone during a launch), [1] exits
 //   hist1[2][4096]        first-digit histograms, by segment parity
 //   fine[2][256][16]      bits 18..15 of the keys in guessed bins, by bin mod 256
 //   cov[2][256]           guesses per bin mod 256: count + (bin >> 8) << 16
-//   hist2[2][256]         8-bit digit passes (fallback)
+//   hist2[4][256]         8-bit digit counts: [par] exchange B (bits 14..7), [2 + p]
+//                         fallback pass p
 //   rec[P][64]            exchange B records
 //   slots[257][pitch]     last digit per workgroup + larger-prefix counts (fallback)
-struct GrpMem {
-  uint32_t* ctl;
-  uint32_t* hist1;
-  uint32_t* fine;
-  uint32_t* cov;
-  uint32_t* hist2;
-  uint32_t* rec;
-  uint32_t* slots;
-};
+namespace gm_off {
+constexpr uint32_t CTL = 0, HIST1 = 64, FINE = HIST1 + 2 * HIST_BINS, COV = FINE + 2 * FINE_SLOTS * 16,
+                   HIST2 = COV + 2 * FINE_SLOTS, REC = HIST2 + 4 * DIG_BINS;
+static_assert(REC % 4 == 0, "records are 16-byte aligned");
+}  // namespace gm_off
 
 __host__ __device__ constexpr uint64_t grp_mem_words(uint32_t P) {
-  return 64u + 2u * HIST_BINS + 2u * FINE_SLOTS * 16u + 2u * FINE_SLOTS + 2u * DIG_BINS + (uint64_t)P * REC_W +
-         (uint64_t)DIG_ROWS * slot_pitch(P);
+  return gm_off::REC + (uint64_t)P * REC_W + (uint64_t)DIG_ROWS * slot_pitch(P);
 }
 
+// the group's memory: one base pointer, pieces at fixed offsets
+struct GrpMem {
+  uint32_t* base;
+  uint32_t P;
+  __device__ __forceinline__ uint32_t* ctl() const { return base + gm_off::CTL; }
+  __device__ __forceinline__ uint32_t* hist1(uint32_t par) const { return base + gm_off::HIST1 + par * HIST_BINS; }
+  __device__ __forceinline__ uint32_t* fine(uint32_t par) const { return base + gm_off::FINE + par * FINE_SLOTS * 16; }
+  __device__ __forceinline__ uint32_t* cov(uint32_t par) const { return base + gm_off::COV + par * FINE_SLOTS; }
+  __device__ __forceinline__ uint32_t* hist2(uint32_t q) const { return base + gm_off::HIST2 + q * DIG_BINS; }
+  __device__ __forceinline__ uint32_t* rec() const { return base + gm_off::REC; }
+  __device__ __forceinline__ uint32_t* slots() const { return base + gm_off::REC + P * REC_W; }
+};
+
 __device__ __forceinline__ GrpMem grp_mem(uint32_t* ws, uint32_t group, uint32_t P) {
-  uint32_t* b = ws + (uint64_t)group * grp_mem_words(P);
   GrpMem g;
-  g.ctl = b;
-  g.hist1 = b + 64;
-  g.fine = g.hist1 + 2 * HIST_BINS;
-  g.cov = g.fine + 2 * FINE_SLOTS * 16;
-  g.hist2 = g.cov + 2 * FINE_SLOTS;
-  g.rec = g.hist2 + 2 * DIG_BINS;                 // 16-byte aligned: ws is, and every piece above is
-  g.slots = g.rec + (uint64_t)P * REC_W;
+  g.base = ws + (uint64_t)group * grp_mem_words(P);
+  g.P = P;
   return g;
 }
 
@@ -185,37 +188,38 @@ __device__ __forceinline__ void dig_reduce(const uint32_t* hist, uint32_t* red) 
 }
 
 // After the second barrier of a segment every workgroup has read the
-// exchange A words of its parity: each clears a slice of them.
+// exchange A words of its parity: each clears a slice of them (histogram,
+// fine counts and coverage lie back to back).
 __device__ __forceinline__ void grp_clear_a(const GrpMem& g, uint32_t par, uint32_t P, uint32_t part) {
   const uint32_t n1 = HIST_BINS, n2 = FINE_SLOTS * 16, n3 = FINE_SLOTS;
-  uint32_t* h1 = g.hist1 + par * n1;
-  uint32_t* f1 = g.fine + par * n2;
-  uint32_t* c1 = g.cov + par * n3;
-  const uint32_t step = P * GRP_NT;
-  for (uint32_t i = part * GRP_NT + threadIdx.x; i < n1 + n2 + n3; i += step) {
+  uint32_t* h1 = g.hist1(par);
+  uint32_t* f1 = g.fine(par);
+  uint32_t* c1 = g.cov(par);
+  for (uint32_t i = part * GRP_NT + threadIdx.x; i < n1 + n2 + n3; i += P * GRP_NT) {
     uint32_t* p = (i < n1) ? h1 + i : (i < n1 + n2) ? f1 + (i - n1) : c1 + (i - n1 - n2);
     st_agent(p, 0u);
   }
 }
 
 // Exact threshold of one segment held by the P workgroups of a group (this
-// one is `part`), k >= 1.  v[j][i] is element i of this thread's run j; with
-// FULL every element is valid, else run j holds n[j] valid elements.  n_wg:
-// valid elements of this workgroup; L: of the segment.
-template <int NT, int R, int E, uint32_t CH, bool FULL>
-__device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const int (&n)[R], uint32_t k, uint32_t n_wg,
-                                                uint64_t L, uint32_t P, uint32_t part, const GrpMem& g,
+// one is `part`), k >= 1.  v[j][i] is element i of this thread's run j.
+// Elements past the segment's end hold +0: they have the smallest key and
+// the highest indices, so with k <= L they rank after every real element and
+// are never kept; the counts below need no bounds checks.  L: the segment's
+// length, rounded to what the group covers when the guess scales k.
+template <int NT, int R, int E, uint32_t CH>
+__device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t k, uint64_t L, uint32_t P,
+                                                uint32_t part, const GrpMem& g,
                                                 GrpSelShared<grp_local_cap(CH)>& sh, GrpSmall& sm, GrpState& gs) {
   constexpr uint32_t CLOC = grp_local_cap(CH);
   const int t = (int)threadIdx.x;
   const uint32_t dummy = HIST_BINS + (uint32_t)lane_id();
-  auto ok = [&](int j, int i) { return FULL || i < n[j]; };
   auto key = [&](int j, int i) { return mag_key(v[j][i]); };
   SelResult res;
   const uint32_t par = gs.iter & 1u;
 
-  // ---- A: bits 30..19 of every key; exact zeros (common after a ReLU) are
-  // counted in registers and added once per wave, off one hot bin
+  // ---- A: bits 30..19 of every key; exact zeros (common after a ReLU, and
+  // the padding) are counted in registers and added once per wave, off one hot bin
   zero_lds<NT>(sh.hist, HIST_BINS);
   __syncthreads();
   uint32_t zc = 0;
@@ -224,9 +228,8 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
 #pragma unroll
     for (int i = 0; i < E; ++i) {
       const uint32_t kk = key(j, i);
-      const bool live = ok(j, i) && kk != 0u;
-      zc += (ok(j, i) && kk == 0u) ? 1u : 0u;
-      atomicAdd(&sh.hist[live ? (kk >> 19) : dummy], 1u);
+      zc += (kk == 0u) ? 1u : 0u;
+      atomicAdd(&sh.hist[kk != 0u ? (kk >> 19) : dummy], 1u);
     }
   {
     const uint32_t zs = wave_sum(zc);
@@ -236,13 +239,15 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
 
   uint32_t prefix, pbits, need;          // known leading bits of T, keys still to place
   bool fine = false;
+  uint32_t lo = 0, hi = 0;
   if (P > 1) {
     // this workgroup's guess: its own bin at the same rank fraction
-    const uint32_t need_loc = (uint32_t)min<uint64_t>(max<uint64_t>(((uint64_t)k * n_wg + L - 1) / L, 1), n_wg);
+    const uint32_t need_loc = (uint32_t)min<uint64_t>(max<uint64_t>(((uint64_t)k * CH + L - 1) / L, 1), CH);
     find_bin<NT, HIST_BINS>(sh.hist, need_loc, sm.scratch, sm.found);
     const uint32_t bh = sm.found[0];
-    const uint32_t lo = bh > 0u ? bh - 1u : 0u, hi = min(bh + 1u, (uint32_t)HIST_BINS - 1u);
-    // bits 18..15 of the (non-zero) keys in bins lo..hi
+    lo = bh > 0u ? bh - 1u : 0u;
+    hi = min(bh + 1u, (uint32_t)HIST_BINS - 1u);
+    // bits 18..15 of the non-zero keys in bins lo..hi
     if (t < 3 * 16) sm.fwin[t] = 0u;
     __syncthreads();
 #pragma unroll
@@ -250,7 +255,7 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
 #pragma unroll
       for (int i = 0; i < E; ++i) {
         const uint32_t kk = key(j, i), b = kk >> 19;
-        const bool in = ok(j, i) && kk != 0u && b >= lo && b <= hi;
+        const bool in = kk != 0u && b >= lo && b <= hi;
         atomicAdd(&sm.fwin[in ? (b - lo) * 16u + ((kk >> 15) & 15u) : 3u * 16u + (uint32_t)lane_id()], 1u);
       }
     __syncthreads();
@@ -262,9 +267,9 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
     }
     __syncthreads();
     // merge into the group's counts
-    uint32_t* h1 = g.hist1 + par * HIST_BINS;
-    uint32_t* f1 = g.fine + par * FINE_SLOTS * 16;
-    uint32_t* c1 = g.cov + par * FINE_SLOTS;
+    uint32_t* h1 = g.hist1(par);
+    uint32_t* f1 = g.fine(par);
+    uint32_t* c1 = g.cov(par);
     for (int b = t; b < HIST_BINS; b += NT)
       if (sh.hist[b]) add_agent(&h1[b], sh.hist[b]);
     if (t < 3 * 16) {
@@ -274,14 +279,17 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
       const uint32_t b = lo + (uint32_t)(t - 3 * 16);
       if (b <= hi) add_agent(&c1[b & (FINE_SLOTS - 1)], 1u + ((b >> 8) << 16));
     }
-    group_sync(g.ctl, P * ++gs.nbar);
+    group_sync(g.ctl(), P * ++gs.nbar);
+    // everybody has read the previous segment's exchange B counts: clear a slice
+    if (gs.iter > 0)
+      for (int b = (int)(part * NT) + t; b < (int)DIG_BINS; b += (int)(P * NT)) st_agent(&g.hist2(par ^ 1u)[b], 0u);
     // one round trip: the merged histogram, the fine counts and coverage of this window
     uint32_t fw = 0;
     if (t < 3 * 16 + 3) {
       const uint32_t b = lo + (uint32_t)(t < 48 ? t / 16 : t - 48);
       if (b <= hi) fw = ld_agent(t < 48 ? &f1[(b & (FINE_SLOTS - 1)) * 16u + (uint32_t)t % 16u] : &c1[b & (FINE_SLOTS - 1)]);
     }
-    find_bin_global<NT>(h1, k, sm.scratch, sm.found);   // its barriers also publish nothing else
+    find_bin_global<NT>(h1, k, sm.scratch, sm.found);
     const uint32_t b1 = sm.found[0];
     need = k - sm.found[1];
     if (t < 3 * 16 + 3) sm.fwin[t] = fw;
@@ -293,9 +301,9 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
       // bits 18..15 of T from the merged fine counts of b1 (every thread alike)
       const uint32_t* f = &sm.fwin[(b1 - lo) * 16u];
       uint32_t acc = 0, f1v = 16;
-      for (int s = 15; s >= 0; --s) {
-        const uint32_t c = f[s];
-        if (acc < need && need <= acc + c) { f1v = (uint32_t)s; break; }
+      for (int q = 15; q >= 0; --q) {
+        const uint32_t c = f[q];
+        if (acc < need && need <= acc + c) { f1v = (uint32_t)q; break; }
         acc += c;
       }
       if (f1v < 16) {
@@ -315,9 +323,9 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
     __syncthreads();
   }
 
-  // ---- B: records (fine mode): keys above the 16-bit prefix, and the keys
-  // that share it, inline
-  const uint32_t rshift = 31u - pbits;               // key bits below the prefix
+  // ---- B (fine mode): each workgroup publishes its count of keys above the
+  // 16-bit prefix and the keys that share it (inline), and adds those keys'
+  // bits 14..7 into a merged histogram
   bool done = false, cleared = false;
   static_assert(REC_P_MAX * REC_W <= CLOC, "the records of a group fit the LDS list");
   if (fine && P <= REC_P_MAX) {
@@ -326,13 +334,16 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
     for (int j = 0; j < R; ++j)
 #pragma unroll
       for (int i = 0; i < E; ++i) {
-        const uint32_t kp = key(j, i) >> rshift;
-        abv += (ok(j, i) && kp > prefix) ? 1u : 0u;
-        cnt += (ok(j, i) && kp == prefix) ? 1u : 0u;
+        const uint32_t kp = key(j, i) >> 15;
+        abv += (kp > prefix) ? 1u : 0u;
+        cnt += (kp == prefix) ? 1u : 0u;
       }
     uint32_t cv[2] = {cnt, abv}, cx[2], ct[2];
     block_excl_scan_multi<NT, 2>(cv, cx, ct, sm.scratch);
-    uint32_t* my = g.rec + (uint64_t)part * REC_W;
+    uint32_t* my = g.rec() + (uint64_t)part * REC_W;
+    uint32_t* h2 = g.hist2(par);
+    if (t < (int)DIG_BINS) sm.red[t] = 0u;
+    __syncthreads();
     if (cnt) {
       uint32_t q = cx[0];
 #pragma unroll
@@ -340,25 +351,31 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
 #pragma unroll
         for (int i = 0; i < E; ++i) {
           const uint32_t kk = key(j, i);
-          if (ok(j, i) && (kk >> rshift) == prefix) {
+          if ((kk >> 15) == prefix) {
             if (q < REC_KEYS) st_agent(&my[2 + q], kk);
+            atomicAdd(&sm.red[(kk >> 7) & 0xFFu], 1u);
             ++q;
           }
         }
     }
+    __syncthreads();
+    if (t < (int)DIG_BINS && sm.red[t]) add_agent(&h2[t], sm.red[t]);
     if (t == 0) { st_agent(&my[0], ct[1]); st_agent(&my[1], ct[0]); }
-    group_sync(g.ctl, P * ++gs.nbar);
+    group_sync(g.ctl(), P * ++gs.nbar);
     grp_clear_a(g, par, P, part);
     cleared = true;
-    // all records, one 16-byte load per thread and pass
+    // one round trip: all records (16-byte loads) and the merged digit counts
+    uint32_t hd = 0;
+    if (t < (int)DIG_BINS) hd = ld_agent(&h2[t]);
     for (uint32_t q = (uint32_t)t; q < P * (REC_W / 4); q += NT) {
-      const uint64_t* src = reinterpret_cast<const uint64_t*>(g.rec) + 2ull * q;
+      const uint64_t* src = reinterpret_cast<const uint64_t*>(g.rec()) + 2ull * q;
       const uint64_t w0 = ld_agent64(src), w1 = ld_agent64(src + 1);
       sh.cand[4 * q] = (uint32_t)w0;
       sh.cand[4 * q + 1] = (uint32_t)(w0 >> 32);
       sh.cand[4 * q + 2] = (uint32_t)w1;
       sh.cand[4 * q + 3] = (uint32_t)(w1 >> 32);
     }
+    if (t < (int)DIG_BINS) sm.red[t] = hd;
     __syncthreads();
     // totals: keys above the prefix before this workgroup and overall,
     // records that did not fit
@@ -373,9 +390,13 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
       bad += rt[2];
     }
     if (bad == 0) {
-      // local select over the inline keys: the remaining 15 bits as digits
-      // of 8 and 7 bits; slot s of the records is key s%64 - 2 of workgroup s/64
+      // bits 14..7 of T from the merged digit counts; bits 6..0 from the
+      // inline keys that share the 24-bit prefix (slot s of the records is
+      // key s%64 - 2 of workgroup s/64)
       const uint32_t need_b = k - abv_all;
+      find_bin<NT, 256>(sm.red, need_b, sm.scratch, sm.found);
+      const uint32_t p24 = (prefix << 8) | sm.found[0];
+      const uint32_t need_c = need_b - sm.found[1];
       constexpr int SPT = (int)(REC_P_MAX * REC_W / NT);
       uint32_t c[SPT];
       bool lower[SPT];
@@ -386,24 +407,12 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
         c[u] = valid ? sh.cand[sl] : ~0u;           // ~0u matches no prefix
         lower[u] = valid && w < part;
       }
-      dig_zero<NT>(sh.hist);
+      if (t < (int)LAST_BINS) sh.hist[t] = 0u;
       __syncthreads();
 #pragma unroll
-      for (int u = 0; u < SPT; ++u) dig_add(sh.hist, (c[u] >> 15) == prefix, (c[u] >> 7) & 0xFFu);
+      for (int u = 0; u < SPT; ++u) atomicAdd(&sh.hist[(c[u] >> 7) == p24 ? (c[u] & 0x7Fu) : dummy], 1u);
       __syncthreads();
-      dig_reduce<NT, 256>(sh.hist, sm.red);
-      __syncthreads();
-      find_bin<NT, 256>(sm.red, need_b, sm.scratch, sm.found);
-      const uint32_t p24 = (prefix << 8) | sm.found[0];
-      const uint32_t need_c = need_b - sm.found[1];
-      dig_zero<NT>(sh.hist);
-      __syncthreads();
-#pragma unroll
-      for (int u = 0; u < SPT; ++u) dig_add(sh.hist, (c[u] >> 7) == p24, c[u] & 0x7Fu);
-      __syncthreads();
-      dig_reduce<NT, 128>(sh.hist, sm.red);
-      __syncthreads();
-      find_bin<NT, 128>(sm.red, need_c, sm.scratch, sm.found);
+      find_bin<NT, LAST_BINS>(sh.hist, need_c, sm.scratch, sm.found);
       res.T = (p24 << 7) | sm.found[0];
       res.r = need_c - sm.found[1];
       // larger keys and ties in lower workgroups' records; both below 2^16
@@ -431,15 +440,17 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
 #pragma unroll
       for (int i = 0; i < E; ++i) {
         const uint32_t kk = key(j, i);
-        dig_add(sh.hist, ok(j, i) && (kk >> (sh8 + 8u)) == prefix, (kk >> sh8) & 0xFFu);
+        dig_add(sh.hist, (kk >> (sh8 + 8u)) == prefix, (kk >> sh8) & 0xFFu);
       }
     __syncthreads();
     dig_reduce<NT, 256>(sh.hist, sm.red);
     __syncthreads();
     if (P > 1) {
-      uint32_t* h2 = g.hist2 + (pass & 1) * DIG_BINS;
+      // at most two passes per segment, each with its own counts (cleared
+      // after the last-digit barrier)
+      uint32_t* h2 = g.hist2(2u + (uint32_t)pass);
       if (t < (int)DIG_BINS && sm.red[t]) add_agent(&h2[t], sm.red[t]);
-      group_sync(g.ctl, P * ++gs.nbar);
+      group_sync(g.ctl(), P * ++gs.nbar);
       if (t < (int)DIG_BINS) sm.red[t] = ld_agent(&h2[t]);
       if (!cleared) { grp_clear_a(g, par, P, part); cleared = true; }
       __syncthreads();
@@ -461,8 +472,8 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
 #pragma unroll
     for (int i = 0; i < E; ++i) {
       const uint32_t kk = key(j, i);
-      dig_add(sh.hist, ok(j, i) && (kk >> lb) == prefix, kk & (nbl - 1u));
-      gtp += (ok(j, i) && (kk >> lb) > prefix) ? 1u : 0u;
+      dig_add(sh.hist, (kk >> lb) == prefix, kk & (nbl - 1u));
+      gtp += ((kk >> lb) > prefix) ? 1u : 0u;
     }
   const uint32_t gtp_wg = block_sum<NT>(gtp, sm.scratch);   // contains barriers
   dig_reduce<NT, 256>(sh.hist, sm.red);
@@ -472,27 +483,29 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
   uint32_t gtpb = 0;
   if (P > 1) {
     const uint32_t pitch = slot_pitch(P);
-    if (t < (int)DIG_BINS) st_agent(&g.slots[(uint64_t)t * pitch + part], sm.red[t]);
-    if (t == 0) st_agent(&g.slots[(uint64_t)DIG_BINS * pitch + part], gtp_wg);
-    group_sync(g.ctl, P * ++gs.nbar);
-    // every digit pass has been read: clear this workgroup's share of them
-    for (int b = (int)(part * NT) + t; b < (int)(2 * DIG_BINS); b += (int)(P * NT)) st_agent(&g.hist2[b], 0u);
+    uint32_t* slots = g.slots();
+    if (t < (int)DIG_BINS) st_agent(&slots[(uint64_t)t * pitch + part], sm.red[t]);
+    if (t == 0) st_agent(&slots[(uint64_t)DIG_BINS * pitch + part], gtp_wg);
+    group_sync(g.ctl(), P * ++gs.nbar);
+    if (!cleared) { grp_clear_a(g, par, P, part); cleared = true; }
+    // every digit pass has been read by everybody: clear a slice of their counts
+    for (int b = (int)(part * NT) + t; b < (int)(2 * DIG_BINS); b += (int)(P * NT)) st_agent(&g.hist2(2)[b], 0u);
     // row `bin` of the slots holds that bin's count in every workgroup; two
     // thread sets split each row and read it in 8-byte pairs
     constexpr int SETS = NT / (int)DIG_BINS;
     const int bin = t % (int)DIG_BINS, set = t / (int)DIG_BINS;
     const uint32_t per = pitch / SETS;          // even: pitch is a multiple of 8
-    const uint64_t* row = reinterpret_cast<const uint64_t*>(g.slots + (uint64_t)bin * pitch + set * per);
+    const uint64_t* row = reinterpret_cast<const uint64_t*>(slots + (uint64_t)bin * pitch + set * per);
     uint32_t a_all = 0, a_bef = 0;
     for (uint32_t q = 0; q < per / 2; ++q) {
       const uint64_t pr = ld_agent64(row + q);
       const uint32_t jw = set * per + 2 * q;
-      const uint32_t lo = (uint32_t)pr, hi = (uint32_t)(pr >> 32);
-      a_all += lo + hi;
-      a_bef += (jw < part ? lo : 0u) + (jw + 1 < part ? hi : 0u);
+      const uint32_t lo2 = (uint32_t)pr, hi2 = (uint32_t)(pr >> 32);
+      a_all += lo2 + hi2;
+      a_bef += (jw < part ? lo2 : 0u) + (jw + 1 < part ? hi2 : 0u);
     }
     uint32_t g_own = 0;
-    for (uint32_t q = (uint32_t)t; q < part; q += NT) g_own += ld_agent(g.slots + (uint64_t)DIG_BINS * pitch + q);
+    for (uint32_t q = (uint32_t)t; q < part; q += NT) g_own += ld_agent(slots + (uint64_t)DIG_BINS * pitch + q);
     uint32_t* red = sh.hist;   // [SETS][2][256] partial sums (free now)
     red[(set * 2) * DIG_BINS + bin] = a_all;
     red[(set * 2 + 1) * DIG_BINS + bin] = a_bef;
@@ -520,32 +533,39 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], const in
   return res;
 }
 
-// Leave the group's workspace zero: every workgroup counts itself out; the
-// last one (all others have finished reading) clears the barrier words, the
-// records and, if the fallback ran, the slots (everything else is cleared in
-// flight).  Nobody waits here.
-template <int NT>
-__device__ __forceinline__ void grp_exit(const GrpMem& g, uint32_t P, const GrpState& gs) {
-  __shared__ uint32_t last_out;
+// Leave the group's workspace zero.  Every workgroup takes an exit ticket
+// once it has read the last exchange words (grp_exit_ticket: the atomic is
+// issued, nobody waits for it); at its very end, the workgroup that drew the
+// last ticket (all others have finished reading) clears the barrier words,
+// the records, exchange B's digit counts of both parities and, if the
+// fallback ran, the slots; everything else is cleared in flight.
+__device__ __forceinline__ uint32_t grp_exit_ticket(const GrpMem& g) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(g.ctl + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    last_out = (prev == P - 1) ? 1u : 0u;
-  }
+  uint32_t prev = 0;
+  if (threadIdx.x == 0) prev = __hip_atomic_fetch_add(g.ctl() + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return prev;   // thread 0's ticket; other threads' values are meaningless
+}
+
+template <int NT>
+__device__ __forceinline__ void grp_exit_finish(const GrpMem& g, uint32_t P, const GrpState& gs, uint32_t ticket,
+                                                uint32_t* flag) {
+  if (threadIdx.x == 0) *flag = (ticket == P - 1) ? 1u : 0u;
   __syncthreads();
-  if (!last_out) return;
+  if (!*flag) return;
   const uint64_t nrec = (uint64_t)P * REC_W;
-  for (uint64_t i = threadIdx.x; i < nrec; i += NT) st_agent(&g.rec[i], 0u);
+  uint32_t* rec = g.rec();
+  for (uint64_t i = threadIdx.x; i < nrec; i += NT) st_agent(&rec[i], 0u);
+  for (uint32_t i = threadIdx.x; i < 2 * DIG_BINS; i += NT) st_agent(&g.hist2(0)[i], 0u);
   if (gs.used_slots) {
     const uint64_t n = (uint64_t)DIG_ROWS * slot_pitch(P);
-    for (uint64_t i = threadIdx.x; i < n; i += NT) st_agent(&g.slots[i], 0u);
+    uint32_t* slots = g.slots();
+    for (uint64_t i = threadIdx.x; i < n; i += NT) st_agent(&slots[i], 0u);
   }
   if (threadIdx.x == 0) {
-    st_agent(g.ctl, 0u);
-    st_agent(g.ctl + 1, 0u);
+    st_agent(g.ctl(), 0u);
+    st_agent(g.ctl() + 1, 0u);
   }
-  __syncthreads();
 }
 
 }  // namespace tc
