@@ -162,7 +162,8 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
                                             uint32_t part, const GrpMem& gm,
                                             GrpShared<(uint32_t)GRP_NT * R * (16 / sizeof(typename Elem<InT>::raw)),
                                                       typename Elem<InT>::raw>& sh,
-                                            GrpSmall& sm, GrpState& gs, bool last_seg, bool& exited) {
+                                            GrpSmall& sm, GrpState& gs, bool last_seg, bool& exited,
+                                            typename Elem<InT>::raw* mlds) {
   using Raw = typename Elem<InT>::raw;
   constexpr int NT = GRP_NT;
   constexpr int E = 16 / (int)sizeof(Raw);
@@ -183,7 +184,7 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
 #pragma unroll
   for (int j = 0; j < R; ++j) {
     const uint32_t off = (uint32_t)(j * NT + t) * E;
-    n[j] = (int)min((uint64_t)E, sat_sub(a.L, c0 + off));
+    n[j] = (int)min((uint32_t)E, (uint32_t)sat_sub(a.L, c0 + off));   // L < 2^32
     if (vec && n[j] == E) load16<Raw, E, true>(xs + off, xr[j]);
     else if (n[j] > 0) load_run_partial<Raw, E, true>(xs + off, n[j], Raw{}, xr[j]);
     else {
@@ -214,9 +215,13 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
         }
       }
     } else {
+      // elements past the segment's end read as +0 (x, m and e alike)
       if (n[j] > 0) {
         if constexpr (SEL == SEL_AQSGD) load_run_partial<Raw, E, true>(ms + off, n[j], Raw{}, mr[j]);
         if constexpr (SEL == SEL_EF) load_run_partial<float, E, true>(es + off, n[j], 0.0f, er[j]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < E; ++i) { mr[j][i] = Raw{}; er[j][i] = 0.0f; }
       }
     }
   }
@@ -228,12 +233,20 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
       float x = Elem<InT>::up(xr[j][i]);
       if constexpr (SEL == SEL_EF) x = x + er[j][i];
       if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(mr[j][i]);
-      v[j][i] = (i < n[j]) ? x : 0.0f;     // past the segment's end: +0
+      v[j][i] = x;     // past the segment's end: +0 - +0 or +0 + 0 = +0
     }
+  // AQSGD: the buffer row waits in LDS for the update (it is not needed
+  // before), which keeps it out of registers during the selection
+  if constexpr (SEL == SEL_AQSGD) {
+#pragma unroll
+    for (int j = 0; j < R; ++j) store16<Raw, E, false>(mlds + (uint32_t)(j * NT + t) * E, mr[j]);
+  }
 
   // ---- selection (elements past the segment's end hold +0: see grp_select)
   SelResult sr;
-  if (a.k == 0) { sr.T = 0xFFFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
+  // k == 0: T above every finite key (the keys of finite values are at most
+  // 0x7F800000), so that nothing is kept
+  if (a.k == 0) { sr.T = 0x7FFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
   else sr = grp_select<NT, R, E, CH>(v, (uint32_t)a.k, a.L, P, part, gm, sh.sel, sm, gs);
   // the group's exchange words have all been read: draw the exit ticket now
   // (its answer is needed only at the end)
@@ -251,8 +264,8 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
     for (int i = 0; i < E; ++i) {
       // padding (+0 past the end) is never kept: it ranks after every element
       const uint32_t kk = mag_key(v[j][i]);
-      gt += (kk > sr.T) ? 1u : 0u;
-      eq += (kk == sr.T) ? 1u : 0u;
+      gt += gt31(kk, sr.T);
+      eq += eq31(kk, sr.T);
     }
     pk[j] = gt | (eq << 16);
   }
@@ -279,29 +292,32 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
 
   // ---- payload into LDS + epilogue (entries not kept write to the lane's
   // dummy slot)
-  bool overflow = false;
+  uint32_t overflow = 0;
 #pragma unroll
   for (int j = 0; j < R; ++j) {
     const uint32_t off = (uint32_t)(j * NT + t) * E;
     uint32_t pos = pos0[j], ties = 0;
     float eo[E];
+    if constexpr (SEL == SEL_AQSGD) load16<Raw, E, false>(mlds + off, mr[j]);
 #pragma unroll
     for (int i = 0; i < E; ++i) {
       const uint32_t kk = mag_key(v[j][i]);
-      const bool tie = kk == sr.T;
-      const bool kept = kk > sr.T || (tie && ties < tie_keep[j]);
-      ties += tie ? 1u : 0u;
+      const uint32_t tie = eq31(kk, sr.T);
+      const uint32_t kept = gt31(kk, sr.T) | (tie & gt31(tie_keep[j], ties));
+      ties += tie;
       const Raw w = Elem<InT>::down(v[j][i]);
-      overflow |= kept && pos >= CH;
-      const uint32_t slot = (kept && pos < CH) ? pos : CH + dummy;
+      const uint32_t fits = gt31(CH, pos);               // pos < CH (never false when kept)
+      overflow |= kept & (fits ^ 1u);
+      const uint32_t slot = pick(kept & fits, pos, CH + dummy);
       sh.st.idx[slot] = (uint32_t)c0 + off + (uint32_t)i;
       sh.st.val[slot] = w;
-      pos += kept ? 1u : 0u;
+      pos += kept;
       if constexpr (SEL == SEL_AQSGD) {
         const Raw upd = Elem<InT>::down(Elem<InT>::up(mr[j][i]) + Elem<InT>::up(w));
-        mr[j][i] = kept ? upd : mr[j][i];
+        if constexpr (sizeof(Raw) == 4) mr[j][i] = __uint_as_float(pick(kept, __float_as_uint(upd), __float_as_uint(mr[j][i])));
+        else mr[j][i] = (Raw)pick(kept, upd, mr[j][i]);
       }
-      if constexpr (SEL == SEL_EF) eo[i] = v[j][i] - (kept ? through<InT>(v[j][i]) : 0.0f);
+      if constexpr (SEL == SEL_EF) eo[i] = v[j][i] - __uint_as_float(pick(kept, __float_as_uint(through<InT>(v[j][i])), 0u));
     }
     // one store instruction of a wavefront covers 1 KiB here: non-temporal
     // stores write whole lines
@@ -360,6 +376,7 @@ __global__ __launch_bounds__(GRP_NT) void k_topk_grp(TopkArgs a) {
   constexpr uint32_t CH = (uint32_t)GRP_NT * R * E;    // elements per workgroup
   __shared__ GrpShared<CH, Raw> sh;
   __shared__ GrpSmall sm;
+  __shared__ __attribute__((aligned(16))) Raw mlds[SEL == SEL_AQSGD ? CH : 8];   // the buffer row (AQSGD)
 
   const uint32_t P = a.P;
   uint32_t group, part;
@@ -376,7 +393,7 @@ __global__ __launch_bounds__(GRP_NT) void k_topk_grp(TopkArgs a) {
 
   for (uint64_t seg = group; seg < a.n_seg; seg += n_groups, ++gs.iter) {
     const bool last_seg = seg + n_groups >= a.n_seg;
-    grp_segment<InT, SEL, R>(a, vec, seg, P, part, gm, sh, sm, gs, last_seg, exited);
+    grp_segment<InT, SEL, R>(a, vec, seg, P, part, gm, sh, sm, gs, last_seg, exited, mlds);
   }
   if (P > 1 && !exited) {
     const uint32_t ticket = grp_exit_ticket(gm);

@@ -192,6 +192,19 @@ __device__ __forceinline__ void copy_lds_to_global(R* __restrict__ dst, const R*
   if ((uint32_t)t < n - done) dst[done + t] = src[done + t];
 }
 
+// 0/1 comparisons of 31-bit keys as integer arithmetic on bit fields: the
+// per-element loops then keep their flags in vector registers (no 64-bit
+// lane masks, which exhaust the scalar registers in long unrolled loops).
+__device__ __forceinline__ uint32_t gt31(uint32_t a, uint32_t b) {   // a > b, both < 2^31
+  return __builtin_amdgcn_ubfe(b - a, 31, 1);
+}
+__device__ __forceinline__ uint32_t eq31(uint32_t a, uint32_t b) {   // a == b, both < 2^31
+  const uint32_t x = a ^ b;
+  return __builtin_amdgcn_ubfe((x - 1u) & ~x, 31, 1);
+}
+// f ? x : y with f in {0, 1}
+__device__ __forceinline__ uint32_t pick(uint32_t f, uint32_t x, uint32_t y) { return ((x ^ y) & (0u - f)) ^ y; }
+
 // a - b clamped at 0, written without a guarded subtraction.  The device
 // compiler of this toolchain can turn `b < a ? a - b : 0` into an unguarded
 // no-wrap subtraction and then use the implied a >= b to fold unrelated

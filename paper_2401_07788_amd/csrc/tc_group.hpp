@@ -228,8 +228,9 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t
 #pragma unroll
     for (int i = 0; i < E; ++i) {
       const uint32_t kk = key(j, i);
-      zc += (kk == 0u) ? 1u : 0u;
-      atomicAdd(&sh.hist[kk != 0u ? (kk >> 19) : dummy], 1u);
+      const uint32_t z = eq31(kk, 0u);
+      zc += z;
+      atomicAdd(&sh.hist[pick(z, dummy, kk >> 19)], 1u);
     }
   {
     const uint32_t zs = wave_sum(zc);
@@ -255,8 +256,9 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t
 #pragma unroll
       for (int i = 0; i < E; ++i) {
         const uint32_t kk = key(j, i), b = kk >> 19;
-        const bool in = kk != 0u && b >= lo && b <= hi;
-        atomicAdd(&sm.fwin[in ? (b - lo) * 16u + ((kk >> 15) & 15u) : 3u * 16u + (uint32_t)lane_id()], 1u);
+        // in the window lo..hi (b - lo < 3, unsigned) and not an exact zero
+        const uint32_t in = gt31(3u, b - lo) & (eq31(kk, 0u) ^ 1u) & (gt31(lo, b) ^ 1u);
+        atomicAdd(&sm.fwin[pick(in, (b - lo) * 16u + ((kk >> 15) & 15u), 3u * 16u + (uint32_t)lane_id())], 1u);
       }
     __syncthreads();
     if (t == 0 && lo == 0u) {
@@ -335,8 +337,8 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t
 #pragma unroll
       for (int i = 0; i < E; ++i) {
         const uint32_t kp = key(j, i) >> 15;
-        abv += (kp > prefix) ? 1u : 0u;
-        cnt += (kp == prefix) ? 1u : 0u;
+        abv += gt31(kp, prefix);
+        cnt += eq31(kp, prefix);
       }
     uint32_t cv[2] = {cnt, abv}, cx[2], ct[2];
     block_excl_scan_multi<NT, 2>(cv, cx, ct, sm.scratch);
