@@ -45,12 +45,14 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E, published
 SOURCES_HASHED = {
-    "aqsgd": ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
-              "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
+    "aqsgd": ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_group.hpp",
+              "paper_2401_07788_amd/csrc/tc_select.hpp", "paper_2401_07788_amd/csrc/tc_device.hpp",
+              "paper_2401_07788_amd/csrc/k_scatter.hip"],
     "lm": ["paper_2401_07788_amd/csrc/k_global.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
            "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
-    "resnet": ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
-               "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
+    "resnet": ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_group.hpp",
+               "paper_2401_07788_amd/csrc/tc_select.hpp", "paper_2401_07788_amd/csrc/tc_device.hpp",
+               "paper_2401_07788_amd/csrc/k_scatter.hip", "paper_2401_07788_amd/csrc/k_quant.hip"],
     "transformer": ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
                     "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
 }

@@ -148,7 +148,8 @@ struct GrpSmall {
   uint32_t scratch[8 * (GRP_NT / WAVE)];
   uint32_t found[2];
   uint32_t red[DIG_BINS];            // one digit's counts, copies summed
-  uint32_t fwin[3 * 16 + WAVE];      // this workgroup's fine counts, then the merged ones
+  uint32_t fwin[3 * 16 + WAVE];      // this workgroup's fine counts of its window
+  uint32_t fmrg[3 * 16 + 3];         // the group's merged fine counts and coverage of that window
   uint32_t misc[8];
 };
 
@@ -294,14 +295,14 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t
     find_bin_global<NT>(h1, k, sm.scratch, sm.found);
     const uint32_t b1 = sm.found[0];
     need = k - sm.found[1];
-    if (t < 3 * 16 + 3) sm.fwin[t] = fw;
+    if (t < 3 * 16 + 3) sm.fmrg[t] = fw;
     __syncthreads();
-    fine = b1 >= lo && b1 <= hi && sm.fwin[48 + (b1 - lo)] == P + ((P * (b1 >> 8)) << 16);
+    fine = b1 >= lo && b1 <= hi && sm.fmrg[48 + (b1 - lo)] == P + ((P * (b1 >> 8)) << 16);
     prefix = b1;
     pbits = 12;
     if (fine) {
       // bits 18..15 of T from the merged fine counts of b1 (every thread alike)
-      const uint32_t* f = &sm.fwin[(b1 - lo) * 16u];
+      const uint32_t* f = &sm.fmrg[(b1 - lo) * 16u];
       uint32_t acc = 0, f1v = 16;
       for (int q = 15; q >= 0; --q) {
         const uint32_t c = f[q];
@@ -331,38 +332,40 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t
   bool done = false, cleared = false;
   static_assert(REC_P_MAX * REC_W <= CLOC, "the records of a group fit the LDS list");
   if (fine && P <= REC_P_MAX) {
-    uint32_t abv = 0, cnt = 0;
+    // this workgroup's counts come from its own histograms: keys in higher
+    // coarse bins plus keys of bin b1 in higher fine bins; the keys sharing
+    // the prefix are those of its fine bin
+    const uint32_t b1 = prefix >> 4, f1 = prefix & 15u;
+    uint32_t abv = 0;
+#pragma unroll
+    for (int q = 0; q < HIST_BINS / NT; ++q) {
+      const uint32_t b = (uint32_t)(q * NT + t);
+      abv += (b > b1) ? sh.hist[b] : 0u;
+    }
+    if (t < 16 && (uint32_t)t > f1) abv += sm.fwin[(b1 - lo) * 16u + (uint32_t)t];
+    const uint32_t abv_wg = block_sum<NT>(abv, sm.scratch);
+    const uint32_t cnt_wg = sm.fwin[(b1 - lo) * 16u + f1];
+    uint32_t* my = g.rec() + (uint64_t)part * REC_W;
+    uint32_t* h2 = g.hist2(par);
+    if (t < (int)DIG_BINS) sm.red[t] = 0u;
+    if (t == 0) sm.misc[1] = 0u;
+    __syncthreads();
+    // the keys sharing the prefix (a few per workgroup) into the record, in
+    // any order, and their bits 14..7 into the digit counts
 #pragma unroll
     for (int j = 0; j < R; ++j)
 #pragma unroll
       for (int i = 0; i < E; ++i) {
-        const uint32_t kp = key(j, i) >> 15;
-        abv += gt31(kp, prefix);
-        cnt += eq31(kp, prefix);
-      }
-    uint32_t cv[2] = {cnt, abv}, cx[2], ct[2];
-    block_excl_scan_multi<NT, 2>(cv, cx, ct, sm.scratch);
-    uint32_t* my = g.rec() + (uint64_t)part * REC_W;
-    uint32_t* h2 = g.hist2(par);
-    if (t < (int)DIG_BINS) sm.red[t] = 0u;
-    __syncthreads();
-    if (cnt) {
-      uint32_t q = cx[0];
-#pragma unroll
-      for (int j = 0; j < R; ++j)
-#pragma unroll
-        for (int i = 0; i < E; ++i) {
-          const uint32_t kk = key(j, i);
-          if ((kk >> 15) == prefix) {
-            if (q < REC_KEYS) st_agent(&my[2 + q], kk);
-            atomicAdd(&sm.red[(kk >> 7) & 0xFFu], 1u);
-            ++q;
-          }
+        const uint32_t kk = key(j, i);
+        if ((kk >> 15) == prefix) {
+          const uint32_t q = atomicAdd(&sm.misc[1], 1u);
+          if (q < REC_KEYS) st_agent(&my[2 + q], kk);
+          atomicAdd(&sm.red[(kk >> 7) & 0xFFu], 1u);
         }
-    }
+      }
     __syncthreads();
     if (t < (int)DIG_BINS && sm.red[t]) add_agent(&h2[t], sm.red[t]);
-    if (t == 0) { st_agent(&my[0], ct[1]); st_agent(&my[1], ct[0]); }
+    if (t == 0) { st_agent(&my[0], abv_wg); st_agent(&my[1], cnt_wg); }
     group_sync(g.ctl(), P * ++gs.nbar);
     grp_clear_a(g, par, P, part);
     cleared = true;
