@@ -11,10 +11,10 @@ example, payload, buffer update) and the receiver (buffer update from the
 payload, reconstruction).  Every input is resident in HBM before timing.
 The timed region is the sequence of K micro-batches (sender then receiver for
 each, on one stream) captured once as a HIP graph and replayed: the launches
-of a stream of micro-batches without per-launch host cost.  Reported beside:
-a pipelined graph (each receiver on a second stream, overlapping the next
+of a stream of micro-batches without per-launch host cost.  With --variants,
+also a pipelined graph (each receiver on a second stream, overlapping the next
 sender as on two pipeline stages; slower on one GPU, where the two compete
-for the compute units), the eager step and an eager two-stream variant.
+for the compute units) and an eager two-stream variant.
 Per-kernel durations for the roofline come from HIP events around each
 kernel of an eager pass over other micro-batches.
 
@@ -102,6 +102,10 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--variants", action="store_true",
+                    help="aqsgd: also time a pipelined graph (each receiver on a second stream) and an eager "
+                         "two-stream run (both slower on one GPU; off by default so that a kernel trace of "
+                         "the default run holds the timed configurations only)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run 5 device copies of 256 MiB (the reference for HBM byte counters)")
     ap.add_argument("--workload", choices=["aqsgd", "lm", "resnet", "transformer"], default="aqsgd",
@@ -183,7 +187,8 @@ def run_aqsgd(args, dev):
     # per-kernel events, serial graph (warm-up, K), pipelined graph (warm-up,
     # K, the timed region), eager two-stream reference; as many epochs as
     # that takes (ids distinct within each micro-batch)
-    need_mb = warm + n_ref + 2 * (warm + steps) + warm + n_ref
+    n_kr = min(50, steps)   # launches per kernel in the per-kernel timing graphs
+    need_mb = warm + n_ref + (warm + steps) + 2 * n_kr + (((warm + steps) + warm + n_ref) if args.variants else 0)
     n_epochs = (need_mb + n_mb - 1) // n_mb
 
     # ---- inputs, resident in HBM; every timed micro-batch is a fresh one
@@ -218,21 +223,17 @@ def run_aqsgd(args, dev):
             tc.aqsgd_reconstruct(pays[0], m_r, ids_dev[j], out=ahats[0])
             if ev: ev[i][2].record(stream)
 
-    # ---- eager: warm-up, then a reference pass with HIP events around each
-    # kernel on the launch stream (the per-kernel durations of the roofline)
+    # ---- eager: warm-up, then a reference pass (host-timed)
     st = torch.cuda.current_stream(dev)
     j = 0
     steps_on(st, j, warm); j += warm
     torch.cuda.synchronize()
     check("during the warm-up")
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_ref)]
     t0 = time.perf_counter()
-    steps_on(st, j, n_ref, ev); j += n_ref
+    steps_on(st, j, n_ref); j += n_ref
     torch.cuda.synchronize()
     eager_ms = (time.perf_counter() - t0) * 1e3 / n_ref
     check("in the eager pass")
-    send_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-    recv_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
 
     # ---- the K micro-batches captured as HIP graphs (the launches of a
     # stream of micro-batches without per-launch host cost), replayed once:
@@ -270,6 +271,40 @@ def run_aqsgd(args, dev):
         torch.cuda.synchronize()
         return time.perf_counter() - t0
 
+    # ---- per-kernel durations for the roofline: n_kr senders of distinct
+    # micro-batches back to back (each with its own payload), then their n_kr
+    # receivers, each set captured as a HIP graph and timed with HIP events on
+    # the stream the graph is launched on; a first pair of graphs over other
+    # micro-batches warms up
+    pays_kr = [tc.empty_topk_payload(B, L, k, torch.float16, dev) for _ in range(n_kr)]
+
+    def senders(j0, n):
+        for i in range(n):
+            tc.aqsgd_step(acts[j0 + i], m_s, ids_dev[j0 + i], k, ws=ws, out=pays_kr[i])
+
+    def receivers(j0, n):
+        for i in range(n):
+            tc.aqsgd_reconstruct(pays_kr[i], m_r, ids_dev[j0 + i], out=ahats[0])
+
+    kev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    for rep in range(2):
+        half = n_kr // 2 if rep == 0 else n_kr
+        gsend = graph_of(senders, j, half)
+        grecv = graph_of(receivers, j, half)
+        j += half
+        torch.cuda.synchronize()
+        with torch.cuda.stream(cap):
+            kev[0].record(cap)
+            gsend.replay()
+            kev[1].record(cap)
+            grecv.replay()
+            kev[2].record(cap)
+        torch.cuda.synchronize()
+        check("in the per-kernel timing graphs")
+    send_ms = kev[0].elapsed_time(kev[1]) / n_kr
+    recv_ms = kev[1].elapsed_time(kev[2]) / n_kr
+    del gsend, grecv
+
     gw = graph_of(lambda j0, n: steps_on(cap, j0, n), j, warm); j += warm
     gs = graph_of(lambda j0, n: steps_on(cap, j0, n), j, steps); j += steps
     gw.replay()
@@ -278,13 +313,15 @@ def run_aqsgd(args, dev):
     wall = timed(gs)
     check("in the timed region")
     ms_per_step = wall * 1e3 / steps
-    gpw = graph_of(pipelined, j, warm); j += warm
-    gp = graph_of(pipelined, j, steps); j += steps
-    gpw.replay()
-    torch.cuda.synchronize()
-    check("during the pipelined graph warm-up")
-    pipelined_ms = timed(gp) * 1e3 / steps
-    check("in the pipelined graph")
+    pipelined_ms = overlap_ms = None
+    if args.variants:
+        gpw = graph_of(pipelined, j, warm); j += warm
+        gp = graph_of(pipelined, j, steps); j += steps
+        gpw.replay()
+        torch.cuda.synchronize()
+        check("during the pipelined graph warm-up")
+        pipelined_ms = timed(gp) * 1e3 / steps
+        check("in the pipelined graph")
 
     # ---- reference: sender of j+1 (stream A) overlapping the receiver of j
     # (stream B), payloads double-buffered
@@ -304,13 +341,14 @@ def run_aqsgd(args, dev):
                 tc.aqsgd_reconstruct(pays[b], m_r, ids_dev[jj], out=ahats[b])
                 freed[b].record(sB)
 
-    overlap_steps(j, warm); j += warm
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    overlap_steps(j, n_ref); j += n_ref
-    torch.cuda.synchronize()
-    overlap_ms = (time.perf_counter() - t0) * 1e3 / n_ref
-    check("in the overlapped reference pass")
+    if args.variants:
+        overlap_steps(j, warm); j += warm
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        overlap_steps(j, n_ref); j += n_ref
+        torch.cuda.synchronize()
+        overlap_ms = (time.perf_counter() - t0) * 1e3 / n_ref
+        check("in the overlapped reference pass")
 
     N = B * L
     boundary_bytes = N * 2
@@ -371,9 +409,7 @@ def run_aqsgd(args, dev):
         "effective_GBps": round(b_alg / (ms_per_step * 1e-3) / 1e9, 2),
         "algorithmic_bytes_per_step": b_alg,
         "kernels_ms": {"aqsgd_send": round(send_ms, 5), "aqsgd_recv": round(recv_ms, 5)},
-        "pipelined_graph_ms_per_step": round(pipelined_ms, 5),
         "eager_ms_per_step": round(eager_ms, 5),
-        "eager_two_stream_ms_per_step": round(overlap_ms, 5),
         "device_copy_GBps": device_copy_gbps(dev),
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
@@ -381,6 +417,9 @@ def run_aqsgd(args, dev):
         "cpu_baseline": cpu,
         "setup_s": round(setup_s, 1),
     }
+    if args.variants:
+        out["pipelined_graph_ms_per_step"] = round(pipelined_ms, 5)
+        out["eager_two_stream_ms_per_step"] = round(overlap_ms, 5)
     return out
 
 

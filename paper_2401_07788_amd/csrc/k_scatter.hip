@@ -133,71 +133,80 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
   }
 }
 
-// The payload entries of a chunk, [j0, j1) of segment `seg`, loaded eight at
-// a time with 16-byte accesses aligned in the whole payload array (rows of
-// k entries need not be aligned), then applied to the chunk held in LDS:
-// buf[i - c0] = out(in(buf[i - c0]) + in(val)).  Entries outside [j0, j1) in
-// the aligned groups are skipped; an index outside the chunk is flagged.
-template <typename T, int NT>
-__device__ __forceinline__ void apply_entries(const ScatterArgs& a, uint64_t seg, uint64_t c0, uint64_t c1,
-                                              uint32_t j0, uint32_t j1, typename Elem<T>::raw* buf) {
-  using R = typename Elem<T>::raw;
+// Payload groups of eight entries, loaded with 16-byte accesses aligned in
+// the whole payload array (rows of k entries need not be aligned): group g of
+// a chunk covers array entries A0 + 8g .. A0 + 8g + 7.  A group reaching past
+// the end of the arrays is read element by element.
+template <typename R>
+struct PayGroup {
+  uint32_t idx[8];
+  R val[8];
+};
+
+template <typename R>
+__device__ __forceinline__ void load_group(const ScatterArgs& a, uint64_t Jg, uint64_t total, PayGroup<R>& g) {
   static_assert(sizeof(R) == 2, "eight 16-bit values per 16-byte access");
-  const uint64_t J0 = seg * a.k + j0, J1 = seg * a.k + j1, total = a.n_seg * a.k;
-  const uint64_t A0 = J0 & ~7ull;
-  const uint32_t ng = (uint32_t)((J1 - A0 + 7) / 8);
-  for (uint32_t gq = threadIdx.x; gq < ng; gq += NT) {
-    const uint64_t Jg = A0 + 8ull * gq;
-    uint32_t ii[8];
-    R vr[8];
-    if (Jg + 8 <= total) {
-      const u32x4 i0 = *reinterpret_cast<const u32x4*>(a.idx + Jg);
-      const u32x4 i1 = *reinterpret_cast<const u32x4*>(a.idx + Jg + 4);
-      const u32x4 vv = *reinterpret_cast<const u32x4*>((const R*)a.val + Jg);
-      __builtin_memcpy(ii, &i0, 16);
-      __builtin_memcpy(ii + 4, &i1, 16);
-      __builtin_memcpy(vr, &vv, 16);
-    } else {
-      // the group runs past the end of the payload arrays: element by element
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint64_t J = Jg + e;
-        ii[e] = (J < total) ? a.idx[J] : 0u;
-        vr[e] = (J < total) ? ((const R*)a.val)[J] : R{};
-      }
-    }
+  if (Jg + 8 <= total) {
+    const u32x4 i0 = *reinterpret_cast<const u32x4*>(a.idx + Jg);
+    const u32x4 i1 = *reinterpret_cast<const u32x4*>(a.idx + Jg + 4);
+    const u32x4 vv = *reinterpret_cast<const u32x4*>((const R*)a.val + Jg);
+    __builtin_memcpy(g.idx, &i0, 16);
+    __builtin_memcpy(g.idx + 4, &i1, 16);
+    __builtin_memcpy(g.val, &vv, 16);
+  } else {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const uint64_t J = Jg + e;
-      if (J >= J0 && J < J1) {
-        const uint32_t i = ii[e];
-        if (i < c0 || i >= c1) raise_error(KERR_BAD_INDEX);
-        else buf[i - c0] = Elem<T>::down(Elem<T>::up(buf[i - c0]) + Elem<T>::up(vr[e]));
-      }
+      g.idx[e] = (J < total) ? a.idx[J] : 0u;
+      g.val[e] = (J < total) ? ((const R*)a.val)[J] : R{};
     }
   }
 }
 
-// AQ-SGD receiver.  Workgroup = one 4096-element chunk of one example's row:
-// the row chunk (m_r) is loaded into registers while the chunk's payload range
-// is read from the block table, written to LDS, updated there with the sent
-// change, and written back to m_r and to a_hat with full-line stores.
+// apply the group's entries that lie in [J0, J1) to the chunk [c0, c1) held
+// in LDS: buf[i - c0] = out(in(buf[i - c0]) + in(val)); an index outside the
+// chunk is flagged
+template <typename T>
+__device__ __forceinline__ void apply_group(const PayGroup<typename Elem<T>::raw>& g, uint64_t Jg, uint64_t J0,
+                                            uint64_t J1, uint64_t c0, uint64_t c1, typename Elem<T>::raw* buf) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const uint64_t J = Jg + e;
+    if (J >= J0 && J < J1) {
+      const uint32_t i = g.idx[e];
+      if (i < c0 || i >= c1) raise_error(KERR_BAD_INDEX);
+      else buf[i - c0] = Elem<T>::down(Elem<T>::up(buf[i - c0]) + Elem<T>::up(g.val[e]));
+    }
+  }
+}
+
+// AQ-SGD receiver.  Workgroup = one 4096-element chunk of one example's row.
+// The example id and the chunk's payload range are read first, together;
+// then the row chunk (m_r) and the chunk's payload entries are loaded at the
+// same time; the row goes to LDS, the entries are applied there, and the
+// updated chunk is written to m_r and to a_hat with full-line stores.
 template <typename T>
 __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
   using R = typename Elem<T>::raw;
   constexpr int PER = 16 / (int)sizeof(R);            // elements per 16-byte access
   constexpr int VPT = (int)(SC_CH / SC_NT);           // elements per thread
+  constexpr int GPT = 2;                              // payload groups per thread held in registers
   static_assert(VPT % PER == 0, "whole 16-byte runs per thread");
   __shared__ R buf[SC_CH];
   __shared__ uint32_t scratch[SC_NT / WAVE + 2];
   const uint64_t nch = (a.L + SC_CH - 1) / SC_CH;
-  // 16-byte paths: 16-bit data, 16-byte aligned rows and payload arrays
-  const bool vec = sizeof(R) == 2 && (a.L % 8) == 0 &&
+  const uint64_t nbt = n_blocks(a.L) + 1;
+  // 16-byte paths: 16-bit data, 16-byte aligned rows and payload arrays, a block table
+  const bool vec = sizeof(R) == 2 && (a.L % 8) == 0 && a.blk != nullptr &&
                    (((uintptr_t)a.m | (uintptr_t)a.y | (uintptr_t)a.idx | (uintptr_t)a.val) & 15u) == 0;
+  const uint64_t total = a.n_seg * a.k;
   for (uint64_t wi = blockIdx.x; wi < a.n_seg * nch; wi += gridDim.x) {
-    const uint64_t b = wi / nch, c0 = (wi % nch) * SC_CH;
+    const uint64_t b = wi / nch, ci = wi % nch, c0 = ci * SC_CH;
     const uint64_t c1 = min(a.L, c0 + SC_CH);
+    // the id and (with a block table) the payload range, in one round trip
     const int64_t id = a.ids[b];
+    uint32_t bj0 = 0, bj1 = 0;
+    if (a.blk) { bj0 = a.blk[b * nbt + ci]; bj1 = a.blk[b * nbt + ci + 1]; }
     if (id < 0 || (uint64_t)id >= a.n_samples) {
       if (threadIdx.x == 0) raise_error(KERR_BAD_ID);
       continue;
@@ -205,34 +214,55 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
     R* row = (R*)a.m + (uint64_t)id * a.L;
     R* out = (R*)a.y + b * a.L;
     const bool full = vec && c1 - c0 == SC_CH;
-    // the buffer row's chunk first: its loads overlap the payload range lookup
     const uint64_t t0 = c0 + (uint64_t)threadIdx.x * VPT;
-    R mr[VPT];
     const int nv = (int)min((uint64_t)VPT, sat_sub(c1, t0));
-    if (full) {
+    R mr[VPT];
+    uint32_t j0 = 0, j1 = 0;
+    bool range_ok = true;
+    bool done = false;
+    if constexpr (sizeof(R) == 2) {
+     if (full) {
+      done = true;
+      // row chunk and payload groups, all loads in flight together
 #pragma unroll
       for (int q = 0; q < VPT / PER; ++q) {
         const u32x4 w = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(row + t0) + q);
         __builtin_memcpy(&mr[q * PER], &w, 16);
       }
-    } else if (nv > 0) {
-      load_run_partial<R, VPT, true>(row + t0, nv, R{}, mr);
-    }
-    const uint32_t* ix = a.idx + b * a.k;
-    const uint32_t* bt = a.blk ? a.blk + b * (n_blocks(a.L) + 1) : nullptr;
-    uint32_t j0, j1;
-    chunk_range(ix, bt, a.k, c0, c1, scratch, j0, j1);
-    if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
-    if (nv > 0) store_run<R, VPT>(&buf[threadIdx.x * VPT], mr);
-    __syncthreads();
-    bool done = false;
-    if constexpr (sizeof(R) == 2) {
-      if (vec && bt) {
-        apply_entries<T, SC_NT>(a, b, c0, c1, j0, j1, buf);
-        done = true;
+      j0 = bj0;
+      j1 = bj1;
+      range_ok = !(j0 > j1 || j1 > a.k || j1 - j0 > c1 - c0);
+      if (!range_ok) j0 = j1 = 0;
+      const uint64_t J0 = b * a.k + j0, J1 = b * a.k + j1, A0 = J0 & ~7ull;
+      const uint32_t ng = (uint32_t)((J1 - A0 + 7) / 8);
+      PayGroup<R> pg[GPT];
+#pragma unroll
+      for (int r = 0; r < GPT; ++r) {
+        const uint32_t gq = threadIdx.x + (uint32_t)r * SC_NT;
+        if (gq < ng) load_group<R>(a, A0 + 8ull * gq, total, pg[r]);
       }
+      store_run<R, VPT>(&buf[threadIdx.x * VPT], mr);
+      __syncthreads();
+#pragma unroll
+      for (int r = 0; r < GPT; ++r) {
+        const uint32_t gq = threadIdx.x + (uint32_t)r * SC_NT;
+        if (gq < ng) apply_group<T>(pg[r], A0 + 8ull * gq, J0, J1, c0, c1, buf);
+      }
+      // a chunk with more entries than the registers hold: the rest in turns
+      for (uint32_t gq = threadIdx.x + GPT * SC_NT; gq < ng; gq += SC_NT) {
+        PayGroup<R> g1;
+        load_group<R>(a, A0 + 8ull * gq, total, g1);
+        apply_group<T>(g1, A0 + 8ull * gq, J0, J1, c0, c1, buf);
+      }
+     }
     }
     if (!done) {
+      if (nv > 0) load_run_partial<R, VPT, true>(row + t0, nv, R{}, mr);
+      const uint32_t* ix = a.idx + b * a.k;
+      const uint32_t* bt = a.blk ? a.blk + b * nbt : nullptr;
+      chunk_range(ix, bt, a.k, c0, c1, scratch, j0, j1);
+      if (nv > 0) store_run<R, VPT>(&buf[threadIdx.x * VPT], mr);
+      __syncthreads();
       for (uint32_t j = j0 + threadIdx.x; j < j1; j += SC_NT) {
         const uint32_t i = ix[j];
         if (!bt && j > j0 && ix[j - 1] >= i) raise_error(KERR_BAD_INDEX);
@@ -240,6 +270,8 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
         else buf[i - c0] = Elem<T>::down(Elem<T>::up(buf[i - c0]) + Elem<T>::up(((const R*)a.val)[b * a.k + j]));
       }
     }
+    if (!range_ok && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
+    if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
     __syncthreads();
     // the updated row chunk to the buffer and to a_hat: thread-contiguous
     // runs, so that each store instruction of a wavefront covers whole lines

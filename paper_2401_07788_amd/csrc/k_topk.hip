@@ -391,9 +391,15 @@ __global__ __launch_bounds__(GRP_NT) void k_topk_grp(TopkArgs a) {
   const uintptr_t al = (uintptr_t)a.x | (uintptr_t)a.e | (uintptr_t)a.m;
   const bool vec = (al & 15u) == 0 && (a.L % E) == 0;
 
-  for (uint64_t seg = group; seg < a.n_seg; seg += n_groups, ++gs.iter) {
-    const bool last_seg = seg + n_groups >= a.n_seg;
-    grp_segment<InT, SEL, R>(a, vec, seg, P, part, gm, sh, sm, gs, last_seg, exited, mlds);
+  if (a.n_seg <= n_groups) {
+    // one segment per group (a straight path: nothing for the compiler to
+    // hoist out of a loop and keep in registers)
+    if (group < a.n_seg) grp_segment<InT, SEL, R>(a, vec, group, P, part, gm, sh, sm, gs, true, exited, mlds);
+  } else {
+    for (uint64_t seg = group; seg < a.n_seg; seg += n_groups, ++gs.iter) {
+      const bool last_seg = seg + n_groups >= a.n_seg;
+      grp_segment<InT, SEL, R>(a, vec, seg, P, part, gm, sh, sm, gs, last_seg, exited, mlds);
+    }
   }
   if (P > 1 && !exited) {
     const uint32_t ticket = grp_exit_ticket(gm);
