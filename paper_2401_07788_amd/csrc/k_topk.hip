@@ -153,6 +153,267 @@ __device__ __forceinline__ void store16(Raw* p, const Raw (&in)[E]) {
   vstore<STREAM>(reinterpret_cast<u32x4*>(p), w);
 }
 
+// Copy n staged entries to dst, leaving some out: rem[0..nr) (nr <= WAVE)
+// holds the staged position of each left-out entry less the number of
+// left-out entries before it (non-decreasing), so that output entry o comes
+// from staged position o + #{i : rem[i] <= o}.  A wavefront writes 64
+// consecutive 16-byte pieces at a time; the few left-out entries that fall
+// among them are counted with ballots and one loop over that set.
+template <int NT, typename T>
+__device__ __forceinline__ void copy_lds_skip(T* __restrict__ dst, const T* src, uint32_t n, const uint32_t* rem,
+                                              uint32_t nr) {
+  constexpr uint32_t PER = 16 / sizeof(T);
+  const uint32_t lane = (uint32_t)lane_id(), wv = threadIdx.x / WAVE;
+  const uint32_t rv = (lane < nr) ? rem[lane] : ~0u;     // lane i holds rem[i]
+  const uint32_t mis = (uint32_t)(((uintptr_t)dst / sizeof(T)) % PER);
+  const uint32_t head = min(n, (PER - mis) % PER);
+  const uint32_t body = (n - head) / PER;
+  const uint32_t done = head + body * PER;
+  // the unaligned head and the tail (fewer than PER entries each): one
+  // entry per lane, by wavefronts 0 and 1
+  if (wv < 2) {
+    const uint32_t o0 = (wv == 0) ? 0u : done, cnt = (wv == 0) ? head : n - done;
+    uint32_t d = (uint32_t)__popcll(__ballot(rv < o0));
+    uint64_t in = __ballot(rv >= o0 && rv < o0 + PER);
+    while (in) {
+      const int i = __builtin_ctzll(in);
+      in &= in - 1;
+      d += ((uint32_t)__builtin_amdgcn_readlane((int)rv, i) <= o0 + lane) ? 1u : 0u;
+    }
+    if (lane < cnt) dst[o0 + lane] = src[o0 + lane + d];
+  }
+  for (uint32_t base = wv * WAVE; base < body; base += NT) {
+    const uint32_t A = head + base * PER;              // the wavefront's first output
+    const uint32_t o = A + lane * PER;                 // this lane's first output
+    const uint32_t d0 = (uint32_t)__popcll(__ballot(rv <= A));
+    uint64_t in = __ballot(rv > A && rv < A + WAVE * PER);
+    uint32_t d[PER];
+#pragma unroll
+    for (uint32_t e = 0; e < PER; ++e) d[e] = d0;
+    while (in) {
+      const int i = __builtin_ctzll(in);
+      in &= in - 1;
+      const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)rv, i);
+#pragma unroll
+      for (uint32_t e = 0; e < PER; ++e) d[e] += (r <= o + e) ? 1u : 0u;
+    }
+    if (base + lane < body) {
+      T tmp[PER];
+#pragma unroll
+      for (uint32_t e = 0; e < PER; ++e) tmp[e] = src[o + e + d[e]];
+      u32x4 w;
+      __builtin_memcpy(&w, tmp, 16);
+      vstore<true>(reinterpret_cast<u32x4*>(dst + o), w);
+    }
+  }
+}
+
+// Exchange B with the payload and buffer work moved ahead (fine mode, 2 <= P
+// <= REC_P_MAX).  The 16-bit prefix `pre` of T already divides the keys:
+// those above it are kept whatever T is, those below are dropped, and only
+// the few on it wait for exchange B.  Before the group's barrier: the keys on
+// the prefix go into the record; then, while the other workgroups arrive,
+// every entry above or on the prefix is staged in LDS in index order and the
+// buffer rows are stored as if only the keys above the prefix were kept.
+// After the barrier one wavefront decides the keys on the prefix and stores
+// the buffer values of the kept ones; the others are left out of the staged
+// list when it is copied out.  Returns
+// false when a record overflowed: nothing decided, the buffer rows are then
+// stored again by the caller.
+template <typename InT, int SEL, int R>
+__device__ __forceinline__ bool grp_early(const TopkArgs& a, bool vec, uint64_t seg, uint32_t P, uint32_t part,
+                                          const GrpMem& gm,
+                                          GrpShared<(uint32_t)GRP_NT * R * (16 / sizeof(typename Elem<InT>::raw)),
+                                                    typename Elem<InT>::raw>& sh,
+                                          GrpSmall& sm, GrpState& gs, const SelA& A,
+                                          float (&v)[R][16 / sizeof(typename Elem<InT>::raw)], const int (&n)[R],
+                                          uint64_t c0, typename Elem<InT>::raw* ms, float* es,
+                                          const typename Elem<InT>::raw* mlds, bool exiting, uint32_t& ticket) {
+  using Raw = typename Elem<InT>::raw;
+  constexpr int NT = GRP_NT;
+  constexpr int E = 16 / (int)sizeof(Raw);
+  constexpr uint32_t CH = (uint32_t)NT * R * E;
+  const int t = (int)threadIdx.x;
+  const uint32_t dummy = (uint32_t)lane_id();
+  const uint32_t pre = A.prefix;   // bits 30..15 of T
+
+  // ---- per run: entries above or on the prefix, and on it (both < 2^16
+  // per workgroup), scanned in index order; the thread's own ones as bit
+  // masks (bit i: element i of the run)
+  static_assert(E <= 8, "two 8-bit masks per run");
+  if (t < (int)DIG_BINS) sm.red[t] = 0u;
+  uint32_t pc[R], ex[R], tot[R], msk[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    uint32_t mm = 0, cm = 0;
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      const uint32_t hi = mag_key(v[j][i]) >> 15;
+      const uint32_t on = eq31(hi, pre);
+      mm |= (gt31(hi, pre) | on) << i;
+      cm |= on << i;
+    }
+    msk[j] = mm | (cm << 8);
+    pc[j] = (uint32_t)__builtin_popcount(mm) | ((uint32_t)__builtin_popcount(cm) << 16);
+  }
+  block_excl_scan_multi<NT, R>(pc, ex, tot, sm.scratch);
+  refresh(v);
+  uint32_t mb[R], cb[R];      // the workgroup's staged entries / keys on the prefix in runs before j
+  uint32_t m_all = 0, c_all = 0;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    mb[j] = m_all;
+    cb[j] = c_all;
+    m_all += tot[j] & 0xFFFFu;
+    c_all += tot[j] >> 16;
+  }
+
+  // ---- the keys on the prefix (a few per workgroup): record slot (index
+  // order), their bits 14..7 into the digit counts, and what deciding them
+  // later needs; a thread visits only the set bits of its masks
+  uint32_t* my = gm.rec() + (uint64_t)part * REC_W;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    uint32_t cm = msk[j] >> 8;
+    if (cm) {
+      uint32_t q = cb[j] + (ex[j] >> 16);
+      const uint32_t sp0 = mb[j] + (ex[j] & 0xFFFFu), mm = msk[j] & 0xFFu;
+      const uint32_t off = (uint32_t)(j * NT + t) * E;
+      do {
+        const uint32_t i = (uint32_t)__builtin_ctz(cm);
+        cm &= cm - 1u;
+        uint32_t kk = mag_key(v[j][0]);
+#pragma unroll
+        for (int ii = 1; ii < E; ++ii) kk = (i == (uint32_t)ii) ? mag_key(v[j][ii]) : kk;
+        if (q < REC_KEYS) {
+          st_agent(&my[2 + q], kk);
+          sm.ckey[q] = kk;
+          sm.coff[q] = off + i;
+          sm.cpos[q] = sp0 + (uint32_t)__builtin_popcount(mm & ((1u << i) - 1u));
+        }
+        atomicAdd(&sm.red[(kk >> 7) & 0xFFu], 1u);
+        ++q;
+      } while (cm);
+    }
+  }
+  __syncthreads();
+  grp_publish_b<NT>(part, gm, sm, gs, m_all - c_all, c_all);
+  refresh(v);
+
+  // ---- while the group arrives: stage the entries above or on the prefix
+  // and store the buffer rows with only the keys above it kept
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const uint32_t off = (uint32_t)(j * NT + t) * E;
+    uint32_t sp = mb[j] + (ex[j] & 0xFFFFu);
+    Raw mr[E];
+    float eo[E];
+    if constexpr (SEL == SEL_AQSGD) load16<Raw, E, false>(mlds + off, mr);
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      const uint32_t mayb = (msk[j] >> i) & 1u, cert = mayb & ~(msk[j] >> (8 + i));
+      const Raw w = Elem<InT>::down(v[j][i]);
+      const uint32_t slot = pick(mayb, sp, CH + dummy);
+      sh.st.idx[slot] = (uint32_t)c0 + off + (uint32_t)i;
+      sh.st.val[slot] = w;
+      sp += mayb;
+      if constexpr (SEL == SEL_AQSGD) {
+        const Raw upd = Elem<InT>::down(Elem<InT>::up(mr[i]) + Elem<InT>::up(w));
+        if constexpr (sizeof(Raw) == 4) mr[i] = __uint_as_float(pick(cert, __float_as_uint(upd), __float_as_uint(mr[i])));
+        else mr[i] = (Raw)pick(cert, upd, mr[i]);
+      }
+      if constexpr (SEL == SEL_EF) eo[i] = v[j][i] - __uint_as_float(pick(cert, __float_as_uint(through<InT>(v[j][i])), 0u));
+    }
+    if (vec && n[j] == E) {
+      if constexpr (SEL == SEL_EF) {
+        store16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&eo[0]));
+        if constexpr (E == 8) store16<float, 4, true>(es + off + 4, *reinterpret_cast<float(*)[4]>(&eo[4]));
+      }
+      if constexpr (SEL == SEL_AQSGD) store16<Raw, E, true>(ms + off, mr);
+    } else if (n[j] > 0) {
+      if constexpr (SEL == SEL_EF) store_run_partial<float, E, true>(es + off, n[j], eo);
+      if constexpr (SEL == SEL_AQSGD) store_run_partial<Raw, E, true>(ms + off, n[j], mr);
+    }
+  }
+
+  SelResult sr;
+  const bool ok = grp_finish_b<NT>((uint32_t)a.k, P, part, gm, sm, gs, A, sr);
+  refresh(v);
+  if (!ok) return false;
+  // every wavefront's buffer stores are complete before some of them are
+  // overwritten from another wavefront below
+  if (exiting) ticket = grp_exit_ticket(gm);
+  else {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+
+  // ---- decide the keys on the prefix (at most REC_KEYS: one wavefront);
+  // the kept ones get their buffer values
+  if (t < WAVE) {
+    const bool has = (uint32_t)t < c_all;
+    const uint32_t key = has ? sm.ckey[t] : 0u;
+    const bool tie = has && key == sr.T;
+    const uint64_t tm = __ballot(tie);
+    const uint32_t quota = min(sat_sub(sr.r, sr.eq_before), (uint32_t)__popcll(tm));   // ties this workgroup keeps
+    const bool kept = (has && key > sr.T) || (tie && lanes_below(tm) < quota);
+    const bool drop = has && !kept;
+    const uint64_t km = __ballot(kept), dm = __ballot(drop);
+    const uint32_t off = has ? sm.coff[t] : 0u;
+    if constexpr (SEL != SEL_PLAIN) {
+      if (kept) {
+        // the value sent is the staged one; the key and its sign give the
+        // exact difference back
+        const Raw w = sh.st.val[sm.cpos[t]];
+        if constexpr (SEL == SEL_AQSGD) {
+          const Raw upd = Elem<InT>::down(Elem<InT>::up(mlds[off]) + Elem<InT>::up(w));
+          __builtin_nontemporal_store(upd, ms + off);
+        }
+        if constexpr (SEL == SEL_EF) {
+          const float x = __uint_as_float(key | (__float_as_uint(Elem<InT>::up(w)) & 0x80000000u));
+          __builtin_nontemporal_store(x - Elem<InT>::up(w), es + off);
+        }
+      }
+    }
+    if (drop) sm.rem[lanes_below(dm)] = sm.cpos[t] - lanes_below(dm);
+    const uint32_t run = has ? off / (uint32_t)(NT * E) : (uint32_t)R;
+    uint32_t rb[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) rb[j] = (uint32_t)__popcll(__ballot(drop && run < (uint32_t)j));
+    if (t == 0) {
+      sm.misc[2] = (uint32_t)__popcll(dm);
+      sm.misc[3] = (uint32_t)__popcll(km);
+      // block table: kept entries below each block boundary this workgroup
+      // covers (boundaries start runs)
+      if (a.blk) {
+        const uint32_t wg_first = sr.gt_before + min(sr.eq_before, sr.r);
+        uint32_t* bt = a.blk + seg * (n_blocks(a.L) + 1);
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+          const uint64_t B = c0 + (uint64_t)j * NT * E;
+          if (B % BLOCK_LEN == 0 && B < a.L) bt[B / BLOCK_LEN] = wg_first + mb[j] - rb[j];
+        }
+        if (part == 0) bt[n_blocks(a.L)] = (uint32_t)a.k;
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- the workgroup's run of the payload, in index order, coalesced
+  const uint32_t n_drop = sm.misc[2];
+  const uint32_t wg_count = (m_all - c_all) + sm.misc[3];
+  const uint32_t wg_first = sr.gt_before + min(sr.eq_before, sr.r);
+  uint32_t* idx = a.idx + seg * a.k;
+  Raw* val = (Raw*)a.val + seg * a.k;
+  if (wg_first + wg_count > a.k) {
+    if (t == 0) raise_error(KERR_INTERNAL);
+  } else {
+    copy_lds_skip<NT>(idx + wg_first, sh.st.idx, wg_count, sm.rem, n_drop);
+    copy_lds_skip<NT>(val + wg_first, sh.st.val, wg_count, sm.rem, n_drop);
+  }
+  return true;
+}
+
 // One segment on one workgroup of its group.  `vec`: every buffer is 16-byte
 // aligned and segments start on 16-byte boundaries, so that whole runs move
 // as single 16-byte accesses; a run cut by the segment's end (or any run
@@ -242,18 +503,36 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
     for (int j = 0; j < R; ++j) store16<Raw, E, false>(mlds + (uint32_t)(j * NT + t) * E, mr[j]);
   }
 
-  // ---- selection (elements past the segment's end hold +0: see grp_select)
+  // ---- selection (elements past the segment's end hold +0: see grp_exchange_a)
   SelResult sr;
-  // k == 0: T above every finite key (the keys of finite values are at most
-  // 0x7F800000), so that nothing is kept
-  if (a.k == 0) { sr.T = 0x7FFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
-  else sr = grp_select<NT, R, E, CH>(v, (uint32_t)a.k, a.L, P, part, gm, sh.sel, sm, gs);
-  // the group's exchange words have all been read: draw the exit ticket now
-  // (its answer is needed only at the end)
   uint32_t ticket = 0;
   const bool exiting = P > 1 && last_seg;
+  if (a.k == 0) {
+    // T above every finite key (the keys of finite values are at most
+    // 0x7F800000), so that nothing is kept
+    sr.T = 0x7FFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0;
+  } else {
+    const SelA A = grp_exchange_a<NT, R, E, CH>(v, (uint32_t)a.k, a.L, P, part, gm, sh.sel, sm, gs);
+    refresh(v);
+    bool cleared = false;
+    if (A.fine && P <= REC_P_MAX) {
+      if (grp_early<InT, SEL, R>(a, vec, seg, P, part, gm, sh, sm, gs, A, v, n, c0, ms, es, mlds, exiting, ticket)) {
+        if (exiting) {
+          grp_exit_finish<NT>(gm, P, gs, ticket, &sm.misc[0]);
+          exited = true;
+        }
+        __syncthreads();
+        return;
+      }
+      cleared = true;
+    }
+    sr = grp_fallback<NT, R, E, CH>(v, P, part, gm, sh.sel, sm, gs, A.prefix, A.pbits, A.need, cleared);
+  }
+  // the group's exchange words have all been read: draw the exit ticket now
+  // (its answer is needed only at the end)
   if (exiting) ticket = grp_exit_ticket(gm);
 
+  refresh(v);
   // ---- placement: keys > T and == T per run, scanned over the workgroup
   // in index order (run-major, then thread); both counts stay below 2^16
   uint32_t pk[R], ex[R], tot[R];
@@ -290,6 +569,7 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
   }
   const uint32_t wg_count = kept_run;
 
+  refresh(v);
   // ---- payload into LDS + epilogue (entries not kept write to the lane's
   // dummy slot)
   uint32_t overflow = 0;

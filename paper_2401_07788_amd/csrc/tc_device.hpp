@@ -65,6 +65,19 @@ __device__ __forceinline__ float through(float v) { return Elem<T>::up(Elem<T>::
 // the unsigned order of keys is the order of |v|, and +0 / -0 share key 0.
 __device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
 
+// Tells the optimiser that register-resident values may have changed (no
+// instruction is emitted).  Called between the phases that each derive keys
+// from the same values, it makes every phase recompute what it needs instead
+// of keeping another phase's derived values alive across barriers, which
+// would exhaust the registers.
+template <int R, int E>
+__device__ __forceinline__ void refresh(float (&v)[R][E]) {
+#pragma unroll
+  for (int j = 0; j < R; ++j)
+#pragma unroll
+    for (int i = 0; i < E; ++i) asm volatile("" : "+v"(v[j][i]));
+}
+
 // ------------------------------------------------------------ vector access
 // Load/store N consecutive raw elements starting at p (element units).
 // Uses 16-byte accesses when the run is 16-byte aligned and a multiple of 16

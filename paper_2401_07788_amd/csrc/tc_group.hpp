@@ -86,14 +86,17 @@ __device__ __forceinline__ GrpMem grp_mem(uint32_t* ws, uint32_t group, uint32_t
 // Barrier among the P workgroups of a group: arrivals are counted in one
 // word that only grows during a launch, so the n-th barrier waits for n*P
 // arrivals and nobody has to reset anything in flight.  Each wave's device-
-// scope stores and atomics complete before its workgroup arrives.  The wait
-// is bounded (co-residency violated): it then raises KERR_TIMEOUT and
-// returns.
-__device__ __forceinline__ void group_sync(uint32_t* ctr, uint32_t target) {
+// scope stores and atomics complete before its workgroup arrives.  Arrival
+// and wait are separate calls so that a workgroup can do work of its own in
+// between.  The wait is bounded (co-residency violated): it then raises
+// KERR_TIMEOUT and returns.
+__device__ __forceinline__ void group_arrive(uint32_t* ctr) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void group_wait(uint32_t* ctr, uint32_t target) {
   if (threadIdx.x == 0) {
-    __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     uint32_t spins = 0;
     while (ld_agent(ctr) < target) {
       __builtin_amdgcn_s_sleep(1);
@@ -105,6 +108,10 @@ __device__ __forceinline__ void group_sync(uint32_t* ctr, uint32_t target) {
     }
   }
   __syncthreads();
+}
+__device__ __forceinline__ void group_sync(uint32_t* ctr, uint32_t target) {
+  group_arrive(ctr);
+  group_wait(ctr, target);
 }
 
 // Exclusive scans of R values per thread across the workgroup in one pass;
@@ -150,7 +157,20 @@ struct GrpSmall {
   uint32_t red[DIG_BINS];            // one digit's counts, copies summed
   uint32_t fwin[3 * 16 + WAVE];      // this workgroup's fine counts of its window
   uint32_t fmrg[3 * 16 + 3];         // the group's merged fine counts and coverage of that window
-  uint32_t misc[8];
+  uint32_t hist7[LAST_BINS + WAVE];  // last 7 bits of T (plus per-lane dummies)
+  uint32_t misc[16];
+  // this workgroup's keys on the 16-bit prefix, in index order (exchange B):
+  // key, chunk offset, staged payload position
+  uint32_t ckey[WAVE], coff[WAVE], cpos[WAVE];
+  uint32_t rem[WAVE];                // staged positions dropped after exchange B, less their rank
+};
+
+// What exchange A leaves: the known leading bits of T, and the keys still to
+// place below them.  fine: the 16-bit prefix is known (every workgroup's guess
+// covered the bin of the k-th key).
+struct SelA {
+  uint32_t prefix, pbits, need;
+  bool fine;
 };
 
 // Per-workgroup state carried across the segments a group handles.
@@ -202,21 +222,19 @@ __device__ __forceinline__ void grp_clear_a(const GrpMem& g, uint32_t par, uint3
   }
 }
 
-// Exact threshold of one segment held by the P workgroups of a group (this
-// one is `part`), k >= 1.  v[j][i] is element i of this thread's run j.
+// Exchange A for one segment held by the P workgroups of a group (this one
+// is `part`), k >= 1.  v[j][i] is element i of this thread's run j.
 // Elements past the segment's end hold +0: they have the smallest key and
 // the highest indices, so with k <= L they rank after every real element and
 // are never kept; the counts below need no bounds checks.  L: the segment's
 // length, rounded to what the group covers when the guess scales k.
 template <int NT, int R, int E, uint32_t CH>
-__device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t k, uint64_t L, uint32_t P,
-                                                uint32_t part, const GrpMem& g,
-                                                GrpSelShared<grp_local_cap(CH)>& sh, GrpSmall& sm, GrpState& gs) {
-  constexpr uint32_t CLOC = grp_local_cap(CH);
+__device__ __forceinline__ SelA grp_exchange_a(float (&v)[R][E], uint32_t k, uint64_t L, uint32_t P,
+                                               uint32_t part, const GrpMem& g,
+                                               GrpSelShared<grp_local_cap(CH)>& sh, GrpSmall& sm, GrpState& gs) {
   const int t = (int)threadIdx.x;
   const uint32_t dummy = HIST_BINS + (uint32_t)lane_id();
   auto key = [&](int j, int i) { return mag_key(v[j][i]); };
-  SelResult res;
   const uint32_t par = gs.iter & 1u;
 
   // ---- A: bits 30..19 of every key; exact zeros (common after a ReLU, and
@@ -252,6 +270,7 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t
     // bits 18..15 of the non-zero keys in bins lo..hi
     if (t < 3 * 16) sm.fwin[t] = 0u;
     __syncthreads();
+    refresh(v);
 #pragma unroll
     for (int j = 0; j < R; ++j)
 #pragma unroll
@@ -325,121 +344,130 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t
     need = k - sm.found[1];
     __syncthreads();
   }
+  SelA A;
+  A.prefix = prefix;
+  A.pbits = pbits;
+  A.need = need;
+  A.fine = fine;
+  return A;
+}
 
-  // ---- B (fine mode): each workgroup publishes its count of keys above the
-  // 16-bit prefix and the keys that share it (inline), and adds those keys'
-  // bits 14..7 into a merged histogram
-  bool done = false, cleared = false;
-  static_assert(REC_P_MAX * REC_W <= CLOC, "the records of a group fit the LDS list");
-  if (fine && P <= REC_P_MAX) {
-    // this workgroup's counts come from its own histograms: keys in higher
-    // coarse bins plus keys of bin b1 in higher fine bins; the keys sharing
-    // the prefix are those of its fine bin
-    const uint32_t b1 = prefix >> 4, f1 = prefix & 15u;
-    uint32_t abv = 0;
+// Exchange B (fine mode), first half.  Before calling, this workgroup has
+// written the keys that share the 16-bit prefix into its record (slots 2..,
+// at most REC_KEYS of them), counted their bits 14..7 into sm.red (followed
+// by a barrier), and knows how many of its keys lie above the prefix
+// (abv_wg) and on it (cnt_wg).  Publishes the counts and arrives at the
+// group's barrier; the workgroup may work on its own until grp_finish_b.
+template <int NT>
+__device__ __forceinline__ void grp_publish_b(uint32_t part, const GrpMem& g, const GrpSmall& sm, GrpState& gs,
+                                              uint32_t abv_wg, uint32_t cnt_wg) {
+  const int t = (int)threadIdx.x;
+  uint32_t* my = g.rec() + (uint64_t)part * REC_W;
+  uint32_t* h2 = g.hist2(gs.iter & 1u);
+  if (t < (int)DIG_BINS && sm.red[t]) add_agent(&h2[t], sm.red[t]);
+  if (t == 0) { st_agent(&my[0], abv_wg); st_agent(&my[1], cnt_wg); }
+  ++gs.nbar;
+  group_arrive(g.ctl());
+}
+
+// Exchange B, second half: waits for the group, reads all records and the
+// merged digit counts in one round trip and finds T, the tie quota and the
+// larger keys and ties of lower workgroups.  Returns false (nothing decided)
+// when some record could not hold its keys; exchange A's words are cleared
+// either way.
+template <int NT>
+__device__ __forceinline__ bool grp_finish_b(uint32_t k, uint32_t P, uint32_t part, const GrpMem& g, GrpSmall& sm,
+                                             GrpState& gs, const SelA& A, SelResult& res) {
+  constexpr int NW = NT / WAVE;
+  constexpr int SPT = (int)(REC_P_MAX * REC_W / NT);
+  static_assert(NT % REC_W == 0 && REC_W == WAVE, "a record is one word per lane of a wavefront");
+  const int t = (int)threadIdx.x, wv = t / WAVE, lane = lane_id();
+  const uint32_t par = gs.iter & 1u;
+  group_wait(g.ctl(), P * gs.nbar);
+  grp_clear_a(g, par, P, part);
+  // lane i of wavefront wv reads word i of records u*NW + wv
+  uint32_t hd = 0;
+  if (t < (int)DIG_BINS) hd = ld_agent(&g.hist2(par)[t]);
+  const uint32_t* rec = g.rec();
+  uint32_t wd[SPT];
 #pragma unroll
-    for (int q = 0; q < HIST_BINS / NT; ++q) {
-      const uint32_t b = (uint32_t)(q * NT + t);
-      abv += (b > b1) ? sh.hist[b] : 0u;
-    }
-    if (t < 16 && (uint32_t)t > f1) abv += sm.fwin[(b1 - lo) * 16u + (uint32_t)t];
-    const uint32_t abv_wg = block_sum<NT>(abv, sm.scratch);
-    const uint32_t cnt_wg = sm.fwin[(b1 - lo) * 16u + f1];
-    uint32_t* my = g.rec() + (uint64_t)part * REC_W;
-    uint32_t* h2 = g.hist2(par);
-    if (t < (int)DIG_BINS) sm.red[t] = 0u;
-    if (t == 0) sm.misc[1] = 0u;
-    __syncthreads();
-    // the keys sharing the prefix (a few per workgroup) into the record, in
-    // any order, and their bits 14..7 into the digit counts
-#pragma unroll
-    for (int j = 0; j < R; ++j)
-#pragma unroll
-      for (int i = 0; i < E; ++i) {
-        const uint32_t kk = key(j, i);
-        if ((kk >> 15) == prefix) {
-          const uint32_t q = atomicAdd(&sm.misc[1], 1u);
-          if (q < REC_KEYS) st_agent(&my[2 + q], kk);
-          atomicAdd(&sm.red[(kk >> 7) & 0xFFu], 1u);
-        }
-      }
-    __syncthreads();
-    if (t < (int)DIG_BINS && sm.red[t]) add_agent(&h2[t], sm.red[t]);
-    if (t == 0) { st_agent(&my[0], abv_wg); st_agent(&my[1], cnt_wg); }
-    group_sync(g.ctl(), P * ++gs.nbar);
-    grp_clear_a(g, par, P, part);
-    cleared = true;
-    // one round trip: all records (16-byte loads) and the merged digit counts
-    uint32_t hd = 0;
-    if (t < (int)DIG_BINS) hd = ld_agent(&h2[t]);
-    for (uint32_t q = (uint32_t)t; q < P * (REC_W / 4); q += NT) {
-      const uint64_t* src = reinterpret_cast<const uint64_t*>(g.rec()) + 2ull * q;
-      const uint64_t w0 = ld_agent64(src), w1 = ld_agent64(src + 1);
-      sh.cand[4 * q] = (uint32_t)w0;
-      sh.cand[4 * q + 1] = (uint32_t)(w0 >> 32);
-      sh.cand[4 * q + 2] = (uint32_t)w1;
-      sh.cand[4 * q + 3] = (uint32_t)(w1 >> 32);
-    }
-    if (t < (int)DIG_BINS) sm.red[t] = hd;
-    __syncthreads();
-    // totals: keys above the prefix before this workgroup and overall,
-    // records that did not fit
-    uint32_t abv_before = 0, abv_all = 0, bad = 0;
-    for (uint32_t w0 = 0; w0 < P; w0 += NT) {
-      const uint32_t w = w0 + (uint32_t)t;
-      const uint32_t aw = (w < P) ? sh.cand[w * REC_W] : 0u, cw = (w < P) ? sh.cand[w * REC_W + 1] : 0u;
-      uint32_t rv[3] = {(w < part) ? aw : 0u, aw, (cw > REC_KEYS) ? 1u : 0u}, rx[3], rt[3];
-      block_excl_scan_multi<NT, 3>(rv, rx, rt, sm.scratch);
-      abv_before += rt[0];
-      abv_all += rt[1];
-      bad += rt[2];
-    }
-    if (bad == 0) {
-      // bits 14..7 of T from the merged digit counts; bits 6..0 from the
-      // inline keys that share the 24-bit prefix (slot s of the records is
-      // key s%64 - 2 of workgroup s/64)
-      const uint32_t need_b = k - abv_all;
-      find_bin<NT, 256>(sm.red, need_b, sm.scratch, sm.found);
-      const uint32_t p24 = (prefix << 8) | sm.found[0];
-      const uint32_t need_c = need_b - sm.found[1];
-      constexpr int SPT = (int)(REC_P_MAX * REC_W / NT);
-      uint32_t c[SPT];
-      bool lower[SPT];
-#pragma unroll
-      for (int u = 0; u < SPT; ++u) {
-        const uint32_t sl = (uint32_t)(u * NT + t), w = sl / REC_W, i = sl % REC_W;
-        const bool valid = w < P && i >= 2u && i - 2u < sh.cand[w * REC_W + 1];
-        c[u] = valid ? sh.cand[sl] : ~0u;           // ~0u matches no prefix
-        lower[u] = valid && w < part;
-      }
-      if (t < (int)LAST_BINS) sh.hist[t] = 0u;
-      __syncthreads();
-#pragma unroll
-      for (int u = 0; u < SPT; ++u) atomicAdd(&sh.hist[(c[u] >> 7) == p24 ? (c[u] & 0x7Fu) : dummy], 1u);
-      __syncthreads();
-      find_bin<NT, LAST_BINS>(sh.hist, need_c, sm.scratch, sm.found);
-      res.T = (p24 << 7) | sm.found[0];
-      res.r = need_c - sm.found[1];
-      // larger keys and ties in lower workgroups' records; both below 2^16
-      uint32_t ge = 0;
-#pragma unroll
-      for (int u = 0; u < SPT; ++u)
-        ge += (lower[u] && c[u] > res.T) ? 1u : ((lower[u] && c[u] == res.T) ? 0x10000u : 0u);
-      const uint32_t sge = block_sum<NT>(ge, sm.scratch);
-      res.gt_before = abv_before + (sge & 0xFFFFu);
-      res.eq_before = sge >> 16;
-      done = true;
-    }
+  for (int u = 0; u < SPT; ++u) {
+    const uint32_t w = (uint32_t)(u * NW + wv);
+    wd[u] = (w < P) ? ld_agent(&rec[(uint64_t)w * REC_W + (uint32_t)lane]) : 0u;
   }
-  if (done) return res;
+  // totals from the record headers (words 0 and 1 sit in lanes 0 and 1)
+  uint32_t cnt[SPT], abv_bef = 0, abv_all = 0, bad = 0;
+#pragma unroll
+  for (int u = 0; u < SPT; ++u) {
+    const uint32_t w = (uint32_t)(u * NW + wv);
+    const uint32_t aw = __builtin_amdgcn_readlane(wd[u], 0);
+    cnt[u] = __builtin_amdgcn_readlane(wd[u], 1);
+    abv_all += aw;
+    abv_bef += (w < part) ? aw : 0u;
+    bad |= (cnt[u] > REC_KEYS) ? 1u : 0u;
+  }
+  uint32_t* tsc = sm.scratch + 5 * NW;   // clear of the scans' words
+  if (lane == 0) { tsc[wv] = abv_bef; tsc[NW + wv] = abv_all; tsc[2 * NW + wv] = bad; }
+  if (t < (int)DIG_BINS) sm.red[t] = hd;
+  if (t < (int)LAST_BINS) sm.hist7[t] = 0u;
+  __syncthreads();
+  abv_bef = 0;
+  abv_all = 0;
+  bad = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) { abv_bef += tsc[i]; abv_all += tsc[NW + i]; bad |= tsc[2 * NW + i]; }
+  if (bad != 0) return false;
+  // bits 14..7 of T from the merged digit counts; bits 6..0 from the inline
+  // keys that share the 24-bit prefix
+  const uint32_t need_b = k - abv_all;
+  find_bin_wave<256>(sm.red, need_b, sm.found);
+  const uint32_t p24 = (A.prefix << 8) | sm.found[0];
+  const uint32_t need_c = need_b - sm.found[1];
+  uint32_t c[SPT];
+  bool lower[SPT];
+#pragma unroll
+  for (int u = 0; u < SPT; ++u) {
+    const uint32_t w = (uint32_t)(u * NW + wv);
+    const bool valid = lane >= 2 && (uint32_t)(lane - 2) < cnt[u];   // cnt is 0 past the last record
+    c[u] = valid ? wd[u] : ~0u;           // ~0u matches no prefix
+    lower[u] = valid && w < part;
+  }
+  const uint32_t dummy = LAST_BINS + (uint32_t)lane;
+#pragma unroll
+  for (int u = 0; u < SPT; ++u) atomicAdd(&sm.hist7[(c[u] >> 7) == p24 ? (c[u] & 0x7Fu) : dummy], 1u);
+  __syncthreads();
+  find_bin_wave<LAST_BINS>(sm.hist7, need_c, sm.found);
+  res.T = (p24 << 7) | sm.found[0];
+  res.r = need_c - sm.found[1];
+  // larger keys and ties in lower workgroups' records; both below 2^16
+  uint32_t ge = 0;
+#pragma unroll
+  for (int u = 0; u < SPT; ++u)
+    ge += (lower[u] && c[u] > res.T) ? 1u : ((lower[u] && c[u] == res.T) ? 0x10000u : 0u);
+  const uint32_t sge = block_sum<NT>(ge, sm.scratch);
+  res.gt_before = abv_bef + (sge & 0xFFFFu);
+  res.eq_before = sge >> 16;
+  return true;
+}
 
-  // ---- fallback: 8-bit digit passes merged through device memory, then a
-  // last digit of at most 8 bits counted per workgroup
+// The exact passes from the prefix exchange A (or B) left: 8-bit digit
+// passes merged through device memory, then a last digit of at most 8 bits
+// counted per workgroup (slots), which also gives what precedes this
+// workgroup.  `cleared`: exchange A's words have already been cleared.
+template <int NT, int R, int E, uint32_t CH>
+__device__ __forceinline__ SelResult grp_fallback(float (&v)[R][E], uint32_t P, uint32_t part, const GrpMem& g,
+                                                  GrpSelShared<grp_local_cap(CH)>& sh, GrpSmall& sm, GrpState& gs,
+                                                  uint32_t prefix, uint32_t pbits, uint32_t need, bool cleared) {
+  const int t = (int)threadIdx.x;
+  auto key = [&](int j, int i) { return mag_key(v[j][i]); };
+  const uint32_t par = gs.iter & 1u;
+  SelResult res;
   gs.used_slots = gs.used_slots || P > 1;
   for (int pass = 0; 31u - pbits > 8u; ++pass) {
     const uint32_t sh8 = 31u - pbits - 8u;         // the digit's lowest bit
     dig_zero<NT>(sh.hist);
     __syncthreads();
+    refresh(v);
 #pragma unroll
     for (int j = 0; j < R; ++j)
 #pragma unroll
@@ -460,7 +488,7 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t
       if (!cleared) { grp_clear_a(g, par, P, part); cleared = true; }
       __syncthreads();
     }
-    find_bin<NT, 256>(sm.red, need, sm.scratch, sm.found);
+    find_bin_wave<256>(sm.red, need, sm.found);
     prefix = (prefix << 8) | sm.found[0];
     pbits += 8;
     need -= sm.found[1];
@@ -471,6 +499,7 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t
   const uint32_t nbl = 1u << lb;
   dig_zero<NT>(sh.hist);
   __syncthreads();
+  refresh(v);
   uint32_t gtp = 0;   // keys with a larger prefix
 #pragma unroll
   for (int j = 0; j < R; ++j)
@@ -527,7 +556,7 @@ __device__ __forceinline__ SelResult grp_select(const float (&v)[R][E], uint32_t
     if (t < (int)DIG_BINS) { hall[t] = sm.red[t]; hbef[t] = 0u; }
   }
   __syncthreads();
-  find_bin<NT, 256>(hall, need, sm.scratch, sm.found);
+  find_bin_wave<256>(hall, need, sm.found);
   const uint32_t d = sm.found[0];
   res.T = (prefix << lb) | d;
   res.r = need - sm.found[1];

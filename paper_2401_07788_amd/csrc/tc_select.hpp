@@ -89,6 +89,33 @@ __device__ __forceinline__ void find_bin_global(const uint32_t* gh, uint32_t nee
   find_bin_loc<NT, BPT>(loc, need, scratch, found);
 }
 
+// ... with a small histogram in LDS, searched by the first wavefront alone
+// (every thread calls; all meet at the closing barrier)
+template <int NB>
+__device__ __forceinline__ void find_bin_wave(const uint32_t* h, uint32_t need, uint32_t* found) {
+  static_assert(NB % WAVE == 0, "whole bins per lane");
+  constexpr int BPL = NB / WAVE;
+  if (threadIdx.x < WAVE) {
+    const int l = lane_id();
+    uint32_t loc[BPL], sum = 0;
+#pragma unroll
+    for (int i = 0; i < BPL; ++i) {
+      loc[i] = h[l * BPL + i];
+      sum += loc[i];
+    }
+    const uint32_t incl = wave_incl_scan(sum);
+    uint32_t acc = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1) - incl;   // bins of higher lanes
+    if (acc < need && need <= acc + sum) {
+#pragma unroll
+      for (int i = BPL - 1; i >= 0; --i) {
+        if (acc + loc[i] >= need) { found[0] = (uint32_t)(l * BPL + i); found[1] = acc; break; }
+        acc += loc[i];
+      }
+    }
+  }
+  __syncthreads();
+}
+
 template <int NT>
 __device__ __forceinline__ void zero_lds(uint32_t* h, int n) {
   for (int b = (int)threadIdx.x; b < n; b += NT) h[b] = 0u;
