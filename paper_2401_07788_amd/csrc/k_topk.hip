@@ -208,6 +208,78 @@ __device__ __forceinline__ void copy_lds_skip(T* __restrict__ dst, const T* src,
   }
 }
 
+// The same for the index and value lists together, four entries per lane
+// and piece, when both destinations sit alike against their 4-entry pieces
+// (the usual case); otherwise one list after the other.
+template <int NT, typename T>
+__device__ __forceinline__ void copy_lds_skip2(uint32_t* __restrict__ di, T* __restrict__ dv, const uint32_t* si,
+                                               const T* sv, uint32_t n, const uint32_t* rem, uint32_t nr) {
+  constexpr uint32_t PER = 4;
+  const uint32_t mis = (uint32_t)(((uintptr_t)di / 4u) % PER);
+  if ((((uintptr_t)dv / sizeof(T)) % PER) != mis || ((uintptr_t)dv % sizeof(T)) != 0) {
+    copy_lds_skip<NT>(di, si, n, rem, nr);
+    copy_lds_skip<NT>(dv, sv, n, rem, nr);
+    return;
+  }
+  const uint32_t lane = (uint32_t)lane_id(), wv = threadIdx.x / WAVE;
+  const uint32_t rv = (lane < nr) ? rem[lane] : ~0u;     // lane i holds rem[i]
+  const uint32_t head = min(n, (PER - mis) % PER);
+  const uint32_t body = (n - head) / PER;
+  const uint32_t done = head + body * PER;
+  if (wv < 2) {
+    const uint32_t o0 = (wv == 0) ? 0u : done, cnt = (wv == 0) ? head : n - done;
+    uint32_t d = (uint32_t)__popcll(__ballot(rv < o0));
+    uint64_t in = __ballot(rv >= o0 && rv < o0 + PER);
+    while (in) {
+      const int i = __builtin_ctzll(in);
+      in &= in - 1;
+      d += ((uint32_t)__builtin_amdgcn_readlane((int)rv, i) <= o0 + lane) ? 1u : 0u;
+    }
+    if (lane < cnt) {
+      di[o0 + lane] = si[o0 + lane + d];
+      dv[o0 + lane] = sv[o0 + lane + d];
+    }
+  }
+  for (uint32_t base = wv * WAVE; base < body; base += NT) {
+    const uint32_t A = head + base * PER;
+    const uint32_t o = A + lane * PER;
+    const uint32_t d0 = (uint32_t)__popcll(__ballot(rv <= A));
+    uint64_t in = __ballot(rv > A && rv < A + WAVE * PER);
+    uint32_t d[PER];
+#pragma unroll
+    for (uint32_t e = 0; e < PER; ++e) d[e] = d0;
+    while (in) {
+      const int i = __builtin_ctzll(in);
+      in &= in - 1;
+      const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)rv, i);
+#pragma unroll
+      for (uint32_t e = 0; e < PER; ++e) d[e] += (r <= o + e) ? 1u : 0u;
+    }
+    if (base + lane < body) {
+      uint32_t ti[PER];
+      T tv[PER];
+#pragma unroll
+      for (uint32_t e = 0; e < PER; ++e) {
+        ti[e] = si[o + e + d[e]];
+        tv[e] = sv[o + e + d[e]];
+      }
+      u32x4 wi;
+      __builtin_memcpy(&wi, ti, 16);
+      vstore<true>(reinterpret_cast<u32x4*>(di + o), wi);
+      if constexpr (sizeof(T) == 4) {
+        u32x4 w;
+        __builtin_memcpy(&w, tv, 16);
+        vstore<true>(reinterpret_cast<u32x4*>(dv + o), w);
+      } else {
+        static_assert(sizeof(T) == 2, "16-bit or 32-bit values");
+        u32x2 w;
+        __builtin_memcpy(&w, tv, 8);
+        vstore<true>(reinterpret_cast<u32x2*>(dv + o), w);
+      }
+    }
+  }
+}
+
 // Exchange B with the payload and buffer work moved ahead (fine mode, 2 <= P
 // <= REC_P_MAX).  The 16-bit prefix `pre` of T already divides the keys:
 // those above it are kept whatever T is, those below are dropped, and only
@@ -347,6 +419,7 @@ __device__ __forceinline__ bool grp_early(const TopkArgs& a, bool vec, uint64_t 
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   }
+  grp_finish_b_lower<NT>(sm, sr);
 
   // ---- decide the keys on the prefix (at most REC_KEYS: one wavefront);
   // the kept ones get their buffer values
@@ -408,8 +481,7 @@ __device__ __forceinline__ bool grp_early(const TopkArgs& a, bool vec, uint64_t 
   if (wg_first + wg_count > a.k) {
     if (t == 0) raise_error(KERR_INTERNAL);
   } else {
-    copy_lds_skip<NT>(idx + wg_first, sh.st.idx, wg_count, sm.rem, n_drop);
-    copy_lds_skip<NT>(val + wg_first, sh.st.val, wg_count, sm.rem, n_drop);
+    copy_lds_skip2<NT>(idx + wg_first, val + wg_first, sh.st.idx, sh.st.val, wg_count, sm.rem, n_drop);
   }
   return true;
 }

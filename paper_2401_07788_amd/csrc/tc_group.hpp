@@ -372,7 +372,8 @@ __device__ __forceinline__ void grp_publish_b(uint32_t part, const GrpMem& g, co
 
 // Exchange B, second half: waits for the group, reads all records and the
 // merged digit counts in one round trip and finds T, the tie quota and the
-// larger keys and ties of lower workgroups.  Returns false (nothing decided)
+// larger keys and ties of lower workgroups (the last after one more barrier,
+// by grp_finish_b_lower).  Returns false (nothing decided)
 // when some record could not hold its keys; exchange A's words are cleared
 // either way.
 template <int NT>
@@ -439,15 +440,27 @@ __device__ __forceinline__ bool grp_finish_b(uint32_t k, uint32_t P, uint32_t pa
   find_bin_wave<LAST_BINS>(sm.hist7, need_c, sm.found);
   res.T = (p24 << 7) | sm.found[0];
   res.r = need_c - sm.found[1];
-  // larger keys and ties in lower workgroups' records; both below 2^16
+  // larger keys and ties in lower workgroups' records (both below 2^16),
+  // summed per wavefront into sm.scratch[0..NW): grp_finish_b_lower adds
+  // them up after the caller's next barrier
   uint32_t ge = 0;
 #pragma unroll
   for (int u = 0; u < SPT; ++u)
     ge += (lower[u] && c[u] > res.T) ? 1u : ((lower[u] && c[u] == res.T) ? 0x10000u : 0u);
-  const uint32_t sge = block_sum<NT>(ge, sm.scratch);
-  res.gt_before = abv_bef + (sge & 0xFFFFu);
-  res.eq_before = sge >> 16;
+  ge = wave_sum(ge);
+  if (lane == 0) sm.scratch[wv] = ge;
+  res.gt_before = abv_bef;
+  res.eq_before = 0;
   return true;
+}
+
+template <int NT>
+__device__ __forceinline__ void grp_finish_b_lower(const GrpSmall& sm, SelResult& res) {
+  uint32_t sge = 0;
+#pragma unroll
+  for (int i = 0; i < NT / WAVE; ++i) sge += sm.scratch[i];
+  res.gt_before += sge & 0xFFFFu;
+  res.eq_before = sge >> 16;
 }
 
 // The exact passes from the prefix exchange A (or B) left: 8-bit digit
