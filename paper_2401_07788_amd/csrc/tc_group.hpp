@@ -240,6 +240,7 @@ __device__ __forceinline__ SelA grp_exchange_a(float (&v)[R][E], uint32_t k, uin
   // ---- A: bits 30..19 of every key; exact zeros (common after a ReLU, and
   // the padding) are counted in registers and added once per wave, off one hot bin
   zero_lds<NT>(sh.hist, HIST_BINS);
+  if (t < 3 * 16) sm.fwin[t] = 0u;
   __syncthreads();
   uint32_t zc = 0;
 #pragma unroll
@@ -251,10 +252,8 @@ __device__ __forceinline__ SelA grp_exchange_a(float (&v)[R][E], uint32_t k, uin
       zc += z;
       atomicAdd(&sh.hist[pick(z, dummy, kk >> 19)], 1u);
     }
-  {
-    const uint32_t zs = wave_sum(zc);
-    if (lane_id() == 0 && zs) atomicAdd(&sh.hist[0], zs);
-  }
+  const uint32_t zs = wave_sum(zc);
+  if (lane_id() == 0 && zs) atomicAdd(&sh.hist[0], zs);
   __syncthreads();
 
   uint32_t prefix, pbits, need;          // known leading bits of T, keys still to place
@@ -267,9 +266,8 @@ __device__ __forceinline__ SelA grp_exchange_a(float (&v)[R][E], uint32_t k, uin
     const uint32_t bh = sm.found[0];
     lo = bh > 0u ? bh - 1u : 0u;
     hi = min(bh + 1u, (uint32_t)HIST_BINS - 1u);
-    // bits 18..15 of the non-zero keys in bins lo..hi
-    if (t < 3 * 16) sm.fwin[t] = 0u;
-    __syncthreads();
+    // bits 18..15 of the keys in bins lo..hi (the exact zeros, whose bits
+    // 18..15 are 0, once per wave)
     refresh(v);
 #pragma unroll
     for (int j = 0; j < R; ++j)
@@ -280,13 +278,7 @@ __device__ __forceinline__ SelA grp_exchange_a(float (&v)[R][E], uint32_t k, uin
         const uint32_t in = gt31(3u, b - lo) & (eq31(kk, 0u) ^ 1u) & (gt31(lo, b) ^ 1u);
         atomicAdd(&sm.fwin[pick(in, (b - lo) * 16u + ((kk >> 15) & 15u), 3u * 16u + (uint32_t)lane_id())], 1u);
       }
-    __syncthreads();
-    if (t == 0 && lo == 0u) {
-      // bin 0 also holds the exact zeros, whose bits 18..15 are 0
-      uint32_t nz = 0;
-      for (int q = 0; q < 16; ++q) nz += sm.fwin[q];
-      sm.fwin[0] += sh.hist[0] - nz;
-    }
+    if (lo == 0u && lane_id() == 0 && zs) atomicAdd(&sm.fwin[0], zs);
     __syncthreads();
     // merge into the group's counts
     uint32_t* h1 = g.hist1(par);
@@ -420,10 +412,6 @@ __device__ __forceinline__ bool grp_finish_b(uint32_t k, uint32_t P, uint32_t pa
   if (bad != 0) return false;
   // bits 14..7 of T from the merged digit counts; bits 6..0 from the inline
   // keys that share the 24-bit prefix
-  const uint32_t need_b = k - abv_all;
-  find_bin_wave<256>(sm.red, need_b, sm.found);
-  const uint32_t p24 = (A.prefix << 8) | sm.found[0];
-  const uint32_t need_c = need_b - sm.found[1];
   uint32_t c[SPT];
   bool lower[SPT];
 #pragma unroll
@@ -433,6 +421,10 @@ __device__ __forceinline__ bool grp_finish_b(uint32_t k, uint32_t P, uint32_t pa
     c[u] = valid ? wd[u] : ~0u;           // ~0u matches no prefix
     lower[u] = valid && w < part;
   }
+  const uint32_t need_b = k - abv_all;
+  find_bin_wave<256>(sm.red, need_b, sm.found);
+  const uint32_t p24 = (A.prefix << 8) | sm.found[0];
+  const uint32_t need_c = need_b - sm.found[1];
   const uint32_t dummy = LAST_BINS + (uint32_t)lane;
 #pragma unroll
   for (int u = 0; u < SPT; ++u) atomicAdd(&sm.hist7[(c[u] >> 7) == p24 ? (c[u] & 0x7Fu) : dummy], 1u);
