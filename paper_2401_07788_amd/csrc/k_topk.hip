@@ -576,6 +576,10 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
   }
 
   // ---- selection (elements past the segment's end hold +0: see grp_exchange_a)
+  // The early path (grp_early) needs registers of its own: with 16 or more
+  // fp32 values (and their residuals) per thread it would spill, so those
+  // layouts take the plain path.
+  constexpr bool EARLY = !(sizeof(Raw) == 4 && R >= 4);
   SelResult sr;
   uint32_t ticket = 0;
   const bool exiting = P > 1 && last_seg;
@@ -587,7 +591,7 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
     const SelA A = grp_exchange_a<NT, R, E, CH>(v, (uint32_t)a.k, a.L, P, part, gm, sh.sel, sm, gs);
     refresh(v);
     bool cleared = false;
-    if (A.fine && P <= REC_P_MAX) {
+    if (EARLY && A.fine && P <= REC_P_MAX) {
       if (grp_early<InT, SEL, R>(a, vec, seg, P, part, gm, sh, sm, gs, A, v, n, c0, ms, es, mlds, exiting, ticket)) {
         if (exiting) {
           grp_exit_finish<NT>(gm, P, gs, ticket, &sm.misc[0]);
