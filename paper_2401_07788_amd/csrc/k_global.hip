@@ -149,6 +149,53 @@ __device__ __forceinline__ void load_tile_values(const GlobalArgs& a, uint64_t t
   }
 }
 
+// One thread's 16 elements of a whole tile as loaded (16-byte accesses),
+// fetched one tile ahead in the band and emit passes, so that the next
+// tile's loads are in flight while this one is worked on.
+template <typename InT, bool EF>
+struct TileRaw {
+  static constexpr int XW = G_VPT * (int)sizeof(typename Elem<InT>::raw) / 16;
+  u32x4 x[XW];
+  u32x4 e[EF ? G_VPT / 4 : 1];
+};
+// whole 16-byte runs: both arrays 16-byte aligned
+__device__ __forceinline__ bool tiles_prefetchable(const GlobalArgs& a) {
+  return (((uintptr_t)a.x | (uintptr_t)a.e) & 15u) == 0;
+}
+// the tile lies wholly inside the segment
+__device__ __forceinline__ bool tile_whole(const GlobalArgs& a, uint64_t tile) {
+  return tile < a.n_tiles && (tile + 1) * G_TILE <= a.L;
+}
+template <typename InT, bool EF>
+__device__ __forceinline__ void tile_fetch(const GlobalArgs& a, uint64_t tile, TileRaw<InT, EF>& r) {
+  using R = typename Elem<InT>::raw;
+  const uint64_t t0 = tile * G_TILE + (uint64_t)threadIdx.x * G_VPT;
+  const u32x4* px = reinterpret_cast<const u32x4*>((const R*)a.x + t0);
+#pragma unroll
+  for (int i = 0; i < TileRaw<InT, EF>::XW; ++i) r.x[i] = __builtin_nontemporal_load(px + i);
+  if constexpr (EF) {
+    const u32x4* pe = reinterpret_cast<const u32x4*>(a.e + t0);
+#pragma unroll
+    for (int i = 0; i < G_VPT / 4; ++i) r.e[i] = __builtin_nontemporal_load(pe + i);
+  }
+}
+template <typename InT, bool EF>
+__device__ __forceinline__ void tile_values(const TileRaw<InT, EF>& r, float (&v)[G_VPT]) {
+  using R = typename Elem<InT>::raw;
+#pragma unroll
+  for (int i = 0; i < G_VPT; ++i) {
+    float x;
+    if constexpr (sizeof(R) == 4) {
+      x = __uint_as_float(r.x[i / 4][i % 4]);
+    } else {
+      const uint32_t w = r.x[i / 8][(i % 8) / 2];
+      x = Elem<InT>::up((R)((i & 1) ? (w >> 16) : (w & 0xFFFFu)));
+    }
+    if constexpr (EF) x = x + __uint_as_float(r.e[i / 4][i % 4]);
+    v[i] = x;
+  }
+}
+
 __device__ __forceinline__ void zero_lds_bins(uint32_t* h, int nb) {
   for (int b = threadIdx.x; b < nb; b += G_NT) h[b] = 0u;
 }
@@ -268,11 +315,18 @@ __global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
   };
   float amin = __builtin_inff(), amax = -__builtin_inff();
   uint32_t above_all = 0;   // workgroup-uniform
+  const bool pf = tiles_prefetchable(a);
+  TileRaw<InT, EF> nxt;
+  bool have = pf && tile_whole(a, blockIdx.x);
+  if (have) tile_fetch<InT, EF>(a, blockIdx.x, nxt);
   for (uint64_t tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
     const uint64_t t0 = tile * G_TILE + (uint64_t)threadIdx.x * G_VPT;
     const int nv = (int)min((uint64_t)G_VPT, sat_sub(a.L, t0));
     float v[G_VPT];
-    load_tile_values<InT, EF>(a, t0, nv, v);
+    if (have) tile_values<InT, EF>(nxt, v);
+    else load_tile_values<InT, EF>(a, t0, nv, v);
+    have = pf && tile_whole(a, tile + gridDim.x);
+    if (have) tile_fetch<InT, EF>(a, tile + gridDim.x, nxt);
     uint32_t inb = 0, above = 0;
 #pragma unroll
     for (int i = 0; i < G_VPT; ++i) {
@@ -611,35 +665,44 @@ __device__ __forceinline__ void write_codes(uint32_t* codes, uint64_t wpg, uint6
   }
 }
 
-// Q = 0: TopK values in the input dtype; Q = b: the kept list quantized
+// Q = 0: TopK values in the input dtype; Q = b: the kept list quantized.
+// Per tile: (1) every thread marks its kept entries (bit masks), the tile's
+// values go to LDS and the kept entries' offsets are compacted there; (2)
+// the kept entries alone (about one in ten) are encoded, written to the
+// payload, and their residual replaces the value in LDS; (3) the dense
+// residual leaves from LDS.  Per-element work is thus only the two key
+// comparisons; the encoding runs on the compacted list.
 template <typename InT, bool EF, uint32_t Q>
 __global__ __launch_bounds__(G_NT) void k_g_emit(GlobalArgs a) {
   using R = typename Elem<InT>::raw;
   constexpr bool QK = Q != 0;
-  // staged payload of one tile: offsets in the tile, and the wire value, the
-  // b-bit code, or the binary32 bits (b = 32); small, so that many tiles are
-  // in flight per compute unit
-  using SV = std::conditional_t<Q == 0, R, std::conditional_t<Q == 32, uint32_t, uint8_t>>;
-  __shared__ uint16_t s_off[G_TILE];
-  __shared__ SV s_val[G_TILE];
+  constexpr bool CODES = QK && Q != 32;   // b-bit codes, packed from LDS
+  __shared__ __attribute__((aligned(16))) uint32_t s_v[G_TILE];   // the tile's values (binary32 bits)
+  __shared__ uint16_t s_off[G_TILE];        // kept entries' offsets in the tile, in order
+  __shared__ uint8_t s_code[CODES ? G_TILE : 1];
   __shared__ uint32_t scratch[G_NT / WAVE + 2];
   __shared__ float s_mm[2 * (G_NT / WAVE)];
   uint32_t* st = a.state;
-  const uint32_t T = (a.k == 0) ? 0xFFFFFFFFu : st[ST_T];
-  const uint32_t r = (a.k == 0) ? 0u : st[ST_R];
+  const bool none = a.k == 0;
+  const uint32_t T = none ? 0u : st[ST_T];
+  const uint32_t r = none ? 0u : st[ST_R];
   // quantize here when lo / hi are known (always for b = 32)
   const bool pre = QK && (Q == 32 || st[ST_PRE] != 0u);
   float lo = 0.0f, range = 0.0f, scale = 0.0f;
-  if (QK && Q != 32 && pre) {
+  if (CODES && pre) {
     lo = __uint_as_float(st[ST_LO]);
     range = __uint_as_float(st[ST_HI]) - lo;
     scale = __uint_as_float(st[ST_SCALE]);
   }
   float kmin = __builtin_inff(), kmax = -__builtin_inff();
+  const bool pf = tiles_prefetchable(a);
+  TileRaw<InT, EF> nxt;
+  bool have = pf && tile_whole(a, blockIdx.x);
+  if (have) tile_fetch<InT, EF>(a, blockIdx.x, nxt);
   for (uint64_t tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
     // the tile's offset (from tcount), loaded together with its data
     uint32_t gt_before = 0, eq_before = 0, rec_gt = 0, rec_eq = 0;
-    if (a.k > 0) {
+    if (!none) {
       // 8-byte loads: the workspace is 8-byte aligned
       const u32x2 cnt2 = *reinterpret_cast<const u32x2*>(a.tiles + 4 * tile);
       const u32x2 pre2 = *reinterpret_cast<const u32x2*>(a.tiles + 4 * tile + 2);
@@ -652,85 +715,100 @@ __global__ __launch_bounds__(G_NT) void k_g_emit(GlobalArgs a) {
     const uint64_t t0 = tile * G_TILE + (uint64_t)threadIdx.x * G_VPT;
     const int nv = (int)min((uint64_t)G_VPT, sat_sub(a.L, t0));
     float v[G_VPT];
-    load_tile_values<InT, EF>(a, t0, nv, v);
-    uint32_t gt = 0, eq = 0;
+    if (have) tile_values<InT, EF>(nxt, v);
+    else load_tile_values<InT, EF>(a, t0, nv, v);
+    have = pf && tile_whole(a, tile + gridDim.x);
+    if (have) tile_fetch<InT, EF>(a, tile + gridDim.x, nxt);
+    // ---- (1) keys > T and == T as bit masks (bit i: element i); keys
+    // and T stay below 2^31, so the sign bit of a difference compares them
+    uint32_t gm = 0, em = 0;
 #pragma unroll
     for (int i = 0; i < G_VPT; ++i) {
-      if (i < nv) {
-        const uint32_t kk = mag_key(v[i]);
-        gt += kk > T;
-        eq += kk == T;
-      }
+      const uint32_t kk = mag_key(v[i]);
+      gm |= ((T - kk) >> 31) << i;
+      em |= (((kk ^ T) - 1u) >> 31) << i;
+    }
+    const uint32_t valid = (nv >= G_VPT) ? 0xFFFFu : ((1u << max(nv, 0)) - 1u);
+    gm &= none ? 0u : valid;
+    em &= none ? 0u : valid;
+#pragma unroll
+    for (int q = 0; q < G_VPT / 4; ++q) {
+      u32x4 w;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = __float_as_uint(v[4 * q + i]);
+      *reinterpret_cast<u32x4*>(&s_v[threadIdx.x * G_VPT + 4 * q]) = w;
     }
     uint32_t tot;
-    const uint32_t ex = block_excl_scan<G_NT>(gt | (eq << 16), scratch, tot);
+    const uint32_t ex = block_excl_scan<G_NT>((uint32_t)__builtin_popcount(gm) | ((uint32_t)__builtin_popcount(em) << 16),
+                                             scratch, tot);
     const uint32_t gt_t = tot & 0xFFFFu, eq_t = tot >> 16;
-    if (a.k > 0 && threadIdx.x == 0 && (rec_gt != gt_t || rec_eq != eq_t)) raise_error(KERR_INTERNAL);
+    if (!none && threadIdx.x == 0 && (rec_gt != gt_t || rec_eq != eq_t)) raise_error(KERR_INTERNAL);
     // ---- placement inside the tile (ties: the lowest indices overall)
     const uint32_t quota_t = min(sat_sub(r, eq_before), eq_t);
     const uint32_t gt_ex = ex & 0xFFFFu, eq_ex = ex >> 16;
     const uint32_t tile_first = gt_before + min(eq_before, r);
     const uint32_t cnt = gt_t + quota_t;
+    uint32_t tie_keep = min(sat_sub(quota_t, eq_ex), (uint32_t)G_VPT);
+    uint32_t km = gm, rest = em;             // kept: larger keys and the first tie_keep ties
+    for (; tie_keep && rest; --tie_keep) {
+      km |= rest & (0u - rest);
+      rest &= rest - 1u;
+    }
     uint32_t lp = gt_ex + min(eq_ex, quota_t);   // position in the tile's part of the payload
-    const uint32_t tie_keep = min(sat_sub(quota_t, eq_ex), (uint32_t)G_VPT);
-    uint32_t ties = 0;
-#pragma unroll
-    for (int i = 0; i < G_VPT; ++i) {
-      bool kept = false;
-      if (i < nv) {
-        const uint32_t kk = mag_key(v[i]);
-        const bool tie = kk == T;
-        kept = kk > T || (tie && ties < tie_keep);
-        ties += tie ? 1u : 0u;
-      }
-      float rec = 0.0f;   // what the receiver holds here (binary32 before its rounding)
-      if (kept) {
-        if (lp < G_TILE) {
-          s_off[lp] = (uint16_t)(threadIdx.x * G_VPT + i);
-          if constexpr (!QK) {
-            s_val[lp] = Elem<InT>::down(v[i]);
-            rec = v[i];
-          } else if constexpr (Q == 32) {
-            s_val[lp] = __float_as_uint(v[i]);
-            rec = v[i];
-          } else {
-            if (pre) {
-              const uint32_t c = quant_code<Q>(v[i], lo, range);
-              s_val[lp] = (uint8_t)c;
-              const float prod = (float)c * scale;
-              rec = lo + prod;
-            }
-          }
-        } else {
-          raise_error(KERR_INTERNAL);
-        }
-        ++lp;
-        if constexpr (QK && Q != 32) { kmin = fminf(kmin, v[i]); kmax = fmaxf(kmax, v[i]); }
-      }
-      if constexpr (EF) {
-        // the residual, in place; without lo / hi the kept entries keep X
-        // here and qpack corrects them
-        v[i] = (kept && (!QK || pre)) ? v[i] - through<InT>(rec) : v[i] - 0.0f;
-      }
+    if (lp + (uint32_t)__builtin_popcount(km) > G_TILE) {
+      raise_error(KERR_INTERNAL);
+      km = 0;
     }
-    if constexpr (EF) {
-      // write-back stores: the four 16-byte stores of a thread fill each
-      // 128-byte line only together, which the L2 merges before writing it
-      if (nv > 0) store_run_partial<float, G_VPT, false>(a.e + t0, nv, v);
-    }
+    for (uint32_t m = km; m; m &= m - 1u) s_off[lp++] = (uint16_t)(threadIdx.x * G_VPT + (uint32_t)__builtin_ctz(m));
     if (a.blk && threadIdx.x == 0) a.blk[tile] = tile_first;
     __syncthreads();
-    // ---- the tile's payload entries, coalesced
+    // ---- (2) the tile's kept entries, compacted: payload, and the
+    // residual at their places in LDS
     const uint32_t n_ok = (uint32_t)min((uint64_t)cnt, sat_sub(a.k, (uint64_t)tile_first));
     if (n_ok < cnt && threadIdx.x == 0) raise_error(KERR_INTERNAL);
     for (uint32_t j = threadIdx.x; j < n_ok; j += G_NT) {
+      const uint32_t off = s_off[j];
+      const float x = __uint_as_float(s_v[off]);
       const uint64_t g = (uint64_t)tile_first + j;
-      a.idx[g] = (uint32_t)(tile * G_TILE + s_off[j]);
-      if constexpr (!QK) ((R*)a.val)[g] = s_val[j];
-      if constexpr (Q == 32) a.codes[g] = s_val[j];
+      a.idx[g] = (uint32_t)(tile * G_TILE + off);
+      float rec = x;   // what the receiver holds here (binary32 before its rounding)
+      bool enc = true;
+      if constexpr (!QK) ((R*)a.val)[g] = Elem<InT>::down(x);
+      if constexpr (Q == 32) a.codes[g] = __float_as_uint(x);
+      if constexpr (CODES) {
+        if (pre) {
+          const uint32_t c = quant_code<Q>(x, lo, range);
+          s_code[j] = (uint8_t)c;
+          const float prod = (float)c * scale;
+          rec = lo + prod;
+        } else {
+          // without lo / hi the kept entries keep X in the residual and
+          // qpack corrects them
+          kmin = fminf(kmin, x);
+          kmax = fmaxf(kmax, x);
+          enc = false;
+        }
+      }
+      if constexpr (EF) {
+        if (enc) s_v[off] = __float_as_uint(x - through<InT>(rec));
+      }
     }
-    if constexpr (QK && Q != 32) {
-      if (pre) write_codes<Q>(a.codes, a.wpg, tile_first, n_ok, s_val, true);
+    __syncthreads();
+    if constexpr (CODES) {
+      if (pre) write_codes<Q>(a.codes, a.wpg, tile_first, n_ok, s_code, true);
+    }
+    // ---- (3) the dense residual; write-back stores: the four 16-byte
+    // stores of a thread fill each 128-byte line only together, which the
+    // L2 merges before writing it
+    if constexpr (EF) {
+      float res[G_VPT];
+#pragma unroll
+      for (int q = 0; q < G_VPT / 4; ++q) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[threadIdx.x * G_VPT + 4 * q]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) res[4 * q + i] = __uint_as_float(w[i]);
+      }
+      if (nv > 0) store_run_partial<float, G_VPT, false>(a.e + t0, nv, res);
     }
     __syncthreads();
   }
@@ -738,7 +816,7 @@ __global__ __launch_bounds__(G_NT) void k_g_emit(GlobalArgs a) {
     if (a.blk) a.blk[a.n_tiles] = (uint32_t)a.k;
     if constexpr (Q == 32) { a.meta[0] = 0.0f; a.meta[1] = 0.0f; }
   }
-  if constexpr (QK && Q != 32) {
+  if constexpr (CODES) {
     if (!pre) {
       block_minmax<G_NT>(kmin, kmax, s_mm);
       if (threadIdx.x == 0) push_minmax(st, ST_MIN, ST_MAX, kmin, kmax);
@@ -886,6 +964,15 @@ hipError_t launch(const void* fn, uint32_t grid, uint32_t nt, const GlobalArgs& 
   return hipLaunchKernel(fn, dim3(grid), dim3(nt), params, 0, st);
 }
 
+// a tile loop's grid: no more workgroups than the compute units hold at once
+// (the rest would start only when the first ones have gone through all
+// their tiles, and run the last stretch at a fraction of the occupancy)
+uint32_t resident_grid(const void* fn, uint32_t grid) {
+  int per_cu = 0;
+  if (!fn || hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, G_NT, 0) != hipSuccess || per_cu < 1) return grid;
+  return std::max<uint32_t>(1, std::min<uint32_t>(grid, (uint32_t)per_cu * (uint32_t)device_cus()));
+}
+
 uint64_t cand_capacity(uint64_t L) { return L / 4 + 4096; }
 
 }  // namespace
@@ -930,14 +1017,20 @@ hipError_t launch_global(int dt, bool ef, uint32_t qbits, const GlobalArgs& args
     const uint64_t n_s = (a.n_tiles + a.sample_stride - 1) / a.sample_stride;
     const uint32_t sgrid = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(n_s, SAMPLE_GRID));
     e = launch(pick_chain(dt, ef, 0), sgrid, G_NT, a, st);
-    for (int which = 1; which <= 4 && e == hipSuccess; ++which) e = launch(pick_chain(dt, ef, which), grid, G_NT, a, st);
+    for (int which = 1; which <= 4 && e == hipSuccess; ++which) {
+      const void* fn = pick_chain(dt, ef, which);
+      e = launch(fn, resident_grid(fn, grid), G_NT, a, st);
+    }
     if (e == hipSuccess && qbits != 0 && qbits != 32) e = launch((const void*)k_g_keptmm, CAND_GRID, G_NT, a, st);
     if (e == hipSuccess) {
       const uint32_t tgrid = (uint32_t)((a.n_tiles + a.tpw - 1) / a.tpw);
       e = launch(pick_chain(dt, ef, 5), tgrid, G_NT, a, st);
     }
   }
-  if (e == hipSuccess) e = launch(pick_emit(dt, ef, qbits), grid, G_NT, a, st);
+  if (e == hipSuccess) {
+    const void* fn = pick_emit(dt, ef, qbits);
+    e = launch(fn, resident_grid(fn, grid), G_NT, a, st);
+  }
   if (e == hipSuccess && qbits != 0 && qbits != 32) {
     const uint64_t work = (a.k + QP_CH - 1) / QP_CH;
     const uint32_t qgrid = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(work, (uint64_t)cus * 8));
