@@ -281,6 +281,7 @@ constexpr uint32_t TL_MAX = 64;   // band: tiles with buffered candidates before
 template <typename InT, bool EF>
 __global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
   __shared__ uint32_t s_cand[CBUF];
+  __shared__ __attribute__((aligned(16))) uint32_t s_vals[G_TILE];   // one tile's values, when it has candidates
   __shared__ uint32_t s_tl_tile[TL_MAX], s_tl_pos[TL_MAX];
   __shared__ uint32_t scratch[G_NT / WAVE + 2];
   __shared__ uint32_t s_base;
@@ -327,15 +328,21 @@ __global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
     else load_tile_values<InT, EF>(a, t0, nv, v);
     have = pf && tile_whole(a, tile + gridDim.x);
     if (have) tile_fetch<InT, EF>(a, tile + gridDim.x, nxt);
-    uint32_t inb = 0, above = 0;
+    // above the band / inside it, as bit masks (bit i: element i); digits
+    // are 12-bit, so the sign bit of a difference compares them
+    uint32_t am = 0, bm = 0;
 #pragma unroll
     for (int i = 0; i < G_VPT; ++i) {
-      if (i < nv) {
-        const uint32_t dg = mag_key(v[i]) >> 19;
-        if (dg > bhi) { ++above; amin = fminf(amin, v[i]); amax = fmaxf(amax, v[i]); }
-        else if (dg >= blo) ++inb;
-      }
+      const uint32_t dg = mag_key(v[i]) >> 19;
+      const uint32_t up = (bhi - dg) >> 31;
+      am |= up << i;
+      bm |= ((~((dg - blo) | (bhi - dg))) >> 31) << i;
+      amin = fminf(amin, up ? v[i] : __builtin_inff());
+      amax = fmaxf(amax, up ? v[i] : -__builtin_inff());
     }
+    const uint32_t valid = (nv >= G_VPT) ? 0xFFFFu : ((1u << max(nv, 0)) - 1u);
+    bm &= valid;
+    const uint32_t above = (uint32_t)__builtin_popcount(am & valid), inb = (uint32_t)__builtin_popcount(bm);
     uint32_t tot;
     uint32_t off = block_excl_scan<G_NT>(inb | (above << 16), scratch, tot) & 0xFFFFu;
     const uint32_t n_t = tot & 0xFFFFu, ab_t = tot >> 16;
@@ -348,14 +355,16 @@ __global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
       if (n_t) { s_tl_tile[ntl] = (uint32_t)tile; s_tl_pos[ntl] = nbuf; }
     }
     if (n_t) {
-      off += nbuf;
+      // the values go through LDS so that only the set bits are visited
 #pragma unroll
-      for (int i = 0; i < G_VPT; ++i) {
-        if (i < nv) {
-          const uint32_t dg = mag_key(v[i]) >> 19;
-          if (dg <= bhi && dg >= blo) s_cand[off++] = __float_as_uint(v[i]);
-        }
+      for (int q = 0; q < G_VPT / 4; ++q) {
+        u32x4 w;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) w[i] = __float_as_uint(v[4 * q + i]);
+        *reinterpret_cast<u32x4*>(&s_vals[threadIdx.x * G_VPT + 4 * q]) = w;
       }
+      off += nbuf;
+      for (uint32_t m = bm; m; m &= m - 1u) s_cand[off++] = s_vals[threadIdx.x * G_VPT + (uint32_t)__builtin_ctz(m)];
       nbuf += n_t;
       ++ntl;
     }
