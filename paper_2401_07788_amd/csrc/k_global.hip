@@ -137,10 +137,10 @@ template <typename InT, bool EF>
 __device__ __forceinline__ void load_tile_values(const GlobalArgs& a, uint64_t t0, int nv, float (&v)[G_VPT]) {
   using R = typename Elem<InT>::raw;
   R xr[G_VPT];
-  if (nv > 0) load_run_partial<R, G_VPT, true>((const R*)a.x + t0, nv, R{}, xr);
+  if (nv > 0) load_run_partial<R, G_VPT, false>((const R*)a.x + t0, nv, R{}, xr);
   if constexpr (EF) {
     float er[G_VPT];
-    if (nv > 0) load_run_partial<float, G_VPT, true>(a.e + t0, nv, 0.0f, er);
+    if (nv > 0) load_run_partial<float, G_VPT, false>(a.e + t0, nv, 0.0f, er);
 #pragma unroll
     for (int i = 0; i < G_VPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) + er[i] : 0.0f;
   } else {
@@ -172,11 +172,11 @@ __device__ __forceinline__ void tile_fetch(const GlobalArgs& a, uint64_t tile, T
   const uint64_t t0 = tile * G_TILE + (uint64_t)threadIdx.x * G_VPT;
   const u32x4* px = reinterpret_cast<const u32x4*>((const R*)a.x + t0);
 #pragma unroll
-  for (int i = 0; i < TileRaw<InT, EF>::XW; ++i) r.x[i] = __builtin_nontemporal_load(px + i);
+  for (int i = 0; i < TileRaw<InT, EF>::XW; ++i) r.x[i] = px[i];
   if constexpr (EF) {
     const u32x4* pe = reinterpret_cast<const u32x4*>(a.e + t0);
 #pragma unroll
-    for (int i = 0; i < G_VPT / 4; ++i) r.e[i] = __builtin_nontemporal_load(pe + i);
+    for (int i = 0; i < G_VPT / 4; ++i) r.e[i] = pe[i];
   }
 }
 template <typename InT, bool EF>

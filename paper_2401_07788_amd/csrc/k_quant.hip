@@ -69,10 +69,10 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
     float v[QVPT];
     {
       R xr[QVPT];
-      if (nv > 0) load_run_partial<R, QVPT, true>((const R*)a.x + off, nv, R{}, xr);
+      if (nv > 0) load_run_partial<R, QVPT, false>((const R*)a.x + off, nv, R{}, xr);
       if constexpr (EF) {
         float er[QVPT];
-        if (nv > 0) load_run_partial<float, QVPT, true>(a.e + off, nv, 0.0f, er);
+        if (nv > 0) load_run_partial<float, QVPT, false>(a.e + off, nv, 0.0f, er);
 #pragma unroll
         for (int i = 0; i < QVPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) + er[i] : 0.0f;
       } else {
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(NT) void k_quant_unpack(UnpackArgs a) {
     const uint64_t wo = (B == 32) ? c0 : (c0 * (uint64_t)B) / 32u;
     const int nw = (int)min((uint64_t)WPT, sat_sub(a.wpg, wo));
     uint32_t w[WPT];
-    load_run_partial<uint32_t, WPT, true>(a.codes + grp * a.wpg + wo, nw, 0u, w);
+    load_run_partial<uint32_t, WPT, false>(a.codes + grp * a.wpg + wo, nw, 0u, w);
     R y[QVPT];
     if constexpr (B == 32) {
 #pragma unroll

@@ -226,7 +226,7 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
       // row chunk and payload groups, all loads in flight together
 #pragma unroll
       for (int q = 0; q < VPT / PER; ++q) {
-        const u32x4 w = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(row + t0) + q);
+        const u32x4 w = reinterpret_cast<const u32x4*>(row + t0)[q];
         __builtin_memcpy(&mr[q * PER], &w, 16);
       }
       j0 = bj0;
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
      }
     }
     if (!done) {
-      if (nv > 0) load_run_partial<R, VPT, true>(row + t0, nv, R{}, mr);
+      if (nv > 0) load_run_partial<R, VPT, false>(row + t0, nv, R{}, mr);
       const uint32_t* ix = a.idx + b * a.k;
       const uint32_t* bt = a.blk ? a.blk + b * nbt : nullptr;
       chunk_range(ix, bt, a.k, c0, c1, scratch, j0, j1);
@@ -274,13 +274,14 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
     if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
     __syncthreads();
     // the updated row chunk to the buffer and to a_hat: thread-contiguous
-    // runs, so that each store instruction of a wavefront covers whole lines
+    // runs of two 16-byte stores, write-back so that the L2 merges the
+    // halves of each line
     if (full) {
 #pragma unroll
       for (int q = 0; q < VPT / PER; ++q) {
         const u32x4 w = *reinterpret_cast<const u32x4*>(&buf[threadIdx.x * VPT + q * PER]);
-        __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(row + t0) + q);
-        __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(out + t0) + q);
+        reinterpret_cast<u32x4*>(row + t0)[q] = w;
+        reinterpret_cast<u32x4*>(out + t0)[q] = w;
       }
     } else {
       copy_lds_to_global<SC_NT, R>(row + c0, buf, (uint32_t)(c1 - c0));

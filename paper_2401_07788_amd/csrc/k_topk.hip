@@ -64,14 +64,14 @@ __global__ __launch_bounds__(WAVE) void k_topk_row(TopkArgs a) {
     {
       R xr[VPT];
       const uint64_t off = seg * a.L + c0;
-      if (nv > 0) load_run_partial<R, VPT, true>((const R*)a.x + off, nv, R{}, xr);
+      if (nv > 0) load_run_partial<R, VPT, false>((const R*)a.x + off, nv, R{}, xr);
       if constexpr (SEL == SEL_EF) {
         float er[VPT];
-        if (nv > 0) load_run_partial<float, VPT, true>(a.e + off, nv, 0.0f, er);
+        if (nv > 0) load_run_partial<float, VPT, false>(a.e + off, nv, 0.0f, er);
 #pragma unroll
         for (int i = 0; i < VPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) + er[i] : 0.0f;
       } else if constexpr (SEL == SEL_AQSGD) {
-        if (nv > 0) load_run_partial<R, VPT, true>((const R*)a.m + mrow + c0, nv, R{}, mr);
+        if (nv > 0) load_run_partial<R, VPT, false>((const R*)a.m + mrow + c0, nv, R{}, mr);
 #pragma unroll
         for (int i = 0; i < VPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) - Elem<InT>::up(mr[i]) : 0.0f;
       } else {
@@ -398,8 +398,8 @@ __device__ __forceinline__ bool grp_early(const TopkArgs& a, bool vec, uint64_t 
     }
     if (vec && n[j] == E) {
       if constexpr (SEL == SEL_EF) {
-        store16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&eo[0]));
-        if constexpr (E == 8) store16<float, 4, true>(es + off + 4, *reinterpret_cast<float(*)[4]>(&eo[4]));
+        store16<float, 4, E == 4>(es + off, *reinterpret_cast<float(*)[4]>(&eo[0]));
+        if constexpr (E == 8) store16<float, 4, false>(es + off + 4, *reinterpret_cast<float(*)[4]>(&eo[4]));
       }
       if constexpr (SEL == SEL_AQSGD) store16<Raw, E, true>(ms + off, mr);
     } else if (n[j] > 0) {
@@ -440,11 +440,11 @@ __device__ __forceinline__ bool grp_early(const TopkArgs& a, bool vec, uint64_t 
         const Raw w = sh.st.val[sm.cpos[t]];
         if constexpr (SEL == SEL_AQSGD) {
           const Raw upd = Elem<InT>::down(Elem<InT>::up(mlds[off]) + Elem<InT>::up(w));
-          __builtin_nontemporal_store(upd, ms + off);
+          ms[off] = upd;
         }
         if constexpr (SEL == SEL_EF) {
           const float x = __uint_as_float(key | (__float_as_uint(Elem<InT>::up(w)) & 0x80000000u));
-          __builtin_nontemporal_store(x - Elem<InT>::up(w), es + off);
+          es[off] = x - Elem<InT>::up(w);
         }
       }
     }
@@ -543,8 +543,8 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
         if constexpr (E == 4) {
           load16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&er[j][0]));
         } else {
-          load16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&er[j][0]));
-          load16<float, 4, true>(es + off + 4, *reinterpret_cast<float(*)[4]>(&er[j][4]));
+          load16<float, 4, false>(es + off, *reinterpret_cast<float(*)[4]>(&er[j][0]));
+          load16<float, 4, false>(es + off + 4, *reinterpret_cast<float(*)[4]>(&er[j][4]));
         }
       }
     } else {
@@ -675,15 +675,16 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
       }
       if constexpr (SEL == SEL_EF) eo[i] = v[j][i] - __uint_as_float(pick(kept, __float_as_uint(through<InT>(v[j][i])), 0u));
     }
-    // one store instruction of a wavefront covers 1 KiB here: non-temporal
-    // stores write whole lines
+    // a run of 16 bytes per lane is one store instruction covering 1 KiB
+    // (non-temporal: whole lines); an fp32 residual of 8 elements is two per
+    // lane, which write-back stores let the L2 merge
     if (vec && n[j] == E) {
       if constexpr (SEL == SEL_EF) {
         if constexpr (E == 4) {
           store16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&eo[0]));
         } else {
-          store16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&eo[0]));
-          store16<float, 4, true>(es + off + 4, *reinterpret_cast<float(*)[4]>(&eo[4]));
+          store16<float, 4, false>(es + off, *reinterpret_cast<float(*)[4]>(&eo[0]));
+          store16<float, 4, false>(es + off + 4, *reinterpret_cast<float(*)[4]>(&eo[4]));
         }
       }
       if constexpr (SEL == SEL_AQSGD) store16<Raw, E, true>(ms + off, mr[j]);

@@ -83,12 +83,13 @@ __device__ __forceinline__ void refresh(float (&v)[R][E]) {
 // Uses 16-byte accesses when the run is 16-byte aligned and a multiple of 16
 // bytes, else 8-byte, else scalar accesses.  STREAM marks data touched once
 // per launch (the boundary tensors): those accesses carry the non-temporal
-// hint so that they do not displace reused lines.  Stores take the hint only
-// where one instruction of a wavefront covers whole 128-byte lines (lane-
-// contiguous 16-byte stores, copy_lds_to_global): a thread's run of several
-// 16-byte stores fills each line only across instructions, which non-
-// temporal stores write out piecewise (measured: up to 1.8x the bytes);
-// write-back stores let the L2 merge them first.
+// hint so that they do not displace reused lines.  Loads and stores take the
+// hint only where one instruction of a wavefront covers whole 128-byte lines
+// (lane-contiguous 16-byte accesses, copy_lds_to_global).  A thread's run of
+// several 16-byte accesses covers each line only across instructions: with
+// the hint, loads then fetch a line more than once and stores write it out
+// piecewise (measured: up to 1.8x the bytes), while cached loads and write-
+// back stores let the L2 serve and merge the pieces.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
