@@ -73,7 +73,7 @@ template <typename WireT, typename OutT, int MODE, int B>
 __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
   using RW = typename Elem<WireT>::raw;
   using RO = typename Elem<OutT>::raw;
-  __shared__ RO buf[SC_CH];
+  __shared__ __attribute__((aligned(16))) RO buf[SC_CH];
   __shared__ uint32_t scratch[SC_NT / WAVE + 2];
   const uint64_t nch = (a.L + SC_CH - 1) / SC_CH;
   for (uint64_t wi = blockIdx.x; wi < a.n_seg * nch; wi += gridDim.x) {
@@ -115,7 +115,8 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
         }
       }
     }
-    for (int i = (int)threadIdx.x; i < (int)SC_CH; i += SC_NT) buf[i] = RO{};
+    static_assert((SC_CH * sizeof(RO)) % (16 * SC_NT) == 0, "the chunk zeroes in 16-byte pieces");
+    for (uint32_t i = threadIdx.x; i < SC_CH * sizeof(RO) / 16; i += SC_NT) reinterpret_cast<u32x4*>(buf)[i] = u32x4{0u, 0u, 0u, 0u};
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < SC_EPT; ++r) {
@@ -192,7 +193,7 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
   constexpr int VPT = (int)(SC_CH / SC_NT);           // elements per thread
   constexpr int GPT = 2;                              // payload groups per thread held in registers
   static_assert(VPT % PER == 0, "whole 16-byte runs per thread");
-  __shared__ R buf[SC_CH];
+  __shared__ __attribute__((aligned(16))) R buf[SC_CH];
   __shared__ uint32_t scratch[SC_NT / WAVE + 2];
   const uint64_t nch = (a.L + SC_CH - 1) / SC_CH;
   const uint64_t nbt = n_blocks(a.L) + 1;

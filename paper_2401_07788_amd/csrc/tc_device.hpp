@@ -194,13 +194,19 @@ __device__ __forceinline__ void copy_lds_to_global(R* __restrict__ dst, const R*
   const uint32_t body = (n - head) / PER;
   const int t = (int)threadIdx.x;
   if ((uint32_t)t < head) dst[t] = src[t];
-  for (uint32_t q = (uint32_t)t; q < body; q += NT) {
-    R tmp[PER];
+  if ((((uintptr_t)(src + head)) & 15u) == 0) {
+    // source pieces 16-byte aligned as well: one LDS read each
+    const u32x4* s4 = reinterpret_cast<const u32x4*>(src + head);
+    for (uint32_t q = (uint32_t)t; q < body; q += NT) vstore<true>(reinterpret_cast<u32x4*>(dst + head + q * PER), s4[q]);
+  } else {
+    for (uint32_t q = (uint32_t)t; q < body; q += NT) {
+      R tmp[PER];
 #pragma unroll
-    for (uint32_t i = 0; i < PER; ++i) tmp[i] = src[head + q * PER + i];
-    u32x4 w;
-    __builtin_memcpy(&w, tmp, 16);
-    vstore<true>(reinterpret_cast<u32x4*>(dst + head + q * PER), w);
+      for (uint32_t i = 0; i < PER; ++i) tmp[i] = src[head + q * PER + i];
+      u32x4 w;
+      __builtin_memcpy(&w, tmp, 16);
+      vstore<true>(reinterpret_cast<u32x4*>(dst + head + q * PER), w);
+    }
   }
   const uint32_t done = head + body * PER;
   if ((uint32_t)t < n - done) dst[done + t] = src[done + t];
