@@ -764,6 +764,196 @@ __global__ __launch_bounds__(GRP_NT) void k_topk_grp(TopkArgs a) {
   }
 }
 
+// ------------------------------------------------------------- LDS engine
+// One workgroup per segment of up to LDS_MAX elements (per-sample CNN
+// activations and gradients): the segment's values v = x (+ e) stay in LDS
+// as binary32 for the whole selection, so no other workgroup takes part and
+// nothing crosses the workgroup.  Loads are lane-consecutive 4-element
+// pieces; three digit passes over LDS (key bits 30..19, 18..7, 6..0) give T
+// and the tie quota; then thread t places its run of LDS_RUN consecutive
+// elements (kept-entry bit masks, one scan), writes its kept entries to the
+// payload and its residual.
+constexpr int LDS_NT = 512;
+constexpr uint32_t LDS_MAX = 32768;
+constexpr uint32_t LDS_RUN = LDS_MAX / LDS_NT;   // 64
+constexpr uint32_t LDS_PIECES = LDS_RUN / 4;     // 4-element pieces per thread
+static_assert(BLOCK_LEN % LDS_RUN == 0, "block boundaries start a thread's run");
+
+// One digit pass: counts of bits [shift, shift + width) of the keys whose
+// bits above them equal `prefix`; the digit holding the need-th largest
+// such key goes to `digit`, need becomes its rank inside that digit.  Exact
+// zeros (their digits are all 0) are counted in registers and added once
+// per wavefront, off one hot bin.
+template <int NT, int NB>
+__device__ __forceinline__ void lds_pass(const uint32_t* s_v, uint32_t L, uint32_t shift, uint32_t prefix,
+                                         uint32_t* s_h, uint32_t* scratch, uint32_t* found, uint32_t& need,
+                                         uint32_t& digit) {
+  constexpr uint32_t width = (NB == 4096) ? 12u : 7u;
+  const uint32_t t = threadIdx.x;
+  for (uint32_t b = t; b < (uint32_t)NB; b += NT) s_h[b] = 0u;
+  __syncthreads();
+  uint32_t zc = 0;
+  for (uint32_t q = t; q * 4 < L; q += NT) {
+    const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[q * 4]);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t kk = w[c] & 0x7FFFFFFFu;
+      const bool in = q * 4 + (uint32_t)c < L && (kk >> (shift + width)) == prefix;
+      zc += (in && kk == 0u) ? 1u : 0u;
+      if (in && kk != 0u) atomicAdd(&s_h[(kk >> shift) & (uint32_t)(NB - 1)], 1u);
+    }
+  }
+  const uint32_t zs = wave_sum(zc);
+  if (lane_id() == 0 && zs) atomicAdd(&s_h[0], zs);
+  __syncthreads();
+  if constexpr (NB == 4096) find_bin<NT, NB>(s_h, need, scratch, found);
+  else find_bin_wave<NB>(s_h, need, found);
+  digit = found[0];
+  need -= found[1];
+  __syncthreads();
+}
+
+template <typename InT, int SEL>
+__global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
+  static_assert(SEL != SEL_AQSGD, "AQ-SGD segments take the group engine");
+  using Raw = typename Elem<InT>::raw;
+  constexpr int NT = LDS_NT;
+  __shared__ __attribute__((aligned(16))) uint32_t s_v[LDS_MAX];   // the segment's values (binary32 bits)
+  __shared__ uint32_t s_h[HIST_BINS];
+  __shared__ uint32_t scratch[NT / WAVE + 2];
+  __shared__ uint32_t found[2];
+  const uint32_t t = threadIdx.x;
+  const uint32_t L = (uint32_t)a.L;   // <= LDS_MAX (the plan guarantees it)
+  const bool vec = ((((uintptr_t)a.x | (uintptr_t)a.e) & 15u) == 0) && (L % 4u) == 0;
+  for (uint64_t seg = blockIdx.x; seg < a.n_seg; seg += gridDim.x) {
+    const Raw* xs = (const Raw*)a.x + seg * a.L;
+    float* es = (SEL == SEL_EF) ? a.e + seg * a.L : nullptr;
+    // ---- values into LDS: piece q = 4 elements, lanes consecutive
+#pragma unroll 4
+    for (uint32_t j = 0; j < LDS_PIECES; ++j) {
+      const uint32_t q = j * NT + t, i0 = q * 4;
+      if (i0 >= L) break;
+      float v4[4];
+      if (vec) {
+        Raw xr[4];
+        load_run<Raw, 4, true>(xs + i0, xr);
+        float er[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        if constexpr (SEL == SEL_EF) load_run<float, 4, true>(es + i0, er);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          float x = Elem<InT>::up(xr[c]);
+          if constexpr (SEL == SEL_EF) x = x + er[c];
+          v4[c] = x;
+        }
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const uint32_t i = i0 + (uint32_t)c;
+          float x = 0.0f;
+          if (i < L) {
+            x = Elem<InT>::up(xs[i]);
+            if constexpr (SEL == SEL_EF) x = x + es[i];
+          }
+          v4[c] = x;
+        }
+      }
+      u32x4 w;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) w[c] = __float_as_uint(v4[c]);
+      *reinterpret_cast<u32x4*>(&s_v[i0]) = w;
+    }
+    __syncthreads();
+
+    // ---- T and the tie quota r (k == 0: T above every finite key)
+    uint32_t T = 0x7FFFFFFFu, r = 0u;
+    if (a.k > 0) {
+      uint32_t need = (uint32_t)a.k, d1, d2, d3;
+      lds_pass<NT, 4096>(s_v, L, 19, 0u, s_h, scratch, found, need, d1);
+      lds_pass<NT, 4096>(s_v, L, 7, d1, s_h, scratch, found, need, d2);
+      lds_pass<NT, LAST_BINS>(s_v, L, 0, (d1 << 12) | d2, s_h, scratch, found, need, d3);
+      T = (d1 << 19) | (d2 << 7) | d3;
+      r = need;
+    }
+
+    // ---- placement: thread t owns [t*LDS_RUN, t*LDS_RUN + LDS_RUN); its
+    // pieces are read in an order rotated by t (fewer LDS bank conflicts),
+    // flags go to bit (element - run start) of two 64-bit masks
+    const uint32_t b0 = t * LDS_RUN;
+    const uint32_t nr = (b0 < L) ? min(LDS_RUN, L - b0) : 0u;
+    uint64_t gm = 0, em = 0;
+#pragma unroll 4
+    for (uint32_t j = 0; j < LDS_PIECES; ++j) {
+      const uint32_t pc = (j + t) % LDS_PIECES;
+      const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[b0 + 4 * pc]);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t kk = w[c] & 0x7FFFFFFFu, bit = 4 * pc + (uint32_t)c;
+        const uint64_t valid = bit < nr ? 1ull : 0ull;
+        gm |= ((kk > T) ? valid : 0ull) << bit;
+        em |= ((kk == T) ? valid : 0ull) << bit;
+      }
+    }
+    const uint32_t gt = (uint32_t)__popcll(gm), eq = (uint32_t)__popcll(em);
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan<NT>(gt | (eq << 16), scratch, tot);   // both < 2^16
+    const uint32_t gt_ex = ex & 0xFFFFu, eq_ex = ex >> 16;
+    // ties kept: the r lowest-indexed ones
+    uint32_t tie_keep = min(sat_sub(r, eq_ex), eq);
+    uint64_t km = gm, rest = em;
+    for (; tie_keep; --tie_keep) {
+      km |= rest & (0ull - rest);
+      rest &= rest - 1ull;
+    }
+    const uint32_t pos0 = gt_ex + min(eq_ex, r);
+    const uint32_t nk = (uint32_t)__popcll(km);
+    uint32_t* idx = a.idx + seg * a.k;
+    Raw* val = (Raw*)a.val + seg * a.k;
+    if ((uint64_t)pos0 + nk > a.k) {
+      raise_error(KERR_INTERNAL);
+      km = 0;
+    }
+    // the kept entries, in index order
+    uint32_t pos = pos0;
+    for (uint64_t m = km; m; m &= m - 1ull) {
+      const uint32_t bit = (uint32_t)__builtin_ctzll(m);
+      idx[pos] = b0 + bit;
+      val[pos] = Elem<InT>::down(__uint_as_float(s_v[b0 + bit]));
+      ++pos;
+    }
+    // block table: kept entries below each block boundary (a boundary
+    // starts a thread's run)
+    if (a.blk) {
+      uint32_t* bt = a.blk + seg * (n_blocks(a.L) + 1);
+      if (b0 % BLOCK_LEN == 0 && b0 < L) bt[b0 / BLOCK_LEN] = pos0;
+      if (t == 0) bt[n_blocks(a.L)] = (uint32_t)a.k;
+    }
+    // the residual: v minus what the receiver holds (write-back stores; a
+    // thread's pieces cover each line only together)
+    if constexpr (SEL == SEL_EF) {
+#pragma unroll 4
+      for (uint32_t j = 0; j < LDS_PIECES; ++j) {
+        const uint32_t pc = (j + t) % LDS_PIECES;
+        if (4 * pc >= nr) continue;
+        const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[b0 + 4 * pc]);
+        float o[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const float v = __uint_as_float(w[c]);
+          const bool kept = (km >> (4 * pc + (uint32_t)c)) & 1ull;
+          o[c] = v - (kept ? through<InT>(v) : 0.0f);
+        }
+        if (vec) store_run<float, 4, false>(es + b0 + 4 * pc, o);
+        else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            if (4 * pc + (uint32_t)c < nr) es[b0 + 4 * pc + c] = o[c];
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // ------------------------------------------------------------------ plans
 namespace {
 
@@ -817,6 +1007,21 @@ const void* pick(int sel, int dt, bool row, int v) {
   return pick_sel<SEL_AQSGD>(dt, row, v);
 }
 
+// LDS engine: plain and EF TopK
+const void* lds_ptr(int sel, int dt) {
+  if (sel == SEL_PLAIN) {
+    if (dt == DT_F32) return (const void*)k_topk_lds<float, SEL_PLAIN>;
+    if (dt == DT_BF16) return (const void*)k_topk_lds<bf16_t, SEL_PLAIN>;
+    return (const void*)k_topk_lds<f16_t, SEL_PLAIN>;
+  }
+  if (sel == SEL_EF) {
+    if (dt == DT_F32) return (const void*)k_topk_lds<float, SEL_EF>;
+    if (dt == DT_BF16) return (const void*)k_topk_lds<bf16_t, SEL_EF>;
+    return (const void*)k_topk_lds<f16_t, SEL_EF>;
+  }
+  return nullptr;
+}
+
 int occupancy(const void* fn, int nt) {
   int blocks = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, nt, 0) != hipSuccess || blocks < 1) blocks = 1;
@@ -828,6 +1033,18 @@ int occupancy(const void* fn, int nt) {
 SegPlan plan_topk(int sel, int dt, uint64_t n_seg, uint64_t L) {
   SegPlan p;
   const uint32_t cus = (uint32_t)device_cus();
+  if (sel != SEL_AQSGD && L > ROW_MAX && L <= LDS_MAX) {
+    // one workgroup per segment, the segment in LDS
+    p.nt = LDS_NT;
+    p.lds = true;
+    p.P = 1;
+    const uint64_t cap = (uint64_t)occupancy(lds_ptr(sel, dt), p.nt) * cus;
+    p.capacity = cap;
+    p.n_groups = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(n_seg, cap));
+    p.grid = p.n_groups;
+    p.ws_words = 0;
+    return p;
+  }
   if (L <= ROW_MAX) {
     // one wavefront per segment: the smallest run length that covers L
     static const int vpts[] = {4, 8, 12, 16, 24, 32};
@@ -878,7 +1095,7 @@ SegPlan plan_topk(int sel, int dt, uint64_t n_seg, uint64_t L) {
 }
 
 hipError_t launch_topk(int sel, int dt, const SegPlan& plan, const TopkArgs& args, hipStream_t st) {
-  const void* fn = pick(sel, dt, plan.nt == WAVE, plan.vpt);
+  const void* fn = plan.lds ? lds_ptr(sel, dt) : pick(sel, dt, plan.nt == WAVE, plan.vpt);
   if (!fn) return hipErrorInvalidValue;
   TopkArgs a = args;
   a.P = plan.P;

@@ -209,10 +209,14 @@ TC_API tc_status tc_workspace_bytes(const tc_codec* c, size_t* bytes) {
   uint64_t words = 0;
   const int dt = dt_ok(c->wire) ? c->wire : TC_F32;
   if (c->kind == TC_TOPK) {
-    // one layout serves the plain, EF and AQ-SGD senders of this shape; a
-    // segment too long for it takes the global chain
-    const tc::SegPlan p = tc::plan_topk(tc::SEL_EF, dt, c->n_seg, c->seg_len);
-    words = (p.n_groups == 0 || p.P > p.capacity) ? tc::global_ws_words(c->seg_len) : p.ws_words;
+    // enough for every sender kind of this shape (plain and EF may hold a
+    // segment in LDS and need none, AQ-SGD keeps the group engine); a
+    // segment too long for them takes the global chain
+    for (int sel : {tc::SEL_EF, tc::SEL_AQSGD}) {
+      const tc::SegPlan p = tc::plan_topk(sel, dt, c->n_seg, c->seg_len);
+      words = std::max<uint64_t>(words, (p.n_groups == 0 || p.P > p.capacity) ? tc::global_ws_words(c->seg_len)
+                                                                              : p.ws_words);
+    }
   } else if (c->kind == TC_QUANT) {
     words = std::max(tc::plan_quant(dt, c->bits, true, c->n_seg, c->seg_len).ws_words,
                      tc::plan_quant(dt, c->bits, false, c->n_seg, c->seg_len).ws_words);

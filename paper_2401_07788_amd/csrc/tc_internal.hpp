@@ -24,6 +24,7 @@ struct SegPlan {
   uint32_t grid = 0;
   uint64_t capacity = 0;   // workgroups of this kernel the device holds at once
   uint64_t ws_words = 0;   // 32-bit words of zero-initialised workspace needed
+  bool lds = false;        // TopK: one workgroup per segment held in LDS (k_topk_lds)
 };
 
 // ------------------------------------------------------------------- TopK

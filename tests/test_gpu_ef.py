@@ -105,6 +105,16 @@ def test_ef_ragged(tc, orc, dt):
     ef_quant_steps(tc, orc, ys, 5, 999, 3)
 
 
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("L", [4099, 32768])
+def test_ef_lds_engine(tc, orc, dt, L):
+    # one workgroup per segment held in LDS; 4099 is not a multiple of the
+    # 4-element pieces (element-wise loads and residual stores)
+    xs = [W.randn((6, L), 8, t).to(dt) for t in range(3)]
+    for num in (1, 3):
+        ef_topk_steps(tc, orc, xs, 6, L, tc.topk_count(L, num, 10))
+
+
 def test_ef_k_edges(tc, orc):
     xs = [W.relu_activation((4, 16384), 6, t) for t in range(2)]
     for k in (0, 16384):

@@ -78,9 +78,41 @@ def test_topk_many_segments_row_layout(tc, orc):
 
 
 def test_topk_many_segments_group_layout(tc, orc):
-    # more long segments than resident groups of workgroups
-    x = make_input("relu", 300, 20000, "f32", seed=3)
-    run_case(tc, orc, x, 300, 20000, tc.topk_count(20000, 1, 10))
+    # more long segments than resident groups of workgroups (segments longer
+    # than one workgroup's LDS holds take the group engine)
+    x = make_input("relu", 200, 40000, "f32", seed=3)
+    run_case(tc, orc, x, 200, 40000, tc.topk_count(40000, 1, 10))
+
+
+# segments of 2049..32768 elements: one workgroup per segment, held in LDS
+LDS_L = [4097, 32767, 32768]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("L", LDS_L)
+@pytest.mark.parametrize("kind", ["normal", "relu", "ties", "zeros"])
+def test_topk_lds_engine(tc, orc, dt, L, kind):
+    x = make_input(kind, 3, L, dt, seed=L + 1)
+    for k in sorted({0, 1, tc.topk_count(L, 1, 10), tc.topk_count(L, 3, 10), L - 1, L}):
+        run_case(tc, orc, x, 3, L, k)
+
+
+def test_topk_lds_engine_many_segments_unaligned(tc, orc):
+    # more segments than resident workgroups, and an input that starts 4
+    # bytes past a 16-byte boundary (element-wise loads)
+    n_seg, L = 600, 12288
+    x = make_input("relu", n_seg, L, "f32", seed=5)
+    buf = torch.empty(n_seg * L + 1, dtype=torch.float32)
+    buf[1:] = x.reshape(-1)
+    xd = buf.cuda()[1:].view(n_seg, L)
+    k = tc.topk_count(L, 1, 10)
+    p = tc.topk_compress(xd, k, n_seg)
+    torch.cuda.synchronize()
+    assert tc.device_errors() == 0
+    oi, ov = orc.topk_compress(raw(x), "f32", n_seg, L, k)
+    assert_bits_equal(raw(p.idx), oi, "idx")
+    assert_bits_equal(raw(p.val), ov, "val")
+    check_block_table(p.blk, oi, L)
 
 
 def test_decompress_rejects_bad_index_without_fault(tc):
