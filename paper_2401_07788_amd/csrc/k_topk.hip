@@ -772,18 +772,21 @@ __global__ __launch_bounds__(GRP_NT) void k_topk_grp(TopkArgs a) {
 // pieces; three digit passes over LDS (key bits 30..19, 18..7, 6..0) give T
 // and the tie quota; then thread t places its run of LDS_RUN consecutive
 // elements (kept-entry bit masks, one scan), writes its kept entries to the
-// payload and its residual.
-constexpr int LDS_NT = 512;
+// payload and its residual.  1024 threads: four waves per SIMD share the
+// per-key work, which is what bounds this kernel.
+constexpr int LDS_NT = 1024;
 constexpr uint32_t LDS_MAX = 32768;
-constexpr uint32_t LDS_RUN = LDS_MAX / LDS_NT;   // 64
+constexpr uint32_t LDS_RUN = LDS_MAX / LDS_NT;   // 32: one bit mask word per thread
 constexpr uint32_t LDS_PIECES = LDS_RUN / 4;     // 4-element pieces per thread
+static_assert(LDS_RUN == 32, "a thread's run is one 32-bit mask");
 static_assert(BLOCK_LEN % LDS_RUN == 0, "block boundaries start a thread's run");
 
 // One digit pass: counts of bits [shift, shift + width) of the keys whose
-// bits above them equal `prefix`; the digit holding the need-th largest
-// such key goes to `digit`, need becomes its rank inside that digit.  Exact
-// zeros (their digits are all 0) are counted in registers and added once
-// per wavefront, off one hot bin.
+// bits above them equal `prefix` (shift + width = 31: every key); the digit
+// holding the need-th largest such key goes to `digit`, need becomes its
+// rank inside that digit.  Exact zeros (their digits are all 0) are counted
+// in registers and added once per wavefront, off one hot bin.  A piece of
+// four keys none of which matches costs one test.
 template <int NT, int NB>
 __device__ __forceinline__ void lds_pass(const uint32_t* s_v, uint32_t L, uint32_t shift, uint32_t prefix,
                                          uint32_t* s_h, uint32_t* scratch, uint32_t* found, uint32_t& need,
@@ -795,12 +798,21 @@ __device__ __forceinline__ void lds_pass(const uint32_t* s_v, uint32_t L, uint32
   uint32_t zc = 0;
   for (uint32_t q = t; q * 4 < L; q += NT) {
     const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[q * 4]);
+    uint32_t kk[4], in = 0;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const uint32_t kk = w[c] & 0x7FFFFFFFu;
-      const bool in = q * 4 + (uint32_t)c < L && (kk >> (shift + width)) == prefix;
-      zc += (in && kk == 0u) ? 1u : 0u;
-      if (in && kk != 0u) atomicAdd(&s_h[(kk >> shift) & (uint32_t)(NB - 1)], 1u);
+      kk[c] = w[c] & 0x7FFFFFFFu;
+      in |= (((kk[c] >> (shift + width)) == prefix) ? 1u : 0u) << c;
+    }
+    if (q * 4 + 4 > L) in &= (1u << (L - q * 4)) - 1u;
+    if (in) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        if ((in >> c) & 1u) {
+          if (kk[c] == 0u) ++zc;
+          else atomicAdd(&s_h[(kk[c] >> shift) & (uint32_t)(NB - 1)], 1u);
+        }
+      }
     }
   }
   const uint32_t zs = wave_sum(zc);
@@ -828,24 +840,41 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
   for (uint64_t seg = blockIdx.x; seg < a.n_seg; seg += gridDim.x) {
     const Raw* xs = (const Raw*)a.x + seg * a.L;
     float* es = (SEL == SEL_EF) ? a.e + seg * a.L : nullptr;
-    // ---- values into LDS: piece q = 4 elements, lanes consecutive
-#pragma unroll 4
-    for (uint32_t j = 0; j < LDS_PIECES; ++j) {
-      const uint32_t q = j * NT + t, i0 = q * 4;
-      if (i0 >= L) break;
-      float v4[4];
-      if (vec) {
-        Raw xr[4];
-        load_run<Raw, 4, true>(xs + i0, xr);
-        float er[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        if constexpr (SEL == SEL_EF) load_run<float, 4, true>(es + i0, er);
+    // ---- values into LDS: piece q = 4 elements, lanes consecutive; loads
+    // go out four pieces at a time (the registers of 1024 threads)
+    if (vec) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          float x = Elem<InT>::up(xr[c]);
-          if constexpr (SEL == SEL_EF) x = x + er[c];
-          v4[c] = x;
+      for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
+        Raw xr[4][4];
+        float er[4][4];
+#pragma unroll
+        for (uint32_t j = 0; j < 4; ++j) {
+          const uint32_t i0 = ((h + j) * NT + t) * 4;
+          if (i0 < L) {
+            load_run<Raw, 4, true>(xs + i0, xr[j]);
+            if constexpr (SEL == SEL_EF) load_run<float, 4, true>(es + i0, er[j]);
+          }
         }
-      } else {
+#pragma unroll
+        for (uint32_t j = 0; j < 4; ++j) {
+          const uint32_t i0 = ((h + j) * NT + t) * 4;
+          if (i0 < L) {
+            u32x4 w;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+              float x = Elem<InT>::up(xr[j][c]);
+              if constexpr (SEL == SEL_EF) x = x + er[j][c];
+              w[c] = __float_as_uint(x);
+            }
+            *reinterpret_cast<u32x4*>(&s_v[i0]) = w;
+          }
+        }
+      }
+    } else {
+      for (uint32_t j = 0; j < LDS_PIECES; ++j) {
+        const uint32_t i0 = (j * NT + t) * 4;
+        if (i0 >= L) break;
+        u32x4 w;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const uint32_t i = i0 + (uint32_t)c;
@@ -854,13 +883,10 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
             x = Elem<InT>::up(xs[i]);
             if constexpr (SEL == SEL_EF) x = x + es[i];
           }
-          v4[c] = x;
+          w[c] = __float_as_uint(x);
         }
+        *reinterpret_cast<u32x4*>(&s_v[i0]) = w;
       }
-      u32x4 w;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) w[c] = __float_as_uint(v4[c]);
-      *reinterpret_cast<u32x4*>(&s_v[i0]) = w;
     }
     __syncthreads();
 
@@ -877,35 +903,40 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
 
     // ---- placement: thread t owns [t*LDS_RUN, t*LDS_RUN + LDS_RUN); its
     // pieces are read in an order rotated by t (fewer LDS bank conflicts),
-    // flags go to bit (element - run start) of two 64-bit masks
+    // flags go to bit (element - run start) of two masks
     const uint32_t b0 = t * LDS_RUN;
     const uint32_t nr = (b0 < L) ? min(LDS_RUN, L - b0) : 0u;
-    uint64_t gm = 0, em = 0;
-#pragma unroll 4
+    uint32_t gm = 0, em = 0;
+#pragma unroll
     for (uint32_t j = 0; j < LDS_PIECES; ++j) {
       const uint32_t pc = (j + t) % LDS_PIECES;
       const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[b0 + 4 * pc]);
+      uint32_t g4 = 0, e4 = 0;
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        const uint32_t kk = w[c] & 0x7FFFFFFFu, bit = 4 * pc + (uint32_t)c;
-        const uint64_t valid = bit < nr ? 1ull : 0ull;
-        gm |= ((kk > T) ? valid : 0ull) << bit;
-        em |= ((kk == T) ? valid : 0ull) << bit;
+        const uint32_t kk = w[c] & 0x7FFFFFFFu;
+        g4 |= ((kk > T) ? 1u : 0u) << c;
+        e4 |= ((kk == T) ? 1u : 0u) << c;
       }
+      gm |= g4 << (4 * pc);
+      em |= e4 << (4 * pc);
     }
-    const uint32_t gt = (uint32_t)__popcll(gm), eq = (uint32_t)__popcll(em);
+    const uint32_t valid = (nr >= 32u) ? 0xFFFFFFFFu : ((1u << nr) - 1u);
+    gm &= valid;
+    em &= valid;
+    const uint32_t gt = (uint32_t)__builtin_popcount(gm), eq = (uint32_t)__builtin_popcount(em);
     uint32_t tot;
     const uint32_t ex = block_excl_scan<NT>(gt | (eq << 16), scratch, tot);   // both < 2^16
     const uint32_t gt_ex = ex & 0xFFFFu, eq_ex = ex >> 16;
     // ties kept: the r lowest-indexed ones
     uint32_t tie_keep = min(sat_sub(r, eq_ex), eq);
-    uint64_t km = gm, rest = em;
+    uint32_t km = gm, rest = em;
     for (; tie_keep; --tie_keep) {
-      km |= rest & (0ull - rest);
-      rest &= rest - 1ull;
+      km |= rest & (0u - rest);
+      rest &= rest - 1u;
     }
     const uint32_t pos0 = gt_ex + min(eq_ex, r);
-    const uint32_t nk = (uint32_t)__popcll(km);
+    const uint32_t nk = (uint32_t)__builtin_popcount(km);
     uint32_t* idx = a.idx + seg * a.k;
     Raw* val = (Raw*)a.val + seg * a.k;
     if ((uint64_t)pos0 + nk > a.k) {
@@ -914,8 +945,8 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
     }
     // the kept entries, in index order
     uint32_t pos = pos0;
-    for (uint64_t m = km; m; m &= m - 1ull) {
-      const uint32_t bit = (uint32_t)__builtin_ctzll(m);
+    for (uint32_t m = km; m; m &= m - 1u) {
+      const uint32_t bit = (uint32_t)__builtin_ctz(m);
       idx[pos] = b0 + bit;
       val[pos] = Elem<InT>::down(__uint_as_float(s_v[b0 + bit]));
       ++pos;
@@ -930,17 +961,17 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
     // the residual: v minus what the receiver holds (write-back stores; a
     // thread's pieces cover each line only together)
     if constexpr (SEL == SEL_EF) {
-#pragma unroll 4
+#pragma unroll 2
       for (uint32_t j = 0; j < LDS_PIECES; ++j) {
         const uint32_t pc = (j + t) % LDS_PIECES;
         if (4 * pc >= nr) continue;
         const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[b0 + 4 * pc]);
+        const uint32_t k4 = km >> (4 * pc);
         float o[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const float v = __uint_as_float(w[c]);
-          const bool kept = (km >> (4 * pc + (uint32_t)c)) & 1ull;
-          o[c] = v - (kept ? through<InT>(v) : 0.0f);
+          o[c] = v - (((k4 >> c) & 1u) ? through<InT>(v) : 0.0f);
         }
         if (vec) store_run<float, 4, false>(es + b0 + 4 * pc, o);
         else {
