@@ -778,6 +778,7 @@ constexpr int LDS_NT = 1024;
 constexpr uint32_t LDS_MAX = 32768;
 constexpr uint32_t LDS_RUN = LDS_MAX / LDS_NT;   // 32: one bit mask word per thread
 constexpr uint32_t LDS_PIECES = LDS_RUN / 4;     // 4-element pieces per thread
+constexpr uint32_t LDS_LIST = 3072;              // keys of one first-pass bin kept in a list
 static_assert(LDS_RUN == 32, "a thread's run is one 32-bit mask");
 static_assert(BLOCK_LEN % LDS_RUN == 0, "block boundaries start a thread's run");
 
@@ -791,6 +792,7 @@ template <int NT, int NB>
 __device__ __forceinline__ void lds_pass(const uint32_t* s_v, uint32_t L, uint32_t shift, uint32_t prefix,
                                          uint32_t* s_h, uint32_t* scratch, uint32_t* found, uint32_t& need,
                                          uint32_t& digit) {
+  static_assert(NB == 4096 || NB == LAST_BINS, "12-bit or 7-bit digits");
   constexpr uint32_t width = (NB == 4096) ? 12u : 7u;
   const uint32_t t = threadIdx.x;
   for (uint32_t b = t; b < (uint32_t)NB; b += NT) s_h[b] = 0u;
@@ -825,6 +827,28 @@ __device__ __forceinline__ void lds_pass(const uint32_t* s_v, uint32_t L, uint32
   __syncthreads();
 }
 
+// The same over the short list of keys of one first-pass bin: bits
+// [shift, shift + width) of the listed keys (all of them for the 12-bit
+// digit; for the 7-bit digit those whose bits 30..7 equal `prefix`).
+template <int NT, int NB>
+__device__ __forceinline__ void lds_pass_list(const uint32_t* s_list, uint32_t n, uint32_t shift, uint32_t* s_h,
+                                              uint32_t* scratch, uint32_t* found, uint32_t& need, uint32_t& digit,
+                                              uint32_t prefix = 0u) {
+  const uint32_t t = threadIdx.x;
+  for (uint32_t b = t; b < (uint32_t)NB; b += NT) s_h[b] = 0u;
+  __syncthreads();
+  for (uint32_t j = t; j < n; j += NT) {
+    const uint32_t kk = s_list[j];
+    if (NB == 4096 || (kk >> 7) == prefix) atomicAdd(&s_h[(kk >> shift) & (uint32_t)(NB - 1)], 1u);
+  }
+  __syncthreads();
+  if constexpr (NB == 4096) find_bin<NT, NB>(s_h, need, scratch, found);
+  else find_bin_wave<NB>(s_h, need, found);
+  digit = found[0];
+  need -= found[1];
+  __syncthreads();
+}
+
 template <typename InT, int SEL>
 __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
   static_assert(SEL != SEL_AQSGD, "AQ-SGD segments take the group engine");
@@ -832,6 +856,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
   constexpr int NT = LDS_NT;
   __shared__ __attribute__((aligned(16))) uint32_t s_v[LDS_MAX];   // the segment's values (binary32 bits)
   __shared__ uint32_t s_h[HIST_BINS];
+  __shared__ uint32_t s_list[LDS_LIST];   // keys of the first pass's bin
   __shared__ uint32_t scratch[NT / WAVE + 2];
   __shared__ uint32_t found[2];
   const uint32_t t = threadIdx.x;
@@ -895,8 +920,45 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
     if (a.k > 0) {
       uint32_t need = (uint32_t)a.k, d1, d2, d3;
       lds_pass<NT, 4096>(s_v, L, 19, 0u, s_h, scratch, found, need, d1);
-      lds_pass<NT, 4096>(s_v, L, 7, d1, s_h, scratch, found, need, d2);
-      lds_pass<NT, LAST_BINS>(s_v, L, 0, (d1 << 12) | d2, s_h, scratch, found, need, d3);
+      // the keys of bin d1 into a short list (wavefront-aggregated appends),
+      // so that the last two passes read only them; a bin holding more
+      // than the list takes the passes over the whole segment
+      if (t == 0) found[0] = 0u;
+      __syncthreads();
+      // (every lane runs every iteration: the scans below need whole wavefronts)
+      for (uint32_t j = 0; j < LDS_PIECES; ++j) {
+        const uint32_t q = j * NT + t;
+        const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[q * 4]);
+        uint32_t in = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) in |= ((((w[c] & 0x7FFFFFFFu) >> 19) == d1) ? 1u : 0u) << c;
+        if (q * 4 >= L) in = 0u;
+        else if (q * 4 + 4 > L) in &= (1u << (L - q * 4)) - 1u;
+        const uint32_t n = (uint32_t)__builtin_popcount(in);
+        const uint32_t incl = wave_incl_scan(n);
+        const uint32_t tot_w = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1);
+        uint32_t base = 0;
+        if (tot_w) {
+          if (lane_id() == 0) base = atomicAdd(&found[0], tot_w);
+          base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
+        }
+        uint32_t o = base + incl - n;
+        for (uint32_t m = in; m; m &= m - 1u) {
+          const uint32_t c = (uint32_t)__builtin_ctz(m);
+          if (o < LDS_LIST) s_list[o] = w[c] & 0x7FFFFFFFu;
+          ++o;
+        }
+      }
+      __syncthreads();
+      const uint32_t nl = found[0];
+      __syncthreads();
+      if (nl <= LDS_LIST) {
+        lds_pass_list<NT, 4096>(s_list, nl, 7, s_h, scratch, found, need, d2);
+        lds_pass_list<NT, LAST_BINS>(s_list, nl, 0, s_h, scratch, found, need, d3, (d1 << 12) | d2);
+      } else {
+        lds_pass<NT, 4096>(s_v, L, 7, d1, s_h, scratch, found, need, d2);
+        lds_pass<NT, LAST_BINS>(s_v, L, 0, (d1 << 12) | d2, s_h, scratch, found, need, d3);
+      }
       T = (d1 << 19) | (d2 << 7) | d3;
       r = need;
     }
