@@ -41,6 +41,7 @@ def lib():
             "tco_topk_indices": (i32, [vp, u64, u64, vp]),
             "tco_topk_compress": (i32, [vp, i32, u64, u64, u64, i32, vp, vp, i32]),
             "tco_topk_decompress": (i32, [vp, vp, i32, u64, u64, u64, vp, i32]),
+            "tco_topk_gather": (i32, [vp, i32, vp, u64, u64, u64, vp, i32, vp]),
             "tco_quant_group_bytes": (u64, [u64, u32]),
             "tco_quant_group": (i32, [vp, u64, u32, vp, vp]),
             "tco_quant_pack": (i32, [vp, i32, u64, u64, u32, vp, vp, i32]),
@@ -129,6 +130,22 @@ def topk_decompress(idx, val, wire, n_seg, L, k, out_dt=None):
     _chk(lib().tco_topk_decompress(_p(idx), _p(val), DT[wire], n_seg, L, k, _p(y), DT[out_dt]),
          "topk_decompress")
     return y
+
+
+def topk_gather(x, dt, idx, n_seg, L, k, e=None, wire=None):
+    """TopK at given indices (Sec. 3.2: gradients compressed at the indices
+    the activations' TopK kept): returns val, or (val, e_next) when e is given
+    (error feedback around this compressor); e is not modified"""
+    wire = wire or dt
+    x = _raw(x, dt)
+    assert x.size == n_seg * L
+    idx = np.ascontiguousarray(idx, np.uint32)
+    assert idx.size == n_seg * k
+    val = np.zeros((n_seg, k), _NP[wire])
+    e2 = None if e is None else np.array(e, dtype=np.float32, copy=True, order="C")
+    _chk(lib().tco_topk_gather(_p(x), DT[dt], None if e2 is None else _p(e2), n_seg, L, k, _p(idx), DT[wire],
+                               _p(val)), "topk_gather")
+    return val if e is None else (val, e2)
 
 
 # --------------------------------------------------------------- quantization

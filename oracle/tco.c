@@ -226,6 +226,41 @@ int tco_topk_decompress(const uint32_t* idx, const void* val, int wire, uint64_t
     return 0;
 }
 
+/* TopK at given indices (Sec. 3.2, the GPT-2 fine-tuning runs: gradients are
+ * compressed at the indices that the TopK of the activations kept, rather
+ * than by a selection of their own; compressing them separately made those
+ * runs diverge).  The message is x at those indices, in index order, in the
+ * wire dtype; the receiver is tco_topk_decompress with the same indices.
+ * With e (non-NULL) it is the Sec. 2.4 error-feedback sender around this
+ * compressor: X = x + e is compressed and e becomes X minus what the
+ * receiver holds (the wire value of X at the indices, +0 elsewhere).  An
+ * index outside the segment is an error. */
+int tco_topk_gather(const void* x, int dt, float* e, uint64_t n_seg, uint64_t L, uint64_t k,
+                    const uint32_t* idx, int wire, void* val) {
+    float* X = (float*)malloc(sizeof(float) * (size_t)(L ? L : 1));
+    float* r = (float*)malloc(sizeof(float) * (size_t)(L ? L : 1));
+    if (!X || !r) { free(X); free(r); return -1; }
+    int bad = 0;
+    for (uint64_t s = 0; s < n_seg && !bad; ++s) {
+        const uint64_t base = s * L;
+        for (uint64_t i = 0; i < L; ++i) {
+            X[i] = load_f32(x, dt, base + i);
+            if (e) X[i] = X[i] + e[base + i];
+            r[i] = 0.0f;
+        }
+        for (uint64_t j = 0; j < k; ++j) {
+            const uint32_t i = idx[s * k + j];
+            if (i >= L) { bad = 1; break; }
+            store_rne(val, wire, s * k + j, X[i]);
+            r[i] = load_f32(val, wire, s * k + j);
+        }
+        if (!bad && e)
+            for (uint64_t i = 0; i < L; ++i) e[base + i] = X[i] - r[i];
+    }
+    free(X); free(r);
+    return bad ? -1 : 0;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Uniform b-bit min-max quantization (Sec. 2.2)                             */
 /* ------------------------------------------------------------------------ */
