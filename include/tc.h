@@ -162,6 +162,26 @@ tc_status tc_topk_compress(const tc_codec* c, const void* x, int dt, const tc_pa
  * reads in->idx/codes/meta and writes lo + code_j*scale at idx_j. */
 tc_status tc_topk_decompress(const tc_codec* c, const tc_payload* in, void* y, int out_dt, void* stream);
 
+/* Sec. 3.2 (the GPT-2 runs, Table 5 and its note): gradients compressed at
+ * the indices that the activations' TopK kept, instead of a selection of
+ * their own (compressing them separately made those runs diverge).
+ *   in->idx  [n_seg][k] strictly ascending indices within each segment, the
+ *            idx of that TopK payload; in->blk, when non-NULL, its block
+ *            table (used only with e)
+ *   x        [n_seg][seg_len] of dtype dt (the gradient)
+ *   val      [n_seg][k] output: x at those indices, in dt (the wire dtype)
+ *   e        NULL, or the Sec. 2.4 residual [n_seg][seg_len] binary32, in-out:
+ *            X = x + e is what is sent, and e <- X - r with r what the
+ *            receiver's dense tensor holds (X's wire value at the indices, +0
+ *            elsewhere)
+ * The receiver is tc_topk_decompress with in->idx (and in->blk) and val.
+ * kind must be TC_TOPK and wire == dt.  An index outside its segment sets
+ * TC_KERR_BAD_INDEX and its entry is sent as +0 (with e, left unchanged in
+ * the residual); with e and no block table, indices that do not ascend set
+ * it too. */
+tc_status tc_topk_gather(const tc_codec* c, const tc_payload* in, const void* x, int dt, float* e, void* val,
+                         void* stream);
+
 /* -------------------------------------------------------- quantization */
 
 /* Sec. 2.2 sender: per group of seg_len elements, lo = min and hi = max (a

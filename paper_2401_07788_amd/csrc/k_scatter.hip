@@ -292,6 +292,88 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
   }
 }
 
+// ---------------------------------------------------------- index reuse
+// TopK at given indices (Sec. 3.2: in the GPT-2 runs the gradients are
+// compressed at the indices that the activations' TopK kept).  The message
+// is x at those indices in x's own dtype; without error feedback every entry
+// is independent.  An index outside the segment sends +0 and is flagged.
+template <typename T>
+__global__ __launch_bounds__(SC_NT) void k_gather(GatherArgs a) {
+  using R = typename Elem<T>::raw;
+  const uint64_t total = a.n_seg * a.k;
+  for (uint64_t g = (uint64_t)blockIdx.x * SC_NT + threadIdx.x; g < total; g += (uint64_t)gridDim.x * SC_NT) {
+    const uint64_t s = g / a.k;
+    const uint32_t i = a.idx[g];
+    R v = R{};
+    if (i < a.L) v = ((const R*)a.x)[s * a.L + i];
+    else raise_error(KERR_BAD_INDEX);
+    ((R*)a.val)[g] = v;
+  }
+}
+
+// With error feedback (Sec. 2.4): X = x + e is compressed and e becomes X
+// minus what the receiver holds, so the whole residual is rewritten.  One
+// 4096-element chunk per iteration: X into LDS, the chunk's entries (range
+// from the block table, else a search of the ascending indices) send X and
+// mark their places, then the residual leaves densely.
+template <typename T>
+__global__ __launch_bounds__(SC_NT) void k_gather_ef(GatherArgs a) {
+  using R = typename Elem<T>::raw;
+  __shared__ float s_x[SC_CH];
+  __shared__ uint8_t s_f[SC_CH];
+  __shared__ uint32_t scratch[SC_NT / WAVE + 2];
+  const uint64_t nch = (a.L + SC_CH - 1) / SC_CH;
+  const uint64_t nbt = n_blocks(a.L) + 1;
+  const uint32_t t = threadIdx.x;
+  for (uint64_t wi = blockIdx.x; wi < a.n_seg * nch; wi += gridDim.x) {
+    const uint64_t seg = wi / nch, c0 = (wi % nch) * SC_CH;
+    const uint64_t c1 = min(a.L, c0 + SC_CH);
+    const uint32_t* ix = a.idx + seg * a.k;
+    const uint32_t* bt = a.blk ? a.blk + seg * nbt : nullptr;
+    uint32_t j0 = 0, j1 = 0;
+    if (a.k > 0) chunk_range(ix, bt, a.k, c0, c1, scratch, j0, j1);
+    // entries past the segment's end belong to no chunk: the last chunk flags them
+    if (c1 == a.L && j1 < a.k && t == 0) raise_error(KERR_BAD_INDEX);
+    // X = x + e, thread-contiguous runs
+    const uint64_t t0 = c0 + (uint64_t)t * SC_VPT;
+    const int nv = (int)min((uint64_t)SC_VPT, sat_sub(c1, t0));
+    R xr[SC_VPT];
+    float er[SC_VPT];
+    if (nv > 0) {
+      load_run_partial<R, SC_VPT, false>((const R*)a.x + seg * a.L + t0, nv, R{}, xr);
+      load_run_partial<float, SC_VPT, false>(a.e + seg * a.L + t0, nv, 0.0f, er);
+    }
+#pragma unroll
+    for (int i = 0; i < SC_VPT; ++i) {
+      s_x[t * SC_VPT + i] = (i < nv) ? Elem<T>::up(xr[i]) + er[i] : 0.0f;
+      s_f[t * SC_VPT + i] = 0;
+    }
+    __syncthreads();
+    for (uint32_t j = j0 + t; j < j1; j += SC_NT) {
+      const uint32_t i = ix[j];
+      if (!bt && j > j0 && ix[j - 1] >= i) raise_error(KERR_BAD_INDEX);
+      if (i < c0 || i >= c1) {
+        raise_error(KERR_BAD_INDEX);
+        ((R*)a.val)[seg * a.k + j] = R{};
+      } else {
+        ((R*)a.val)[seg * a.k + j] = Elem<T>::down(s_x[i - c0]);
+        s_f[i - c0] = 1;
+      }
+    }
+    __syncthreads();
+    if (nv > 0) {
+      float o[SC_VPT];
+#pragma unroll
+      for (int i = 0; i < SC_VPT; ++i) {
+        const float X = s_x[t * SC_VPT + i];
+        o[i] = X - (s_f[t * SC_VPT + i] ? through<T>(X) : 0.0f);
+      }
+      store_run_partial<float, SC_VPT, false>(a.e + seg * a.L + t0, nv, o);
+    }
+    __syncthreads();
+  }
+}
+
 namespace {
 
 uint32_t scatter_grid(uint64_t n_seg, uint64_t L) {
@@ -345,6 +427,24 @@ hipError_t launch_aqsgd_recv(int dt, const ScatterArgs& args, hipStream_t st) {
   ScatterArgs a = args;
   void* params[] = {&a};
   return hipLaunchKernel(fn, dim3(scatter_grid(a.n_seg, a.L)), dim3(SC_NT), params, 0, st);
+}
+
+hipError_t launch_gather(int dt, const GatherArgs& args, hipStream_t st) {
+  GatherArgs a = args;
+  void* params[] = {&a};
+  const void* fn;
+  uint64_t work;
+  if (a.e) {
+    fn = (dt == DT_F32) ? (const void*)k_gather_ef<float>
+       : (dt == DT_BF16) ? (const void*)k_gather_ef<bf16_t> : (const void*)k_gather_ef<f16_t>;
+    work = a.n_seg * ((a.L + SC_CH - 1) / SC_CH);
+  } else {
+    fn = (dt == DT_F32) ? (const void*)k_gather<float>
+       : (dt == DT_BF16) ? (const void*)k_gather<bf16_t> : (const void*)k_gather<f16_t>;
+    work = (a.n_seg * a.k + SC_NT - 1) / SC_NT;
+  }
+  const uint32_t grid = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(work, (uint64_t)device_cus() * 8));
+  return hipLaunchKernel(fn, dim3(grid), dim3(SC_NT), params, 0, st);
 }
 
 TC_DEFINE_ERROR_READER(errors_scatter)

@@ -297,6 +297,30 @@ TC_API tc_status tc_topk_decompress(const tc_codec* c, const tc_payload* in, voi
   return TC_OK;
 }
 
+TC_API tc_status tc_topk_gather(const tc_codec* c, const tc_payload* in, const void* x, int dt, float* e,
+                                void* val, void* stream) {
+  tc_status s = check_codec(c, 1 << TC_TOPK);
+  if (s != TC_OK) return s;
+  if (!dt_ok(dt)) return fail(TC_ERR_DTYPE, "dtype %d", dt);
+  if (c->wire != dt) return fail(TC_ERR_DTYPE, "wire dtype %d must equal the input dtype %d", c->wire, dt);
+  if (c->n_seg * c->seg_len == 0) return TC_OK;
+  if (!x) return fail(TC_ERR_NULL, "input is NULL");
+  if (c->k > 0 && (!in || !in->idx || !val)) return fail(TC_ERR_NULL, "indices or val is NULL");
+  if (c->k == 0 && !e) return TC_OK;
+  tc::GatherArgs a{};
+  a.idx = (c->k > 0) ? in->idx : nullptr;
+  a.blk = (c->k > 0 && in) ? in->blk : nullptr;
+  a.x = x;
+  a.e = e;
+  a.val = val;
+  a.n_seg = c->n_seg;
+  a.L = c->seg_len;
+  a.k = c->k;
+  hipError_t he = tc::launch_gather(dt, a, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "topk gather launch");
+  return TC_OK;
+}
+
 TC_API tc_status tc_quant_pack(const tc_codec* c, const void* x, int dt, const tc_payload* out, void* ws,
                                size_t ws_bytes, void* stream) {
   tc_status s = check_codec(c, 1 << TC_QUANT);

@@ -87,6 +87,18 @@ struct ScatterArgs {
   uint64_t n_seg, L, k, wpg;
 };
 hipError_t launch_topk_decompress(int wire, int out_dt, const ScatterArgs& a, hipStream_t st);
+
+// TopK at given indices (another tensor's TopK payload), optionally inside
+// error feedback
+struct GatherArgs {
+  const uint32_t* idx;   // [n_seg][k], ascending per segment
+  const uint32_t* blk;   // optional block table of that payload
+  const void* x;         // [n_seg][L]
+  float* e;              // EF residual [n_seg][L] (in-out) or nullptr
+  void* val;             // [n_seg][k] in x's dtype
+  uint64_t n_seg, L, k;
+};
+hipError_t launch_gather(int dt, const GatherArgs& a, hipStream_t st);
 hipError_t launch_aqsgd_recv(int dt, const ScatterArgs& a, hipStream_t st);
 
 // ------------------------------------------------ segments too long to hold

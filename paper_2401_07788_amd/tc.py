@@ -77,6 +77,8 @@ EXPORTS = {
     "tc_topk_compress": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.POINTER(Payload), C.c_void_p,
                                    C.c_size_t, C.c_void_p]),
     "tc_topk_decompress": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.c_void_p, C.c_int, C.c_void_p]),
+    "tc_topk_gather": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.c_void_p, C.c_int, C.POINTER(C.c_float),
+                                 C.c_void_p, C.c_void_p]),
     "tc_quant_pack": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.POINTER(Payload), C.c_void_p,
                                 C.c_size_t, C.c_void_p]),
     "tc_quant_unpack": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.c_void_p, C.c_int, C.c_void_p]),
@@ -222,6 +224,25 @@ def topk_decompress(pl: TopkPayload, seg_len: int, out_dtype=None, use_blk: bool
     _check(lib().tc_topk_decompress(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(pl.idx.device)),
            "tc_topk_decompress")
     return y
+
+
+def topk_gather(pl: TopkPayload, x: torch.Tensor, e: torch.Tensor = None, use_blk: bool = True,
+                out: torch.Tensor = None) -> torch.Tensor:
+    """x viewed as [n_seg, seg_len] at the indices of another tensor's TopK payload
+    (the values sent in x's dtype); with e (float32, updated in place), X = x + e is
+    sent and e <- X - received.  The receiver is topk_decompress(pl._replace(val=...))."""
+    _need_gpu(pl.idx, pl.blk, x, e, out)
+    n_seg, k = pl.idx.shape
+    L = x.numel() // n_seg
+    if e is not None and (e.dtype != torch.float32 or e.numel() != x.numel()):
+        raise ValueError("e must be float32 with x's element count")
+    val = out if out is not None else torch.empty((n_seg, k), dtype=x.dtype, device=x.device)
+    c = codec(TC_TOPK, n_seg, L, k, wire=_dt(x))
+    p = Payload(_ptr(pl.idx), None, None, None, _ptr(pl.blk) if use_blk else None)
+    ep = None if e is None else C.cast(e.data_ptr(), C.POINTER(C.c_float))
+    _check(lib().tc_topk_gather(C.byref(c), C.byref(p), _ptr(x), _dt(x), ep, _ptr(val), _stream(x.device)),
+           "tc_topk_gather")
+    return val
 
 
 # ------------------------------------------------------------- quantization
