@@ -430,10 +430,13 @@ EF_WORKLOADS = {
                    shape=(128, 128, 16, 16), n_seg=128, gen="relu", dtype="f32",
                    main=("topk", 1, 10), variants=[("topk", 3, 10), ("quant", 2), ("quant", 4), ("quant", 8)]),
     # transformer boundary: bf16 hidden states 8 x 512 x 768 with outlier
-    # channels, one segment / group per token row; TopK 10 % + EF, variant Q4 + EF
+    # channels, one segment / group per token row; TopK 10 % + EF, variants
+    # Q4 + EF and the backward gradient (N(0, 1e-4)) compressed at the
+    # activations' kept indices, alone and with EF
     "transformer": dict(desc="GPT-2-small boundary: 8 x 512 x 768 bf16 hidden states with 4 outlier channels x20, "
                              "per-token-row segments", shape=(8, 512, 768), n_seg=8 * 512, gen="hidden",
-                        dtype="bf16", main=("topk", 1, 10), variants=[("quant", 4)]),
+                        dtype="bf16", main=("topk", 1, 10),
+                        variants=[("quant", 4), ("reuse", 1, 10, False), ("reuse", 1, 10, True)]),
 }
 
 
@@ -481,6 +484,30 @@ def run_ef(args, dev, name):
             def recv():
                 tc.topk_decompress(pl, L, out=y)
             label = f"TopK {100 * codec[1] // codec[2]} % + EF"
+        elif codec[0] == "reuse":
+            # the gradient of a boundary tensor sent at the indices its TopK
+            # kept in the forward pass (one forward payload, rotating gradients)
+            k = tc.topk_count(L, codec[1], codec[2])
+            fwd = tc.topk_compress(xs[0], k, n_seg)
+            gs = [(1e-4 * W.randn((n_seg, L), args.seed, 1000 + i, device=dev)).to(tdt) for i in range(n_sets)]
+            ef = codec[3]
+            val = torch.empty((n_seg, k), dtype=tdt, device=dev)
+            pl = fwd._replace(val=val)
+            blk_bytes = 4 * n_seg * (tc.n_blocks(L) + 1)
+            payload = n_seg * k * esz
+
+            def send(i):
+                tc.topk_gather(fwd, gs[i % n_sets], e=es[i % n_sets] if ef else None, out=val)
+
+            def recv():
+                tc.topk_decompress(pl, L, out=y)
+            label = f"gradient at the activations' TopK {100 * codec[1] // codec[2]} % indices" + (" + EF" if ef else "")
+            if ef:   # read g, read e, write e, read idx (+ table), write values
+                send_bytes = esz * N + 8 * N + 4 * n_seg * k + blk_bytes + payload
+            else:    # read idx, read the values there, write them
+                send_bytes = 4 * n_seg * k + 2 * payload
+            recv_bytes = 4 * n_seg * k + blk_bytes + payload + esz * N
+            return send, recv, send_bytes, recv_bytes, label
         else:
             b = codec[1]
             codes = torch.empty((n_seg, tc.quant_group_bytes(L, b)), dtype=torch.uint8, device=dev)
