@@ -425,10 +425,12 @@ def run_aqsgd(args, dev):
 
 EF_WORKLOADS = {
     # ResNet-18 boundary: post-ReLU activations 128 x 128x16x16 fp32, one
-    # segment / group per sample; TopK 10 % + EF, variants TopK 30 %, Q2/4/8 + EF
+    # segment / group per sample; TopK 10 % + EF, variants TopK 30 %, Q2/4/8 + EF,
+    # EF21 + TopK 10 % (one fp32 buffer row per sample on each side)
     "resnet": dict(desc="ResNet-18 boundary: 128 x 128x16x16 fp32 post-ReLU activations, per-sample segments",
                    shape=(128, 128, 16, 16), n_seg=128, gen="relu", dtype="f32",
-                   main=("topk", 1, 10), variants=[("topk", 3, 10), ("quant", 2), ("quant", 4), ("quant", 8)]),
+                   main=("topk", 1, 10),
+                   variants=[("topk", 3, 10), ("quant", 2), ("quant", 4), ("quant", 8), ("ef21", 1, 10)]),
     # transformer boundary: bf16 hidden states 8 x 512 x 768 with outlier
     # channels, one segment / group per token row; TopK 10 % + EF, variants
     # Q4 + EF and the backward gradient (N(0, 1e-4)) compressed at the
@@ -484,6 +486,25 @@ def run_ef(args, dev, name):
             def recv():
                 tc.topk_decompress(pl, L, out=y)
             label = f"TopK {100 * codec[1] // codec[2]} % + EF"
+        elif codec[0] == "ef21":
+            # g <- g + TopK(x - g) on the sender, the same on the receiver's g_r
+            k = tc.topk_count(L, codec[1], codec[2])
+            pl = tc.empty_topk_payload(n_seg, L, k, tdt, dev)
+            g = torch.zeros((n_seg, L), dtype=tdt, device=dev)
+            g_r = torch.zeros((n_seg, L), dtype=tdt, device=dev)
+            c = tc.codec(tc.TC_TOPK, n_seg, L, k, wire=tc._dt(xs[0]))
+            ws = tc.workspace(c, dev)
+            payload = n_seg * (k * (4 + esz) + 4 * (tc.n_blocks(L) + 1))
+
+            def send(i):
+                tc.ef21_step(xs[i % n_sets], g, k, ws=ws, out=pl)
+
+            def recv():
+                tc.ef21_reconstruct(pl, g_r, out=y)
+            label = f"EF21 + TopK {100 * codec[1] // codec[2]} %"
+            send_bytes = 3 * esz * N + payload   # read x, read g, write g, write payload
+            recv_bytes = payload + 3 * esz * N   # read payload, read g_r, write g_r and the received tensor
+            return send, recv, send_bytes, recv_bytes, label
         elif codec[0] == "reuse":
             # the gradient of a boundary tensor sent at the indices its TopK
             # kept in the forward pass (one forward payload, rotating gradients)

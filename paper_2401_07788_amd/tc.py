@@ -393,6 +393,31 @@ def aqsgd_step(a: torch.Tensor, m: torch.Tensor, ids: torch.Tensor, k: int, ws=N
     return out
 
 
+_ROW_IDS = {}
+
+
+def _row_ids(n: int, device) -> torch.Tensor:
+    """ids 0..n-1 on device (kept, so that a captured graph holds no allocation)"""
+    key = (n, str(device))
+    t = _ROW_IDS.get(key)
+    if t is None:
+        t = _ROW_IDS[key] = torch.arange(n, dtype=torch.int64, device=device)
+    return t
+
+
+def ef21_step(x: torch.Tensor, g: torch.Tensor, k: int, ws=None, out: TopkPayload = None, blk: bool = True):
+    """EF21 sender (Sec. 2.4): send C(x - g) with C = TopK, then g <- g + C(x - g);
+    x and g are [n_seg, seg_len] of one dtype, g (the previously sent value) is
+    updated in place.  This is the Sec. 2.5 AQ-SGD sender with one buffer row
+    per segment (ids 0..n_seg-1)."""
+    return aqsgd_step(x, g, _row_ids(g.shape[0], g.device), k, ws=ws, out=out, blk=blk)
+
+
+def ef21_reconstruct(pl: TopkPayload, g_r: torch.Tensor, out=None, use_blk: bool = True):
+    """EF21 receiver: g_r <- g_r + received; returns g_r (a copy in `out` if given)"""
+    return aqsgd_reconstruct(pl, g_r, _row_ids(g_r.shape[0], g_r.device), out=out, use_blk=use_blk)
+
+
 def aqsgd_reconstruct(pl: TopkPayload, m_r: torch.Tensor, ids: torch.Tensor, out=None, use_blk: bool = True):
     """receiver: m_r[ids] += received; returns a_hat = m_r[ids].  m_r is updated in place."""
     _need_gpu(pl.idx, pl.val, pl.blk, m_r, ids)

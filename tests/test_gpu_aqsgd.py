@@ -109,3 +109,28 @@ def test_aqsgd_full_size(tc, orc):
     assert torch.equal(m_s[untouched].view(torch.int16), ref.view(torch.int16))
     del m_s, m_r
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("shape", [(128, 32768), (6, 100003)])
+def test_ef21_parity(tc, orc, shape):
+    # EF21 (Sec. 2.4): g <- g + TopK(x - g) on both sides, one row per segment
+    B, L = shape
+    k = tc.topk_count(L, 1, 10)
+    g = torch.zeros((B, L), dtype=torch.float32, device="cuda")
+    g_r = g.clone()
+    go = np.zeros((B, L), np.float32)
+    go_r = go.copy()
+    ids = np.arange(B)
+    for t in range(3):
+        x = W.relu_activation((B, L), 3, t)
+        p = tc.ef21_step(x.cuda(), g, k)
+        out = tc.ef21_reconstruct(p, g_r)
+        torch.cuda.synchronize()
+        assert tc.device_errors() == 0
+        oi, ov = orc.aqsgd_send(raw(x), go, "f32", ids, k)
+        orc.aqsgd_recv(oi, ov, go_r, "f32", ids, k)
+        assert_bits_equal(raw(p.idx), oi, f"idx step {t}")
+        assert_bits_equal(raw(p.val), ov, f"val step {t}")
+        assert_bits_equal(raw(g), go, f"g step {t}")
+        assert_bits_equal(raw(g_r), go_r, f"g_r step {t}")
+        assert_bits_equal(raw(out), go_r, f"received step {t}")

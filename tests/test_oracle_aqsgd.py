@@ -85,3 +85,29 @@ def test_rejects_out_of_range_ids(orc):
     a = np.zeros((1, 8), np.uint16)
     with pytest.raises(ValueError):
         orc.aqsgd_send(a, m, "f16", np.array([4]), 2)
+
+
+def test_ef21_reaches_a_fixed_input(orc):
+    # EF21 (Sec. 2.4): g <- g + C(x - g) is AQ-SGD with one buffer row per
+    # segment.  With binary32 values and x held fixed, each step sends the k
+    # largest remaining differences exactly, so the difference shrinks and g
+    # equals x after ceil(L / k) steps, on both sides
+    rng = np.random.default_rng(11)
+    B, L, k = 3, 500, 60
+    x = rng.standard_normal((B, L)).astype(np.float32)
+    g = np.zeros((B, L), np.float32)
+    g_r = g.copy()
+    ids = np.arange(B)
+    prev = np.abs(x - g).sum()
+    for t in range(-(-L // k)):
+        before = g.copy()
+        idx, val = orc.aqsgd_send(x, g, "f32", ids, k)
+        orc.aqsgd_recv(idx, val, g_r, "f32", ids, k)
+        assert (g == g_r).all()
+        for b in range(B):
+            # the message is the difference at the sent indices
+            assert (val[b] == (x[b] - before[b])[idx[b]]).all()
+        diff = np.abs(x - g).sum()
+        assert diff < prev or diff == 0.0
+        prev = diff
+    assert (g == x).all()
