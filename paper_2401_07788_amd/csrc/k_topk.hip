@@ -766,14 +766,15 @@ __global__ __launch_bounds__(GRP_NT) void k_topk_grp(TopkArgs a) {
 
 // ------------------------------------------------------------- LDS engine
 // One workgroup per segment of up to LDS_MAX elements (per-sample CNN
-// activations and gradients): the segment's values v = x (+ e) stay in LDS
-// as binary32 for the whole selection, so no other workgroup takes part and
-// nothing crosses the workgroup.  Loads are lane-consecutive 4-element
-// pieces; three digit passes over LDS (key bits 30..19, 18..7, 6..0) give T
-// and the tie quota; then thread t places its run of LDS_RUN consecutive
-// elements (kept-entry bit masks, one scan), writes its kept entries to the
-// payload and its residual.  1024 threads: four waves per SIMD share the
-// per-key work, which is what bounds this kernel.
+// activations and gradients, short AQ-SGD / EF21 rows): the segment's values
+// v = x (+ e), or a - m, stay in LDS as binary32 for the whole selection, so
+// no other workgroup takes part and nothing crosses the workgroup.  Loads are
+// lane-consecutive 4-element pieces; three digit passes over LDS (key bits
+// 30..19, 18..7, 6..0) give T and the tie quota; then thread t places its run
+// of LDS_RUN consecutive elements (kept-entry bit masks, one scan), writes
+// its kept entries to the payload and its residual (EF) or moves the buffer
+// row at its kept entries (AQ-SGD).  1024 threads: four waves per SIMD share
+// the per-key work, which is what bounds this kernel.
 constexpr int LDS_NT = 1024;
 constexpr uint32_t LDS_MAX = 32768;
 constexpr uint32_t LDS_RUN = LDS_MAX / LDS_NT;   // 32: one bit mask word per thread
@@ -851,7 +852,6 @@ __device__ __forceinline__ void lds_pass_list(const uint32_t* s_list, uint32_t n
 
 template <typename InT, int SEL>
 __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
-  static_assert(SEL != SEL_AQSGD, "AQ-SGD segments take the group engine");
   using Raw = typename Elem<InT>::raw;
   constexpr int NT = LDS_NT;
   __shared__ __attribute__((aligned(16))) uint32_t s_v[LDS_MAX];   // the segment's values (binary32 bits)
@@ -861,16 +861,26 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
   __shared__ uint32_t found[2];
   const uint32_t t = threadIdx.x;
   const uint32_t L = (uint32_t)a.L;   // <= LDS_MAX (the plan guarantees it)
-  const bool vec = ((((uintptr_t)a.x | (uintptr_t)a.e) & 15u) == 0) && (L % 4u) == 0;
+  const bool vec = ((((uintptr_t)a.x | (uintptr_t)a.e | (uintptr_t)a.m) & 15u) == 0) && (L % 4u) == 0;
   for (uint64_t seg = blockIdx.x; seg < a.n_seg; seg += gridDim.x) {
     const Raw* xs = (const Raw*)a.x + seg * a.L;
     float* es = (SEL == SEL_EF) ? a.e + seg * a.L : nullptr;
+    // AQ-SGD: the example's buffer row; v = a - m
+    Raw* ms = nullptr;
+    if constexpr (SEL == SEL_AQSGD) {
+      const int64_t id = a.ids[seg];
+      if (id < 0 || (uint64_t)id >= a.n_samples) {
+        if (t == 0) raise_error(KERR_BAD_ID);
+        continue;                  // every thread skips alike
+      }
+      ms = (Raw*)a.m + (uint64_t)id * a.L;
+    }
     // ---- values into LDS: piece q = 4 elements, lanes consecutive; loads
     // go out four pieces at a time (the registers of 1024 threads)
     if (vec) {
 #pragma unroll
       for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
-        Raw xr[4][4];
+        Raw xr[4][4], mr[4][4];
         float er[4][4];
 #pragma unroll
         for (uint32_t j = 0; j < 4; ++j) {
@@ -878,6 +888,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
           if (i0 < L) {
             load_run<Raw, 4, true>(xs + i0, xr[j]);
             if constexpr (SEL == SEL_EF) load_run<float, 4, true>(es + i0, er[j]);
+            if constexpr (SEL == SEL_AQSGD) load_run<Raw, 4, true>(ms + i0, mr[j]);
           }
         }
 #pragma unroll
@@ -889,6 +900,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
             for (int c = 0; c < 4; ++c) {
               float x = Elem<InT>::up(xr[j][c]);
               if constexpr (SEL == SEL_EF) x = x + er[j][c];
+              if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(mr[j][c]);
               w[c] = __float_as_uint(x);
             }
             *reinterpret_cast<u32x4*>(&s_v[i0]) = w;
@@ -907,6 +919,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
           if (i < L) {
             x = Elem<InT>::up(xs[i]);
             if constexpr (SEL == SEL_EF) x = x + es[i];
+            if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(ms[i]);
           }
           w[c] = __float_as_uint(x);
         }
@@ -1013,6 +1026,29 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
       val[pos] = Elem<InT>::down(__uint_as_float(s_v[b0 + bit]));
       ++pos;
     }
+    // AQ-SGD: the buffer row moves by the sent values at the kept entries
+    // only; per half of the run, that half's buffer values are loaded at once
+    if constexpr (SEL == SEL_AQSGD) {
+#pragma unroll
+      for (uint32_t hh = 0; hh < LDS_RUN; hh += 16) {
+        const uint32_t kh = (km >> hh) & 0xFFFFu;
+        if (kh == 0u) continue;
+        Raw mo[16];
+        if (vec && hh + 16 <= nr) {
+          load_run<Raw, 16, false>(ms + b0 + hh, mo);
+        } else {
+#pragma unroll
+          for (uint32_t c = 0; c < 16; ++c) mo[c] = (hh + c < nr) ? ms[b0 + hh + c] : Raw{};
+        }
+#pragma unroll
+        for (uint32_t c = 0; c < 16; ++c) {
+          if ((kh >> c) & 1u) {
+            const Raw w = Elem<InT>::down(__uint_as_float(s_v[b0 + hh + c]));
+            ms[b0 + hh + c] = Elem<InT>::down(Elem<InT>::up(mo[c]) + Elem<InT>::up(w));
+          }
+        }
+      }
+    }
     // block table: kept entries below each block boundary (a boundary
     // starts a thread's run)
     if (a.blk) {
@@ -1100,7 +1136,7 @@ const void* pick(int sel, int dt, bool row, int v) {
   return pick_sel<SEL_AQSGD>(dt, row, v);
 }
 
-// LDS engine: plain and EF TopK
+// LDS engine: plain, EF and AQ-SGD TopK
 const void* lds_ptr(int sel, int dt) {
   if (sel == SEL_PLAIN) {
     if (dt == DT_F32) return (const void*)k_topk_lds<float, SEL_PLAIN>;
@@ -1112,7 +1148,9 @@ const void* lds_ptr(int sel, int dt) {
     if (dt == DT_BF16) return (const void*)k_topk_lds<bf16_t, SEL_EF>;
     return (const void*)k_topk_lds<f16_t, SEL_EF>;
   }
-  return nullptr;
+  if (dt == DT_F32) return (const void*)k_topk_lds<float, SEL_AQSGD>;
+  if (dt == DT_BF16) return (const void*)k_topk_lds<bf16_t, SEL_AQSGD>;
+  return (const void*)k_topk_lds<f16_t, SEL_AQSGD>;
 }
 
 int occupancy(const void* fn, int nt) {
@@ -1126,7 +1164,7 @@ int occupancy(const void* fn, int nt) {
 SegPlan plan_topk(int sel, int dt, uint64_t n_seg, uint64_t L) {
   SegPlan p;
   const uint32_t cus = (uint32_t)device_cus();
-  if (sel != SEL_AQSGD && L > ROW_MAX && L <= LDS_MAX) {
+  if (L > ROW_MAX && L <= LDS_MAX) {
     // one workgroup per segment, the segment in LDS
     p.nt = LDS_NT;
     p.lds = true;

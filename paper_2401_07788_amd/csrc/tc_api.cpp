@@ -209,9 +209,9 @@ TC_API tc_status tc_workspace_bytes(const tc_codec* c, size_t* bytes) {
   uint64_t words = 0;
   const int dt = dt_ok(c->wire) ? c->wire : TC_F32;
   if (c->kind == TC_TOPK) {
-    // enough for every sender kind of this shape (plain and EF may hold a
-    // segment in LDS and need none, AQ-SGD keeps the group engine); a
-    // segment too long for them takes the global chain
+    // enough for every sender kind of this shape (the plans of EF and
+    // AQ-SGD differ where a plan has to fit a resident group); a segment too
+    // long for them takes the global chain
     for (int sel : {tc::SEL_EF, tc::SEL_AQSGD}) {
       const tc::SegPlan p = tc::plan_topk(sel, dt, c->n_seg, c->seg_len);
       words = std::max<uint64_t>(words, (p.n_groups == 0 || p.P > p.capacity) ? tc::global_ws_words(c->seg_len)

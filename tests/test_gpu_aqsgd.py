@@ -42,7 +42,7 @@ def aq_steps(tc, orc, m0, ids_list, acts, k, check_rows=None):
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16", "f32"])
-@pytest.mark.parametrize("L", [1000, 100003])
+@pytest.mark.parametrize("L", [1000, 12289, 16384, 100003])
 def test_aqsgd_small(tc, orc, dt, L):
     n_samples, B = 24, 4
     m0 = W.randn((n_samples, L), 1, 0).to(TORCH[dt])
