@@ -10,10 +10,13 @@
 // the whole kernel: inputs are read once, the selection works on registers
 // and LDS, and the outputs are written once.
 //
-// Two engines:
+// Three engines:
 //   k_topk_row : one wavefront per segment of up to 2048 elements (token
-//                rows); bitwise select with ballots, no LDS, no barriers.
-//   k_topk_grp : P workgroups of 512 threads per segment (samples,
+//                rows); radix select over 8-bit digits with a wavefront-
+//                private LDS histogram, one wavefront scan per digit.
+//   k_topk_lds : one 1024-thread workgroup per segment of up to 32,768
+//                elements (per-sample tensors), the segment held in LDS.
+//   k_topk_grp : P workgroups of 512 threads per segment (long samples,
 //                examples); striped register layout, two cross-workgroup
 //                exchanges (tc_group.hpp), payload staged in LDS and written
 //                in index order with full-line stores.
@@ -45,6 +48,7 @@ template <typename InT, int SEL, int VPT>
 __global__ __launch_bounds__(WAVE) void k_topk_row(TopkArgs a) {
   using R = typename Elem<InT>::raw;
   __shared__ uint32_t scratch[2];
+  __shared__ __attribute__((aligned(16))) uint32_t hist[256];
   for (uint64_t seg = blockIdx.x; seg < a.n_seg; seg += gridDim.x) {
     const uint64_t c0 = (uint64_t)threadIdx.x * VPT;
     const int nv = (int)min((uint64_t)VPT, sat_sub(a.L, c0));
@@ -85,7 +89,7 @@ __global__ __launch_bounds__(WAVE) void k_topk_row(TopkArgs a) {
 
     SelResult sr;
     if (a.k == 0) { sr.T = 0xFFFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0; }
-    else sr = bitwise_select<VPT>(key, nv, (uint32_t)a.k);
+    else sr = wave_radix_select<VPT>(key, nv, (uint32_t)a.k, hist);
     const Placement pl = place<WAVE, VPT>(key, nv, sr, scratch);
 
     uint32_t* idx = a.idx + seg * a.k;

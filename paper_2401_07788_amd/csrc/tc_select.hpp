@@ -6,8 +6,8 @@
 //   key > T, or key == T and the entry is among the r lowest-index ties.
 //
 // Shared pieces: bin search over histograms (in LDS or merged in device
-// memory), and the one-wavefront strategy for short segments (a token row),
-// which fixes T bit by bit counting with ballots: no LDS, no barriers.  The
+// memory), and the one-wavefront strategy for short segments (a token row):
+// a radix select over 8-bit digits with a wavefront-private histogram.  The
 // several-workgroup strategy is in tc_group.hpp.
 #pragma once
 
@@ -121,23 +121,50 @@ __device__ __forceinline__ void zero_lds(uint32_t* h, int n) {
   for (int b = (int)threadIdx.x; b < n; b += NT) h[b] = 0u;
 }
 
-// Exact threshold for a segment held entirely by one wavefront (NT == 64).
+// Exact threshold for a segment held entirely by one wavefront (NT == 64):
+// radix select over 8-bit digits of the key from bit 23 down, then its last
+// 7 bits, with one 256-bin histogram in LDS private to the wavefront (`hist`,
+// 16-byte aligned); each digit is found with one wavefront scan (lane l owns
+// bins 4l..4l+3).
 template <int VPT>
-__device__ __forceinline__ SelResult bitwise_select(const uint32_t (&key)[VPT], int nv, uint32_t k) {
-  uint32_t T = 0u;
-  for (int bit = 30; bit >= 0; --bit) {
-    const uint32_t cand = T | (1u << bit);
-    uint32_t cnt = 0;
+__device__ __forceinline__ SelResult wave_radix_select(const uint32_t (&key)[VPT], int nv, uint32_t k,
+                                                       uint32_t* hist) {
+  const uint32_t lane = (uint32_t)lane_id();
+  uint32_t prefix = 0u, need = k, pbits = 0u;
 #pragma unroll
-    for (int v = 0; v < VPT; ++v) cnt += (uint32_t)__popcll(__ballot(v < nv && key[v] >= cand));
-    if (cnt >= k) T = cand;
+  for (int pass = 0; pass < 4; ++pass) {
+    const uint32_t width = (pass < 3) ? 8u : 7u;
+    const uint32_t shift = 31u - pbits - width;
+    reinterpret_cast<u32x4*>(hist)[lane] = u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < VPT; ++i)
+      if (i < nv && (key[i] >> (shift + width)) == prefix) atomicAdd(&hist[(key[i] >> shift) & ((1u << width) - 1u)], 1u);
+    __syncthreads();
+    const u32x4 h = reinterpret_cast<const u32x4*>(hist)[lane];
+    const uint32_t sum = h[0] + h[1] + h[2] + h[3];
+    const uint32_t incl = wave_incl_scan(sum);
+    uint32_t acc = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1) - incl;   // bins of higher lanes
+    uint32_t d = 0u;
+    const bool here = acc < need && need <= acc + sum;
+    if (here) {
+#pragma unroll
+      for (int c = 3; c >= 0; --c) {
+        if (acc + h[c] >= need) { d = 4u * lane + (uint32_t)c; break; }
+        acc += h[c];
+      }
+    }
+    const int src = __builtin_ctzll(__ballot(here));
+    d = (uint32_t)__builtin_amdgcn_readlane((int)d, src);
+    acc = (uint32_t)__builtin_amdgcn_readlane((int)acc, src);
+    prefix = (prefix << width) | d;
+    need -= acc;
+    pbits += width;
+    __syncthreads();
   }
-  uint32_t gt = 0;
-#pragma unroll
-  for (int v = 0; v < VPT; ++v) gt += (uint32_t)__popcll(__ballot(v < nv && key[v] > T));
   SelResult res;
-  res.T = T;
-  res.r = k - gt;
+  res.T = prefix;
+  res.r = need;
   res.gt_before = 0u;
   res.eq_before = 0u;
   return res;
