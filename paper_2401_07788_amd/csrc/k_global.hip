@@ -14,15 +14,17 @@
 //            band holds the k-th key)
 //   pass 1-3 the three radix digits (12/12/7 bits) -> threshold T and the tie
 //            quota r, over the candidate list when the band held the k-th
-//            key, else over the whole segment
-//   keptmm   (quantized kept list) min / max of the kept values from the
-//            candidate list and the band pass, so that emit can quantize
-//   emit     one ordered pass over tiles: counts, decoupled look-back for
-//            the tile's payload offset, payload staged in LDS and written
-//            coalesced, the dense residual, the block table
-//   qpack    (quantized kept list, only when keptmm could not fix min / max)
-//            codes, meta and the residual at the kept entries
-//   clean    tile words, candidate list and state back to zero
+//            key, else over the whole segment; when the band is narrow the
+//            band pass counts its digits and pass 1 has nothing left to do
+//   tcount   per-tile counts and offsets; (quantized kept list) on the way,
+//            the min / max of the kept candidates, so that with the band's
+//            values emit can quantize
+//   emit     one ordered pass over tiles: kept entries marked, encoded from
+//            a compacted list, payload written coalesced, the dense
+//            residual, the block table
+//   finish   (quantized kept list, only when min / max could not be fixed in
+//            advance) codes, meta and the residual at the kept entries; then
+//            tile words, candidate list and state back to zero
 // The input is read twice on the candidate path (band, emit), plus the
 // sample.
 //
@@ -62,6 +64,7 @@ enum : int {
   ST_TPOS, ST_TNEG,     // candidates with key == T, by sign
   ST_PRE,               // 1: lo / hi / scale known before emit
   ST_LO, ST_HI, ST_SCALE,
+  ST_P1,                // 1: the band pass already found the first digit (pass 1 has nothing to do)
   ST_SPREAD = 64,       // spread counters: NSLOT slots + a top word, SLOT_WORDS apart
   SP_WORDS = (NSLOT + 1) * SLOT_WORDS,
   SP_DONE = ST_SPREAD,                  // kernel completion (top word: slots done)
@@ -71,7 +74,9 @@ enum : int {
   SP_AMAX = SP_AMIN + SP_WORDS,
   ST_WORDS = 2048
 };
-static_assert(SP_AMAX + SP_WORDS <= ST_WORDS, "state words");
+constexpr uint32_t BD_MAX = 32;    // band digits counted per digit in the band pass (narrower bands)
+constexpr int SP_BD = SP_AMAX + SP_WORDS;   // [NSLOT][BD_MAX] candidates per band digit
+static_assert(SP_BD + NSLOT * BD_MAX <= ST_WORDS, "state words");
 
 __device__ __forceinline__ uint32_t* slot(uint32_t* st, int sp, uint32_t c) { return st + sp + SLOT_WORDS * c; }
 
@@ -286,7 +291,9 @@ __global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
   __shared__ uint32_t scratch[G_NT / WAVE + 2];
   __shared__ uint32_t s_base;
   __shared__ float s_mm[2 * (G_NT / WAVE)];
+  __shared__ uint32_t s_bd[BD_MAX];   // this workgroup's candidates per band digit
   uint32_t* st = a.state;
+  if (threadIdx.x < BD_MAX) s_bd[threadIdx.x] = 0u;
   // the quantized kept list's emit ORs codes into the words it shares with
   // neighbouring tiles: they start at zero
   if (a.codes) {
@@ -294,6 +301,7 @@ __global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
     for (uint64_t i = (uint64_t)blockIdx.x * G_NT + threadIdx.x; i < a.wpg; i += gsz) a.codes[i] = 0u;
   }
   const uint32_t blo = st[ST_BLO], bhi = st[ST_BHI];
+  const bool count_digits = bhi - blo < BD_MAX;   // the band's digits are counted here
   const uint32_t c = blockIdx.x % a.n_sub;
   const uint64_t capc = sub_cap(a);
   uint32_t nbuf = 0, ntl = 0;   // workgroup-uniform
@@ -364,7 +372,11 @@ __global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
         *reinterpret_cast<u32x4*>(&s_vals[threadIdx.x * G_VPT + 4 * q]) = w;
       }
       off += nbuf;
-      for (uint32_t m = bm; m; m &= m - 1u) s_cand[off++] = s_vals[threadIdx.x * G_VPT + (uint32_t)__builtin_ctz(m)];
+      for (uint32_t m = bm; m; m &= m - 1u) {
+        const uint32_t bits = s_vals[threadIdx.x * G_VPT + (uint32_t)__builtin_ctz(m)];
+        s_cand[off++] = bits;
+        if (count_digits) atomicAdd(&s_bd[((bits & 0x7FFFFFFFu) >> 19) - blo], 1u);
+      }
       nbuf += n_t;
       ++ntl;
     }
@@ -372,6 +384,8 @@ __global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
   if (nbuf) flush();
   block_minmax<G_NT>(amin, amax, s_mm);
   const uint32_t cs = blockIdx.x % NSLOT;
+  if (count_digits && threadIdx.x <= bhi - blo && s_bd[threadIdx.x])
+    add_agent(&st[SP_BD + cs * BD_MAX + threadIdx.x], s_bd[threadIdx.x]);
   if (threadIdx.x == 0) {
     if (above_all) add_agent(slot(st, SP_ABOVE, cs), above_all);
     if (amin <= amax) {
@@ -393,6 +407,21 @@ __global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
   st[ST_ABOVE] = (uint32_t)ab;
   st[ST_FAST] = fast ? 1u : 0u;
   st[ST_NEED1] = fast ? (uint32_t)(a.k - ab) : (uint32_t)a.k;
+  // the first digit of T from the band's per-digit counts, when they were kept
+  if (fast && count_digits) {
+    uint32_t need = (uint32_t)(a.k - ab), acc = 0;
+    for (uint32_t d = bhi + 1; d-- > blo;) {
+      uint32_t cnt = 0;
+      for (uint32_t c = 0; c < NSLOT; ++c) cnt += ld_agent(&st[SP_BD + c * BD_MAX + (d - blo)]);
+      if (acc + cnt >= need) {
+        st[ST_B1] = d;
+        st[ST_NEED2] = need - acc;
+        st[ST_P1] = 1u;
+        break;
+      }
+      acc += cnt;
+    }
+  }
   // values above the band, for the kept list's min / max
   st[ST_AMIN] = slot_max(st, SP_AMIN);
   st[ST_AMAX] = slot_max(st, SP_AMAX);
@@ -419,6 +448,7 @@ __global__ __launch_bounds__(G_NT) void k_g_pass(GlobalArgs a) {
   __shared__ uint32_t scratch[G_NT / WAVE + 2];
   __shared__ uint32_t found[2];
   uint32_t* st = a.state;
+  if (PASS == 1 && st[ST_P1] != 0u) return;   // the band pass found the first digit
   const bool fast = st[ST_FAST] != 0u;
   zero_lds_bins(hist, NB);
   __syncthreads();
@@ -469,35 +499,38 @@ __global__ __launch_bounds__(G_NT) void k_g_pass(GlobalArgs a) {
 }
 
 // ------------------------------------------------------------------ keptmm
-// min / max of the kept values, from the candidate list (keys == T are the
-// ties; keys > T in the list are kept) and the values above the band.  The r
-// kept ties are the lowest-indexed ones; the list does not keep indices, so
-// when ties of both signs exist and only some are kept, the tie values can
-// decide lo or hi only if no kept value lies beyond +-|T| on that side; then
-// the quantization is left to qpack.
-__global__ __launch_bounds__(G_NT) void k_g_keptmm(GlobalArgs a) {
-  __shared__ uint32_t scratch[G_NT / WAVE + 2];
-  __shared__ float s_mm[2 * (G_NT / WAVE)];
-  uint32_t* st = a.state;
-  if (st[ST_FAST] == 0u) return;
-  const uint32_t T = st[ST_T];
+// Min / max of the kept values, from the candidate list (keys == T are the
+// ties; keys > T in the list are kept) and the values above the band; tcount
+// reads every candidate once and gathers these on the way.  The r kept ties
+// are the lowest-indexed ones; the list does not keep indices, so when ties
+// of both signs exist and only some are kept, the tie values can decide lo
+// or hi only if no kept value lies beyond +-|T| on that side; then the
+// quantization is left to qpack.
+struct KeptMM {
   float mn = __builtin_inff(), mx = -__builtin_inff();
   uint32_t tp = 0, tn = 0;
-  for_candidates(a, [&](uint32_t bits) {
+  __device__ __forceinline__ void add(uint32_t bits, uint32_t T) {
     const uint32_t kk = bits & 0x7FFFFFFFu;
     if (kk > T) { const float v = __uint_as_float(bits); mn = fminf(mn, v); mx = fmaxf(mx, v); }
     else if (kk == T) { if (bits >> 31) ++tn; else ++tp; }
-  });
-  block_minmax<G_NT>(mn, mx, s_mm);
-  const uint32_t tps = block_sum<G_NT>(tp, scratch);
-  const uint32_t tns = block_sum<G_NT>(tn, scratch);
+  }
+};
+
+// the workgroup's part into the state (all threads call)
+__device__ __forceinline__ void keptmm_push(uint32_t* st, KeptMM& m, uint32_t* scratch, float* s_mm) {
+  block_minmax<G_NT>(m.mn, m.mx, s_mm);
+  const uint32_t tps = block_sum<G_NT>(m.tp, scratch);
+  const uint32_t tns = block_sum<G_NT>(m.tn, scratch);
   if (threadIdx.x == 0) {
-    push_minmax(st, ST_AMIN, ST_AMAX, mn, mx);
+    push_minmax(st, ST_AMIN, ST_AMAX, m.mn, m.mx);
     if (tps) add_agent(&st[ST_TPOS], tps);
     if (tns) add_agent(&st[ST_TNEG], tns);
   }
-  if (!last_block(st)) return;
-  if (threadIdx.x != 0) return;
+}
+
+// lo / hi / scale of the kept list, once every workgroup has pushed (one thread)
+__device__ __forceinline__ void keptmm_final(const GlobalArgs& a, uint32_t* st) {
+  const uint32_t T = st[ST_T];
   const uint32_t wmin = ld_agent(&st[ST_AMIN]), wmax = ld_agent(&st[ST_AMAX]);
   float lo = wmax ? from_order_key(~wmin) : __builtin_inff();
   float hi = wmax ? from_order_key(wmax) : -__builtin_inff();
@@ -548,9 +581,13 @@ template <typename InT, bool EF>
 __global__ __launch_bounds__(G_NT) void k_g_tcount(GlobalArgs a) {
   __shared__ uint32_t s_gt[TPW_MAX], s_eq[TPW_MAX];
   __shared__ uint32_t scratch[G_NT / WAVE + 2];
+  __shared__ float s_mm[2 * (G_NT / WAVE)];
   uint32_t* st = a.state;
   const bool fast = st[ST_FAST] != 0u;
   const uint32_t T = st[ST_T];
+  // the quantized kept list's min / max come from the candidates read here
+  const bool mm = fast && a.bits != 0 && a.bits != 32;
+  KeptMM kmm;
   const uint64_t t_lo = (uint64_t)blockIdx.x * a.tpw;
   const uint32_t nt = (uint32_t)min((uint64_t)a.tpw, sat_sub(a.n_tiles, t_lo));
   if (fast) {
@@ -562,9 +599,10 @@ __global__ __launch_bounds__(G_NT) void k_g_tcount(GlobalArgs a) {
       uint32_t gt = 0, eq = 0;
       if ((uint64_t)off + n <= a.cand_cap) {
         for (uint32_t j = lane; j < n; j += WAVE) {
-          const uint32_t kk = a.cand[off + j] & 0x7FFFFFFFu;
+          const uint32_t bits = a.cand[off + j], kk = bits & 0x7FFFFFFFu;
           gt += kk > T;
           eq += kk == T;
+          if (mm) kmm.add(bits, T);
         }
       } else if (lane == 0) {
         raise_error(KERR_INTERNAL);
@@ -612,7 +650,9 @@ __global__ __launch_bounds__(G_NT) void k_g_tcount(GlobalArgs a) {
     st_agent(&a.wgs[2 * blockIdx.x], gtot);
     st_agent(&a.wgs[2 * blockIdx.x + 1], etot);
   }
+  if (mm) keptmm_push(st, kmm, scratch, s_mm);
   if (!last_block(st)) return;
+  if (mm && threadIdx.x == 0) keptmm_final(a, st);
   // exclusive prefix of the workgroup totals, four per thread
   constexpr int PER = (int)(TC_GRID / G_NT);
   uint32_t gw[PER], ew[PER], gs = 0, es = 0;
@@ -833,19 +873,17 @@ __global__ __launch_bounds__(G_NT) void k_g_emit(GlobalArgs a) {
   }
 }
 
-// ------------------------------------------------------------------ qpack
-// Only when emit could not quantize: codes of the kept list (one min-max
-// group), meta, and the residual at the kept entries, where emit left X.
+// ------------------------------------------------------------ qpack, clean
 // Chunks of 8192 entries start on word boundaries for every b.
 constexpr int QP_VPT = 32;
 constexpr uint32_t QP_CH = (uint32_t)G_NT * QP_VPT;
 
+// Only when emit could not quantize: codes of the kept list (one min-max
+// group), meta, and the residual at the kept entries, where emit left X.
 template <uint32_t B, typename OutT>
-__global__ __launch_bounds__(G_NT) void k_g_qpack(GlobalArgs a) {
+__device__ __forceinline__ void qpack_body(const GlobalArgs& a, uint8_t* s_code) {
   static_assert((QP_CH * B) % 32 == 0, "chunks on word boundaries");
-  __shared__ uint8_t s_code[QP_CH];
   const uint32_t* st = a.state;
-  if (st[ST_PRE]) return;
   constexpr uint32_t LV = (1u << B) - 1u;
   float lo = 0.0f, hi = 0.0f, scale = 0.0f;
   if (a.k > 0) {
@@ -884,12 +922,19 @@ __global__ __launch_bounds__(G_NT) void k_g_qpack(GlobalArgs a) {
   }
 }
 
-// back to the zero-filled workspace: tile words, the used part of the
-// candidate list (its offset depends on the segment length, so a later call
-// may find tile words there), then the state words (the last workgroup, once
-// every workgroup has read the candidate counts)
-__global__ __launch_bounds__(G_NT) void k_g_clean(GlobalArgs a) {
+// The chain's last kernel.  B != 0 (the quantized kept list): first the
+// qpack work when emit could not quantize.  Then back to the zero-filled
+// workspace: tile words, the used part of the candidate list (its offset
+// depends on the segment length, so a later call may find tile words there),
+// then the state words (the last workgroup, once every workgroup has read
+// the candidate counts and the state).
+template <uint32_t B, typename OutT>
+__global__ __launch_bounds__(G_NT) void k_g_finish(GlobalArgs a) {
+  __shared__ uint8_t s_code[B ? QP_CH : 1];
   uint32_t* st = a.state;
+  if constexpr (B != 0) {
+    if (st[ST_PRE] == 0u) qpack_body<B, OutT>(a, s_code);   // k == 0 too: meta (0, 0)
+  }
   const uint64_t gsz = (uint64_t)gridDim.x * G_NT, t = (uint64_t)blockIdx.x * G_NT + threadIdx.x;
   for (uint64_t i = t; i < 4 * a.n_tiles; i += gsz) st_agent(&a.tiles[i], 0u);
   for (uint64_t i = t; i < 2 * TC_GRID; i += gsz) st_agent(&a.wgs[i], 0u);
@@ -946,24 +991,25 @@ const void* pick_emit(int dt, bool ef, uint32_t q) {
   return emit_ptr<f16_t>(ef, q);
 }
 
+// the last kernel: qpack's work for b-bit kept lists (b = 0: none), then clean
 template <typename OutT>
-const void* qpack_ptr(uint32_t b) {
+const void* finish_ptr(uint32_t b) {
   switch (b) {
-    case 1: return (const void*)k_g_qpack<1, OutT>;
-    case 2: return (const void*)k_g_qpack<2, OutT>;
-    case 3: return (const void*)k_g_qpack<3, OutT>;
-    case 4: return (const void*)k_g_qpack<4, OutT>;
-    case 5: return (const void*)k_g_qpack<5, OutT>;
-    case 6: return (const void*)k_g_qpack<6, OutT>;
-    case 7: return (const void*)k_g_qpack<7, OutT>;
-    case 8: return (const void*)k_g_qpack<8, OutT>;
+    case 1: return (const void*)k_g_finish<1, OutT>;
+    case 2: return (const void*)k_g_finish<2, OutT>;
+    case 3: return (const void*)k_g_finish<3, OutT>;
+    case 4: return (const void*)k_g_finish<4, OutT>;
+    case 5: return (const void*)k_g_finish<5, OutT>;
+    case 6: return (const void*)k_g_finish<6, OutT>;
+    case 7: return (const void*)k_g_finish<7, OutT>;
+    case 8: return (const void*)k_g_finish<8, OutT>;
   }
-  return nullptr;
+  return (const void*)k_g_finish<0, OutT>;
 }
-const void* pick_qpack(int out_dt, uint32_t b) {
-  if (out_dt == DT_F32) return qpack_ptr<float>(b);
-  if (out_dt == DT_BF16) return qpack_ptr<bf16_t>(b);
-  return qpack_ptr<f16_t>(b);
+const void* pick_finish(int out_dt, uint32_t b) {
+  if (out_dt == DT_F32) return finish_ptr<float>(b);
+  if (out_dt == DT_BF16) return finish_ptr<bf16_t>(b);
+  return finish_ptr<f16_t>(b);
 }
 
 hipError_t launch(const void* fn, uint32_t grid, uint32_t nt, const GlobalArgs& args, hipStream_t st) {
@@ -1014,7 +1060,6 @@ void global_ws_carve(uint32_t* ws, uint64_t L, GlobalArgs& a) {
 hipError_t launch_global(int dt, bool ef, uint32_t qbits, const GlobalArgs& args, hipStream_t st) {
   // the quantized kept list needs the residual buffer (qpack reads X there)
   if (qbits != 0 && !ef) return hipErrorInvalidValue;
-  const uint32_t cus = (uint32_t)device_cus();
   const uint32_t grid = chain_grid(args.n_tiles);
   GlobalArgs a = args;
   if (a.n_sub < 1 || a.n_sub > NSLOT || a.n_sub > grid || a.tpw < 1 || a.tpw > TPW_MAX ||
@@ -1030,7 +1075,6 @@ hipError_t launch_global(int dt, bool ef, uint32_t qbits, const GlobalArgs& args
       const void* fn = pick_chain(dt, ef, which);
       e = launch(fn, resident_grid(fn, grid), G_NT, a, st);
     }
-    if (e == hipSuccess && qbits != 0 && qbits != 32) e = launch((const void*)k_g_keptmm, CAND_GRID, G_NT, a, st);
     if (e == hipSuccess) {
       const uint32_t tgrid = (uint32_t)((a.n_tiles + a.tpw - 1) / a.tpw);
       e = launch(pick_chain(dt, ef, 5), tgrid, G_NT, a, st);
@@ -1040,12 +1084,10 @@ hipError_t launch_global(int dt, bool ef, uint32_t qbits, const GlobalArgs& args
     const void* fn = pick_emit(dt, ef, qbits);
     e = launch(fn, resident_grid(fn, grid), G_NT, a, st);
   }
-  if (e == hipSuccess && qbits != 0 && qbits != 32) {
-    const uint64_t work = (a.k + QP_CH - 1) / QP_CH;
-    const uint32_t qgrid = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(work, (uint64_t)cus * 8));
-    e = launch(pick_qpack(dt, qbits), qgrid, G_NT, a, st);
+  if (e == hipSuccess) {
+    const uint32_t qb = (qbits != 32) ? qbits : 0u;
+    e = launch(pick_finish(dt, qb), std::min<uint32_t>(grid, 1024), G_NT, a, st);
   }
-  if (e == hipSuccess) e = launch((const void*)k_g_clean, std::min<uint32_t>(grid, 1024), G_NT, a, st);
   return e;
 }
 

@@ -115,8 +115,10 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
         }
       }
     }
-    static_assert((SC_CH * sizeof(RO)) % (16 * SC_NT) == 0, "the chunk zeroes in 16-byte pieces");
-    for (uint32_t i = threadIdx.x; i < SC_CH * sizeof(RO) / 16; i += SC_NT) reinterpret_cast<u32x4*>(buf)[i] = u32x4{0u, 0u, 0u, 0u};
+    // the chunk's part of the buffer zeroed in 16-byte pieces (a short
+    // segment's chunk is the segment)
+    const uint32_t nz = (uint32_t)(((c1 - c0) * sizeof(RO) + 15) / 16);
+    for (uint32_t i = threadIdx.x; i < nz; i += SC_NT) reinterpret_cast<u32x4*>(buf)[i] = u32x4{0u, 0u, 0u, 0u};
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < SC_EPT; ++r) {
