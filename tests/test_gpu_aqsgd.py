@@ -134,3 +134,17 @@ def test_ef21_parity(tc, orc, shape):
         assert_bits_equal(raw(g), go, f"g step {t}")
         assert_bits_equal(raw(g_r), go_r, f"g_r step {t}")
         assert_bits_equal(raw(out), go_r, f"received step {t}")
+
+
+def test_aqsgd_per_token_row(tc, orc):
+    # a second AQ-SGD workload: one buffer row per 768-element token row,
+    # TopK 30 % of each row (k = 231); row ids = example id * rows + row
+    n_ex, rows, H, B = 12, 64, 768, 4
+    m0 = W.randn((n_ex * rows, H), 7, 0).to(torch.float16)
+    ex_ids = W.epoch_ids(n_ex, B, seed=7)
+    ids_list, acts = [], []
+    for t in range(3):
+        rid = (ex_ids[t].view(B, 1) * rows + torch.arange(rows).view(1, rows)).reshape(-1)
+        ids_list.append(rid)
+        acts.append(W.drifted_activation(m0, rid, 7, 20 + t))
+    aq_steps(tc, orc, m0, ids_list, acts, tc.topk_count(H, 3, 10), check_rows=np.arange(n_ex * rows))
