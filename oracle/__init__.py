@@ -52,6 +52,10 @@ def lib():
             "tco_topk_quant_decompress": (i32, [vp, vp, vp, u64, u64, u64, u32, vp, i32]),
             "tco_aqsgd_send": (i32, [vp, vp, i32, u64, u64, vp, u64, u64, vp, vp, i32]),
             "tco_aqsgd_recv": (i32, [vp, vp, vp, i32, u64, u64, vp, u64, u64, vp]),
+            "tco_efmix_kx": (u64, [u64]),
+            "tco_efmix_ke": (u64, [u64]),
+            "tco_efmix_send": (i32, [vp, i32, vp, u64, u64, u64, vp, vp, vp, vp]),
+            "tco_efmix_recv": (i32, [vp, vp, vp, vp, i32, u64, u64, u64, vp, i32]),
             "tco_to_f32": (None, [vp, i32, u64, vp]),
             "tco_from_f32": (None, [vp, u64, i32, vp]),
             "tco_through": (C.c_float, [i32, C.c_float]),
@@ -243,3 +247,34 @@ def aqsgd_recv(idx, val, m_r, dt, ids, k):
     _chk(lib().tco_aqsgd_recv(_p(idx), _p(val), _p(m_r), DT[dt], n_samples, L, _p(ids), ids.size, k,
                               _p(a_hat)), "aqsgd_recv")
     return a_hat
+
+
+# ------------------------------------------------------------------ EF-mixed
+def efmix_counts(k: int) -> tuple[int, int]:
+    """(k_x, k_e): entries of the input and of the error buffer in a budget of k"""
+    return int(lib().tco_efmix_kx(k)), int(lib().tco_efmix_ke(k))
+
+
+def efmix_send(x, dt, e, n_seg, L, k):
+    """returns (idx_x, val_x, idx_e, val_e, e_next); e is not modified"""
+    kx, ke = efmix_counts(k)
+    x = _raw(x, dt)
+    e2 = np.array(e, dtype=np.float32, copy=True, order="C")
+    idx_x = np.zeros((n_seg, kx), np.uint32)
+    val_x = np.zeros((n_seg, kx), _NP[dt])
+    idx_e = np.zeros((n_seg, ke), np.uint32)
+    val_e = np.zeros((n_seg, ke), _NP[dt])
+    _chk(lib().tco_efmix_send(_p(x), DT[dt], _p(e2), n_seg, L, k, _p(idx_x), _p(val_x), _p(idx_e), _p(val_e)),
+         "efmix_send")
+    return idx_x, val_x, idx_e, val_e, e2
+
+
+def efmix_recv(idx_x, val_x, idx_e, val_e, wire, n_seg, L, k, out_dt="f32"):
+    """the receiver's dense [n_seg, L] in out_dt"""
+    idx_x = np.ascontiguousarray(idx_x, np.uint32)
+    idx_e = np.ascontiguousarray(idx_e, np.uint32)
+    val_x, val_e = _raw(val_x, wire), _raw(val_e, wire)
+    y = np.zeros((n_seg, L), _NP[out_dt])
+    _chk(lib().tco_efmix_recv(_p(idx_x), _p(val_x), _p(idx_e), _p(val_e), DT[wire], n_seg, L, k, _p(y),
+                              DT[out_dt]), "efmix_recv")
+    return y

@@ -17,6 +17,8 @@
  *     decompress back to the original scale.
  *   - error feedback (Sec. 2.4): e = X - C(X); the next round sends C(X + e),
  *     with one global buffer per compression operator.
+ *   - EF-mixed (Sec. 2.4): half of the TopK budget on the input, half on the
+ *     error buffer; both lists are sent and added by the receiver.
  *   - AQ-SGD (Sec. 2.5): a buffer per training example; the change of the
  *     activation against that buffer is compressed and sent, and both sides
  *     add the sent message to their copy of the buffer.
@@ -541,6 +543,81 @@ int tco_aqsgd_recv(const uint32_t* idx, const void* val, void* m_r, int dt, uint
         for (uint64_t i = 0; i < L; ++i) store_rne(a_hat, dt, b * L + i, load_f32(m_r, dt, row + i));
     }
     return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* EF-mixed (Sec. 2.4): half of the K% budget goes to the largest entries of */
+/* the input, the other half to the largest entries of the error buffer.     */
+/* The paper does not spell out the arithmetic; our reading:                 */
+/*   k_x = k - floor(k/2) entries of x (the input gets the odd one),        */
+/*   k_e = floor(k/2) entries of e, each picked by tco_topk_indices on its   */
+/*   own vector (the sets may overlap);                                      */
+/*   the message is the two lists, each in x's dtype (dt); the receiver's    */
+/*   dense tensor starts at +0, takes the x list's values at its indices and */
+/*   then adds the e list's values at its indices (binary32 sum, rounded     */
+/*   once to out_dt), so the sent tensor is C_kx(x) + C_ke(e);               */
+/*   the buffer becomes everything not sent:                                 */
+/*     e'_i = (x_i - [i in S_x] dt(x_i)) + (e_i - [i in S_e] dt(e_i))        */
+/*   in binary32, which is x + e minus what the receiver holds.              */
+/* x is [n_seg][L] of dtype dt; e (binary32) is updated in place; idx_x /   */
+/* val_x are [n_seg][k_x], idx_e / val_e are [n_seg][k_e].                  */
+/* ------------------------------------------------------------------------ */
+uint64_t tco_efmix_kx(uint64_t k) { return k - k / 2; }
+uint64_t tco_efmix_ke(uint64_t k) { return k / 2; }
+
+int tco_efmix_send(const void* x, int dt, float* e, uint64_t n_seg, uint64_t L, uint64_t k,
+                   uint32_t* idx_x, void* val_x, uint32_t* idx_e, void* val_e) {
+    const uint64_t kx = tco_efmix_kx(k), ke = tco_efmix_ke(k);
+    if (k > L) return -1;
+    float* xv = (float*)malloc(sizeof(float) * (size_t)(L ? L : 1));
+    float* ev = (float*)malloc(sizeof(float) * (size_t)(L ? L : 1));
+    uint8_t* in_x = (uint8_t*)malloc((size_t)(L ? L : 1));
+    uint8_t* in_e = (uint8_t*)malloc((size_t)(L ? L : 1));
+    int bad = (!xv || !ev || !in_x || !in_e);
+    for (uint64_t s = 0; s < n_seg && !bad; ++s) {
+        const uint64_t base = s * L;
+        for (uint64_t i = 0; i < L; ++i) {
+            xv[i] = load_f32(x, dt, base + i);
+            ev[i] = e[base + i];
+            in_x[i] = in_e[i] = 0;
+        }
+        uint32_t* ix = idx_x + s * kx;
+        uint32_t* ie = idx_e + s * ke;
+        if (tco_topk_indices(xv, L, kx, ix) != 0 || tco_topk_indices(ev, L, ke, ie) != 0) { bad = 1; break; }
+        for (uint64_t j = 0; j < kx; ++j) { store_rne(val_x, dt, s * kx + j, xv[ix[j]]); in_x[ix[j]] = 1; }
+        for (uint64_t j = 0; j < ke; ++j) { store_rne(val_e, dt, s * ke + j, ev[ie[j]]); in_e[ie[j]] = 1; }
+        for (uint64_t i = 0; i < L; ++i) {
+            const float rx = xv[i] - (in_x[i] ? through(dt, xv[i]) : 0.0f);
+            const float re = ev[i] - (in_e[i] ? through(dt, ev[i]) : 0.0f);
+            e[base + i] = rx + re;
+        }
+    }
+    free(xv); free(ev); free(in_x); free(in_e);
+    return bad ? -1 : 0;
+}
+
+int tco_efmix_recv(const uint32_t* idx_x, const void* val_x, const uint32_t* idx_e, const void* val_e,
+                   int wire, uint64_t n_seg, uint64_t L, uint64_t k, void* y, int out_dt) {
+    const uint64_t kx = tco_efmix_kx(k), ke = tco_efmix_ke(k);
+    float* d = (float*)malloc(sizeof(float) * (size_t)(L ? L : 1));
+    if (!d) return -1;
+    int bad = 0;
+    for (uint64_t s = 0; s < n_seg && !bad; ++s) {
+        for (uint64_t i = 0; i < L; ++i) d[i] = 0.0f;
+        for (uint64_t j = 0; j < kx && !bad; ++j) {
+            const uint32_t i = idx_x[s * kx + j];
+            if (i >= L) bad = 1;
+            else d[i] = load_f32(val_x, wire, s * kx + j);
+        }
+        for (uint64_t j = 0; j < ke && !bad; ++j) {
+            const uint32_t i = idx_e[s * ke + j];
+            if (i >= L) bad = 1;
+            else d[i] = d[i] + load_f32(val_e, wire, s * ke + j);
+        }
+        for (uint64_t i = 0; i < L && !bad; ++i) store_rne(y, out_dt, s * L + i, d[i]);
+    }
+    free(d);
+    return bad ? -1 : 0;
 }
 
 /* helpers for tests: bulk conversions (exact upcast, RNE downcast) */
