@@ -211,6 +211,29 @@ tc_status tc_quant_unpack(const tc_codec* c, const tc_payload* in, void* y, int 
 tc_status tc_ef_step(const tc_codec* c, const void* x, int dt, float* e, const tc_payload* out,
                      void* ws, size_t ws_bytes, void* stream);
 
+/* Sec. 2.4, EF-mixed: half of the TopK budget k goes to the input, half to
+ * the error buffer.  Per segment (binary32 arithmetic):
+ *   (idx_x, v_x) = TopK(x, k_x),  k_x = k - floor(k/2), v_x sent in dt
+ *   (idx_e, v_e) = TopK(e, k_e),  k_e = floor(k/2),     v_e = e rounded to dt
+ *   e_i <- (x_i - [i in idx_x] v_x) + (e_i - [i in idx_e] v_e)
+ * so e becomes x + e minus the sent tensor C(x) + C(e).  Both selections use
+ * TopK's order (larger |v| first, ties to the lower index) and each list is in
+ * ascending index order; the two lists may share indices.  x: [n_seg][seg_len]
+ * dt; e: [n_seg][seg_len] binary32, in-out, zero at the first step; out_x holds
+ * idx [n_seg][k_x], val [n_seg][k_x] (dt) and an optional block table; out_e
+ * the same with k_e.  kind must be TC_TOPK with wire == dt; seg_len is at most
+ * 32,768 (one workgroup holds the segment), else TC_ERR_ARG. */
+tc_status tc_efmix_step(const tc_codec* c, const void* x, int dt, float* e, const tc_payload* out_x,
+                        const tc_payload* out_e, void* stream);
+
+/* Sec. 2.4, EF-mixed receiver: y [n_seg][seg_len] in out_dt starts at +0,
+ * takes v_x at idx_x, then adds v_e at idx_e (binary32 sum), rounded once to
+ * out_dt.  Payload lists as tc_efmix_step writes them (wire dtype c->wire);
+ * any seg_len.  An index outside its segment, or (without a block table) a
+ * list that is not strictly ascending, is reported by tc_device_errors. */
+tc_status tc_efmix_reconstruct(const tc_codec* c, const tc_payload* in_x, const tc_payload* in_e, void* y,
+                               int out_dt, void* stream);
+
 /* ---------------------------------------------------------------- AQ-SGD */
 
 /* Sec. 2.5 sender with TopK: for each b < n_ids, with id = ids[b]:

@@ -294,6 +294,64 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
   }
 }
 
+// ------------------------------------------------------------- EF-mixed
+// Receiver of EF-mixed (Sec. 2.4): the dense tensor starts at +0, takes the
+// input list's values at its indices, then adds the error buffer's list at
+// its indices (binary32; the two lists may share indices), and is rounded
+// once to the output dtype.  Workgroup iteration = one 4096-element chunk of
+// one segment, built in LDS as binary32; each list's range in the chunk comes
+// from its block table, else from a search of its ascending indices.
+template <typename WireT, typename OutT>
+__global__ __launch_bounds__(SC_NT) void k_efmix_scatter(ScatterArgs a) {
+  using RW = typename Elem<WireT>::raw;
+  using RO = typename Elem<OutT>::raw;
+  __shared__ __attribute__((aligned(16))) float buf[SC_CH];
+  __shared__ uint32_t scratch[SC_NT / WAVE + 2];
+  const uint64_t nch = (a.L + SC_CH - 1) / SC_CH;
+  const uint64_t nbt = n_blocks(a.L) + 1;
+  const uint32_t t = threadIdx.x;
+  for (uint64_t wi = blockIdx.x; wi < a.n_seg * nch; wi += gridDim.x) {
+    const uint64_t seg = wi / nch, c0 = (wi % nch) * SC_CH;
+    const uint64_t c1 = min(a.L, c0 + SC_CH);
+    const uint32_t n = (uint32_t)(c1 - c0);
+    for (uint32_t q = t; q * 4 < n; q += SC_NT) reinterpret_cast<u32x4*>(buf)[q] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int list = 0; list < 2; ++list) {
+      const uint64_t k = list ? a.k2 : a.k;
+      const uint32_t* ix = (list ? a.idx2 : a.idx) + seg * k;
+      const uint32_t* btab = list ? a.blk2 : a.blk;
+      const uint32_t* bt = btab ? btab + seg * nbt : nullptr;
+      const RW* vv = (const RW*)(list ? a.val2 : a.val) + seg * k;
+      uint32_t j0 = 0, j1 = 0;
+      if (k > 0) chunk_range(ix, bt, k, c0, c1, scratch, j0, j1);
+      // entries past the segment's end belong to no chunk: the last chunk flags them
+      if (c1 == a.L && j1 < k && t == 0) raise_error(KERR_BAD_INDEX);
+      __syncthreads();   // the zeroed chunk, then the first list, are in place
+      for (uint32_t j = j0 + t; j < j1; j += SC_NT) {
+        const uint32_t i = ix[j];
+        if (!bt && j > j0 && ix[j - 1] >= i) raise_error(KERR_BAD_INDEX);
+        if (i < c0 || i >= c1) {
+          raise_error(KERR_BAD_INDEX);
+        } else {
+          const float v = Elem<WireT>::up(vv[j]);
+          buf[i - c0] = list ? buf[i - c0] + v : v;
+        }
+      }
+    }
+    __syncthreads();
+    // rounded to the output dtype: thread-contiguous runs of SC_VPT elements
+    const uint32_t b0 = t * SC_VPT;
+    if (b0 < n) {
+      const int nv = (int)min((uint32_t)SC_VPT, n - b0);
+      RO o[SC_VPT];
+#pragma unroll
+      for (int c = 0; c < SC_VPT; ++c) o[c] = Elem<OutT>::down(buf[b0 + c]);
+      store_run_partial<RO, SC_VPT, false>((RO*)a.y + seg * a.L + c0 + b0, nv, o);
+    }
+    __syncthreads();
+  }
+}
+
 // ---------------------------------------------------------- index reuse
 // TopK at given indices (Sec. 3.2: in the GPT-2 runs the gradients are
 // compressed at the indices that the activations' TopK kept).  The message
@@ -418,6 +476,21 @@ hipError_t launch_topk_decompress(int wire, int out_dt, const ScatterArgs& args,
     fn = (out_dt == DT_F32) ? codes_ptr<float>(b) : (out_dt == DT_BF16) ? codes_ptr<bf16_t>(b) : codes_ptr<f16_t>(b);
   }
   if (!fn) return hipErrorInvalidValue;
+  ScatterArgs a = args;
+  void* params[] = {&a};
+  return hipLaunchKernel(fn, dim3(scatter_grid(a.n_seg, a.L)), dim3(SC_NT), params, 0, st);
+}
+
+template <typename WireT>
+const void* efmix_ptr(int out_dt) {
+  if (out_dt == DT_F32) return (const void*)k_efmix_scatter<WireT, float>;
+  if (out_dt == DT_BF16) return (const void*)k_efmix_scatter<WireT, bf16_t>;
+  return (const void*)k_efmix_scatter<WireT, f16_t>;
+}
+
+hipError_t launch_efmix_recv(int wire, int out_dt, const ScatterArgs& args, hipStream_t st) {
+  const void* fn = (wire == DT_F32) ? efmix_ptr<float>(out_dt)
+                 : (wire == DT_BF16) ? efmix_ptr<bf16_t>(out_dt) : efmix_ptr<f16_t>(out_dt);
   ScatterArgs a = args;
   void* params[] = {&a};
   return hipLaunchKernel(fn, dim3(scatter_grid(a.n_seg, a.L)), dim3(SC_NT), params, 0, st);

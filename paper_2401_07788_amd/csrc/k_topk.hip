@@ -854,6 +854,125 @@ __device__ __forceinline__ void lds_pass_list(const uint32_t* s_list, uint32_t n
   __syncthreads();
 }
 
+// T (the key of the k-th largest |v| in s_v[0..L)) and the tie quota r:
+// the number of keys equal to T that are kept (k == 0: T above every
+// finite key).  Ends with every thread past a barrier.
+template <int NT>
+__device__ __forceinline__ void lds_threshold(const uint32_t* s_v, uint32_t L, uint32_t k, uint32_t* s_h,
+                                              uint32_t* s_list, uint32_t* scratch, uint32_t* found, uint32_t& T,
+                                              uint32_t& r) {
+  const uint32_t t = threadIdx.x;
+  T = 0x7FFFFFFFu;
+  r = 0u;
+  if (k > 0) {
+    uint32_t need = k, d1, d2, d3;
+    lds_pass<NT, 4096>(s_v, L, 19, 0u, s_h, scratch, found, need, d1);
+    // the keys of bin d1 into a short list (wavefront-aggregated appends),
+    // so that the last two passes read only them; a bin holding more
+    // than the list takes the passes over the whole segment
+    if (t == 0) found[0] = 0u;
+    __syncthreads();
+    // (every lane runs every iteration: the scans below need whole wavefronts)
+    for (uint32_t j = 0; j < LDS_PIECES; ++j) {
+      const uint32_t q = j * NT + t;
+      const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[q * 4]);
+      uint32_t in = 0;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) in |= ((((w[c] & 0x7FFFFFFFu) >> 19) == d1) ? 1u : 0u) << c;
+      if (q * 4 >= L) in = 0u;
+      else if (q * 4 + 4 > L) in &= (1u << (L - q * 4)) - 1u;
+      const uint32_t n = (uint32_t)__builtin_popcount(in);
+      const uint32_t incl = wave_incl_scan(n);
+      const uint32_t tot_w = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1);
+      uint32_t base = 0;
+      if (tot_w) {
+        if (lane_id() == 0) base = atomicAdd(&found[0], tot_w);
+        base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
+      }
+      uint32_t o = base + incl - n;
+      for (uint32_t m = in; m; m &= m - 1u) {
+        const uint32_t c = (uint32_t)__builtin_ctz(m);
+        if (o < LDS_LIST) s_list[o] = w[c] & 0x7FFFFFFFu;
+        ++o;
+      }
+    }
+    __syncthreads();
+    const uint32_t nl = found[0];
+    __syncthreads();
+    if (nl <= LDS_LIST) {
+      lds_pass_list<NT, 4096>(s_list, nl, 7, s_h, scratch, found, need, d2);
+      lds_pass_list<NT, LAST_BINS>(s_list, nl, 0, s_h, scratch, found, need, d3, (d1 << 12) | d2);
+    } else {
+      lds_pass<NT, 4096>(s_v, L, 7, d1, s_h, scratch, found, need, d2);
+      lds_pass<NT, LAST_BINS>(s_v, L, 0, (d1 << 12) | d2, s_h, scratch, found, need, d3);
+    }
+    T = (d1 << 19) | (d2 << 7) | d3;
+    r = need;
+  }
+}
+
+// Placement: thread t owns the run [b0, b0 + nr) of LDS_RUN consecutive
+// elements; its pieces are read in an order rotated by t (fewer LDS bank
+// conflicts) and flags go to bit (element - b0) of two masks.  The kept
+// entries go to idx / val (in index order) and the block table (or null);
+// returns the thread's kept-entry mask.
+template <typename InT, int NT>
+__device__ __forceinline__ uint32_t lds_place(const uint32_t* s_v, uint32_t L, uint32_t b0, uint32_t nr, uint32_t T,
+                                              uint32_t r, uint32_t k, uint32_t* idx, typename Elem<InT>::raw* val,
+                                              uint32_t* bt, uint32_t* scratch) {
+  const uint32_t t = threadIdx.x;
+  uint32_t gm = 0, em = 0;
+#pragma unroll
+  for (uint32_t j = 0; j < LDS_PIECES; ++j) {
+    const uint32_t pc = (j + t) % LDS_PIECES;
+    const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[b0 + 4 * pc]);
+    uint32_t g4 = 0, e4 = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t kk = w[c] & 0x7FFFFFFFu;
+      g4 |= ((kk > T) ? 1u : 0u) << c;
+      e4 |= ((kk == T) ? 1u : 0u) << c;
+    }
+    gm |= g4 << (4 * pc);
+    em |= e4 << (4 * pc);
+  }
+  const uint32_t valid = (nr >= 32u) ? 0xFFFFFFFFu : ((1u << nr) - 1u);
+  gm &= valid;
+  em &= valid;
+  const uint32_t gt = (uint32_t)__builtin_popcount(gm), eq = (uint32_t)__builtin_popcount(em);
+  uint32_t tot;
+  const uint32_t ex = block_excl_scan<NT>(gt | (eq << 16), scratch, tot);   // both < 2^16
+  const uint32_t gt_ex = ex & 0xFFFFu, eq_ex = ex >> 16;
+  // ties kept: the r lowest-indexed ones
+  uint32_t tie_keep = min(sat_sub(r, eq_ex), eq);
+  uint32_t km = gm, rest = em;
+  for (; tie_keep; --tie_keep) {
+    km |= rest & (0u - rest);
+    rest &= rest - 1u;
+  }
+  const uint32_t pos0 = gt_ex + min(eq_ex, r);
+  const uint32_t nk = (uint32_t)__builtin_popcount(km);
+  if (pos0 + nk > k) {
+    raise_error(KERR_INTERNAL);
+    km = 0;
+  }
+  // the kept entries, in index order
+  uint32_t pos = pos0;
+  for (uint32_t m = km; m; m &= m - 1u) {
+    const uint32_t bit = (uint32_t)__builtin_ctz(m);
+    idx[pos] = b0 + bit;
+    val[pos] = Elem<InT>::down(__uint_as_float(s_v[b0 + bit]));
+    ++pos;
+  }
+  // block table: kept entries below each block boundary (a boundary
+  // starts a thread's run)
+  if (bt) {
+    if (b0 % BLOCK_LEN == 0 && b0 < L) bt[b0 / BLOCK_LEN] = pos0;
+    if (t == 0) bt[n_blocks(L)] = k;
+  }
+  return km;
+}
+
 template <typename InT, int SEL>
 __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
   using Raw = typename Elem<InT>::raw;
@@ -868,7 +987,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
   const bool vec = ((((uintptr_t)a.x | (uintptr_t)a.e | (uintptr_t)a.m) & 15u) == 0) && (L % 4u) == 0;
   for (uint64_t seg = blockIdx.x; seg < a.n_seg; seg += gridDim.x) {
     const Raw* xs = (const Raw*)a.x + seg * a.L;
-    float* es = (SEL == SEL_EF) ? a.e + seg * a.L : nullptr;
+    float* es = (SEL == SEL_EF || SEL == SEL_EFMIX) ? a.e + seg * a.L : nullptr;
     // AQ-SGD: the example's buffer row; v = a - m
     Raw* ms = nullptr;
     if constexpr (SEL == SEL_AQSGD) {
@@ -932,104 +1051,14 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
     }
     __syncthreads();
 
-    // ---- T and the tie quota r (k == 0: T above every finite key)
-    uint32_t T = 0x7FFFFFFFu, r = 0u;
-    if (a.k > 0) {
-      uint32_t need = (uint32_t)a.k, d1, d2, d3;
-      lds_pass<NT, 4096>(s_v, L, 19, 0u, s_h, scratch, found, need, d1);
-      // the keys of bin d1 into a short list (wavefront-aggregated appends),
-      // so that the last two passes read only them; a bin holding more
-      // than the list takes the passes over the whole segment
-      if (t == 0) found[0] = 0u;
-      __syncthreads();
-      // (every lane runs every iteration: the scans below need whole wavefronts)
-      for (uint32_t j = 0; j < LDS_PIECES; ++j) {
-        const uint32_t q = j * NT + t;
-        const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[q * 4]);
-        uint32_t in = 0;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) in |= ((((w[c] & 0x7FFFFFFFu) >> 19) == d1) ? 1u : 0u) << c;
-        if (q * 4 >= L) in = 0u;
-        else if (q * 4 + 4 > L) in &= (1u << (L - q * 4)) - 1u;
-        const uint32_t n = (uint32_t)__builtin_popcount(in);
-        const uint32_t incl = wave_incl_scan(n);
-        const uint32_t tot_w = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1);
-        uint32_t base = 0;
-        if (tot_w) {
-          if (lane_id() == 0) base = atomicAdd(&found[0], tot_w);
-          base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
-        }
-        uint32_t o = base + incl - n;
-        for (uint32_t m = in; m; m &= m - 1u) {
-          const uint32_t c = (uint32_t)__builtin_ctz(m);
-          if (o < LDS_LIST) s_list[o] = w[c] & 0x7FFFFFFFu;
-          ++o;
-        }
-      }
-      __syncthreads();
-      const uint32_t nl = found[0];
-      __syncthreads();
-      if (nl <= LDS_LIST) {
-        lds_pass_list<NT, 4096>(s_list, nl, 7, s_h, scratch, found, need, d2);
-        lds_pass_list<NT, LAST_BINS>(s_list, nl, 0, s_h, scratch, found, need, d3, (d1 << 12) | d2);
-      } else {
-        lds_pass<NT, 4096>(s_v, L, 7, d1, s_h, scratch, found, need, d2);
-        lds_pass<NT, LAST_BINS>(s_v, L, 0, (d1 << 12) | d2, s_h, scratch, found, need, d3);
-      }
-      T = (d1 << 19) | (d2 << 7) | d3;
-      r = need;
-    }
-
-    // ---- placement: thread t owns [t*LDS_RUN, t*LDS_RUN + LDS_RUN); its
-    // pieces are read in an order rotated by t (fewer LDS bank conflicts),
-    // flags go to bit (element - run start) of two masks
+    // ---- T and the tie quota r, then the kept entries of thread t's run
+    uint32_t T, r;
+    lds_threshold<NT>(s_v, L, (uint32_t)a.k, s_h, s_list, scratch, found, T, r);
     const uint32_t b0 = t * LDS_RUN;
     const uint32_t nr = (b0 < L) ? min(LDS_RUN, L - b0) : 0u;
-    uint32_t gm = 0, em = 0;
-#pragma unroll
-    for (uint32_t j = 0; j < LDS_PIECES; ++j) {
-      const uint32_t pc = (j + t) % LDS_PIECES;
-      const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[b0 + 4 * pc]);
-      uint32_t g4 = 0, e4 = 0;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const uint32_t kk = w[c] & 0x7FFFFFFFu;
-        g4 |= ((kk > T) ? 1u : 0u) << c;
-        e4 |= ((kk == T) ? 1u : 0u) << c;
-      }
-      gm |= g4 << (4 * pc);
-      em |= e4 << (4 * pc);
-    }
-    const uint32_t valid = (nr >= 32u) ? 0xFFFFFFFFu : ((1u << nr) - 1u);
-    gm &= valid;
-    em &= valid;
-    const uint32_t gt = (uint32_t)__builtin_popcount(gm), eq = (uint32_t)__builtin_popcount(em);
-    uint32_t tot;
-    const uint32_t ex = block_excl_scan<NT>(gt | (eq << 16), scratch, tot);   // both < 2^16
-    const uint32_t gt_ex = ex & 0xFFFFu, eq_ex = ex >> 16;
-    // ties kept: the r lowest-indexed ones
-    uint32_t tie_keep = min(sat_sub(r, eq_ex), eq);
-    uint32_t km = gm, rest = em;
-    for (; tie_keep; --tie_keep) {
-      km |= rest & (0u - rest);
-      rest &= rest - 1u;
-    }
-    const uint32_t pos0 = gt_ex + min(eq_ex, r);
-    const uint32_t nk = (uint32_t)__builtin_popcount(km);
-    uint32_t* idx = a.idx + seg * a.k;
-    Raw* val = (Raw*)a.val + seg * a.k;
-    if ((uint64_t)pos0 + nk > a.k) {
-      raise_error(KERR_INTERNAL);
-      km = 0;
-    }
-    // the kept entries, in index order
-    uint32_t pos = pos0;
-    for (uint32_t m = km; m; m &= m - 1u) {
-      const uint32_t bit = (uint32_t)__builtin_ctz(m);
-      idx[pos] = b0 + bit;
-      val[pos] = Elem<InT>::down(__uint_as_float(s_v[b0 + bit]));
-      ++pos;
-    }
+    const uint32_t km = lds_place<InT, NT>(s_v, L, b0, nr, T, r, (uint32_t)a.k, a.idx + seg * a.k,
+                                           (Raw*)a.val + seg * a.k,
+                                           a.blk ? a.blk + seg * (n_blocks(a.L) + 1) : nullptr, scratch);
     // AQ-SGD: the buffer row moves by the sent values at the kept entries
     // only; per half of the run, that half's buffer values are loaded at once
     if constexpr (SEL == SEL_AQSGD) {
@@ -1053,13 +1082,6 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
         }
       }
     }
-    // block table: kept entries below each block boundary (a boundary
-    // starts a thread's run)
-    if (a.blk) {
-      uint32_t* bt = a.blk + seg * (n_blocks(a.L) + 1);
-      if (b0 % BLOCK_LEN == 0 && b0 < L) bt[b0 / BLOCK_LEN] = pos0;
-      if (t == 0) bt[n_blocks(a.L)] = (uint32_t)a.k;
-    }
     // the residual: v minus what the receiver holds (write-back stores; a
     // thread's pieces cover each line only together)
     if constexpr (SEL == SEL_EF) {
@@ -1074,6 +1096,75 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
         for (int c = 0; c < 4; ++c) {
           const float v = __uint_as_float(w[c]);
           o[c] = v - (((k4 >> c) & 1u) ? through<InT>(v) : 0.0f);
+        }
+        if (vec) store_run<float, 4, false>(es + b0 + 4 * pc, o);
+        else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            if (4 * pc + (uint32_t)c < nr) es[b0 + 4 * pc + c] = o[c];
+        }
+      }
+    }
+    // EF-mixed (Sec. 2.4): the buffer takes the LDS for its own selection;
+    // then e' = (x minus what was sent of it) + (e minus what was sent of
+    // e).  x is exact in its dtype, so its share is x off the kept entries
+    // and +0 on them; x is read again for it rather than held in registers.
+    if constexpr (SEL == SEL_EFMIX) {
+      __syncthreads();
+      // the buffer into LDS, in the input's piece layout
+      if (vec) {
+#pragma unroll
+        for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
+          float er[4][4];
+#pragma unroll
+          for (uint32_t j = 0; j < 4; ++j) {
+            const uint32_t i0 = ((h + j) * NT + t) * 4;
+            if (i0 < L) load_run<float, 4, true>(es + i0, er[j]);
+          }
+#pragma unroll
+          for (uint32_t j = 0; j < 4; ++j) {
+            const uint32_t i0 = ((h + j) * NT + t) * 4;
+            if (i0 < L)
+              *reinterpret_cast<u32x4*>(&s_v[i0]) = u32x4{__float_as_uint(er[j][0]), __float_as_uint(er[j][1]),
+                                                          __float_as_uint(er[j][2]), __float_as_uint(er[j][3])};
+          }
+        }
+      } else {
+        for (uint32_t j = 0; j < LDS_PIECES; ++j) {
+          const uint32_t i0 = (j * NT + t) * 4;
+          if (i0 >= L) break;
+          u32x4 w;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) w[c] = __float_as_uint((i0 + (uint32_t)c < L) ? es[i0 + c] : 0.0f);
+          *reinterpret_cast<u32x4*>(&s_v[i0]) = w;
+        }
+      }
+      __syncthreads();
+      uint32_t T2, r2;
+      lds_threshold<NT>(s_v, L, (uint32_t)a.k2, s_h, s_list, scratch, found, T2, r2);
+      const uint32_t km2 = lds_place<InT, NT>(s_v, L, b0, nr, T2, r2, (uint32_t)a.k2, a.idx2 + seg * a.k2,
+                                              (Raw*)a.val2 + seg * a.k2,
+                                              a.blk2 ? a.blk2 + seg * (n_blocks(a.L) + 1) : nullptr, scratch);
+#pragma unroll
+      for (uint32_t j = 0; j < LDS_PIECES; ++j) {
+        const uint32_t pc = (j + t) % LDS_PIECES;
+        if (4 * pc >= nr) continue;
+        Raw xr[4];
+        if (vec) {
+          load_run<Raw, 4, false>(xs + b0 + 4 * pc, xr);
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) xr[c] = (4 * pc + (uint32_t)c < nr) ? xs[b0 + 4 * pc + c] : Raw{};
+        }
+        const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[b0 + 4 * pc]);
+        const uint32_t kx4 = km >> (4 * pc), ke4 = km2 >> (4 * pc);
+        float o[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const float xv = Elem<InT>::up(xr[c]);
+          const float rx = xv - (((kx4 >> c) & 1u) ? xv : 0.0f);
+          const float v = __uint_as_float(w[c]);
+          o[c] = rx + (v - (((ke4 >> c) & 1u) ? through<InT>(v) : 0.0f));
         }
         if (vec) store_run<float, 4, false>(es + b0 + 4 * pc, o);
         else {
@@ -1140,7 +1231,7 @@ const void* pick(int sel, int dt, bool row, int v) {
   return pick_sel<SEL_AQSGD>(dt, row, v);
 }
 
-// LDS engine: plain, EF and AQ-SGD TopK
+// LDS engine: plain, EF, AQ-SGD and EF-mixed TopK
 const void* lds_ptr(int sel, int dt) {
   if (sel == SEL_PLAIN) {
     if (dt == DT_F32) return (const void*)k_topk_lds<float, SEL_PLAIN>;
@@ -1151,6 +1242,11 @@ const void* lds_ptr(int sel, int dt) {
     if (dt == DT_F32) return (const void*)k_topk_lds<float, SEL_EF>;
     if (dt == DT_BF16) return (const void*)k_topk_lds<bf16_t, SEL_EF>;
     return (const void*)k_topk_lds<f16_t, SEL_EF>;
+  }
+  if (sel == SEL_EFMIX) {
+    if (dt == DT_F32) return (const void*)k_topk_lds<float, SEL_EFMIX>;
+    if (dt == DT_BF16) return (const void*)k_topk_lds<bf16_t, SEL_EFMIX>;
+    return (const void*)k_topk_lds<f16_t, SEL_EFMIX>;
   }
   if (dt == DT_F32) return (const void*)k_topk_lds<float, SEL_AQSGD>;
   if (dt == DT_BF16) return (const void*)k_topk_lds<bf16_t, SEL_AQSGD>;
@@ -1165,21 +1261,26 @@ int occupancy(const void* fn, int nt) {
 
 }  // namespace
 
+static_assert(LDS_MAX == LDS_SEG_MAX, "one LDS-engine segment length");
+
+// one workgroup per segment, the segment in LDS
+SegPlan plan_lds(int sel, int dt, uint64_t n_seg) {
+  SegPlan p;
+  p.nt = LDS_NT;
+  p.lds = true;
+  p.P = 1;
+  const uint64_t cap = (uint64_t)occupancy(lds_ptr(sel, dt), p.nt) * (uint32_t)device_cus();
+  p.capacity = cap;
+  p.n_groups = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(n_seg, cap));
+  p.grid = p.n_groups;
+  p.ws_words = 0;
+  return p;
+}
+
 SegPlan plan_topk(int sel, int dt, uint64_t n_seg, uint64_t L) {
   SegPlan p;
   const uint32_t cus = (uint32_t)device_cus();
-  if (L > ROW_MAX && L <= LDS_MAX) {
-    // one workgroup per segment, the segment in LDS
-    p.nt = LDS_NT;
-    p.lds = true;
-    p.P = 1;
-    const uint64_t cap = (uint64_t)occupancy(lds_ptr(sel, dt), p.nt) * cus;
-    p.capacity = cap;
-    p.n_groups = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(n_seg, cap));
-    p.grid = p.n_groups;
-    p.ws_words = 0;
-    return p;
-  }
+  if (L > ROW_MAX && L <= LDS_MAX) return plan_lds(sel, dt, n_seg);
   if (L <= ROW_MAX) {
     // one wavefront per segment: the smallest run length that covers L
     static const int vpts[] = {4, 8, 12, 16, 24, 32};

@@ -366,6 +366,69 @@ TC_API tc_status tc_ef_step(const tc_codec* c, const void* x, int dt, float* e, 
   return global_topk(c->bits, c, x, dt, e, out, ws, ws_bytes, stream);
 }
 
+TC_API tc_status tc_efmix_step(const tc_codec* c, const void* x, int dt, float* e, const tc_payload* out_x,
+                               const tc_payload* out_e, void* stream) {
+  tc_status s = check_codec(c, 1 << TC_TOPK);
+  if (s != TC_OK) return s;
+  if (!dt_ok(dt)) return fail(TC_ERR_DTYPE, "dtype %d", dt);
+  if (c->wire != dt) return fail(TC_ERR_DTYPE, "wire dtype %d must equal the input dtype %d", c->wire, dt);
+  if (!out_x || !out_e) return fail(TC_ERR_NULL, "payload is NULL");
+  if (c->n_seg * c->seg_len == 0) return TC_OK;
+  if (c->seg_len > tc::LDS_SEG_MAX)
+    return fail(TC_ERR_ARG, "EF-mixed segments hold at most %llu elements (got %llu)",
+                (unsigned long long)tc::LDS_SEG_MAX, (unsigned long long)c->seg_len);
+  if (!x || !e) return fail(TC_ERR_NULL, "input or error buffer is NULL");
+  const uint64_t kx = c->k - c->k / 2, ke = c->k / 2;
+  if (kx > 0 && (!out_x->idx || !out_x->val)) return fail(TC_ERR_NULL, "input list idx/val is NULL");
+  if (ke > 0 && (!out_e->idx || !out_e->val)) return fail(TC_ERR_NULL, "buffer list idx/val is NULL");
+  const tc::SegPlan p = tc::plan_lds(tc::SEL_EFMIX, dt, c->n_seg);
+  tc::TopkArgs a{};
+  a.x = x;
+  a.e = e;
+  a.idx = out_x->idx;
+  a.val = out_x->val;
+  a.blk = out_x->blk;
+  a.k = kx;
+  a.idx2 = out_e->idx;
+  a.val2 = out_e->val;
+  a.blk2 = out_e->blk;
+  a.k2 = ke;
+  a.n_seg = c->n_seg;
+  a.L = c->seg_len;
+  hipError_t he = tc::launch_topk(tc::SEL_EFMIX, dt, p, a, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "efmix launch");
+  return TC_OK;
+}
+
+TC_API tc_status tc_efmix_reconstruct(const tc_codec* c, const tc_payload* in_x, const tc_payload* in_e, void* y,
+                                      int out_dt, void* stream) {
+  tc_status s = check_codec(c, 1 << TC_TOPK);
+  if (s != TC_OK) return s;
+  if (!dt_ok(c->wire)) return fail(TC_ERR_DTYPE, "wire dtype %d", c->wire);
+  if (!dt_ok(out_dt)) return fail(TC_ERR_DTYPE, "out dtype %d", out_dt);
+  if (!in_x || !in_e) return fail(TC_ERR_NULL, "payload is NULL");
+  if (c->n_seg * c->seg_len == 0) return TC_OK;
+  if (!y) return fail(TC_ERR_NULL, "output is NULL");
+  const uint64_t kx = c->k - c->k / 2, ke = c->k / 2;
+  if (kx > 0 && (!in_x->idx || !in_x->val)) return fail(TC_ERR_NULL, "input list idx/val is NULL");
+  if (ke > 0 && (!in_e->idx || !in_e->val)) return fail(TC_ERR_NULL, "buffer list idx/val is NULL");
+  tc::ScatterArgs a{};
+  a.idx = in_x->idx;
+  a.blk = in_x->blk;
+  a.val = in_x->val;
+  a.k = kx;
+  a.idx2 = in_e->idx;
+  a.blk2 = in_e->blk;
+  a.val2 = in_e->val;
+  a.k2 = ke;
+  a.y = y;
+  a.n_seg = c->n_seg;
+  a.L = c->seg_len;
+  hipError_t he = tc::launch_efmix_recv(c->wire, out_dt, a, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "efmix reconstruct launch");
+  return TC_OK;
+}
+
 TC_API tc_status tc_aqsgd_step(const tc_codec* c, const void* a, int dt, void* m, uint64_t n_samples,
                                const int64_t* ids, uint32_t n_ids, const tc_payload* out, void* ws,
                                size_t ws_bytes, void* stream) {

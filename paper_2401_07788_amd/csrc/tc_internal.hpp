@@ -28,7 +28,7 @@ struct SegPlan {
 };
 
 // ------------------------------------------------------------------- TopK
-enum SelKind : int { SEL_PLAIN = 0, SEL_EF = 1, SEL_AQSGD = 2 };
+enum SelKind : int { SEL_PLAIN = 0, SEL_EF = 1, SEL_AQSGD = 2, SEL_EFMIX = 3 };
 
 struct TopkArgs {
   const void* x;         // PLAIN/EF: [n_seg][L] input; AQSGD: activations [n_seg][L]
@@ -42,12 +42,21 @@ struct TopkArgs {
   uint64_t n_seg, L, k;
   uint32_t P;
   uint32_t* ws;
+  // EFMIX: the error buffer's list (idx, val, blk above hold the input's)
+  uint32_t* idx2;        // [n_seg][k2]
+  void* val2;            // [n_seg][k2] in the input dtype
+  uint32_t* blk2;        // optional block table of that list
+  uint64_t k2;
 };
 
 constexpr uint64_t BLOCK_LEN = 4096;   // TC_BLOCK_LEN
 __host__ __device__ constexpr uint64_t n_blocks(uint64_t L) { return (L + BLOCK_LEN - 1) / BLOCK_LEN; }
 
 SegPlan plan_topk(int sel, int dt, uint64_t n_seg, uint64_t L);
+// the LDS engine (one workgroup per segment of at most LDS_SEG_MAX elements)
+// for any such length; EF-mixed always takes it
+constexpr uint64_t LDS_SEG_MAX = 32768;
+SegPlan plan_lds(int sel, int dt, uint64_t n_seg);
 hipError_t launch_topk(int sel, int dt, const SegPlan& plan, const TopkArgs& a, hipStream_t st);
 
 // ----------------------------------------------------------- quantization
@@ -85,8 +94,14 @@ struct ScatterArgs {
   const int64_t* ids;
   uint64_t n_samples;
   uint64_t n_seg, L, k, wpg;
+  // EF-mixed: the error buffer's list, added after the input's
+  const uint32_t* idx2;  // [n_seg][k2]
+  const uint32_t* blk2;  // optional block table of that list
+  const void* val2;      // [n_seg][k2] wire values
+  uint64_t k2;
 };
 hipError_t launch_topk_decompress(int wire, int out_dt, const ScatterArgs& a, hipStream_t st);
+hipError_t launch_efmix_recv(int wire, int out_dt, const ScatterArgs& a, hipStream_t st);
 
 // TopK at given indices (another tensor's TopK payload), optionally inside
 // error feedback

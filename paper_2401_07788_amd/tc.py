@@ -84,6 +84,10 @@ EXPORTS = {
     "tc_quant_unpack": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.c_void_p, C.c_int, C.c_void_p]),
     "tc_ef_step": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.POINTER(C.c_float), C.POINTER(Payload),
                              C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tc_efmix_step": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.POINTER(C.c_float), C.POINTER(Payload),
+                                C.POINTER(Payload), C.c_void_p]),
+    "tc_efmix_reconstruct": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.POINTER(Payload), C.c_void_p, C.c_int,
+                                       C.c_void_p]),
     "tc_aqsgd_step": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.c_void_p, C.c_uint64, C.c_void_p,
                                 C.c_uint32, C.POINTER(Payload), C.c_void_p, C.c_size_t, C.c_void_p]),
     "tc_aqsgd_reconstruct": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.c_void_p, C.c_int, C.c_uint64,
@@ -372,6 +376,56 @@ def topk_quant_decompress(pl: TopkQuantPayload, seg_len: int, out_dtype=torch.fl
     p = Payload(_ptr(pl.idx), None, _ptr(pl.codes), _ptr(pl.meta), _ptr(pl.blk) if use_blk else None)
     _check(lib().tc_topk_decompress(C.byref(c), C.byref(p), _ptr(y), _DT[out_dtype], _stream(pl.idx.device)),
            "tc_topk_decompress")
+    return y
+
+
+# ----------------------------------------------------------------- EF-mixed
+def efmix_counts(k: int) -> tuple:
+    """(k_x, k_e): the input's and the error buffer's share of a budget of k"""
+    return k - k // 2, k // 2
+
+
+def efmix_step(x: torch.Tensor, e: torch.Tensor, k: int, n_seg: int, out=None, blk: bool = True):
+    """EF-mixed sender: TopK of x (k_x) and of e (k_e), both sent; e (float32,
+    updated in place) keeps what was not sent.  Returns (payload_x, payload_e)."""
+    _need_gpu(x, e)
+    if e.dtype != torch.float32 or e.numel() != x.numel():
+        raise ValueError("e must be float32 with x's element count")
+    L = x.numel() // n_seg
+    kx, ke = efmix_counts(k)
+    c = codec(TC_TOPK, n_seg, L, k, wire=_dt(x))
+    if out is None:
+        out = (empty_topk_payload(n_seg, L, kx, x.dtype, x.device, blk),
+               empty_topk_payload(n_seg, L, ke, x.dtype, x.device, blk))
+    px, pe = out
+    if px.idx.shape != (n_seg, kx) or pe.idx.shape != (n_seg, ke):
+        raise ValueError("payload shapes do not match the budget")
+    a = Payload(_ptr(px.idx), _ptr(px.val), None, None, _ptr(px.blk))
+    b = Payload(_ptr(pe.idx), _ptr(pe.val), None, None, _ptr(pe.blk))
+    _check(lib().tc_efmix_step(C.byref(c), _ptr(x), _dt(x), C.cast(e.data_ptr(), C.POINTER(C.c_float)),
+                               C.byref(a), C.byref(b), _stream(x.device)), "tc_efmix_step")
+    return out
+
+
+def efmix_reconstruct(px: TopkPayload, pe: TopkPayload, seg_len: int, out_dtype=None, use_blk: bool = True,
+                      out: torch.Tensor = None):
+    """dense [n_seg, seg_len]: the input's list written, the buffer's list added"""
+    _need_gpu(px.idx, px.val, pe.idx, pe.val, out)
+    n_seg, kx = px.idx.shape
+    ke = pe.idx.shape[1]
+    if pe.idx.shape[0] != n_seg or kx - ke not in (0, 1):
+        raise ValueError("the two lists do not come from one EF-mixed budget")
+    if out is not None:
+        if out.numel() != n_seg * seg_len:
+            raise ValueError("out has the wrong element count")
+        out_dtype = out.dtype
+    out_dtype = out_dtype or px.val.dtype
+    c = codec(TC_TOPK, n_seg, seg_len, kx + ke, wire=_dt(px.val))
+    y = out if out is not None else torch.empty((n_seg, seg_len), dtype=out_dtype, device=px.idx.device)
+    a = Payload(_ptr(px.idx), _ptr(px.val), None, None, _ptr(px.blk) if use_blk else None)
+    b = Payload(_ptr(pe.idx), _ptr(pe.val), None, None, _ptr(pe.blk) if use_blk else None)
+    _check(lib().tc_efmix_reconstruct(C.byref(c), C.byref(a), C.byref(b), _ptr(y), _DT[out_dtype],
+                                      _stream(px.idx.device)), "tc_efmix_reconstruct")
     return y
 
 
