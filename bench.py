@@ -461,11 +461,13 @@ def run_aqsgd(args, dev):
 EF_WORKLOADS = {
     # ResNet-18 boundary: post-ReLU activations 128 x 128x16x16 fp32, one
     # segment / group per sample; TopK 10 % + EF, variants TopK 30 %, Q2/4/8 + EF,
-    # EF21 + TopK 10 % (one fp32 buffer row per sample on each side)
+    # EF21 + TopK 10 % (one fp32 buffer row per sample on each side) and
+    # EF-mixed TopK 10 % (half of the budget on x, half on the fp32 buffer)
     "resnet": dict(desc="ResNet-18 boundary: 128 x 128x16x16 fp32 post-ReLU activations, per-sample segments",
                    shape=(128, 128, 16, 16), n_seg=128, gen="relu", dtype="f32",
                    main=("topk", 1, 10),
-                   variants=[("topk", 3, 10), ("quant", 2), ("quant", 4), ("quant", 8), ("ef21", 1, 10)]),
+                   variants=[("topk", 3, 10), ("quant", 2), ("quant", 4), ("quant", 8), ("ef21", 1, 10),
+                             ("efmix", 1, 10)]),
     # transformer boundary: bf16 hidden states 8 x 512 x 768 with outlier
     # channels, one segment / group per token row; TopK 10 % + EF, variants
     # Q4 + EF and the backward gradient (N(0, 1e-4)) compressed at the
@@ -540,6 +542,19 @@ def run_ef(args, dev, name):
             send_bytes = 3 * esz * N + payload   # read x, read g, write g, write payload
             recv_bytes = payload + 3 * esz * N   # read payload, read g_r, write g_r and the received tensor
             return send, recv, send_bytes, recv_bytes, label
+        elif codec[0] == "efmix":
+            # TopK of x and of e, half of the budget each; both lists sent
+            k = tc.topk_count(L, codec[1], codec[2])
+            kx, ke = tc.efmix_counts(k)
+            pls = (tc.empty_topk_payload(n_seg, L, kx, tdt, dev), tc.empty_topk_payload(n_seg, L, ke, tdt, dev))
+            payload = n_seg * (k * (4 + esz) + 8 * (tc.n_blocks(L) + 1))
+
+            def send(i):
+                tc.efmix_step(xs[i % n_sets], es[i % n_sets], k, n_seg, out=pls)
+
+            def recv():
+                tc.efmix_reconstruct(pls[0], pls[1], L, out=y)
+            label = f"EF-mixed TopK {100 * codec[1] // codec[2]} % (half on x, half on the buffer)"
         elif codec[0] == "reuse":
             # the gradient of a boundary tensor sent at the indices its TopK
             # kept in the forward pass (one forward payload, rotating gradients)

@@ -1009,7 +1009,8 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
         for (uint32_t j = 0; j < 4; ++j) {
           const uint32_t i0 = ((h + j) * NT + t) * 4;
           if (i0 < L) {
-            load_run<Raw, 4, true>(xs + i0, xr[j]);
+            // (EF-mixed reads x again at the end: cached loads keep it in L2)
+            load_run<Raw, 4, SEL != SEL_EFMIX>(xs + i0, xr[j]);
             if constexpr (SEL == SEL_EF) load_run<float, 4, true>(es + i0, er[j]);
             if constexpr (SEL == SEL_AQSGD) load_run<Raw, 4, true>(ms + i0, mr[j]);
           }
@@ -1082,33 +1083,39 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
         }
       }
     }
-    // the residual: v minus what the receiver holds (write-back stores; a
-    // thread's pieces cover each line only together)
+    // the residual: v minus what the receiver holds, in the load's layout
+    // (lanes consecutive: whole lines per wavefront store); the kept masks
+    // of the runs go through LDS
     if constexpr (SEL == SEL_EF) {
-#pragma unroll 2
+      s_h[t] = km;
+      uint32_t tq = t;
+      asm volatile("" : "+v"(tq));   // addresses computed here, not ahead of the loop
+      __syncthreads();
+#pragma unroll
       for (uint32_t j = 0; j < LDS_PIECES; ++j) {
-        const uint32_t pc = (j + t) % LDS_PIECES;
-        if (4 * pc >= nr) continue;
-        const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[b0 + 4 * pc]);
-        const uint32_t k4 = km >> (4 * pc);
+        const uint32_t i0 = (j * NT + tq) * 4;
+        if (i0 >= L) continue;
+        const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[i0]);
+        const uint32_t k4 = s_h[i0 / LDS_RUN] >> (i0 % LDS_RUN);
         float o[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const float v = __uint_as_float(w[c]);
           o[c] = v - (((k4 >> c) & 1u) ? through<InT>(v) : 0.0f);
         }
-        if (vec) store_run<float, 4, false>(es + b0 + 4 * pc, o);
+        if (vec) store_run<float, 4, true>(es + i0, o);
         else {
 #pragma unroll
           for (int c = 0; c < 4; ++c)
-            if (4 * pc + (uint32_t)c < nr) es[b0 + 4 * pc + c] = o[c];
+            if (i0 + (uint32_t)c < L) es[i0 + c] = o[c];
         }
       }
     }
     // EF-mixed (Sec. 2.4): the buffer takes the LDS for its own selection;
     // then e' = (x minus what was sent of it) + (e minus what was sent of
     // e).  x is exact in its dtype, so its share is x off the kept entries
-    // and +0 on them; x is read again for it rather than held in registers.
+    // and +0 on them; x is read again for it rather than held in registers
+    // through the second selection.
     if constexpr (SEL == SEL_EFMIX) {
       __syncthreads();
       // the buffer into LDS, in the input's piece layout
@@ -1145,32 +1152,55 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
       const uint32_t km2 = lds_place<InT, NT>(s_v, L, b0, nr, T2, r2, (uint32_t)a.k2, a.idx2 + seg * a.k2,
                                               (Raw*)a.val2 + seg * a.k2,
                                               a.blk2 ? a.blk2 + seg * (n_blocks(a.L) + 1) : nullptr, scratch);
+      // the residual in the load's layout (piece q = 4 elements, lanes
+      // consecutive: whole lines per wavefront access); the kept masks of
+      // the runs go through LDS, x is loaded for all pieces first
+      s_h[t] = km;
+      s_h[NT + t] = km2;
+      // (opaque copies of the row pointer and of the thread index: the
+      // addresses below are neither merged with the first loads of x nor
+      // computed ahead of the loop, either of which holds registers through
+      // both selections)
+      uint64_t xa = (uint64_t)(uintptr_t)xs;
+      uint32_t tq = t;
+      asm volatile("" : "+s"(xa), "+v"(tq));
+      const Raw* xs2 = (const Raw*)(uintptr_t)xa;
+      __syncthreads();
+      // four pieces at a time: their loads of x go out together
 #pragma unroll
-      for (uint32_t j = 0; j < LDS_PIECES; ++j) {
-        const uint32_t pc = (j + t) % LDS_PIECES;
-        if (4 * pc >= nr) continue;
-        Raw xr[4];
-        if (vec) {
-          load_run<Raw, 4, false>(xs + b0 + 4 * pc, xr);
-        } else {
+      for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
+        Raw xr[4][4];
 #pragma unroll
-          for (int c = 0; c < 4; ++c) xr[c] = (4 * pc + (uint32_t)c < nr) ? xs[b0 + 4 * pc + c] : Raw{};
+        for (uint32_t j = 0; j < 4; ++j) {
+          const uint32_t i0 = ((h + j) * NT + tq) * 4;
+          if (vec) {
+            if (i0 < L) load_run<Raw, 4, false>(xs2 + i0, xr[j]);
+          } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) xr[j][c] = (i0 + (uint32_t)c < L) ? xs2[i0 + c] : Raw{};
+          }
         }
-        const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[b0 + 4 * pc]);
-        const uint32_t kx4 = km >> (4 * pc), ke4 = km2 >> (4 * pc);
-        float o[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const float xv = Elem<InT>::up(xr[c]);
-          const float rx = xv - (((kx4 >> c) & 1u) ? xv : 0.0f);
-          const float v = __uint_as_float(w[c]);
-          o[c] = rx + (v - (((ke4 >> c) & 1u) ? through<InT>(v) : 0.0f));
-        }
-        if (vec) store_run<float, 4, false>(es + b0 + 4 * pc, o);
-        else {
+        for (uint32_t j = 0; j < 4; ++j) {
+          const uint32_t i0 = ((h + j) * NT + tq) * 4;
+          if (i0 >= L) continue;
+          const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[i0]);
+          const uint32_t sh = i0 % LDS_RUN;
+          const uint32_t kx4 = s_h[i0 / LDS_RUN] >> sh, ke4 = s_h[NT + i0 / LDS_RUN] >> sh;
+          float o[4];
 #pragma unroll
-          for (int c = 0; c < 4; ++c)
-            if (4 * pc + (uint32_t)c < nr) es[b0 + 4 * pc + c] = o[c];
+          for (int c = 0; c < 4; ++c) {
+            const float xv = Elem<InT>::up(xr[j][c]);
+            const float rx = xv - (((kx4 >> c) & 1u) ? xv : 0.0f);
+            const float v = __uint_as_float(w[c]);
+            o[c] = rx + (v - (((ke4 >> c) & 1u) ? through<InT>(v) : 0.0f));
+          }
+          if (vec) store_run<float, 4, true>(es + i0, o);
+          else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+              if (i0 + (uint32_t)c < L) es[i0 + c] = o[c];
+          }
         }
       }
     }
