@@ -136,6 +136,74 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
   }
 }
 
+// Receiver of short segments (token rows, at most SR_MAX elements): one
+// wavefront per row and nothing shared across wavefronts, so a row costs no
+// workgroup barrier and no range lookup.  The row is built in a slice of LDS
+// private to the wavefront: zeroed, the row's entries written (their loads
+// issued first), then stored in lane-consecutive 16-byte pieces.  Indices
+// must be below L and strictly ascending; the block table is only checked.
+constexpr uint32_t SR_MAX = 2048;
+constexpr int SR_WAVES = SC_NT / WAVE;
+static_assert(SR_MAX <= BLOCK_LEN, "a row is one block of the block table");
+
+template <typename WireT, typename OutT>
+__global__ __launch_bounds__(SC_NT) void k_topk_scatter_row(ScatterArgs a) {
+  using RW = typename Elem<WireT>::raw;
+  using RO = typename Elem<OutT>::raw;
+  constexpr uint32_t PER = 16 / sizeof(RO);
+  constexpr int EPL = 4;   // entries per lane per round, loads in flight together
+  __shared__ __attribute__((aligned(16))) RO buf[SR_WAVES][SR_MAX];
+  const uint32_t w = threadIdx.x / WAVE, lane = (uint32_t)lane_id();
+  RO* b = buf[w];
+  const uint32_t L = (uint32_t)a.L, k = (uint32_t)a.k;   // k <= L <= SR_MAX (the launcher checks)
+  const bool vec = (((uintptr_t)a.y | (L * sizeof(RO))) & 15u) == 0;
+  const uint64_t stride = (uint64_t)gridDim.x * SR_WAVES;
+  for (uint64_t s = (uint64_t)blockIdx.x * SR_WAVES + w; s < a.n_seg; s += stride) {
+    const uint32_t* ix = a.idx + s * a.k;
+    const RW* vv = (const RW*)a.val + s * a.k;
+    // a block table, when given, must describe the row's one block
+    if (a.blk && lane == 0) {
+      const uint32_t* bt = a.blk + s * (n_blocks(a.L) + 1);
+      if (bt[0] != 0u || bt[1] != k) raise_error(KERR_BAD_INDEX);
+    }
+    for (uint32_t q = lane; q * PER < L; q += WAVE) reinterpret_cast<u32x4*>(b)[q] = u32x4{0u, 0u, 0u, 0u};
+    for (uint32_t j0 = 0; j0 < k; j0 += EPL * WAVE) {
+      uint32_t ei[EPL], ep[EPL];
+      RW ev[EPL];
+#pragma unroll
+      for (int r = 0; r < EPL; ++r) {
+        const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
+        ei[r] = 0xFFFFFFFFu;
+        ep[r] = 0u;
+        if (j < k) {
+          ei[r] = ix[j];
+          ev[r] = vv[j];
+          if (j > 0) ep[r] = ix[j - 1] + 1u;   // the smallest index allowed here
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < EPL; ++r) {
+        const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
+        if (j < k) {
+          if (ei[r] >= L || ei[r] < ep[r]) raise_error(KERR_BAD_INDEX);
+          else b[ei[r]] = Elem<OutT>::down(Elem<WireT>::up(ev[r]));
+        }
+      }
+    }
+    // (a wavefront's LDS accesses complete in program order)
+    __builtin_amdgcn_wave_barrier();
+    RO* yr = (RO*)a.y + s * a.L;
+    for (uint32_t q = lane; q * PER < L; q += WAVE) {
+      if (vec && q * PER + PER <= L) {
+        reinterpret_cast<u32x4*>(yr)[q] = reinterpret_cast<const u32x4*>(b)[q];
+      } else {
+        for (uint32_t c = q * PER; c < min(L, q * PER + PER); ++c) yr[c] = b[c];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
 // Payload groups of eight entries, loaded with 16-byte accesses aligned in
 // the whole payload array (rows of k entries need not be aligned): group g of
 // a chunk covers array entries A0 + 8g .. A0 + 8g + 7.  A group reaching past
@@ -448,6 +516,13 @@ const void* val_ptr(int out_dt) {
   return (const void*)k_topk_scatter<WireT, f16_t, MODE_VAL, 0>;
 }
 
+template <typename WireT>
+const void* row_ptr(int out_dt) {
+  if (out_dt == DT_F32) return (const void*)k_topk_scatter_row<WireT, float>;
+  if (out_dt == DT_BF16) return (const void*)k_topk_scatter_row<WireT, bf16_t>;
+  return (const void*)k_topk_scatter_row<WireT, f16_t>;
+}
+
 template <typename OutT>
 const void* codes_ptr(uint32_t b) {
   switch (b) {
@@ -478,6 +553,14 @@ hipError_t launch_topk_decompress(int wire, int out_dt, const ScatterArgs& args,
   if (!fn) return hipErrorInvalidValue;
   ScatterArgs a = args;
   void* params[] = {&a};
+  if (wire >= 0 && a.L <= SR_MAX) {
+    // one wavefront per row
+    const void* fr = (wire == DT_F32) ? row_ptr<float>(out_dt) : (wire == DT_BF16) ? row_ptr<bf16_t>(out_dt)
+                                                                                  : row_ptr<f16_t>(out_dt);
+    const uint64_t wgs = (a.n_seg + SR_WAVES - 1) / SR_WAVES;
+    const uint32_t grid = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(wgs, (uint64_t)device_cus() * 8));
+    return hipLaunchKernel(fr, dim3(grid), dim3(SC_NT), params, 0, st);
+  }
   return hipLaunchKernel(fn, dim3(scatter_grid(a.n_seg, a.L)), dim3(SC_NT), params, 0, st);
 }
 
