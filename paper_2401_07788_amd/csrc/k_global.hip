@@ -101,12 +101,14 @@ __device__ __forceinline__ void push_minmax(uint32_t* st, int wmin, int wmax, fl
 // device-scope update the other workgroups made before finishing.  Each
 // workgroup counts in slot (blockIdx % 8); the last of a slot counts in the
 // top word.
-__device__ __forceinline__ bool last_block(uint32_t* st) {
+// G: the workgroups that take part (blockIdx < G; the whole grid by default).
+__device__ __forceinline__ bool last_block(uint32_t* st, uint32_t G = 0u) {
   __shared__ uint32_t s_last;
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
-    const uint32_t G = gridDim.x, c = blockIdx.x % NSLOT;
+    if (G == 0u) G = gridDim.x;
+    const uint32_t c = blockIdx.x % NSLOT;
     const uint32_t n_c = (G - 1 - c) / NSLOT + 1;   // workgroups of this slot
     const uint32_t n_slots = min(G, NSLOT);
     uint32_t* sc = slot(st, SP_DONE, c);
@@ -436,7 +438,20 @@ __device__ __forceinline__ void for_candidates(const GlobalArgs& a, F&& f) {
   for (uint32_t c = 0; c < a.n_sub; ++c) {
     const uint64_t n = min((uint64_t)a.state[SP_NCAND + SLOT_WORDS * c], capc);
     const uint32_t* list = a.cand + c * capc;
-    for (uint64_t j = (uint64_t)blockIdx.x * G_NT + threadIdx.x; j < n; j += (uint64_t)G * G_NT) f(list[j]);
+    // eight loads in flight per thread before any is used
+    constexpr int U = 8;
+    const uint64_t stride = (uint64_t)G * G_NT;
+    for (uint64_t j0 = (uint64_t)blockIdx.x * G_NT + threadIdx.x; j0 < n; j0 += U * stride) {
+      uint32_t v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const uint64_t j = j0 + (uint64_t)u * stride;
+        v[u] = (j < n) ? list[j] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (j0 + (uint64_t)u * stride < n) f(v[u]);
+    }
   }
 }
 
@@ -450,6 +465,10 @@ __global__ __launch_bounds__(G_NT) void k_g_pass(GlobalArgs a) {
   uint32_t* st = a.state;
   if (PASS == 1 && st[ST_P1] != 0u) return;   // the band pass found the first digit
   const bool fast = st[ST_FAST] != 0u;
+  // the candidate list is read by the first CAND_GRID workgroups only; the
+  // rest leave at once and do not count towards the last workgroup
+  const uint32_t G = fast ? min(gridDim.x, CAND_GRID) : gridDim.x;
+  if (blockIdx.x >= G) return;
   zero_lds_bins(hist, NB);
   __syncthreads();
   const uint32_t b1 = (PASS >= 2) ? st[ST_B1] : 0u;
@@ -484,7 +503,7 @@ __global__ __launch_bounds__(G_NT) void k_g_pass(GlobalArgs a) {
   __syncthreads();
   uint32_t* gh = a.hist + (uint64_t)PASS * HIST_BINS;   // histograms 1..3
   merge_bins(hist, gh, NB);
-  if (!last_block(st)) return;
+  if (!last_block(st, G)) return;
   take_bins(hist, gh, NB);
   const uint32_t need = (PASS == 1) ? st[ST_NEED1] : (PASS == 2) ? st[ST_NEED2] : st[ST_NEED3];
   find_bin<G_NT, NB>(hist, need, scratch, found);
@@ -522,7 +541,13 @@ __device__ __forceinline__ void keptmm_push(uint32_t* st, KeptMM& m, uint32_t* s
   const uint32_t tps = block_sum<G_NT>(m.tp, scratch);
   const uint32_t tns = block_sum<G_NT>(m.tn, scratch);
   if (threadIdx.x == 0) {
-    push_minmax(st, ST_AMIN, ST_AMAX, m.mn, m.mx);
+    // the band pass's slots (already reduced into ST_AMIN / ST_AMAX, whose
+    // values they still hold): one slot per eighth of the workgroups
+    if (m.mn <= m.mx) {
+      const uint32_t cs = blockIdx.x % NSLOT;
+      __hip_atomic_fetch_max(slot(st, SP_AMIN, cs), ~order_key(m.mn), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_max(slot(st, SP_AMAX, cs), order_key(m.mx), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     if (tps) add_agent(&st[ST_TPOS], tps);
     if (tns) add_agent(&st[ST_TNEG], tns);
   }
@@ -531,7 +556,8 @@ __device__ __forceinline__ void keptmm_push(uint32_t* st, KeptMM& m, uint32_t* s
 // lo / hi / scale of the kept list, once every workgroup has pushed (one thread)
 __device__ __forceinline__ void keptmm_final(const GlobalArgs& a, uint32_t* st) {
   const uint32_t T = st[ST_T];
-  const uint32_t wmin = ld_agent(&st[ST_AMIN]), wmax = ld_agent(&st[ST_AMAX]);
+  const uint32_t wmin = max(ld_agent(&st[ST_AMIN]), slot_max(st, SP_AMIN));
+  const uint32_t wmax = max(ld_agent(&st[ST_AMAX]), slot_max(st, SP_AMAX));
   float lo = wmax ? from_order_key(~wmin) : __builtin_inff();
   float hi = wmax ? from_order_key(wmax) : -__builtin_inff();
   const uint32_t r = st[ST_R];
@@ -591,25 +617,51 @@ __global__ __launch_bounds__(G_NT) void k_g_tcount(GlobalArgs a) {
   const uint64_t t_lo = (uint64_t)blockIdx.x * a.tpw;
   const uint32_t nt = (uint32_t)min((uint64_t)a.tpw, sat_sub(a.n_tiles, t_lo));
   if (fast) {
-    // one wavefront per tile
+    // one wavefront per tile, GT tiles of a wavefront at a time: their
+    // records, then the first 2 * WAVE candidates of each, are loaded
+    // together (two round trips per GT tiles instead of two per tile)
+    constexpr uint32_t NW = G_NT / WAVE, GT = 4;
     const uint32_t w = threadIdx.x / WAVE, lane = (uint32_t)lane_id();
-    for (uint32_t i = w; i < nt; i += G_NT / WAVE) {
-      const uint32_t* rec = a.tiles + 4 * (t_lo + i);
-      const uint32_t ab = rec[0], off = rec[1], n = rec[2];
-      uint32_t gt = 0, eq = 0;
-      if ((uint64_t)off + n <= a.cand_cap) {
-        for (uint32_t j = lane; j < n; j += WAVE) {
-          const uint32_t bits = a.cand[off + j], kk = bits & 0x7FFFFFFFu;
-          gt += kk > T;
-          eq += kk == T;
-          if (mm) kmm.add(bits, T);
+    auto take = [&](uint32_t bits, uint32_t& gt, uint32_t& eq) {
+      const uint32_t kk = bits & 0x7FFFFFFFu;
+      gt += kk > T;
+      eq += kk == T;
+      if (mm) kmm.add(bits, T);
+    };
+    for (uint32_t i0 = w; i0 < nt; i0 += NW * GT) {
+      uint32_t ab[GT], off[GT], n[GT], c0[GT], c1[GT];
+#pragma unroll
+      for (uint32_t r = 0; r < GT; ++r) {
+        const uint32_t i = i0 + r * NW;
+        ab[r] = off[r] = n[r] = 0u;
+        if (i < nt) {
+          const uint32_t* rec = a.tiles + 4 * (t_lo + i);
+          ab[r] = rec[0];
+          off[r] = rec[1];
+          n[r] = rec[2];
         }
-      } else if (lane == 0) {
-        raise_error(KERR_INTERNAL);
       }
-      gt = wave_sum(gt);
-      eq = wave_sum(eq);
-      if (lane == 0) { s_gt[i] = ab + gt; s_eq[i] = eq; }
+#pragma unroll
+      for (uint32_t r = 0; r < GT; ++r) {
+        const bool ok = (uint64_t)off[r] + n[r] <= a.cand_cap;
+        c0[r] = (ok && lane < n[r]) ? a.cand[off[r] + lane] : 0u;
+        c1[r] = (ok && lane + WAVE < n[r]) ? a.cand[off[r] + lane + WAVE] : 0u;
+      }
+#pragma unroll
+      for (uint32_t r = 0; r < GT; ++r) {
+        const uint32_t i = i0 + r * NW;
+        uint32_t gt = 0, eq = 0;
+        if ((uint64_t)off[r] + n[r] <= a.cand_cap) {
+          if (lane < n[r]) take(c0[r], gt, eq);
+          if (lane + WAVE < n[r]) take(c1[r], gt, eq);
+          for (uint32_t j = lane + 2 * WAVE; j < n[r]; j += WAVE) take(a.cand[off[r] + j], gt, eq);
+        } else if (lane == 0) {
+          raise_error(KERR_INTERNAL);
+        }
+        gt = wave_sum(gt);
+        eq = wave_sum(eq);
+        if (lane == 0 && i < nt) { s_gt[i] = ab[r] + gt; s_eq[i] = eq; }
+      }
     }
   } else {
     for (uint32_t i = 0; i < nt; ++i) {
@@ -1072,8 +1124,13 @@ hipError_t launch_global(int dt, bool ef, uint32_t qbits, const GlobalArgs& args
     const uint32_t sgrid = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(n_s, SAMPLE_GRID));
     e = launch(pick_chain(dt, ef, 0), sgrid, G_NT, a, st);
     for (int which = 1; which <= 4 && e == hipSuccess; ++which) {
+      // band reads the whole segment; the digit passes read the candidate
+      // list (CAND_GRID workgroups) unless the band missed, and are launched
+      // with two workgroups per compute unit at most
       const void* fn = pick_chain(dt, ef, which);
-      e = launch(fn, resident_grid(fn, grid), G_NT, a, st);
+      uint32_t g = resident_grid(fn, grid);
+      if (which >= 2) g = std::min<uint32_t>(g, std::max<uint32_t>(CAND_GRID, 2u * (uint32_t)device_cus()));
+      e = launch(fn, g, G_NT, a, st);
     }
     if (e == hipSuccess) {
       const uint32_t tgrid = (uint32_t)((a.n_tiles + a.tpw - 1) / a.tpw);
