@@ -106,6 +106,8 @@ def main():
                     help="aqsgd: also time a pipelined graph (each receiver on a second stream) and an eager "
                          "two-stream run (both slower on one GPU; off by default so that a kernel trace of "
                          "the default run holds the timed configurations only)")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="time the main configuration only (for counter and trace runs of its kernels)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run 5 device copies of 256 MiB (the reference for HBM byte counters)")
     ap.add_argument("--workload", choices=["aqsgd", "lm", "resnet", "transformer"], default="aqsgd",
@@ -317,32 +319,34 @@ def run_aqsgd(args, dev):
     # 768-element token row (k = 231), one buffer row per token row; the
     # micro-batches already used serve again (the kernels' cost does not
     # depend on the drift)
-    H = 768
-    RPE = L // H                                  # token rows per example
-    kr = tc.topk_count(H, 3, 10)
-    m_s_rows, m_r_rows = m_s.view(n_samples * RPE, H), m_r.view(n_samples * RPE, H)
-    acts_rows = acts.view(need_mb, B * RPE, H)
-    row_ids = (ids_dev.view(-1, B, 1) * RPE + torch.arange(RPE, device=dev).view(1, 1, RPE)).reshape(-1, B * RPE)
-    pay_rows = tc.empty_topk_payload(B * RPE, H, kr, torch.float16, dev)
-    ahat_rows = torch.empty((B * RPE, H), dtype=torch.float16, device=dev)
-    ws_rows = tc.workspace(tc.codec(tc.TC_TOPK, B * RPE, H, kr, wire=tc.TC_F16), dev)
-    n_rows_steps = min(20, steps)
+    rows_ms = None
+    if not args.no_variants:
+        H = 768
+        RPE = L // H                                  # token rows per example
+        kr = tc.topk_count(H, 3, 10)
+        m_s_rows, m_r_rows = m_s.view(n_samples * RPE, H), m_r.view(n_samples * RPE, H)
+        acts_rows = acts.view(need_mb, B * RPE, H)
+        row_ids = (ids_dev.view(-1, B, 1) * RPE + torch.arange(RPE, device=dev).view(1, 1, RPE)).reshape(-1, B * RPE)
+        pay_rows = tc.empty_topk_payload(B * RPE, H, kr, torch.float16, dev)
+        ahat_rows = torch.empty((B * RPE, H), dtype=torch.float16, device=dev)
+        ws_rows = tc.workspace(tc.codec(tc.TC_TOPK, B * RPE, H, kr, wire=tc.TC_F16), dev)
+        n_rows_steps = min(20, steps)
 
-    def row_steps(j0, n):
-        for i in range(n):
-            jj = (j0 + i) % need_mb
-            tc.aqsgd_step(acts_rows[jj], m_s_rows, row_ids[jj], kr, ws=ws_rows, out=pay_rows)
-            tc.aqsgd_reconstruct(pay_rows, m_r_rows, row_ids[jj], out=ahat_rows)
+        def row_steps(j0, n):
+            for i in range(n):
+                jj = (j0 + i) % need_mb
+                tc.aqsgd_step(acts_rows[jj], m_s_rows, row_ids[jj], kr, ws=ws_rows, out=pay_rows)
+                tc.aqsgd_reconstruct(pay_rows, m_r_rows, row_ids[jj], out=ahat_rows)
 
-    grw = graph_of(row_steps, 0, warm)
-    grs = graph_of(row_steps, warm, n_rows_steps)
-    grw.replay()
-    torch.cuda.synchronize()
-    check("during the per-row warm-up")
-    rows_ms = timed(grs) * 1e3 / n_rows_steps
-    check("in the per-row graph")
-    rows_bytes = 2 * (2 * B * L + 2 * B * L + 2 * B * L) + 2 * (B * RPE * kr * 6 + B * RPE * 8)
-    del grw, grs
+        grw = graph_of(row_steps, 0, warm)
+        grs = graph_of(row_steps, warm, n_rows_steps)
+        grw.replay()
+        torch.cuda.synchronize()
+        check("during the per-row warm-up")
+        rows_ms = timed(grs) * 1e3 / n_rows_steps
+        check("in the per-row graph")
+        rows_bytes = 2 * (2 * B * L + 2 * B * L + 2 * B * L) + 2 * (B * RPE * kr * 6 + B * RPE * 8)
+        del grw, grs
 
     pipelined_ms = overlap_ms = None
     if args.variants:
@@ -441,10 +445,11 @@ def run_aqsgd(args, dev):
         "algorithmic_bytes_per_step": b_alg,
         "kernels_ms": {"aqsgd_send": round(send_ms, 5), "aqsgd_recv": round(recv_ms, 5)},
         "eager_ms_per_step": round(eager_ms, 5),
-        "variants": {"per token row: TopK 30 % of each 768-element row (k = 231), one buffer row per token row": {
-            "ms_per_step": round(rows_ms, 5),
-            "boundary_GBps": round(2 * B * L / (rows_ms * 1e-3) / 1e9, 2),
-            "pct_hbm_peak": round(100.0 * rows_bytes / (rows_ms * 1e-3) / (HBM_PEAK_GBPS * 1e9), 3)}},
+        "variants": {} if rows_ms is None else {
+            "per token row: TopK 30 % of each 768-element row (k = 231), one buffer row per token row": {
+                "ms_per_step": round(rows_ms, 5),
+                "boundary_GBps": round(2 * B * L / (rows_ms * 1e-3) / 1e9, 2),
+                "pct_hbm_peak": round(100.0 * rows_bytes / (rows_ms * 1e-3) / (HBM_PEAK_GBPS * 1e9), 3)}},
         "device_copy_GBps": device_copy_gbps(dev),
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
@@ -630,7 +635,7 @@ def run_ef(args, dev, name):
 
     ms_per_step, (send_ms, recv_ms), sb, rb, label = measure(cfg["main"], steps, True)
     variants = {}
-    for v in cfg["variants"]:
+    for v in ([] if args.no_variants else cfg["variants"]):
         vms, vev, vsb, vrb, vlabel = measure(v, max(10, steps // 4), True)
         variants[vlabel] = {"ms_per_step": round(vms, 5), "boundary_GBps": round(esz * N / (vms * 1e-3) / 1e9, 2),
                             "pct_hbm_peak": round(100 * (vsb + vrb) / (vms * 1e-3) / (HBM_PEAK_GBPS * 1e9), 3),
