@@ -71,3 +71,25 @@ def test_efmix_rejects_long_segments(tc):
     e = torch.zeros_like(x)
     with pytest.raises(tc.TCError):
         tc.efmix_step(x, e, 100, 1)
+
+
+def test_efmix_unaligned_buffers(tc, orc):
+    # x and e start one element past a 16-byte boundary: element-wise loads
+    # and stores throughout
+    n_seg, L = 6, 8192
+    k = tc.topk_count(L, 1, 10)
+    xs = [W.relu_activation((n_seg, L), 14, t) for t in range(3)]
+    xb = torch.empty(n_seg * L + 1, dtype=torch.float32, device="cuda")
+    eb = torch.zeros(n_seg * L + 1, dtype=torch.float32, device="cuda")
+    e_gpu = eb[1:]
+    e_orc = np.zeros((n_seg, L), np.float32)
+    for t, x in enumerate(xs):
+        xb[1:] = x.reshape(-1).cuda()
+        px, pe = tc.efmix_step(xb[1:].view(n_seg, L), e_gpu, k, n_seg)
+        torch.cuda.synchronize()
+        assert tc.device_errors() == 0
+        ix, vx, ie, ve, e_orc = orc.efmix_send(raw(x), "f32", e_orc, n_seg, L, k)
+        assert_bits_equal(raw(px.idx), ix, f"idx_x step {t}")
+        assert_bits_equal(raw(pe.idx), ie, f"idx_e step {t}")
+        assert_bits_equal(raw(pe.val), ve, f"val_e step {t}")
+        assert_bits_equal(raw(e_gpu).reshape(n_seg, L), e_orc, f"e step {t}")

@@ -143,3 +143,22 @@ def test_decompress_flags_bad_block_table(tc):
     tc.topk_decompress(tc.TopkPayload(idx, val, blk), 100)
     torch.cuda.synchronize()
     assert tc.device_errors(clear=True) & tc.TC_KERR_BAD_INDEX
+
+
+@pytest.mark.parametrize("L", [1, 7, 37, 768, 2048, 2049])
+@pytest.mark.parametrize("out_dt", ["f32", "f16"])
+def test_decompress_rows_unaligned_output(tc, orc, L, out_dt):
+    # the one-wavefront-per-row receiver (L <= 2048) and the chunk receiver
+    # (2049) into an output that starts one element past a 16-byte boundary,
+    # bf16 wire widened (f32) or converted (f16), many rows
+    n_seg = 300
+    x = make_input("ties", n_seg, L, "bf16", seed=L + 3)
+    k = tc.topk_count(L, 1, 10)
+    p = tc.topk_compress(x.cuda(), k, n_seg)
+    buf = torch.empty(n_seg * L + 1, dtype=TORCH[out_dt], device="cuda")
+    y = buf[1:].view(n_seg, L)
+    tc.topk_decompress(p, L, out=y)
+    torch.cuda.synchronize()
+    assert tc.device_errors() == 0
+    oi, ov = orc.topk_compress(raw(x), "bf16", n_seg, L, k)
+    assert_bits_equal(raw(y), orc.topk_decompress(oi, ov, "bf16", n_seg, L, k, out_dt=out_dt), "dense")
