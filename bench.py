@@ -34,6 +34,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import platform
@@ -59,10 +60,16 @@ SOURCES_HASHED = {
 
 
 def kernel_source_hash(workload: str) -> str:
+    """hash of the kernel sources a workload runs, comments and blank space
+    left out (a comment edit does not make a counter summary stale)"""
     h = hashlib.sha256()
     for p in SOURCES_HASHED[workload]:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        lines = [ln.strip() for ln in text.splitlines()]
+        h.update("\n".join(ln for ln in lines if ln).encode())
     return h.hexdigest()[:16]
 
 

@@ -4,9 +4,12 @@
 // updated row).
 //
 // Each workgroup owns a chunk [c0, c1) of one segment's dense output.  It
-// finds the payload entries that fall into its chunk with a cooperative
-// search of the ascending index list, builds the chunk in LDS, and writes it
-// out with full-width stores, so the dense output is written exactly once.
+// finds the payload entries that fall into its chunk (block table, else a
+// cooperative search of the ascending index list), builds the chunk in LDS,
+// and writes it out with full-width stores, so the dense output is written
+// exactly once.  Rows of up to 2048 elements take one wavefront each
+// instead.  Also here: the EF-mixed receiver (two lists, the second added)
+// and TopK at given indices (index reuse for gradients).
 #include <algorithm>
 
 #include "tc_internal.hpp"

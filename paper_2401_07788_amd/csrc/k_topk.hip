@@ -6,9 +6,12 @@
 //   EF    : v = x + e                              -> payload, e <- v - r
 //           r = what the receiver gets: wire(v) at kept entries, +0 elsewhere
 //   AQSGD : v = a - m[id]                          -> payload, m[id][kept] += wire(v)
-// The segment (a sample, a token row, a whole example) stays in registers for
-// the whole kernel: inputs are read once, the selection works on registers
-// and LDS, and the outputs are written once.
+// and, in the LDS engine only, two selections (EF-mixed, Sec. 2.4):
+//   EFMIX : TopK(x) and TopK(e) over halves of the budget -> two payloads,
+//           e <- (x - r_x) + (e - r_e)
+// The segment (a sample, a token row, a whole example) stays in registers or
+// LDS for the whole kernel: inputs are read once (EF-mixed reads x twice),
+// the selection works on registers and LDS, and the outputs are written once.
 //
 // Three engines:
 //   k_topk_row : one wavefront per segment of up to 2048 elements (token
