@@ -473,21 +473,23 @@ def run_aqsgd(args, dev):
 EF_WORKLOADS = {
     # ResNet-18 boundary: post-ReLU activations 128 x 128x16x16 fp32, one
     # segment / group per sample; TopK 10 % + EF, variants TopK 30 %, Q2/4/8 + EF,
+    # the backward direction (gradients 1e-3 * N(0, 1), TopK 10 % + EF),
     # EF21 + TopK 10 % (one fp32 buffer row per sample on each side) and
     # EF-mixed TopK 10 % (half of the budget on x, half on the fp32 buffer)
     "resnet": dict(desc="ResNet-18 boundary: 128 x 128x16x16 fp32 post-ReLU activations, per-sample segments",
-                   shape=(128, 128, 16, 16), n_seg=128, gen="relu", dtype="f32",
+                   shape=(128, 128, 16, 16), n_seg=128, gen="relu", dtype="f32", grad_sigma=1e-3,
                    main=("topk", 1, 10),
-                   variants=[("topk", 3, 10), ("quant", 2), ("quant", 4), ("quant", 8), ("ef21", 1, 10),
-                             ("efmix", 1, 10)]),
+                   variants=[("topk", 3, 10), ("quant", 2), ("quant", 4), ("quant", 8), ("grad", 1, 10),
+                             ("ef21", 1, 10), ("efmix", 1, 10)]),
     # transformer boundary: bf16 hidden states 8 x 512 x 768 with outlier
     # channels, one segment / group per token row; TopK 10 % + EF, variants
-    # Q4 + EF and the backward gradient (N(0, 1e-4)) compressed at the
-    # activations' kept indices, alone and with EF
+    # Q4 + EF, the backward gradient (1e-4 N(0, 1)) with its own TopK 10 % +
+    # EF, and the same gradient compressed at the activations' kept indices,
+    # alone and with EF
     "transformer": dict(desc="GPT-2-small boundary: 8 x 512 x 768 bf16 hidden states with 4 outlier channels x20, "
                              "per-token-row segments", shape=(8, 512, 768), n_seg=8 * 512, gen="hidden",
-                        dtype="bf16", main=("topk", 1, 10),
-                        variants=[("quant", 4), ("reuse", 1, 10, False), ("reuse", 1, 10, True)]),
+                        dtype="bf16", grad_sigma=1e-4, main=("topk", 1, 10),
+                        variants=[("quant", 4), ("grad", 1, 10), ("reuse", 1, 10, False), ("reuse", 1, 10, True)]),
 }
 
 
@@ -554,6 +556,23 @@ def run_ef(args, dev, name):
             send_bytes = 3 * esz * N + payload   # read x, read g, write g, write payload
             recv_bytes = payload + 3 * esz * N   # read payload, read g_r, write g_r and the received tensor
             return send, recv, send_bytes, recv_bytes, label
+        elif codec[0] == "grad":
+            # the backward direction: small-sigma gradients, TopK + EF per sample
+            k = tc.topk_count(L, codec[1], codec[2])
+            sigma = cfg["grad_sigma"]
+            gs = [W.normal_gradient((n_seg, L), sigma, args.seed, 2000 + i, device=dev).to(tdt)
+                  for i in range(n_sets)]
+            pl = tc.empty_topk_payload(n_seg, L, k, tdt, dev)
+            c = tc.codec(tc.TC_TOPK, n_seg, L, k, wire=tc._dt(xs[0]))
+            ws = tc.workspace(c, dev)
+            payload = n_seg * (k * (4 + esz) + 4 * (tc.n_blocks(L) + 1))
+
+            def send(i):
+                tc.ef_step_topk(gs[i % n_sets], es[i % n_sets], k, n_seg, ws=ws, out=pl)
+
+            def recv():
+                tc.topk_decompress(pl, L, out=y)
+            label = f"gradients ({sigma:g} N(0, 1)): TopK {100 * codec[1] // codec[2]} % + EF"
         elif codec[0] == "efmix":
             # TopK of x and of e, half of the budget each; both lists sent
             k = tc.topk_count(L, codec[1], codec[2])
