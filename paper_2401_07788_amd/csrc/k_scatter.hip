@@ -423,6 +423,99 @@ __global__ __launch_bounds__(SC_NT) void k_efmix_scatter(ScatterArgs a) {
   }
 }
 
+// AQ-SGD receiver for rows of up to SR_MAX elements (one buffer row per
+// token row): one wavefront per row, in a slice of LDS of its own.  The row's
+// payload entries do not depend on the id, so they are loaded with the id;
+// the buffer row follows, goes to LDS, takes the entries (a read-modify-write
+// per entry: the indices of a valid row are distinct) and leaves for m_r and
+// a_hat in lane-consecutive 16-byte pieces.
+template <typename T>
+__global__ __launch_bounds__(SC_NT) void k_aqsgd_recv_row(ScatterArgs a) {
+  using R = typename Elem<T>::raw;
+  constexpr uint32_t PER = 16 / sizeof(R);
+  constexpr int EPL = 4;   // entries per lane per round
+  __shared__ __attribute__((aligned(16))) R buf[SR_WAVES][SR_MAX];
+  const uint32_t w = threadIdx.x / WAVE, lane = (uint32_t)lane_id();
+  R* b = buf[w];
+  const uint32_t L = (uint32_t)a.L, k = (uint32_t)a.k;   // k <= L <= SR_MAX (the launcher checks)
+  const bool vec = (((uintptr_t)a.m | (uintptr_t)a.y | (L * sizeof(R))) & 15u) == 0;
+  const uint64_t stride = (uint64_t)gridDim.x * SR_WAVES;
+  for (uint64_t s = (uint64_t)blockIdx.x * SR_WAVES + w; s < a.n_seg; s += stride) {
+    const uint32_t* ix = a.idx + s * a.k;
+    const R* vv = (const R*)a.val + s * a.k;
+    const int64_t id = a.ids[s];
+    // the first round of entries goes out with the id
+    uint32_t ei[EPL], ep[EPL];
+    R ev[EPL];
+#pragma unroll
+    for (int r = 0; r < EPL; ++r) {
+      const uint32_t j = (uint32_t)r * WAVE + lane;
+      ei[r] = 0xFFFFFFFFu;
+      ep[r] = 0u;
+      if (j < k) {
+        ei[r] = ix[j];
+        ev[r] = vv[j];
+        if (j > 0) ep[r] = ix[j - 1] + 1u;   // the smallest index allowed here
+      }
+    }
+    if (id < 0 || (uint64_t)id >= a.n_samples) {
+      if (lane == 0) raise_error(KERR_BAD_ID);
+      continue;
+    }
+    if (a.blk && lane == 0) {
+      const uint32_t* bt = a.blk + s * (n_blocks(a.L) + 1);
+      if (bt[0] != 0u || bt[1] != k) raise_error(KERR_BAD_INDEX);
+    }
+    R* row = (R*)a.m + (uint64_t)id * a.L;
+    for (uint32_t q = lane; q * PER < L; q += WAVE) {
+      if (vec && q * PER + PER <= L) {
+        reinterpret_cast<u32x4*>(b)[q] = reinterpret_cast<const u32x4*>(row)[q];
+      } else {
+        for (uint32_t c = q * PER; c < min(L, q * PER + PER); ++c) b[c] = row[c];
+      }
+    }
+    // (a wavefront's LDS accesses complete in program order)
+    for (uint32_t j0 = 0; j0 < k; j0 += EPL * WAVE) {
+      if (j0 > 0) {
+#pragma unroll
+        for (int r = 0; r < EPL; ++r) {
+          const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
+          ei[r] = 0xFFFFFFFFu;
+          ep[r] = 0u;
+          if (j < k) {
+            ei[r] = ix[j];
+            ev[r] = vv[j];
+            ep[r] = ix[j - 1] + 1u;
+          }
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < EPL; ++r) {
+        const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
+        if (j < k) {
+          if (ei[r] >= L || ei[r] < ep[r]) raise_error(KERR_BAD_INDEX);
+          else b[ei[r]] = Elem<T>::down(Elem<T>::up(b[ei[r]]) + Elem<T>::up(ev[r]));
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    R* out = (R*)a.y + s * a.L;
+    for (uint32_t q = lane; q * PER < L; q += WAVE) {
+      if (vec && q * PER + PER <= L) {
+        const u32x4 v4 = reinterpret_cast<const u32x4*>(b)[q];
+        reinterpret_cast<u32x4*>(row)[q] = v4;
+        reinterpret_cast<u32x4*>(out)[q] = v4;
+      } else {
+        for (uint32_t c = q * PER; c < min(L, q * PER + PER); ++c) {
+          row[c] = b[c];
+          out[c] = b[c];
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
 // ---------------------------------------------------------- index reuse
 // TopK at given indices (Sec. 3.2: in the GPT-2 runs the gradients are
 // compressed at the indices that the activations' TopK kept).  The message
@@ -583,10 +676,18 @@ hipError_t launch_efmix_recv(int wire, int out_dt, const ScatterArgs& args, hipS
 }
 
 hipError_t launch_aqsgd_recv(int dt, const ScatterArgs& args, hipStream_t st) {
-  const void* fn = (dt == DT_F32) ? (const void*)k_aqsgd_recv<float>
-                 : (dt == DT_BF16) ? (const void*)k_aqsgd_recv<bf16_t> : (const void*)k_aqsgd_recv<f16_t>;
   ScatterArgs a = args;
   void* params[] = {&a};
+  if (a.L <= SR_MAX) {
+    // one wavefront per row
+    const void* fr = (dt == DT_F32) ? (const void*)k_aqsgd_recv_row<float>
+                   : (dt == DT_BF16) ? (const void*)k_aqsgd_recv_row<bf16_t> : (const void*)k_aqsgd_recv_row<f16_t>;
+    const uint64_t wgs = (a.n_seg + SR_WAVES - 1) / SR_WAVES;
+    const uint32_t grid = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(wgs, (uint64_t)device_cus() * 8));
+    return hipLaunchKernel(fr, dim3(grid), dim3(SC_NT), params, 0, st);
+  }
+  const void* fn = (dt == DT_F32) ? (const void*)k_aqsgd_recv<float>
+                 : (dt == DT_BF16) ? (const void*)k_aqsgd_recv<bf16_t> : (const void*)k_aqsgd_recv<f16_t>;
   return hipLaunchKernel(fn, dim3(scatter_grid(a.n_seg, a.L)), dim3(SC_NT), params, 0, st);
 }
 
