@@ -213,11 +213,25 @@ __device__ __forceinline__ void merge_bins(const uint32_t* h, uint32_t* gh, int 
     if (h[b]) add_agent(&gh[b], h[b]);
 }
 
-// the last workgroup: copy a device histogram into LDS and zero it
+// the last workgroup: copy a device histogram into LDS and zero it.  A
+// thread's loads all go out before any is used (one round trip, not one per
+// bin).
 __device__ __forceinline__ void take_bins(uint32_t* h, uint32_t* gh, int nb) {
-  for (int b = threadIdx.x; b < nb; b += G_NT) {
-    h[b] = ld_agent(&gh[b]);
-    st_agent(&gh[b], 0u);
+  constexpr int PER = HIST_BINS / G_NT;
+  static_assert(HIST_BINS % G_NT == 0, "whole bins per thread");
+  uint32_t v[PER];
+#pragma unroll
+  for (int r = 0; r < PER; ++r) {
+    const int b = (int)threadIdx.x + r * G_NT;
+    v[r] = (b < nb) ? ld_agent(&gh[b]) : 0u;
+  }
+#pragma unroll
+  for (int r = 0; r < PER; ++r) {
+    const int b = (int)threadIdx.x + r * G_NT;
+    if (b < nb) {
+      h[b] = v[r];
+      st_agent(&gh[b], 0u);
+    }
   }
   __syncthreads();
 }
@@ -396,37 +410,67 @@ __global__ __launch_bounds__(G_NT) void k_g_band(GlobalArgs a) {
     }
   }
   if (!last_block(st)) return;
-  if (threadIdx.x != 0) return;
-  const uint64_t ab = slot_sum(st, SP_ABOVE);
-  uint64_t nc = 0;
-  bool fits = true;
-  for (uint32_t q = 0; q < a.n_sub; ++q) {
-    const uint32_t n = ld_agent(slot(st, SP_NCAND, q));
-    nc += n;
-    fits = fits && n <= capc;
+  // the decision, on the first wavefront: each lane loads its slots and
+  // digit counts at once (one round trip), wavefront sums and a scan combine them
+  if (threadIdx.x >= WAVE) return;
+  const uint32_t lane = threadIdx.x;
+  uint32_t abv = 0, ncv = 0, bad = 0, mnv = 0, mxv = 0;
+  if (lane < NSLOT) {
+    abv = ld_agent(slot(st, SP_ABOVE, lane));
+    mnv = ld_agent(slot(st, SP_AMIN, lane));
+    mxv = ld_agent(slot(st, SP_AMAX, lane));
   }
-  const bool fast = fits && ab < a.k && a.k <= ab + nc;
-  st[ST_ABOVE] = (uint32_t)ab;
-  st[ST_FAST] = fast ? 1u : 0u;
-  st[ST_NEED1] = fast ? (uint32_t)(a.k - ab) : (uint32_t)a.k;
-  // the first digit of T from the band's per-digit counts, when they were kept
+  if (lane < a.n_sub) {
+    ncv = ld_agent(slot(st, SP_NCAND, lane));
+    bad = ncv > capc ? 1u : 0u;
+  }
+  // lane j: band digit bhi - j (the band's digits from the top)
+  const uint32_t nd = bhi - blo + 1u;
+  uint32_t cnt = 0;
+  if (count_digits && lane < nd) {
+    uint32_t c8[NSLOT];
+#pragma unroll
+    for (uint32_t c = 0; c < NSLOT; ++c) c8[c] = ld_agent(&st[SP_BD + c * BD_MAX + (bhi - lane - blo)]);
+#pragma unroll
+    for (uint32_t c = 0; c < NSLOT; ++c) cnt += c8[c];
+  }
+  // counts are below 2^31 (seg_len < 2^31), so 32-bit sums do not wrap
+  const uint32_t ab = wave_sum(abv), nc = wave_sum(ncv);
+  const bool fits = wave_sum(bad) == 0u;
+  const bool fast = fits && ab < a.k && a.k <= (uint64_t)ab + nc;
+  uint32_t b1 = 0, need2 = 0;
+  bool p1 = false;
   if (fast && count_digits) {
-    uint32_t need = (uint32_t)(a.k - ab), acc = 0;
-    for (uint32_t d = bhi + 1; d-- > blo;) {
-      uint32_t cnt = 0;
-      for (uint32_t c = 0; c < NSLOT; ++c) cnt += ld_agent(&st[SP_BD + c * BD_MAX + (d - blo)]);
-      if (acc + cnt >= need) {
-        st[ST_B1] = d;
-        st[ST_NEED2] = need - acc;
-        st[ST_P1] = 1u;
-        break;
-      }
-      acc += cnt;
+    const uint32_t need = (uint32_t)(a.k - ab);
+    const uint32_t incl = wave_incl_scan(cnt);
+    const uint64_t hit = __ballot(lane < nd && incl >= need);
+    if (hit) {
+      const uint32_t j = (uint32_t)__builtin_ctzll(hit);
+      const uint32_t before = (uint32_t)__builtin_amdgcn_readlane((int)(incl - cnt), (int)j);
+      b1 = bhi - j;
+      need2 = need - before;
+      p1 = true;
     }
   }
   // values above the band, for the kept list's min / max
-  st[ST_AMIN] = slot_max(st, SP_AMIN);
-  st[ST_AMAX] = slot_max(st, SP_AMAX);
+  uint32_t amn = mnv, amx = mxv;
+#pragma unroll
+  for (int o = 1; o < NSLOT; o <<= 1) {
+    amn = max(amn, (uint32_t)__shfl_xor((int)amn, o));
+    amx = max(amx, (uint32_t)__shfl_xor((int)amx, o));
+  }
+  if (lane == 0) {
+    st[ST_ABOVE] = ab;
+    st[ST_FAST] = fast ? 1u : 0u;
+    st[ST_NEED1] = fast ? (uint32_t)(a.k - ab) : (uint32_t)a.k;
+    if (p1) {
+      st[ST_B1] = b1;
+      st[ST_NEED2] = need2;
+      st[ST_P1] = 1u;
+    }
+    st[ST_AMIN] = amn;
+    st[ST_AMAX] = amx;
+  }
 }
 
 // f(value bits) over every candidate, on the first CAND_GRID workgroups
