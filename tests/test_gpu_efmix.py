@@ -93,3 +93,12 @@ def test_efmix_unaligned_buffers(tc, orc):
         assert_bits_equal(raw(pe.idx), ie, f"idx_e step {t}")
         assert_bits_equal(raw(pe.val), ve, f"val_e step {t}")
         assert_bits_equal(raw(e_gpu).reshape(n_seg, L), e_orc, f"e step {t}")
+
+
+def test_efmix_more_segments_than_workgroups(tc, orc):
+    # more segments than resident workgroups (one per compute unit): each
+    # workgroup takes several segments in turn, LDS reused between them
+    n_seg, L = 600, 3000
+    k = tc.topk_count(L, 1, 10)
+    xs = [W.randn((n_seg, L), 15, t) for t in range(2)]
+    efmix_steps(tc, orc, xs, n_seg, L, k)
