@@ -148,3 +148,12 @@ def test_aqsgd_per_token_row(tc, orc):
         ids_list.append(rid)
         acts.append(W.drifted_activation(m0, rid, 7, 20 + t))
     aq_steps(tc, orc, m0, ids_list, acts, tc.topk_count(H, 3, 10), check_rows=np.arange(n_ex * rows))
+
+
+def test_aqsgd_rows_several_per_wavefront(tc, orc):
+    # the one-wavefront-per-row receiver with more rows than wavefronts
+    n_samples, L, n_ids = 10000, 64, 9000
+    m0 = W.randn((n_samples, L), 16, 0).to(torch.float16)
+    ids = torch.randperm(n_samples, generator=torch.Generator().manual_seed(16))[:n_ids]
+    acts = [W.drifted_activation(m0, ids, 16, 1)]
+    aq_steps(tc, orc, m0, [ids], acts, tc.topk_count(L, 3, 10))

@@ -162,3 +162,17 @@ def test_decompress_rows_unaligned_output(tc, orc, L, out_dt):
     assert tc.device_errors() == 0
     oi, ov = orc.topk_compress(raw(x), "bf16", n_seg, L, k)
     assert_bits_equal(raw(y), orc.topk_decompress(oi, ov, "bf16", n_seg, L, k, out_dt=out_dt), "dense")
+
+
+def test_decompress_rows_several_per_wavefront(tc, orc):
+    # more rows than the row receiver's wavefronts (8 workgroups of 4 per
+    # compute unit): each wavefront builds several rows in its LDS slice
+    n_seg, L = 9000, 37
+    x = make_input("normal", n_seg, L, "f16", seed=21)
+    k = tc.topk_count(L, 3, 10)
+    p = tc.topk_compress(x.cuda(), k, n_seg)
+    y = tc.topk_decompress(p, L)
+    torch.cuda.synchronize()
+    assert tc.device_errors() == 0
+    oi, ov = orc.topk_compress(raw(x), "f16", n_seg, L, k)
+    assert_bits_equal(raw(y), orc.topk_decompress(oi, ov, "f16", n_seg, L, k), "dense")
