@@ -859,8 +859,11 @@ __device__ __forceinline__ void lds_pass_list(const uint32_t* s_list, uint32_t n
 
 // T (the key of the k-th largest |v| in s_v[0..L)) and the tie quota r:
 // the number of keys equal to T that are kept (k == 0: T above every
-// finite key).  Ends with every thread past a barrier.
-template <int NT>
+// finite key).  Ends with every thread past a barrier.  LIST: the keys of
+// the first digit's bin go to a short list for the last two passes (else
+// those passes read the whole segment, which the two selections of EF-mixed
+// find faster).
+template <int NT, bool LIST = true>
 __device__ __forceinline__ void lds_threshold(const uint32_t* s_v, uint32_t L, uint32_t k, uint32_t* s_h,
                                               uint32_t* s_list, uint32_t* scratch, uint32_t* found, uint32_t& T,
                                               uint32_t& r) {
@@ -870,38 +873,41 @@ __device__ __forceinline__ void lds_threshold(const uint32_t* s_v, uint32_t L, u
   if (k > 0) {
     uint32_t need = k, d1, d2, d3;
     lds_pass<NT, 4096>(s_v, L, 19, 0u, s_h, scratch, found, need, d1);
-    // the keys of bin d1 into a short list (wavefront-aggregated appends),
-    // so that the last two passes read only them; a bin holding more
-    // than the list takes the passes over the whole segment
-    if (t == 0) found[0] = 0u;
-    __syncthreads();
-    // (every lane runs every iteration: the scans below need whole wavefronts)
-    for (uint32_t j = 0; j < LDS_PIECES; ++j) {
-      const uint32_t q = j * NT + t;
-      const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[q * 4]);
-      uint32_t in = 0;
+    uint32_t nl = LDS_LIST + 1u;
+    if constexpr (LIST) {
+      // the keys of bin d1 into a short list (wavefront-aggregated appends),
+      // so that the last two passes read only them; a bin holding more
+      // than the list takes the passes over the whole segment
+      if (t == 0) found[0] = 0u;
+      __syncthreads();
+      // (every lane runs every iteration: the scans below need whole wavefronts)
+      for (uint32_t j = 0; j < LDS_PIECES; ++j) {
+        const uint32_t q = j * NT + t;
+        const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[q * 4]);
+        uint32_t in = 0;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) in |= ((((w[c] & 0x7FFFFFFFu) >> 19) == d1) ? 1u : 0u) << c;
-      if (q * 4 >= L) in = 0u;
-      else if (q * 4 + 4 > L) in &= (1u << (L - q * 4)) - 1u;
-      const uint32_t n = (uint32_t)__builtin_popcount(in);
-      const uint32_t incl = wave_incl_scan(n);
-      const uint32_t tot_w = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1);
-      uint32_t base = 0;
-      if (tot_w) {
-        if (lane_id() == 0) base = atomicAdd(&found[0], tot_w);
-        base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
+        for (int c = 0; c < 4; ++c) in |= ((((w[c] & 0x7FFFFFFFu) >> 19) == d1) ? 1u : 0u) << c;
+        if (q * 4 >= L) in = 0u;
+        else if (q * 4 + 4 > L) in &= (1u << (L - q * 4)) - 1u;
+        const uint32_t n = (uint32_t)__builtin_popcount(in);
+        const uint32_t incl = wave_incl_scan(n);
+        const uint32_t tot_w = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1);
+        uint32_t base = 0;
+        if (tot_w) {
+          if (lane_id() == 0) base = atomicAdd(&found[0], tot_w);
+          base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
+        }
+        uint32_t o = base + incl - n;
+        for (uint32_t m = in; m; m &= m - 1u) {
+          const uint32_t c = (uint32_t)__builtin_ctz(m);
+          if (o < LDS_LIST) s_list[o] = w[c] & 0x7FFFFFFFu;
+          ++o;
+        }
       }
-      uint32_t o = base + incl - n;
-      for (uint32_t m = in; m; m &= m - 1u) {
-        const uint32_t c = (uint32_t)__builtin_ctz(m);
-        if (o < LDS_LIST) s_list[o] = w[c] & 0x7FFFFFFFu;
-        ++o;
-      }
+      __syncthreads();
+      nl = found[0];
+      __syncthreads();
     }
-    __syncthreads();
-    const uint32_t nl = found[0];
-    __syncthreads();
     if (nl <= LDS_LIST) {
       lds_pass_list<NT, 4096>(s_list, nl, 7, s_h, scratch, found, need, d2);
       lds_pass_list<NT, LAST_BINS>(s_list, nl, 0, s_h, scratch, found, need, d3, (d1 << 12) | d2);
@@ -1057,7 +1063,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
 
     // ---- T and the tie quota r, then the kept entries of thread t's run
     uint32_t T, r;
-    lds_threshold<NT>(s_v, L, (uint32_t)a.k, s_h, s_list, scratch, found, T, r);
+    lds_threshold<NT, SEL != SEL_EFMIX>(s_v, L, (uint32_t)a.k, s_h, s_list, scratch, found, T, r);
     const uint32_t b0 = t * LDS_RUN;
     const uint32_t nr = (b0 < L) ? min(LDS_RUN, L - b0) : 0u;
     const uint32_t km = lds_place<InT, NT>(s_v, L, b0, nr, T, r, (uint32_t)a.k, a.idx + seg * a.k,
@@ -1151,7 +1157,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
       }
       __syncthreads();
       uint32_t T2, r2;
-      lds_threshold<NT>(s_v, L, (uint32_t)a.k2, s_h, s_list, scratch, found, T2, r2);
+      lds_threshold<NT, false>(s_v, L, (uint32_t)a.k2, s_h, s_list, scratch, found, T2, r2);
       const uint32_t km2 = lds_place<InT, NT>(s_v, L, b0, nr, T2, r2, (uint32_t)a.k2, a.idx2 + seg * a.k2,
                                               (Raw*)a.val2 + seg * a.k2,
                                               a.blk2 ? a.blk2 + seg * (n_blocks(a.L) + 1) : nullptr, scratch);
