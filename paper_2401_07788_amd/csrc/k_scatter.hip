@@ -297,10 +297,12 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
     if constexpr (sizeof(R) == 2) {
      if (full) {
       done = true;
-      // row chunk and payload groups, all loads in flight together
+      // row chunk and payload groups, all loads in flight together; the
+      // row in lane-consecutive 16-byte pieces (piece q * SC_NT + thread:
+      // whole lines per wavefront access)
 #pragma unroll
       for (int q = 0; q < VPT / PER; ++q) {
-        const u32x4 w = reinterpret_cast<const u32x4*>(row + t0)[q];
+        const u32x4 w = vload<true>(reinterpret_cast<const u32x4*>(row + c0) + q * SC_NT + threadIdx.x);
         __builtin_memcpy(&mr[q * PER], &w, 16);
       }
       j0 = bj0;
@@ -315,7 +317,12 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
         const uint32_t gq = threadIdx.x + (uint32_t)r * SC_NT;
         if (gq < ng) load_group<R>(a, A0 + 8ull * gq, total, pg[r]);
       }
-      store_run<R, VPT>(&buf[threadIdx.x * VPT], mr);
+#pragma unroll
+      for (int q = 0; q < VPT / PER; ++q) {
+        u32x4 w;
+        __builtin_memcpy(&w, &mr[q * PER], 16);
+        reinterpret_cast<u32x4*>(buf)[q * SC_NT + threadIdx.x] = w;
+      }
       __syncthreads();
 #pragma unroll
       for (int r = 0; r < GPT; ++r) {
@@ -347,15 +354,15 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
     if (!range_ok && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
     if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
     __syncthreads();
-    // the updated row chunk to the buffer and to a_hat: thread-contiguous
-    // runs of two 16-byte stores, write-back so that the L2 merges the
-    // halves of each line
+    // the updated row chunk to the buffer and to a_hat in lane-consecutive
+    // 16-byte pieces (whole lines per wavefront store)
     if (full) {
 #pragma unroll
       for (int q = 0; q < VPT / PER; ++q) {
-        const u32x4 w = *reinterpret_cast<const u32x4*>(&buf[threadIdx.x * VPT + q * PER]);
-        reinterpret_cast<u32x4*>(row + t0)[q] = w;
-        reinterpret_cast<u32x4*>(out + t0)[q] = w;
+        const uint32_t pc = (uint32_t)q * SC_NT + threadIdx.x;
+        const u32x4 w = reinterpret_cast<const u32x4*>(buf)[pc];
+        vstore<true>(reinterpret_cast<u32x4*>(row + c0) + pc, w);
+        vstore<true>(reinterpret_cast<u32x4*>(out + c0) + pc, w);
       }
     } else {
       copy_lds_to_global<SC_NT, R>(row + c0, buf, (uint32_t)(c1 - c0));
