@@ -698,12 +698,100 @@ hipError_t launch_aqsgd_recv(int dt, const ScatterArgs& args, hipStream_t st) {
   return hipLaunchKernel(fn, dim3(scatter_grid(a.n_seg, a.L)), dim3(SC_NT), params, 0, st);
 }
 
+// The same for rows of up to SR_MAX elements (token rows): one wavefront per
+// row in a slice of LDS of its own.  The row's indices are loaded first (they
+// do not depend on the data), X = x + e goes to the slice in lane-consecutive
+// pieces, each entry sends X and leaves X minus its wire value in the slice,
+// and the slice leaves as the new residual.
+template <typename T>
+__global__ __launch_bounds__(SC_NT) void k_gather_ef_row(GatherArgs a) {
+  using R = typename Elem<T>::raw;
+  constexpr int EPL = 4;   // entries per lane per round
+  __shared__ __attribute__((aligned(16))) float buf[SR_WAVES][SR_MAX];
+  const uint32_t w = threadIdx.x / WAVE, lane = (uint32_t)lane_id();
+  float* b = buf[w];
+  const uint32_t L = (uint32_t)a.L, k = (uint32_t)a.k;   // k <= L <= SR_MAX (the launcher checks)
+  const bool vec = ((((uintptr_t)a.x | (uintptr_t)a.e) & 15u) == 0) && (L % 4u) == 0;
+  const uint64_t stride = (uint64_t)gridDim.x * SR_WAVES;
+  for (uint64_t s = (uint64_t)blockIdx.x * SR_WAVES + w; s < a.n_seg; s += stride) {
+    const uint32_t* ix = a.idx + s * a.k;
+    R* vo = (R*)a.val + s * a.k;
+    const R* xs = (const R*)a.x + s * a.L;
+    float* es = a.e + s * a.L;
+    if (a.blk && lane == 0) {
+      const uint32_t* bt = a.blk + s * (n_blocks(a.L) + 1);
+      if (bt[0] != 0u || bt[1] != k) raise_error(KERR_BAD_INDEX);
+    }
+    // X = x + e into the slice, four elements per piece
+    for (uint32_t q = lane; q * 4 < L; q += WAVE) {
+      if (vec) {
+        R xr[4];
+        float er[4];
+        load_run<R, 4, false>(xs + q * 4, xr);
+        load_run<float, 4, false>(es + q * 4, er);
+        float o[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) o[c] = Elem<T>::up(xr[c]) + er[c];
+        u32x4 v4;
+        __builtin_memcpy(&v4, o, 16);
+        reinterpret_cast<u32x4*>(b)[q] = v4;
+      } else {
+        for (uint32_t c = q * 4; c < min(L, q * 4 + 4); ++c) b[c] = Elem<T>::up(xs[c]) + es[c];
+      }
+    }
+    // (a wavefront's LDS accesses complete in program order)
+    for (uint32_t j0 = 0; j0 < k; j0 += EPL * WAVE) {
+      uint32_t ei[EPL], ep[EPL];
+#pragma unroll
+      for (int r = 0; r < EPL; ++r) {
+        const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
+        ei[r] = 0xFFFFFFFFu;
+        ep[r] = 0u;
+        if (j < k) {
+          ei[r] = ix[j];
+          if (j > 0) ep[r] = ix[j - 1] + 1u;   // the smallest index allowed here
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < EPL; ++r) {
+        const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
+        if (j < k) {
+          const uint32_t i = ei[r];
+          if (i >= L) {
+            raise_error(KERR_BAD_INDEX);
+            vo[j] = R{};
+          } else {
+            if (i < ep[r]) raise_error(KERR_BAD_INDEX);
+            const float X = b[i];
+            vo[j] = Elem<T>::down(X);
+            b[i] = X - through<T>(X);
+          }
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (uint32_t q = lane; q * 4 < L; q += WAVE) {
+      if (vec) {
+        vstore<true>(reinterpret_cast<u32x4*>(es) + q, reinterpret_cast<const u32x4*>(b)[q]);
+      } else {
+        for (uint32_t c = q * 4; c < min(L, q * 4 + 4); ++c) es[c] = b[c];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
 hipError_t launch_gather(int dt, const GatherArgs& args, hipStream_t st) {
   GatherArgs a = args;
   void* params[] = {&a};
   const void* fn;
   uint64_t work;
-  if (a.e) {
+  if (a.e && a.L <= SR_MAX) {
+    // one wavefront per row
+    fn = (dt == DT_F32) ? (const void*)k_gather_ef_row<float>
+       : (dt == DT_BF16) ? (const void*)k_gather_ef_row<bf16_t> : (const void*)k_gather_ef_row<f16_t>;
+    work = (a.n_seg + SR_WAVES - 1) / SR_WAVES;
+  } else if (a.e) {
     fn = (dt == DT_F32) ? (const void*)k_gather_ef<float>
        : (dt == DT_BF16) ? (const void*)k_gather_ef<bf16_t> : (const void*)k_gather_ef<f16_t>;
     work = a.n_seg * ((a.L + SC_CH - 1) / SC_CH);

@@ -36,7 +36,7 @@ def test_gather_parity(tc, orc, dt, n_seg, L):
 
 
 @pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16])
-@pytest.mark.parametrize("n_seg,L", [(4096, 768), (3, 50001), (2, 4096 * 3)])
+@pytest.mark.parametrize("n_seg,L", [(4096, 768), (5, 999), (9000, 37), (3, 50001), (2, 4096 * 3)])
 @pytest.mark.parametrize("use_blk", [True, False])
 def test_gather_ef_parity(tc, orc, dt, n_seg, L, use_blk):
     k = tc.topk_count(L, 1, 10)
