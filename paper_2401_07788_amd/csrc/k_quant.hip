@@ -159,17 +159,20 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
   if (P > 1) group_exit<NT>(bar, P, slots, 2ull * P);
 }
 
+// Receiver: thread = one run of QVPT consecutive elements of one group; a
+// workgroup iteration takes NT consecutive runs over all groups, so short
+// groups (token rows) share a workgroup instead of leaving most of its
+// threads idle.
 template <typename OutT, int B, int NT>
 __global__ __launch_bounds__(NT) void k_quant_unpack(UnpackArgs a) {
   using R = typename Elem<OutT>::raw;
   constexpr int WPT = (B == 32) ? QVPT : QVPT * B / 32;
-  constexpr uint64_t CH = (uint64_t)NT * QVPT;
-  const uint64_t nch = (a.G + CH - 1) / CH;
-  for (uint64_t wi = blockIdx.x; wi < a.n_grp * nch; wi += gridDim.x) {
-    const uint64_t grp = wi / nch, ch = wi % nch;
-    const uint64_t c0 = ch * CH + (uint64_t)threadIdx.x * QVPT;
-    const int nv = (int)min((uint64_t)QVPT, sat_sub(a.G, c0));
-    if (nv == 0) continue;
+  const uint64_t rpg = (a.G + QVPT - 1) / QVPT;        // runs per group
+  const uint64_t n_runs = a.n_grp * rpg;
+  for (uint64_t run = (uint64_t)blockIdx.x * NT + threadIdx.x; run < n_runs; run += (uint64_t)gridDim.x * NT) {
+    const uint64_t grp = run / rpg;
+    const uint64_t c0 = (run % rpg) * QVPT;
+    const int nv = (int)min((uint64_t)QVPT, a.G - c0);
     const uint64_t wo = (B == 32) ? c0 : (c0 * (uint64_t)B) / 32u;
     const int nw = (int)min((uint64_t)WPT, sat_sub(a.wpg, wo));
     uint32_t w[WPT];
@@ -281,8 +284,8 @@ hipError_t launch_unpack(int out_dt, uint32_t bits, const UnpackArgs& args, hipS
   const void* fn = (out_dt == DT_F32) ? unpack_ptr<float>(bits)
                  : (out_dt == DT_BF16) ? unpack_ptr<bf16_t>(bits) : unpack_ptr<f16_t>(bits);
   if (!fn) return hipErrorInvalidValue;
-  const uint64_t CH = 256ull * QVPT;
-  const uint64_t work = args.n_grp * ((args.G + CH - 1) / CH);
+  const uint64_t runs = args.n_grp * ((args.G + QVPT - 1) / QVPT);
+  const uint64_t work = (runs + 255) / 256;   // workgroups of 256 runs
   const uint64_t grid = std::max<uint64_t>(1, std::min<uint64_t>(work, (uint64_t)device_cus() * 8));
   UnpackArgs a = args;
   void* params[] = {&a};
