@@ -53,8 +53,9 @@ def test_gather_ef_parity(tc, orc, dt, n_seg, L, use_blk):
         assert_bits_equal(raw(e_gpu).reshape(n_seg, L), e_orc, f"e step {t}")
 
 
-def test_gather_k_edges(tc, orc):
-    n_seg, L = 3, 5000
+@pytest.mark.parametrize("n_seg,L", [(3, 5000), (70, 768)])
+def test_gather_k_edges(tc, orc, n_seg, L):
+    # the chunk kernel (5000) and the one-wavefront-per-row kernel (768)
     x = W.randn((n_seg, L), 9, 1)
     for k in (0, L):
         pl = fwd_payload(tc, n_seg, L, k, torch.float32, 9)
