@@ -392,39 +392,63 @@ __global__ __launch_bounds__(SC_NT) void k_efmix_scatter(ScatterArgs a) {
     const uint64_t seg = wi / nch, c0 = (wi % nch) * SC_CH;
     const uint64_t c1 = min(a.L, c0 + SC_CH);
     const uint32_t n = (uint32_t)(c1 - c0);
+    const uint64_t kk[2] = {a.k, a.k2};
+    const uint32_t* ixl[2] = {a.idx + seg * a.k, a.idx2 + seg * a.k2};
+    const uint32_t* btl[2] = {a.blk ? a.blk + seg * nbt : nullptr, a.blk2 ? a.blk2 + seg * nbt : nullptr};
+    const RW* vl[2] = {(const RW*)a.val + seg * a.k, (const RW*)a.val2 + seg * a.k2};
+    // both lists' ranges in the chunk (block tables: one round trip for both)
+    uint32_t r0[2] = {0u, 0u}, r1[2] = {0u, 0u};
+    if (btl[0] && btl[1]) {
+      const uint64_t c = c0 / SC_CH;
+#pragma unroll
+      for (int l = 0; l < 2; ++l) { r0[l] = btl[l][c]; r1[l] = btl[l][c + 1]; }
+#pragma unroll
+      for (int l = 0; l < 2; ++l) {
+        if (r0[l] > r1[l] || r1[l] > kk[l] || r1[l] - r0[l] > n) {
+          if (t == 0) raise_error(KERR_BAD_INDEX);
+          r0[l] = r1[l] = 0u;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int l = 0; l < 2; ++l)
+        if (kk[l] > 0) chunk_range(ixl[l], btl[l], kk[l], c0, c1, scratch, r0[l], r1[l]);
+    }
+    // entries past the segment's end belong to no chunk: the last chunk flags them
+#pragma unroll
+    for (int l = 0; l < 2; ++l)
+      if (c1 == a.L && r1[l] < kk[l] && t == 0) raise_error(KERR_BAD_INDEX);
+    // this thread's first entry of each list, both loaded together
+    uint32_t fi[2];
+    float fv[2];
+#pragma unroll
+    for (int l = 0; l < 2; ++l) {
+      const uint32_t j = r0[l] + t;
+      fi[l] = (j < r1[l]) ? ixl[l][j] : 0u;
+      fv[l] = (j < r1[l]) ? Elem<WireT>::up(vl[l][j]) : 0.0f;
+    }
     for (uint32_t q = t; q * 4 < n; q += SC_NT) reinterpret_cast<u32x4*>(buf)[q] = u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-    for (int list = 0; list < 2; ++list) {
-      const uint64_t k = list ? a.k2 : a.k;
-      const uint32_t* ix = (list ? a.idx2 : a.idx) + seg * k;
-      const uint32_t* btab = list ? a.blk2 : a.blk;
-      const uint32_t* bt = btab ? btab + seg * nbt : nullptr;
-      const RW* vv = (const RW*)(list ? a.val2 : a.val) + seg * k;
-      uint32_t j0 = 0, j1 = 0;
-      if (k > 0) chunk_range(ix, bt, k, c0, c1, scratch, j0, j1);
-      // entries past the segment's end belong to no chunk: the last chunk flags them
-      if (c1 == a.L && j1 < k && t == 0) raise_error(KERR_BAD_INDEX);
+    for (int l = 0; l < 2; ++l) {
       __syncthreads();   // the zeroed chunk, then the first list, are in place
-      for (uint32_t j = j0 + t; j < j1; j += SC_NT) {
-        const uint32_t i = ix[j];
-        if (!bt && j > j0 && ix[j - 1] >= i) raise_error(KERR_BAD_INDEX);
-        if (i < c0 || i >= c1) {
-          raise_error(KERR_BAD_INDEX);
-        } else {
-          const float v = Elem<WireT>::up(vv[j]);
-          buf[i - c0] = list ? buf[i - c0] + v : v;
-        }
+      for (uint32_t j = r0[l] + t; j < r1[l]; j += SC_NT) {
+        const bool first = j == r0[l] + t;
+        const uint32_t i = first ? fi[l] : ixl[l][j];
+        const float v = first ? fv[l] : Elem<WireT>::up(vl[l][j]);
+        if (!btl[l] && j > r0[l] && ixl[l][j - 1] >= i) raise_error(KERR_BAD_INDEX);
+        if (i < c0 || i >= c1) raise_error(KERR_BAD_INDEX);
+        else buf[i - c0] = l ? buf[i - c0] + v : v;
       }
     }
     __syncthreads();
-    // rounded to the output dtype: thread-contiguous runs of SC_VPT elements
-    const uint32_t b0 = t * SC_VPT;
-    if (b0 < n) {
-      const int nv = (int)min((uint32_t)SC_VPT, n - b0);
-      RO o[SC_VPT];
+    // rounded to the output dtype, in lane-consecutive pieces of four
+    RO* yc = (RO*)a.y + seg * a.L + c0;
+    for (uint32_t q = t; q * 4 < n; q += SC_NT) {
+      const int nv = (int)min(4u, n - q * 4);
+      RO o[4];
 #pragma unroll
-      for (int c = 0; c < SC_VPT; ++c) o[c] = Elem<OutT>::down(buf[b0 + c]);
-      store_run_partial<RO, SC_VPT, false>((RO*)a.y + seg * a.L + c0 + b0, nv, o);
+      for (int c = 0; c < 4; ++c) o[c] = Elem<OutT>::down(buf[q * 4 + c]);
+      store_run_partial<RO, 4, false>(yc + q * 4, nv, o);
     }
     __syncthreads();
   }
