@@ -159,7 +159,13 @@ tc_status tc_topk_compress(const tc_codec* c, const void* x, int dt, const tc_pa
 
 /* Sec. 2.3 receiver: y [n_seg][seg_len] of dtype out_dt, +0 everywhere except
  * y[s][idx[s][j]] = the sent value.  TC_TOPK reads in->idx/val; TC_TOPK_QUANT
- * reads in->idx/codes/meta and writes lo + code_j*scale at idx_j. */
+ * reads in->idx/codes/meta and writes lo + code_j*scale at idx_j.  in->blk,
+ * when non-NULL, is the sender's block table (it gives each chunk its range;
+ * for segments of up to 2048 elements it is only checked).  An index outside
+ * its segment, a list that is not strictly ascending where the range comes
+ * from a search (or, for segments of up to 2048 elements, anywhere), or a
+ * block table that does not fit the list is reported by tc_device_errors;
+ * the rest of the tensor is still written. */
 tc_status tc_topk_decompress(const tc_codec* c, const tc_payload* in, void* y, int out_dt, void* stream);
 
 /* Sec. 3.2 (the GPT-2 runs, Table 5 and its note): gradients compressed at
@@ -249,7 +255,9 @@ tc_status tc_aqsgd_step(const tc_codec* c, const void* a, int dt, void* m, uint6
 
 /* Sec. 2.5 receiver: applies the same update to its own copy m_r of the
  * buffer and writes the updated rows: a_hat[b] = m_r[ids[b]] after the
- * update.  m_r: [n_samples][seg_len] dt, in-out; a_hat: [n_ids][seg_len] dt. */
+ * update.  m_r: [n_samples][seg_len] dt, in-out; a_hat: [n_ids][seg_len] dt.
+ * An id outside [0, n_samples) skips its row and an index outside its
+ * segment skips its entry; both are reported by tc_device_errors. */
 tc_status tc_aqsgd_reconstruct(const tc_codec* c, const tc_payload* in, void* m_r, int dt,
                                uint64_t n_samples, const int64_t* ids, uint32_t n_ids, void* a_hat,
                                void* stream);
