@@ -99,7 +99,7 @@ __device__ __forceinline__ void group_wait(uint32_t* ctr, uint32_t target) {
   if (threadIdx.x == 0) {
     uint32_t spins = 0;
     while (ld_agent(ctr) < target) {
-      __builtin_amdgcn_s_sleep(1);
+      __builtin_amdgcn_s_sleep(0);
       ++spins;
       if ((spins & 1023u) == 0u &&
           (__hip_atomic_load(&g_kernel_errors, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & KERR_TIMEOUT))
