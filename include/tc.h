@@ -44,6 +44,22 @@
  *             are sized to fit the device at once, and their waits are
  *             bounded (TC_KERR_TIMEOUT), but two of them should not share the
  *             device with other long-running kernels on concurrent streams.
+ *             Once TC_KERR_TIMEOUT is set on a device, every later such
+ *             kernel gives up its waits early and its results are invalid
+ *             until tc_device_errors(..., clear = 1) resets the bit and the
+ *             workspaces are zero-filled again.
+ *   Preconditions  The release library (libtc.so) assumes, without checking:
+ *             finite inputs, |x + e| at most half the binary32 maximum (so
+ *             that a quantization range hi - lo is finite), AQ-SGD changes
+ *             a - m[id] and updated values m[id] + v that fit the buffer's
+ *             dtype, distinct AQ-SGD ids within one call (two workgroups
+ *             would otherwise update one buffer row at once), and no overlap
+ *             between any two of a call's buffers (e and m are in-out on
+ *             their own).  The debug library (libtc_debug.so, the same
+ *             sources built with TC_DEBUG) checks all of these before the
+ *             launch and returns TC_ERR_PRECONDITION, with nothing enqueued,
+ *             when one fails.  Its checks read device data and synchronize
+ *             the stream, so its calls cannot be captured into a graph.
  */
 #ifndef TC_H
 #define TC_H
@@ -62,7 +78,8 @@ typedef enum {
   TC_ERR_DTYPE = 3,      /* dtype not supported for this operation */
   TC_ERR_WORKSPACE = 4,  /* workspace missing or smaller than tc_workspace_bytes() */
   TC_ERR_HIP = 5,        /* the HIP runtime refused the launch (see tc_last_error) */
-  TC_ERR_ALIGN = 6       /* a code buffer or the workspace is misaligned */
+  TC_ERR_PRECONDITION = 6, /* debug library only: an assumption below does not hold */
+  TC_ERR_ALIGN = 7       /* a code buffer or the workspace is misaligned */
 } tc_status;
 
 typedef enum { TC_F32 = 0, TC_BF16 = 1, TC_F16 = 2 } tc_dtype;
@@ -231,6 +248,11 @@ tc_status tc_ef_step(const tc_codec* c, const void* x, int dt, float* e, const t
  * 32,768 (one workgroup holds the segment), else TC_ERR_ARG. */
 tc_status tc_efmix_step(const tc_codec* c, const void* x, int dt, float* e, const tc_payload* out_x,
                         const tc_payload* out_e, void* stream);
+
+/* Sec. 2.4, EF-mixed: how a budget of k entries splits between the input's
+ * list (k_x = k - floor(k/2), the odd entry goes to the input) and the error
+ * buffer's list (k_e = floor(k/2)).  Either output pointer may be NULL. */
+void tc_efmix_counts(uint64_t k, uint64_t* k_x, uint64_t* k_e);
 
 /* Sec. 2.4, EF-mixed receiver: y [n_seg][seg_len] in out_dt starts at +0,
  * takes v_x at idx_x, then adds v_e at idx_e (binary32 sum), rounded once to

@@ -4,6 +4,12 @@ Every translation unit is compiled for gfx950 only, with IEEE binary32
 arithmetic (no FMA contraction, denormals kept) and without packed-fp32
 instruction selection, then linked into one shared library that exports the
 C ABI of include/tc.h and nothing else.
+
+libtc_debug.so is the same library with the C-ABI layer compiled with
+TC_DEBUG: before each launch it checks the preconditions the release library
+assumes (finite inputs, distinct AQ-SGD ids, no overlapping buffers) and
+returns TC_ERR_PRECONDITION when one fails; the check kernels of k_check.hip
+are linked into it only.
 """
 from __future__ import annotations
 
@@ -16,7 +22,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libtc.so")
-SOURCES = ["k_topk.hip", "k_quant.hip", "k_scatter.hip", "k_global.hip", "tc_api.cpp"]
+LIB_DEBUG = os.path.join(HERE, "libtc_debug.so")
+KERNELS = ["k_topk.hip", "k_quant.hip", "k_scatter.hip", "k_global.hip"]
+API = "tc_api.cpp"
+CHECKS = "k_check.hip"
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fvisibility=hidden", "-Wall",
@@ -31,9 +40,11 @@ def _hipcc():
     return "hipcc"
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+def _compile(src: str, verbose: bool, debug: bool = False) -> str:
+    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ("_debug" if debug else "") + ".o")
     cmd = [_hipcc(), *COMMON]
+    if debug:
+        cmd += ["-DTC_DEBUG"]
     if src.endswith(".hip"):
         cmd += ["-x", "hip", *DEVICE]
     cmd += ["-c", os.path.join(CSRC, src), "-o", obj]
@@ -45,19 +56,26 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False, jobs: int | None = None) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    jobs = jobs or min(len(SOURCES), max(1, (os.cpu_count() or 2)))
-    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib: str, verbose: bool):
+    tmp = lib + ".tmp"
     cmd = [_hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False, jobs: int | None = None) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    units = [(s, False) for s in KERNELS + [API, CHECKS]] + [(API, True)]
+    jobs = jobs or min(len(units), max(1, (os.cpu_count() or 2)))
+    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = dict(zip(units, ex.map(lambda u: _compile(u[0], verbose, u[1]), units)))
+    kernels = [objs[(s, False)] for s in KERNELS]
+    _link(kernels + [objs[(API, False)]], LIB, verbose)
+    _link(kernels + [objs[(CHECKS, False)], objs[(API, True)]], LIB_DEBUG, verbose)
     return LIB
 
 

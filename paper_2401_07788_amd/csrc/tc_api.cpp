@@ -6,6 +6,8 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
+#include <vector>
 
 #include "../../include/tc.h"
 #include "tc_internal.hpp"
@@ -84,6 +86,66 @@ tc_status check_resident(const tc::SegPlan& p) {
   return TC_OK;
 }
 
+#ifdef TC_DEBUG
+// ---- precondition checks of the debug library (see "Preconditions" in tc.h)
+struct Span {
+  const void* p;
+  uint64_t bytes;
+  const char* name;
+};
+
+// no two of a call's buffers overlap
+tc_status check_disjoint(std::initializer_list<Span> spans) {
+  for (auto i = spans.begin(); i != spans.end(); ++i)
+    for (auto j = i + 1; j != spans.end(); ++j) {
+      if (!i->p || !j->p || i->bytes == 0 || j->bytes == 0) continue;
+      const uintptr_t a0 = (uintptr_t)i->p, b0 = (uintptr_t)j->p;
+      if (a0 < b0 + j->bytes && b0 < a0 + i->bytes)
+        return fail(TC_ERR_PRECONDITION, "%s and %s overlap", i->name, j->name);
+    }
+  return TC_OK;
+}
+
+// AQ-SGD: no sample id twice in one call (read back through the stream)
+tc_status check_ids_distinct(const int64_t* ids, uint64_t n_ids, void* stream) {
+  if (n_ids < 2) return TC_OK;
+  std::vector<int64_t> h(n_ids);
+  hipError_t e = hipMemcpyAsync(h.data(), ids, n_ids * sizeof(int64_t), hipMemcpyDeviceToHost, (hipStream_t)stream);
+  if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "reading the ids for the precondition check");
+  std::sort(h.begin(), h.end());
+  for (size_t i = 1; i < h.size(); ++i)
+    if (h[i] == h[i - 1]) return fail(TC_ERR_PRECONDITION, "sample id %lld appears twice in one call", (long long)h[i]);
+  return TC_OK;
+}
+
+tc_status check_flags(hipError_t e, uint32_t flags, const char* what) {
+  if (e != hipSuccess) return hip_fail(e, what);
+  if (flags & tc::CHK_NONFINITE) return fail(TC_ERR_PRECONDITION, "%s: a value is not finite", what);
+  if (flags & tc::CHK_RANGE)
+    return fail(TC_ERR_PRECONDITION, "%s: a value is too large for its range or update to stay finite", what);
+  return TC_OK;
+}
+
+tc_status check_values(int dt, const void* x, const float* e, uint64_t n, void* stream) {
+  uint32_t flags = 0;
+  const hipError_t he = tc::check_values(dt, x, e, n, (hipStream_t)stream, &flags);
+  return check_flags(he, flags, "input check");
+}
+
+#define TC_PRECONDITION(expr)            \
+  do {                                   \
+    const tc_status s_ = (expr);         \
+    if (s_ != TC_OK) return s_;          \
+  } while (0)
+#else
+#define TC_PRECONDITION(expr) \
+  do {                        \
+  } while (0)
+#endif
+
+uint64_t bytes_of(uint64_t n, int dt) { return n * tc::dt_size(dt); }
+
 // TopK of segments too long to keep on chip, one segment after the other
 // (see k_global.hip); qbits != 0 quantizes the kept list (needs e)
 tc_status global_topk(uint32_t qbits, const tc_codec* c, const void* x, int dt, float* e, const tc_payload* out,
@@ -127,6 +189,25 @@ tc_status topk_common(int sel, const tc_codec* c, const void* x, int dt, float* 
   if (sel == tc::SEL_EF && !e) return fail(TC_ERR_NULL, "error buffer is NULL");
   if (sel == tc::SEL_AQSGD && (!m || !ids)) return fail(TC_ERR_NULL, "buffer or ids is NULL");
   if (c->k > 0 && (!out->idx || !out->val)) return fail(TC_ERR_NULL, "payload idx/val is NULL");
+  const uint64_t nb = tc::n_blocks(c->seg_len) + 1;
+  TC_PRECONDITION(check_disjoint({{x, bytes_of(n, dt), "input"},
+                                  {e, 4 * n, "e"},
+                                  {m, bytes_of(n_samples * c->seg_len, dt), "m"},
+                                  {ids, 8 * c->n_seg, "ids"},
+                                  {out->idx, 4 * c->n_seg * c->k, "payload idx"},
+                                  {out->val, bytes_of(c->n_seg * c->k, dt), "payload val"},
+                                  {out->blk, 4 * c->n_seg * nb, "payload blk"},
+                                  {ws, ws_bytes, "workspace"}}));
+  if (sel == tc::SEL_AQSGD) {
+    TC_PRECONDITION(check_ids_distinct(ids, c->n_seg, stream));
+#ifdef TC_DEBUG
+    uint32_t flags = 0;
+    const hipError_t he = tc::check_aqsgd(dt, x, m, ids, c->n_seg, c->seg_len, n_samples, (hipStream_t)stream, &flags);
+    TC_PRECONDITION(check_flags(he, flags, "AQ-SGD input check"));
+#endif
+  } else {
+    TC_PRECONDITION(check_values(dt, x, e, n, stream));
+  }
   // k == 0: an empty payload (and, for AQ-SGD, an unchanged buffer); only a
   // requested block table still has to be written
   if (c->k == 0 && !out->blk && (sel == tc::SEL_PLAIN || sel == tc::SEL_AQSGD)) return TC_OK;
@@ -167,6 +248,12 @@ tc_status quant_common(bool ef, const tc_codec* c, const void* x, int dt, float*
   if (ef && !e) return fail(TC_ERR_NULL, "error buffer is NULL");
   if (!out->codes || !out->meta) return fail(TC_ERR_NULL, "payload codes/meta is NULL");
   if (((uintptr_t)out->codes & 3u) != 0) return fail(TC_ERR_ALIGN, "codes must be 4-byte aligned");
+  TC_PRECONDITION(check_disjoint({{x, bytes_of(n, dt), "input"},
+                                  {e, 4 * n, "e"},
+                                  {out->codes, c->n_seg * tc_quant_group_bytes(c->seg_len, c->bits), "codes"},
+                                  {out->meta, 8 * c->n_seg, "meta"},
+                                  {ws, ws_bytes, "workspace"}}));
+  TC_PRECONDITION(check_values(dt, x, e, n, stream));
   const tc::SegPlan p = tc::plan_quant(dt, c->bits, ef, c->n_seg, c->seg_len);
   tc_status s = check_resident(p);
   if (s != TC_OK) return s;
@@ -227,6 +314,12 @@ TC_API tc_status tc_workspace_bytes(const tc_codec* c, size_t* bytes) {
   return TC_OK;
 }
 
+TC_API void tc_efmix_counts(uint64_t k, uint64_t* k_x, uint64_t* k_e) {
+  // reading E5: the input's list takes the odd entry
+  if (k_x) *k_x = k - k / 2;
+  if (k_e) *k_e = k / 2;
+}
+
 TC_API const char* tc_status_str(int s) {
   switch (s) {
     case TC_OK: return "ok";
@@ -235,6 +328,7 @@ TC_API const char* tc_status_str(int s) {
     case TC_ERR_DTYPE: return "unsupported dtype";
     case TC_ERR_WORKSPACE: return "workspace missing or too small";
     case TC_ERR_HIP: return "HIP runtime error";
+    case TC_ERR_PRECONDITION: return "precondition violated (debug library)";
     case TC_ERR_ALIGN: return "misaligned buffer";
   }
   return "unknown status";
@@ -281,6 +375,13 @@ TC_API tc_status tc_topk_decompress(const tc_codec* c, const tc_payload* in, voi
     if (((uintptr_t)in->codes & 3u) != 0) return fail(TC_ERR_ALIGN, "codes must be 4-byte aligned");
     wire = -(int)c->bits;
   }
+  TC_PRECONDITION(check_disjoint(
+      {{in->idx, 4 * c->n_seg * c->k, "payload idx"},
+       {c->kind == TC_TOPK ? in->val : nullptr, bytes_of(c->n_seg * c->k, c->wire), "payload val"},
+       {c->kind == TC_TOPK_QUANT ? in->codes : nullptr, c->n_seg * tc_quant_group_bytes(c->k, c->bits), "codes"},
+       {c->kind == TC_TOPK_QUANT ? in->meta : nullptr, 8 * c->n_seg, "meta"},
+       {in->blk, 4 * c->n_seg * (tc::n_blocks(c->seg_len) + 1), "payload blk"},
+       {y, bytes_of(c->n_seg * c->seg_len, out_dt), "output"}}));
   tc::ScatterArgs a{};
   a.idx = in->idx;
   a.blk = in->blk;
@@ -306,6 +407,13 @@ TC_API tc_status tc_topk_gather(const tc_codec* c, const tc_payload* in, const v
   if (c->n_seg * c->seg_len == 0) return TC_OK;
   if (!x) return fail(TC_ERR_NULL, "input is NULL");
   if (c->k > 0 && (!in || !in->idx || !val)) return fail(TC_ERR_NULL, "indices or val is NULL");
+  TC_PRECONDITION(check_disjoint({{c->k > 0 ? in->idx : nullptr, 4 * c->n_seg * c->k, "payload idx"},
+                                  {c->k > 0 ? in->blk : nullptr, 4 * c->n_seg * (tc::n_blocks(c->seg_len) + 1),
+                                   "payload blk"},
+                                  {x, bytes_of(c->n_seg * c->seg_len, dt), "input"},
+                                  {e, 4 * c->n_seg * c->seg_len, "e"},
+                                  {val, bytes_of(c->n_seg * c->k, dt), "val"}}));
+  TC_PRECONDITION(check_values(dt, x, e, c->n_seg * c->seg_len, stream));
   if (c->k == 0 && !e) return TC_OK;
   tc::GatherArgs a{};
   a.idx = (c->k > 0) ? in->idx : nullptr;
@@ -336,6 +444,9 @@ TC_API tc_status tc_quant_unpack(const tc_codec* c, const tc_payload* in, void* 
   if (c->n_seg * c->seg_len == 0) return TC_OK;
   if (!y || !in->codes || !in->meta) return fail(TC_ERR_NULL, "output, codes or meta is NULL");
   if (((uintptr_t)in->codes & 3u) != 0) return fail(TC_ERR_ALIGN, "codes must be 4-byte aligned");
+  TC_PRECONDITION(check_disjoint({{in->codes, c->n_seg * tc_quant_group_bytes(c->seg_len, c->bits), "codes"},
+                                  {in->meta, 8 * c->n_seg, "meta"},
+                                  {y, bytes_of(c->n_seg * c->seg_len, out_dt), "output"}}));
   tc::UnpackArgs a{};
   a.codes = (const uint32_t*)in->codes;
   a.meta = in->meta;
@@ -363,6 +474,15 @@ TC_API tc_status tc_ef_step(const tc_codec* c, const void* x, int dt, float* e, 
   if (c->k > 0 && (!out->idx || !out->codes || !out->meta)) return fail(TC_ERR_NULL, "payload idx/codes/meta is NULL");
   if (!out->meta) return fail(TC_ERR_NULL, "payload meta is NULL");
   if (((uintptr_t)out->codes & 3u) != 0) return fail(TC_ERR_ALIGN, "codes must be 4-byte aligned");
+  const uint64_t n = c->n_seg * c->seg_len;
+  TC_PRECONDITION(check_disjoint({{x, bytes_of(n, dt), "input"},
+                                  {e, 4 * n, "e"},
+                                  {out->idx, 4 * c->n_seg * c->k, "payload idx"},
+                                  {out->codes, c->n_seg * tc_quant_group_bytes(c->k, c->bits), "codes"},
+                                  {out->meta, 8 * c->n_seg, "meta"},
+                                  {out->blk, 4 * c->n_seg * (tc::n_blocks(c->seg_len) + 1), "payload blk"},
+                                  {ws, ws_bytes, "workspace"}}));
+  TC_PRECONDITION(check_values(dt, x, e, n, stream));
   return global_topk(c->bits, c, x, dt, e, out, ws, ws_bytes, stream);
 }
 
@@ -378,9 +498,20 @@ TC_API tc_status tc_efmix_step(const tc_codec* c, const void* x, int dt, float* 
     return fail(TC_ERR_ARG, "EF-mixed segments hold at most %llu elements (got %llu)",
                 (unsigned long long)tc::LDS_SEG_MAX, (unsigned long long)c->seg_len);
   if (!x || !e) return fail(TC_ERR_NULL, "input or error buffer is NULL");
-  const uint64_t kx = c->k - c->k / 2, ke = c->k / 2;
+  uint64_t kx = 0, ke = 0;
+  tc_efmix_counts(c->k, &kx, &ke);
   if (kx > 0 && (!out_x->idx || !out_x->val)) return fail(TC_ERR_NULL, "input list idx/val is NULL");
   if (ke > 0 && (!out_e->idx || !out_e->val)) return fail(TC_ERR_NULL, "buffer list idx/val is NULL");
+  const uint64_t n = c->n_seg * c->seg_len, nb = tc::n_blocks(c->seg_len) + 1;
+  TC_PRECONDITION(check_disjoint({{x, bytes_of(n, dt), "input"},
+                                  {e, 4 * n, "e"},
+                                  {out_x->idx, 4 * c->n_seg * kx, "input list idx"},
+                                  {out_x->val, bytes_of(c->n_seg * kx, dt), "input list val"},
+                                  {out_x->blk, 4 * c->n_seg * nb, "input list blk"},
+                                  {out_e->idx, 4 * c->n_seg * ke, "buffer list idx"},
+                                  {out_e->val, bytes_of(c->n_seg * ke, dt), "buffer list val"},
+                                  {out_e->blk, 4 * c->n_seg * nb, "buffer list blk"}}));
+  TC_PRECONDITION(check_values(dt, x, e, n, stream));
   const tc::SegPlan p = tc::plan_lds(tc::SEL_EFMIX, dt, c->n_seg);
   tc::TopkArgs a{};
   a.x = x;
@@ -409,9 +540,18 @@ TC_API tc_status tc_efmix_reconstruct(const tc_codec* c, const tc_payload* in_x,
   if (!in_x || !in_e) return fail(TC_ERR_NULL, "payload is NULL");
   if (c->n_seg * c->seg_len == 0) return TC_OK;
   if (!y) return fail(TC_ERR_NULL, "output is NULL");
-  const uint64_t kx = c->k - c->k / 2, ke = c->k / 2;
+  uint64_t kx = 0, ke = 0;
+  tc_efmix_counts(c->k, &kx, &ke);
   if (kx > 0 && (!in_x->idx || !in_x->val)) return fail(TC_ERR_NULL, "input list idx/val is NULL");
   if (ke > 0 && (!in_e->idx || !in_e->val)) return fail(TC_ERR_NULL, "buffer list idx/val is NULL");
+  const uint64_t nb = tc::n_blocks(c->seg_len) + 1;
+  TC_PRECONDITION(check_disjoint({{in_x->idx, 4 * c->n_seg * kx, "input list idx"},
+                                  {in_x->val, bytes_of(c->n_seg * kx, c->wire), "input list val"},
+                                  {in_x->blk, 4 * c->n_seg * nb, "input list blk"},
+                                  {in_e->idx, 4 * c->n_seg * ke, "buffer list idx"},
+                                  {in_e->val, bytes_of(c->n_seg * ke, c->wire), "buffer list val"},
+                                  {in_e->blk, 4 * c->n_seg * nb, "buffer list blk"},
+                                  {y, bytes_of(c->n_seg * c->seg_len, out_dt), "output"}}));
   tc::ScatterArgs a{};
   a.idx = in_x->idx;
   a.blk = in_x->blk;
@@ -453,6 +593,13 @@ TC_API tc_status tc_aqsgd_reconstruct(const tc_codec* c, const tc_payload* in, v
   if (c->seg_len != 0 && n_samples > UINT64_MAX / c->seg_len) return fail(TC_ERR_ARG, "n_samples * seg_len overflows");
   if (!m_r || !ids || !a_hat) return fail(TC_ERR_NULL, "buffer, ids or output is NULL");
   if (c->k > 0 && (!in->idx || !in->val)) return fail(TC_ERR_NULL, "payload idx/val is NULL");
+  TC_PRECONDITION(check_disjoint({{in->idx, 4 * c->n_seg * c->k, "payload idx"},
+                                  {in->val, bytes_of(c->n_seg * c->k, dt), "payload val"},
+                                  {in->blk, 4 * c->n_seg * (tc::n_blocks(c->seg_len) + 1), "payload blk"},
+                                  {m_r, bytes_of(n_samples * c->seg_len, dt), "m_r"},
+                                  {ids, 8 * c->n_seg, "ids"},
+                                  {a_hat, bytes_of(c->n_seg * c->seg_len, dt), "output"}}));
+  TC_PRECONDITION(check_ids_distinct(ids, c->n_seg, stream));
   tc::ScatterArgs a{};
   a.idx = in->idx;
   a.blk = in->blk;

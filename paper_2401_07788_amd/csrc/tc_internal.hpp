@@ -118,8 +118,9 @@ hipError_t launch_aqsgd_recv(int dt, const ScatterArgs& a, hipStream_t st);
 
 // ------------------------------------------------ segments too long to hold
 // TopK over one segment with a chain of kernels (a sampled band, candidate
-// or whole-segment radix passes, an ordered emit with decoupled look-back,
-// the kept-list quantizer)
+// or whole-segment radix passes, per-tile counts and their offsets, an emit
+// pass that writes each tile's kept entries at its offset, the kept-list
+// quantizer)
 struct GlobalArgs {
   const void* x;         // [L] input
   float* e;              // [L] residual (in-out) or nullptr
@@ -143,6 +144,14 @@ struct GlobalArgs {
 uint64_t global_ws_words(uint64_t L);
 void global_ws_carve(uint32_t* ws, uint64_t L, GlobalArgs& a);
 hipError_t launch_global(int dt, bool ef, uint32_t qbits, const GlobalArgs& a, hipStream_t st);
+
+// ------------------------------------ preconditions (debug library only)
+// Bits the check kernels of k_check.hip report; each call synchronizes the
+// stream and returns the bits found (and clears them).
+enum : uint32_t { CHK_NONFINITE = 1u, CHK_RANGE = 2u };
+hipError_t check_values(int dt, const void* x, const float* e, uint64_t n, hipStream_t st, uint32_t* flags);
+hipError_t check_aqsgd(int dt, const void* a, const void* m, const int64_t* ids, uint64_t n_ids, uint64_t L,
+                       uint64_t n_samples, hipStream_t st, uint32_t* flags);
 
 // sticky kernel error bits of each kernel translation unit
 hipError_t errors_topk(uint32_t* bits, bool clear);

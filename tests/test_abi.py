@@ -27,14 +27,49 @@ def tcmod():
     return tc
 
 
-def test_exports_match_header(tcmod):
+@pytest.mark.parametrize("which", ["LIB_PATH", "DEBUG_LIB_PATH"])
+def test_exports_match_header(tcmod, which):
     declared = _declared()
     assert "tc_aqsgd_step" in declared and "tc_topk_compress" in declared
-    out = subprocess.run(["nm", "-D", "--defined-only", tcmod.LIB_PATH], capture_output=True, text=True,
+    path = getattr(tcmod, which)
+    out = subprocess.run(["nm", "-D", "--defined-only", path], capture_output=True, text=True,
                          check=True).stdout
     exported = sorted({ln.split()[-1] for ln in out.splitlines() if " T " in ln})
     assert exported == declared
     assert sorted(tcmod.EXPORTS) == declared
+    tcmod.load(path)
+
+
+def test_efmix_counts_from_the_library(tcmod, orc):
+    for k in (0, 1, 2, 3277, 3278, 2 ** 40 + 1):
+        assert tcmod.efmix_counts(k) == orc.efmix_counts(k)
+        assert sum(tcmod.efmix_counts(k)) == k
+
+
+def test_debug_library_refuses_overlapping_buffers(tcmod):
+    """the aliasing precondition is checked on the host before any device
+    call, so it runs here; the release library does not check it"""
+    D = tcmod.load(tcmod.DEBUG_LIB_PATH)
+    R = tcmod.load(tcmod.LIB_PATH)
+    n_seg, L, k = 2, 1000, 10
+    c = tcmod.Codec(1, 0, 0, 0, n_seg, L, k)
+    base = 1 << 40                      # never dereferenced: the checks fail first
+    x = C.c_void_p(base)
+    e_overlap = C.cast(C.c_void_p(base + 4 * L), C.POINTER(C.c_float))
+    p = tcmod.Payload(base + (1 << 30), base + (2 << 30), None, None, None)
+    assert D.tc_ef_step(C.byref(c), x, 0, e_overlap, C.byref(p), None, 0, None) == tcmod.TC_ERR_PRECONDITION
+    assert b"overlap" in D.tc_last_error()
+    # a payload whose values run into its indices
+    p2 = tcmod.Payload(base + (1 << 30), base + (1 << 30) + 4, None, None, None)
+    c2 = tcmod.Codec(1, 0, 0, 0, n_seg, L, k)
+    assert D.tc_topk_compress(C.byref(c2), x, 0, C.byref(p2), None, 0, None) == tcmod.TC_ERR_PRECONDITION
+    # the receiver side: AQ-SGD output over the buffer
+    c3 = tcmod.Codec(1, 2, 0, 0, n_seg, L, k)
+    p3 = tcmod.Payload(base + (1 << 30), base + (2 << 30), None, None, None)
+    m_r = C.c_void_p(base)
+    assert D.tc_aqsgd_reconstruct(C.byref(c3), C.byref(p3), m_r, 2, 4, C.c_void_p(base + (3 << 30)), n_seg,
+                                  C.c_void_p(base + 2 * L), None) == tcmod.TC_ERR_PRECONDITION
+    assert R.tc_status_str(tcmod.TC_ERR_PRECONDITION)
 
 
 def test_host_helpers(tcmod, orc):
@@ -44,8 +79,8 @@ def test_host_helpers(tcmod, orc):
         assert tcmod.quant_group_bytes(G, b) == orc.quant_group_bytes(G, b)
     assert tcmod.quant_group_bytes(10, 32) == 40
     assert tcmod.quant_group_bytes(10, 9) == 0
-    for s in range(7):
-        assert tcmod.status_str(s)
+    for s in range(8):
+        assert tcmod.status_str(s) != "unknown status"
 
 
 def test_validation_before_any_device_call(tcmod):
