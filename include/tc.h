@@ -17,7 +17,9 @@
  *   Memory    All tensor pointers are device pointers (hipMalloc or a torch
  *             tensor's data).  The caller allocates and owns every buffer;
  *             the library allocates no device memory and keeps no pointer
- *             after a call returns.
+ *             after a call returns.  The one exception is the scratch array
+ *             of tc_aqsgd_step_noalloc, a fixed-size device global of the
+ *             library itself.
  *   Streams   `stream` is a hipStream_t (NULL = the default stream).  Work is
  *             enqueued asynchronously; TC_OK means "enqueued".  Kernel-side
  *             faults in the data (an out-of-range sample id or payload index,
@@ -274,6 +276,23 @@ tc_status tc_efmix_reconstruct(const tc_codec* c, const tc_payload* in_x, const 
 tc_status tc_aqsgd_step(const tc_codec* c, const void* a, int dt, void* m, uint64_t n_samples,
                         const int64_t* ids, uint32_t n_ids, const tc_payload* out, void* ws,
                         size_t ws_bytes, void* stream);
+
+/* For callers that cannot allocate device memory (code under stream or graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * tc_aqsgd_step above, with the same arguments and results bit for bit, but
+ * without a workspace argument.  The kernels use instead a scratch array of
+ * TC_NOALLOC_SCRATCH_BYTES that the library holds on each device it runs on
+ * until the process ends; this call allocates nothing.  A shape that needs
+ * more scratch than that fails with TC_ERR_WORKSPACE and nothing enqueued
+ * (the need never exceeds tc_workspace_bytes()).  The first call on a device
+ * looks up that device's copy and enqueues a clearing kernel on `stream`.
+ * Every call on one device shares its scratch, so two calls that overlap in
+ * time on one device (concurrent streams, host threads) race and both give
+ * invalid results.  After TC_KERR_TIMEOUT, tc_device_errors(..., clear = 1)
+ * clears the current device's scratch again. */
+#define TC_NOALLOC_SCRATCH_BYTES (4u << 20)
+tc_status tc_aqsgd_step_noalloc(const tc_codec* c, const void* a, int dt, void* m, uint64_t n_samples,
+                                const int64_t* ids, uint32_t n_ids, const tc_payload* out, void* stream);
 
 /* Sec. 2.5 receiver: applies the same update to its own copy m_r of the
  * buffer and writes the updated rows: a_hat[b] = m_r[ids[b]] after the

@@ -23,7 +23,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libtc.so")
 LIB_DEBUG = os.path.join(HERE, "libtc_debug.so")
-KERNELS = ["k_topk.hip", "k_quant.hip", "k_scatter.hip", "k_global.hip"]
+KERNELS = ["k_topk.hip", "k_quant.hip", "k_scatter.hip", "k_global.hip", "k_scratch.hip"]
 API = "tc_api.cpp"
 CHECKS = "k_check.hip"
 ARCH = "gfx950"

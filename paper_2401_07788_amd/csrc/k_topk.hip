@@ -1366,6 +1366,7 @@ SegPlan plan_topk(int sel, int dt, uint64_t n_seg, uint64_t L) {
   // selection kind of the same layout
   const uint64_t ws_groups = std::min<uint64_t>(n_seg, std::max<uint64_t>(1, (uint64_t)cus * 4 / p.P));
   p.ws_words = (p.P > 1) ? ws_groups * grp_mem_words(p.P) : 0;
+  p.ws_used = (p.P > 1) ? groups * grp_mem_words(p.P) : 0;
   return p;
 }
 

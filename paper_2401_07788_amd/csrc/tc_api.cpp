@@ -14,6 +14,8 @@
 
 #define TC_API extern "C" __attribute__((visibility("default")))
 
+static_assert(TC_NOALLOC_SCRATCH_BYTES == tc::NOALLOC_SCRATCH_BYTES, "one scratch size");
+
 namespace tc {
 
 int device_cus() {
@@ -146,6 +148,15 @@ tc_status check_values(int dt, const void* x, const float* e, uint64_t n, void* 
 
 uint64_t bytes_of(uint64_t n, int dt) { return n * tc::dt_size(dt); }
 
+tc_status check_aqsgd_args(const tc_codec* c, uint64_t n_samples, uint32_t n_ids) {
+  tc_status s = check_codec(c, 1 << TC_TOPK);
+  if (s != TC_OK) return s;
+  if (c->n_seg != n_ids) return fail(TC_ERR_ARG, "codec.n_seg %llu != n_ids %u", (unsigned long long)c->n_seg, n_ids);
+  if (n_ids > 0 && n_samples == 0) return fail(TC_ERR_ARG, "n_samples is 0");
+  if (c->seg_len != 0 && n_samples > UINT64_MAX / c->seg_len) return fail(TC_ERR_ARG, "n_samples * seg_len overflows");
+  return TC_OK;
+}
+
 // TopK of segments too long to keep on chip, one segment after the other
 // (see k_global.hip); qbits != 0 quantizes the kept list (needs e)
 tc_status global_topk(uint32_t qbits, const tc_codec* c, const void* x, int dt, float* e, const tc_payload* out,
@@ -178,8 +189,10 @@ tc_status global_topk(uint32_t qbits, const tc_codec* c, const void* x, int dt, 
   return TC_OK;
 }
 
+// noalloc: the workspace is the library's own scratch (ws, ws_bytes unused)
 tc_status topk_common(int sel, const tc_codec* c, const void* x, int dt, float* e, void* m, uint64_t n_samples,
-                      const int64_t* ids, const tc_payload* out, void* ws, size_t ws_bytes, void* stream) {
+                      const int64_t* ids, const tc_payload* out, void* ws, size_t ws_bytes, void* stream,
+                      bool noalloc = false) {
   if (!dt_ok(dt)) return fail(TC_ERR_DTYPE, "dtype %d", dt);
   if (c->wire != dt) return fail(TC_ERR_DTYPE, "wire dtype %d must equal the input dtype %d", c->wire, dt);
   if (!out) return fail(TC_ERR_NULL, "payload is NULL");
@@ -218,8 +231,22 @@ tc_status topk_common(int sel, const tc_codec* c, const void* x, int dt, float* 
     g_err[0] = 0;
     return global_topk(0, c, x, dt, e, out, ws, ws_bytes, stream);   // too long for one resident group
   }
-  s = check_ws(p, ws, ws_bytes);
-  if (s != TC_OK) return s;
+  if (noalloc) {
+    const uint64_t need = p.ws_used * 4u;
+    if (need > tc::NOALLOC_SCRATCH_BYTES)
+      return fail(TC_ERR_WORKSPACE, "this shape needs %llu bytes of scratch, the allocation-free entry point holds %llu",
+                  (unsigned long long)need, (unsigned long long)tc::NOALLOC_SCRATCH_BYTES);
+    ws = nullptr;
+    ws_bytes = 0;
+    if (need > 0) {
+      const hipError_t he = tc::noalloc_scratch(&ws, (hipStream_t)stream);
+      if (he != hipSuccess) return hip_fail(he, "scratch set-up");
+      ws_bytes = tc::NOALLOC_SCRATCH_BYTES;
+    }
+  } else {
+    s = check_ws(p, ws, ws_bytes);
+    if (s != TC_OK) return s;
+  }
   tc::TopkArgs a{};
   a.x = x;
   a.e = e;
@@ -347,6 +374,9 @@ TC_API tc_status tc_device_errors(uint32_t* bits, int clear) {
   uint32_t g = 0;
   if ((e = tc::errors_global(&g, clear != 0)) != hipSuccess) return hip_fail(e, "error word (global)");
   *bits = a | b | d | g;
+  // a wait that gave up leaves the allocation-free entry point's scratch dirty
+  if (clear && (*bits & TC_KERR_TIMEOUT) && (e = tc::noalloc_scratch_reset()) != hipSuccess)
+    return hip_fail(e, "clearing the scratch");
   return TC_OK;
 }
 
@@ -572,12 +602,16 @@ TC_API tc_status tc_efmix_reconstruct(const tc_codec* c, const tc_payload* in_x,
 TC_API tc_status tc_aqsgd_step(const tc_codec* c, const void* a, int dt, void* m, uint64_t n_samples,
                                const int64_t* ids, uint32_t n_ids, const tc_payload* out, void* ws,
                                size_t ws_bytes, void* stream) {
-  tc_status s = check_codec(c, 1 << TC_TOPK);
+  const tc_status s = check_aqsgd_args(c, n_samples, n_ids);
   if (s != TC_OK) return s;
-  if (c->n_seg != n_ids) return fail(TC_ERR_ARG, "codec.n_seg %llu != n_ids %u", (unsigned long long)c->n_seg, n_ids);
-  if (n_ids > 0 && n_samples == 0) return fail(TC_ERR_ARG, "n_samples is 0");
-  if (c->seg_len != 0 && n_samples > UINT64_MAX / c->seg_len) return fail(TC_ERR_ARG, "n_samples * seg_len overflows");
   return topk_common(tc::SEL_AQSGD, c, a, dt, nullptr, m, n_samples, ids, out, ws, ws_bytes, stream);
+}
+
+TC_API tc_status tc_aqsgd_step_noalloc(const tc_codec* c, const void* a, int dt, void* m, uint64_t n_samples,
+                                       const int64_t* ids, uint32_t n_ids, const tc_payload* out, void* stream) {
+  const tc_status s = check_aqsgd_args(c, n_samples, n_ids);
+  if (s != TC_OK) return s;
+  return topk_common(tc::SEL_AQSGD, c, a, dt, nullptr, m, n_samples, ids, out, nullptr, 0, stream, true);
 }
 
 TC_API tc_status tc_aqsgd_reconstruct(const tc_codec* c, const tc_payload* in, void* m_r, int dt, uint64_t n_samples,

@@ -24,6 +24,7 @@ struct SegPlan {
   uint32_t grid = 0;
   uint64_t capacity = 0;   // workgroups of this kernel the device holds at once
   uint64_t ws_words = 0;   // 32-bit words of zero-initialised workspace needed
+  uint64_t ws_used = 0;    // of which this launch touches (its n_groups groups)
   bool lds = false;        // TopK: one workgroup per segment held in LDS (k_topk_lds)
 };
 
@@ -161,5 +162,10 @@ hipError_t errors_global(uint32_t* bits, bool clear);
 
 // device properties (cached per device)
 int device_cus();
+
+// ---- library-owned scratch of the allocation-free entry point (k_scratch.hip)
+constexpr uint64_t NOALLOC_SCRATCH_BYTES = 4ull << 20;    // TC_NOALLOC_SCRATCH_BYTES
+hipError_t noalloc_scratch(void** ptr, hipStream_t st);
+hipError_t noalloc_scratch_reset();
 
 }  // namespace tc

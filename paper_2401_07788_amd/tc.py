@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(_HERE, "libtc.so")
 # the same library with its preconditions checked before every launch
 # (TC_ERR_PRECONDITION); chosen with use_debug_library() or TC_DEBUG=1
 DEBUG_LIB_PATH = os.path.join(_HERE, "libtc_debug.so")
-TC_ERR_PRECONDITION = 6
+(TC_OK, TC_ERR_NULL, TC_ERR_ARG, TC_ERR_DTYPE, TC_ERR_WORKSPACE, TC_ERR_HIP, TC_ERR_PRECONDITION,
+ TC_ERR_ALIGN) = range(8)
 
 TC_F32, TC_BF16, TC_F16 = 0, 1, 2
 TC_TOPK, TC_QUANT, TC_TOPK_QUANT = 1, 2, 3
@@ -94,6 +95,8 @@ EXPORTS = {
                                        C.c_void_p]),
     "tc_aqsgd_step": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.c_void_p, C.c_uint64, C.c_void_p,
                                 C.c_uint32, C.POINTER(Payload), C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tc_aqsgd_step_noalloc": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.c_void_p, C.c_uint64,
+                                        C.c_void_p, C.c_uint32, C.POINTER(Payload), C.c_void_p]),
     "tc_aqsgd_reconstruct": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.c_void_p, C.c_int, C.c_uint64,
                                        C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p]),
     "tc_efmix_counts": (None, [C.c_uint64, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]),
@@ -525,9 +528,8 @@ def efmix_reconstruct(px: TopkPayload, pe: TopkPayload, seg_len: int, out_dtype=
 
 
 # ------------------------------------------------------------------- AQ-SGD
-def aqsgd_step(a: torch.Tensor, m: torch.Tensor, ids: torch.Tensor, k: int, ws=None, out: TopkPayload = None,
-               blk: bool = True):
-    """sender: d = a - m[ids]; send TopK(d); m[ids] += sent.  m is updated in place."""
+def _aqsgd_prepare(a, m, ids, k, out, blk):
+    """shape checks of the AQ-SGD sender; returns (codec, n_ids, out, Payload)"""
     if ids.dtype != torch.int64 or a.dtype != m.dtype:
         raise TypeError("ids must be int64 and a, m share a dtype")
     if m.dim() != 2:
@@ -544,10 +546,30 @@ def aqsgd_step(a: torch.Tensor, m: torch.Tensor, ids: torch.Tensor, k: int, ws=N
     _need_gpu(a, m, ids)
     if out is None:
         out = empty_topk_payload(n_ids, L, k, a.dtype, a.device, blk)
-    p = Payload(_ptr(out.idx), _ptr(out.val), None, None, _ptr(out.blk))
+    return c, n_ids, out, Payload(_ptr(out.idx), _ptr(out.val), None, None, _ptr(out.blk))
+
+
+def aqsgd_step(a: torch.Tensor, m: torch.Tensor, ids: torch.Tensor, k: int, ws=None, out: TopkPayload = None,
+               blk: bool = True):
+    """sender: d = a - m[ids]; send TopK(d); m[ids] += sent.  m is updated in place."""
+    c, n_ids, out, p = _aqsgd_prepare(a, m, ids, k, out, blk)
     w, wn = _ws_args(c, a.device, ws)
     _check(lib().tc_aqsgd_step(C.byref(c), _ptr(a), _dt(a), _ptr(m), m.shape[0], _ptr(ids), n_ids, C.byref(p),
                                w, wn, _stream(a.device)), "tc_aqsgd_step")
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 4 << 20   # TC_NOALLOC_SCRATCH_BYTES
+
+
+def aqsgd_step_noalloc(a: torch.Tensor, m: torch.Tensor, ids: torch.Tensor, k: int, out: TopkPayload = None,
+                       blk: bool = True):
+    """aqsgd_step through the entry point that allocates nothing (its scratch is
+    the library's own, shared by every call on the device); pass `out` to keep
+    this call free of allocations on the Python side too."""
+    c, n_ids, out, p = _aqsgd_prepare(a, m, ids, k, out, blk)
+    _check(lib().tc_aqsgd_step_noalloc(C.byref(c), _ptr(a), _dt(a), _ptr(m), m.shape[0], _ptr(ids), n_ids,
+                                       C.byref(p), _stream(a.device)), "tc_aqsgd_step_noalloc")
     return out
 
 

@@ -107,3 +107,23 @@ def test_validation_before_any_device_call(tcmod):
     # empty tensors are a no-op that succeeds
     c = tcmod.Codec(1, 0, 0, 0, 0, 10, 0)
     assert L.tc_topk_compress(C.byref(c), None, 0, C.byref(p), None, 0, None) == 0
+
+
+def test_noalloc_refuses_shapes_beyond_its_scratch(tcmod):
+    """the allocation-free AQ-SGD sender checks the scratch a shape needs
+    against its fixed maximum on the host, before any device call (pointers
+    below are never dereferenced)"""
+    R = tcmod.load(tcmod.LIB_PATH)
+    base = 1 << 40
+    n_ids, L, k = 600, 40000, 12000     # many two-workgroup segments at once
+    c = tcmod.Codec(1, 2, 0, 0, n_ids, L, k)
+    p = tcmod.Payload(base + (1 << 34), base + (2 << 34), None, None, None)
+    a, m, ids = C.c_void_p(base), C.c_void_p(base + (1 << 32)), C.c_void_p(base + (3 << 34))
+    st = R.tc_aqsgd_step_noalloc(C.byref(c), a, 2, m, 1000, ids, n_ids, C.byref(p), None)
+    assert st == tcmod.TC_ERR_WORKSPACE
+    assert b"scratch" in R.tc_last_error()
+    # the argument checks of tc_aqsgd_step come first
+    assert R.tc_aqsgd_step_noalloc(C.byref(c), a, 2, m, 1000, ids, n_ids - 1, C.byref(p), None) == 2
+    assert R.tc_aqsgd_step_noalloc(C.byref(c), a, 2, m, 0, ids, n_ids, C.byref(p), None) == 2
+    assert R.tc_aqsgd_step_noalloc(None, a, 2, m, 1000, ids, n_ids, C.byref(p), None) == 1
+    assert tcmod.NOALLOC_SCRATCH_BYTES == 4 << 20
