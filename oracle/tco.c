@@ -557,8 +557,11 @@ int tco_aqsgd_recv(const uint32_t* idx, const void* val, void* m_r, int dt, uint
 /*   then adds the e list's values at its indices (binary32 sum, rounded     */
 /*   once to out_dt), so the sent tensor is C_kx(x) + C_ke(e);               */
 /*   the buffer becomes everything not sent:                                 */
-/*     e'_i = (x_i - [i in S_x] dt(x_i)) + (e_i - [i in S_e] dt(e_i))        */
-/*   in binary32, which is x + e minus what the receiver holds.              */
+/*     e'_i = (x_i - [i in S_x] dt(x_i)) + (e_i - [i in S_e] dt(e_i) + c_i)  */
+/*   in binary32, which is x + e minus what the receiver holds.  c_i is 0    */
+/*   except where both lists hold i: there the receiver's tensor (in the     */
+/*   wire dtype dt) holds u_i = x_i + dt(e_i) (binary32 sum) rounded once to */
+/*   dt, so the part that rounding drops, c_i = u_i - dt(u_i), stays behind. */
 /* x is [n_seg][L] of dtype dt; e (binary32) is updated in place; idx_x /   */
 /* val_x are [n_seg][k_x], idx_e / val_e are [n_seg][k_e].                  */
 /* ------------------------------------------------------------------------ */
@@ -588,7 +591,11 @@ int tco_efmix_send(const void* x, int dt, float* e, uint64_t n_seg, uint64_t L, 
         for (uint64_t j = 0; j < ke; ++j) { store_rne(val_e, dt, s * ke + j, ev[ie[j]]); in_e[ie[j]] = 1; }
         for (uint64_t i = 0; i < L; ++i) {
             const float rx = xv[i] - (in_x[i] ? through(dt, xv[i]) : 0.0f);
-            const float re = ev[i] - (in_e[i] ? through(dt, ev[i]) : 0.0f);
+            float re = ev[i] - (in_e[i] ? through(dt, ev[i]) : 0.0f);
+            if (in_x[i] && in_e[i]) {
+                const float u = through(dt, xv[i]) + through(dt, ev[i]);   /* the receiver's sum */
+                re = re + (u - through(dt, u));
+            }
             e[base + i] = rx + re;
         }
     }

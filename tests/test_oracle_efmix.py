@@ -6,8 +6,11 @@ Checked against: a worked example computed by hand (two steps, with an index
 picked by both halves and a tie broken towards the lower index), numpy
 selections of the largest magnitudes, exact conservation x + e = received + e'
 on integer data (every sum exact), the bfloat16 rounding remainder of a sent
-buffer entry written out by hand, and the edge cases (k = 0, 1 and L, the first
-step from an empty buffer, an index outside the segment)."""
+buffer entry written out by hand, an index held by both lists whose received
+sum rounds in the wire dtype (worked by hand, and conservation on
+non-integer data where every binary32 operation is exact but the wire's
+roundings are not), and the edge cases (k = 0, 1 and L, the first step from an
+empty buffer, an index outside the segment)."""
 import numpy as np
 import pytest
 
@@ -79,6 +82,74 @@ def test_bf16_wire_remainder_stays_in_buffer(orc):
     assert e1.tolist() == [[0.0, 2.0 ** -10, 0.0, 0.0]]
     y = orc.efmix_recv(ix, vx, ie, ve, "bf16", 1, L, k, out_dt="f32")
     assert y.tolist() == [[0.0, 1.0, 0.0, 0.0]]
+
+
+def test_shared_index_keeps_what_the_receivers_rounding_drops(orc):
+    # index 0 is the largest entry of both x and e.  The receiver holds
+    # bf16(1 + 2^-8): 1 + 2^-8 lies halfway between 1 and 1 + 2^-7 and rounds
+    # to the even neighbour 1.0, so the buffer must keep 2^-8 there
+    L, k = 4, 2
+    x = np.array([[1.0, 0.25, -0.5, 0.125]], np.float32)
+    xr = (x.view(np.uint32) >> 16).astype(np.uint16)      # exact in bfloat16
+    e = np.array([[2.0 ** -8, 0.0, 0.0, 0.0]], np.float32)
+    ix, vx, ie, ve, e1 = orc.efmix_send(xr, "bf16", e, 1, L, k)
+    assert ix.tolist() == [[0]] and ie.tolist() == [[0]]
+    assert vx.tolist() == [[0x3F80]] and ve.tolist() == [[0x3B80]]   # 1.0 and 2^-8
+    y = orc.efmix_recv(ix, vx, ie, ve, "bf16", 1, L, k, out_dt="bf16")
+    assert y.tolist() == [[0x3F80, 0, 0, 0]]
+    assert e1.tolist() == [[2.0 ** -8, 0.25, -0.5, 0.125]]
+
+
+def orc_round(v, dt):
+    """round binary32 to the wire dtype (RNE) with numpy alone, back to binary32"""
+    v = np.asarray(v, np.float32)
+    if dt == "f16":
+        return v.astype(np.float16).astype(np.float32)
+    b = v.view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16 << 16
+    return b.astype(np.uint32).view(np.float32)
+
+
+def _wire_bits(v, dt):
+    """binary32 values exact in dt -> the dt's raw pattern"""
+    if dt == "f16":
+        return v.astype(np.float16).view(np.uint16)
+    return (v.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def _to_f32(r, dt):
+    if dt == "f16":
+        return r.view(np.float16).astype(np.float32)
+    return (r.astype(np.uint32) << 16).view(np.float32)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+def test_conservation_with_shared_indices_off_the_wire_grid(orc, dt):
+    # values are multiples of 2^-6 below 2^9 in magnitude: every binary32
+    # sum and difference below is exact, while the wire dtype keeps only 8
+    # (bf16) or 11 (f16) significant bits.  The buffer is largest where x is,
+    # so the two lists share indices, and their sums fall off the wire's grid.
+    # With the receiver in the wire dtype, x + e == received + e' must hold
+    # bit for bit; dropping c_i (the receiver's rounding at shared indices)
+    # breaks it.
+    rng = np.random.default_rng(77 if dt == "bf16" else 78)
+    n_seg, L, k = 2, 4000, 800
+    e = (rng.integers(-2 ** 12, 2 ** 12, (n_seg, L)) / 64.0).astype(np.float32)
+    shared_off_grid = 0
+    for step in range(4):
+        x = orc_round((rng.integers(-2 ** 10, 2 ** 10, (n_seg, L)) / 64.0).astype(np.float32), dt)
+        hot = np.argsort(-np.abs(e), axis=1)[:, : k // 3]     # x large where e is
+        np.put_along_axis(x, hot, orc_round(np.take_along_axis(e, hot, 1) * 0.75 + 3.0, dt), 1)
+        ix, vx, ie, ve, e_next = orc.efmix_send(_wire_bits(x, dt), dt, e, n_seg, L, k)
+        y = orc.efmix_recv(ix, vx, ie, ve, dt, n_seg, L, k, out_dt=dt)
+        yf = _to_f32(y, dt)
+        assert np.array_equal((x + e).view(np.uint32), (yf + e_next).view(np.uint32)), f"step {step}"
+        for s in range(n_seg):
+            both = np.intersect1d(ix[s], ie[s])
+            u = x[s, both] + orc_round(e[s, both], dt)
+            shared_off_grid += int((orc_round(u, dt) != u).sum())
+        e = e_next
+    assert shared_off_grid > 50
 
 
 def test_first_step_from_empty_buffer(orc):
