@@ -1124,7 +1124,9 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
     // then e' = (x minus what was sent of it) + (e minus what was sent of
     // e).  x is exact in its dtype, so its share is x off the kept entries
     // and +0 on them; x is read again for it rather than held in registers
-    // through the second selection.
+    // through the second selection.  Where both lists hold an index the
+    // receiver rounds u = x + wire(e) (binary32) once to the wire dtype, and
+    // the part that rounding drops, u - wire(u), stays in the buffer too.
     if constexpr (SEL == SEL_EFMIX) {
       __syncthreads();
       // the buffer into LDS, in the input's piece layout
@@ -1200,9 +1202,16 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
             const float xv = Elem<InT>::up(xr[j][c]);
-            const float rx = xv - (((kx4 >> c) & 1u) ? xv : 0.0f);
+            const bool in_x = (kx4 >> c) & 1u, in_e = (ke4 >> c) & 1u;
+            const float rx = xv - (in_x ? xv : 0.0f);
             const float v = __uint_as_float(w[c]);
-            o[c] = rx + (v - (((ke4 >> c) & 1u) ? through<InT>(v) : 0.0f));
+            const float ve = through<InT>(v);
+            float re = v - (in_e ? ve : 0.0f);
+            if (in_x && in_e) {
+              const float u = xv + ve;
+              re = re + (u - through<InT>(u));
+            }
+            o[c] = rx + re;
           }
           if (vec) store_run<float, 4, true>(es + i0, o);
           else {

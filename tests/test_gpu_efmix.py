@@ -102,3 +102,55 @@ def test_efmix_more_segments_than_workgroups(tc, orc):
     k = tc.topk_count(L, 1, 10)
     xs = [W.randn((n_seg, L), 15, t) for t in range(2)]
     efmix_steps(tc, orc, xs, n_seg, L, k)
+
+
+def _round_np(v, dt):
+    """binary32 -> the wire dtype (RNE) -> binary32, with numpy alone"""
+    v = np.asarray(v, np.float32)
+    if dt == "f16":
+        return v.astype(np.float16).astype(np.float32)
+    b = v.view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16 << 16
+    return b.astype(np.uint32).view(np.float32)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+@pytest.mark.parametrize("L", [4000, 4099, 32768])
+def test_efmix_shared_indices_conserve(tc, orc, dt, L):
+    # multiples of 2^-6 below 2^9: every binary32 step is exact while the
+    # wire keeps 8 (bf16) or 11 (f16) significant bits.  x is large where the
+    # buffer is, so the two lists share indices whose sums fall off the wire
+    # grid; with the receiver in the wire dtype, x + e == received + e' bit
+    # for bit, on the GPU's own outputs and the oracle's alike
+    rng = np.random.default_rng(L + (0 if dt == "bf16" else 1))
+    n_seg = 3
+    k = tc.topk_count(L, 2, 10)
+    e_np = (rng.integers(-2 ** 12, 2 ** 12, (n_seg, L)) / 64.0).astype(np.float32)
+    e_gpu = torch.from_numpy(e_np.copy()).reshape(-1).cuda()
+    e_orc = e_np.copy()
+    shared_off_grid = 0
+    for t in range(3):
+        x = _round_np((rng.integers(-2 ** 10, 2 ** 10, (n_seg, L)) / 64.0).astype(np.float32), dt)
+        hot = np.argsort(-np.abs(e_orc), axis=1, kind="stable")[:, : k // 3]
+        np.put_along_axis(x, hot, _round_np(np.take_along_axis(e_orc, hot, 1) * 0.75 + 3.0, dt), 1)
+        xt = torch.from_numpy(x).to(TORCH[dt]).cuda()
+        e_before = raw(e_gpu).reshape(n_seg, L).copy()
+        px, pe = tc.efmix_step(xt, e_gpu, k, n_seg)
+        y = tc.efmix_reconstruct(px, pe, L, out_dtype=TORCH[dt], use_blk=(t % 2 == 0))
+        torch.cuda.synchronize()
+        assert tc.device_errors() == 0
+        ix, vx, ie, ve, e_orc = orc.efmix_send(raw(xt), dt, e_orc, n_seg, L, k)
+        assert_bits_equal(raw(px.idx), ix, f"idx_x step {t}")
+        assert_bits_equal(raw(pe.idx), ie, f"idx_e step {t}")
+        assert_bits_equal(raw(px.val), vx, f"val_x step {t}")
+        assert_bits_equal(raw(pe.val), ve, f"val_e step {t}")
+        e_after = raw(e_gpu).reshape(n_seg, L)
+        assert_bits_equal(e_after, e_orc, f"e step {t}")
+        yf = y.float().cpu().numpy()
+        lhs = (x + e_before).view(np.uint32)
+        assert np.array_equal(lhs, (yf + e_after).view(np.uint32)), f"conservation step {t}"
+        for s in range(n_seg):
+            both = np.intersect1d(ix[s], ie[s])
+            u = x[s, both] + _round_np(e_before[s, both], dt)
+            shared_off_grid += int((_round_np(u, dt) != u).sum())
+    assert shared_off_grid > 20
