@@ -16,7 +16,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# TCO_LIB names another build of tco.c (the sanitized one of the test suite)
+_LIB_PATH = os.environ.get("TCO_LIB") or os.path.join(_HERE, "liboracle.so")
 
 DT = {"f32": 0, "bf16": 1, "f16": 2}
 _NP = {"f32": np.float32, "bf16": np.uint16, "f16": np.uint16}
