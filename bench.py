@@ -57,6 +57,7 @@ SOURCES_HASHED = {
     "transformer": ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
                     "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
 }
+SOURCES_HASHED["cnn"] = SOURCES_HASHED["resnet"]
 
 
 def kernel_source_hash(workload: str) -> str:
@@ -117,9 +118,13 @@ def main():
                     help="time the main configuration only (for counter and trace runs of its kernels)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run 5 device copies of 256 MiB (the reference for HBM byte counters)")
-    ap.add_argument("--workload", choices=["aqsgd", "lm", "resnet", "transformer"], default="aqsgd",
+    ap.add_argument("--workload", choices=["aqsgd", "lm", "resnet", "transformer", "cnn"], default="aqsgd",
                     help="aqsgd: the AQ-SGD boundary (default); lm: the large language model micro-batch stream; "
-                         "resnet / transformer: error feedback on a CNN / transformer boundary")
+                         "resnet / transformer: error feedback on a CNN / transformer boundary; cnn: the tiny CNN "
+                         "boundary, forward and backward")
+    ap.add_argument("--codec", default=None,
+                    help="resnet / transformer / cnn: time this codec alone (e.g. grad:1:10, ef21:1:10, efmix:1:10, "
+                         "reuse:1:10:ef, quant:4) instead of the workload's main codec and variants")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the boundary compressors run per device and this build has no "
@@ -170,6 +175,32 @@ def device_copy_gbps(dev, n_bytes=1 << 30, reps=5):
     gbps = 2 * n_bytes * reps / (a.elapsed_time(b) * 1e-3) / 1e9
     del src, dst
     return round(gbps, 1)
+
+
+def replay_timed(g):
+    """replay a captured graph once: (HIP-event ms on the launch stream, host
+    wall-clock ms), the device synchronized on both sides"""
+    import torch
+    st = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    a.record(st)
+    g.replay()
+    b.record(st)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b), (time.perf_counter() - t0) * 1e3
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 def check_errors(where):
@@ -274,11 +305,8 @@ def run_aqsgd(args, dev):
         return g
 
     def timed(g):
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        g.replay()
-        torch.cuda.synchronize()
-        return time.perf_counter() - t0
+        """seconds of one replay, from HIP events on the launch stream"""
+        return replay_timed(g)[0] * 1e-3
 
     # ---- per-kernel durations for the roofline: n_kr senders of distinct
     # micro-batches back to back (each with its own payload), then their n_kr
@@ -319,9 +347,10 @@ def run_aqsgd(args, dev):
     gw.replay()
     torch.cuda.synchronize()
     check("during the graph warm-up")
-    wall = timed(gs)
+    ev_ms, wall_ms = replay_timed(gs)
     check("in the timed region")
-    ms_per_step = wall * 1e3 / steps
+    ms_per_step = ev_ms / steps
+    wall_ms_per_step = wall_ms / steps
     # ---- a second AQ-SGD workload on the same buffers: TopK 30 % of each
     # 768-element token row (k = 231), one buffer row per token row; the
     # micro-batches already used serve again (the kernels' cost does not
@@ -420,10 +449,24 @@ def run_aqsgd(args, dev):
             oracle.aqsgd_recv(oi, ov, rows_r, "f16", local, k)
             spent += time.perf_counter() - t1
             done += 1
+        # the same sample's first micro-batches again on one thread
+        done1, spent1 = 0, 0.0
+        while done1 < done and (spent1 < args.cpu_seconds / 3 or done1 < 1):
+            rows = raw16(cpu_rows[done1]).copy()
+            rows_r = rows.copy()
+            a_np = raw16(acts[done1].cpu())
+            t1 = time.perf_counter()
+            oi, ov = oracle.aqsgd_send(a_np, rows, "f16", local, k, threads=1)
+            oracle.aqsgd_recv(oi, ov, rows_r, "f16", local, k)
+            spent1 += time.perf_counter() - t1
+            done1 += 1
         cpu = {"value": round(boundary_bytes * done / spent / 1e9, 4), "unit": "GB/s", "cores": cores,
                "kind": "oracle",
                "sample": f"{done} micro-batches of the same workload (8 examples x 512x768 fp16, TopK 30%), "
-                         f"sender + receiver, {spent:.1f} s on {platform.processor() or platform.machine()}"}
+                         f"sender + receiver, {spent:.1f} s on {cores} threads",
+               "single_thread": {"value": round(boundary_bytes * done1 / spent1 / 1e9, 4), "unit": "GB/s",
+                                 "sample": f"the first {done1} of those micro-batches, {spent1:.1f} s on one thread"},
+               "cpu_model": cpu_model()}
 
     out = {
         "metric": "boundary-tensor GB/s through compress+decompress+EF; % of HBM peak",
@@ -452,6 +495,7 @@ def run_aqsgd(args, dev):
         "algorithmic_bytes_per_step": b_alg,
         "kernels_ms": {"aqsgd_send": round(send_ms, 5), "aqsgd_recv": round(recv_ms, 5)},
         "eager_ms_per_step": round(eager_ms, 5),
+        "wall_ms_per_step": round(wall_ms_per_step, 5),
         "variants": {} if rows_ms is None else {
             "per token row: TopK 30 % of each 768-element row (k = 231), one buffer row per token row": {
                 "ms_per_step": round(rows_ms, 5),
@@ -486,11 +530,30 @@ EF_WORKLOADS = {
     # Q4 + EF, the backward gradient (1e-4 N(0, 1)) with its own TopK 10 % +
     # EF, and the same gradient compressed at the activations' kept indices,
     # alone and with EF
+    # the tiny CNN boundary: post-ReLU activations 32 x 256x8x8 fp32 forward
+    # and gradients 1e-3 * N(0, 1) backward, TopK 10 % + EF per sample on
+    # both; one step = both directions, sender and receiver of each
+    "cnn": dict(desc="tiny CNN boundary: 32 x 256x8x8 fp32 post-ReLU activations and 1e-3 N(0, 1) gradients, "
+                     "per-sample segments", shape=(32, 256, 8, 8), n_seg=32, gen="relu", dtype="f32",
+                grad_sigma=1e-3, main=("fwdbwd", 1, 10), variants=[]),
     "transformer": dict(desc="GPT-2-small boundary: 8 x 512 x 768 bf16 hidden states with 4 outlier channels x20, "
                              "per-token-row segments", shape=(8, 512, 768), n_seg=8 * 512, gen="hidden",
                         dtype="bf16", grad_sigma=1e-4, main=("topk", 1, 10),
                         variants=[("quant", 4), ("grad", 1, 10), ("reuse", 1, 10, False), ("reuse", 1, 10, True)]),
 }
+
+
+def parse_codec(spec: str):
+    """--codec text -> a variant tuple: topk:1:10, quant:4, grad:1:10, ef21:1:10,
+    efmix:1:10, reuse:1:10 (reuse:1:10:ef with error feedback), fwdbwd:1:10"""
+    f = spec.split(":")
+    if f[0] == "quant" and len(f) == 2:
+        return ("quant", int(f[1]))
+    if f[0] == "reuse" and len(f) in (3, 4):
+        return ("reuse", int(f[1]), int(f[2]), len(f) == 4 and f[3] == "ef")
+    if f[0] in ("topk", "grad", "ef21", "efmix", "fwdbwd") and len(f) == 3:
+        return (f[0], int(f[1]), int(f[2]))
+    raise SystemExit(f"unknown --codec {spec!r}")
 
 
 def run_ef(args, dev, name):
@@ -524,6 +587,31 @@ def run_ef(args, dev, name):
 
     def make(codec):
         """(send(i), recv(), bytes sent, bytes received) for one codec"""
+        if codec[0] == "fwdbwd":
+            # forward: activations, TopK + EF; backward: gradients, TopK + EF,
+            # each direction with its own residual
+            k = tc.topk_count(L, codec[1], codec[2])
+            sigma = cfg["grad_sigma"]
+            gs = [W.normal_gradient((n_seg, L), sigma, args.seed, 2000 + i, device=dev).to(tdt)
+                  for i in range(n_sets)]
+            egs = [torch.zeros((n_seg, L), dtype=torch.float32, device=dev) for _ in range(n_sets)]
+            pls = [tc.empty_topk_payload(n_seg, L, k, tdt, dev) for _ in range(2)]
+            ys = [y, torch.empty_like(y)]
+            c = tc.codec(tc.TC_TOPK, n_seg, L, k, wire=tc._dt(xs[0]))
+            ws = tc.workspace(c, dev)
+            payload = n_seg * (k * (4 + esz) + 4 * (tc.n_blocks(L) + 1))
+
+            def send(i):
+                tc.ef_step_topk(xs[i % n_sets], es[i % n_sets], k, n_seg, ws=ws, out=pls[0])
+                tc.ef_step_topk(gs[i % n_sets], egs[i % n_sets], k, n_seg, ws=ws, out=pls[1])
+
+            def recv():
+                tc.topk_decompress(pls[0], L, out=ys[0])
+                tc.topk_decompress(pls[1], L, out=ys[1])
+            label = f"forward and backward, TopK {100 * codec[1] // codec[2]} % + EF each"
+            send_bytes = 2 * (esz * N + 8 * N + payload)
+            recv_bytes = 2 * (payload + esz * N)
+            return send, recv, send_bytes, recv_bytes, label
         if codec[0] == "topk":
             k = tc.topk_count(L, codec[1], codec[2])
             pl = tc.empty_topk_payload(n_seg, L, k, tdt, dev)
@@ -628,6 +716,8 @@ def run_ef(args, dev, name):
         recv_bytes = payload + esz * N                   # read payload, write the dense tensor
         return send, recv, send_bytes, recv_bytes, label
 
+    wall_ms = {}
+
     def measure(codec, n_steps, with_events):
         send, recv, sb, rb, label = make(codec)
         st = torch.cuda.current_stream(dev)
@@ -652,45 +742,66 @@ def run_ef(args, dev, name):
                 send(i); recv()
         g.replay()   # warm-up replay
         torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        g.replay()
-        torch.cuda.synchronize()
-        ms = (time.perf_counter() - t0) * 1e3 / n_steps
+        ev_total, wall_total = replay_timed(g)
         check_errors(f"in the timed region ({label})")
-        return ms, ev_ms, sb, rb, label
+        wall_ms[label] = wall_total / n_steps
+        return ev_total / n_steps, ev_ms, sb, rb, label
 
-    ms_per_step, (send_ms, recv_ms), sb, rb, label = measure(cfg["main"], steps, True)
+    main_codec, var_codecs = cfg["main"], cfg["variants"]
+    if args.codec:
+        main_codec, var_codecs = parse_codec(args.codec), []
+    ms_per_step, (send_ms, recv_ms), sb, rb, label = measure(main_codec, steps, True)
     variants = {}
-    for v in ([] if args.no_variants else cfg["variants"]):
+    for v in ([] if args.no_variants else var_codecs):
         vms, vev, vsb, vrb, vlabel = measure(v, max(10, steps // 4), True)
         variants[vlabel] = {"ms_per_step": round(vms, 5), "boundary_GBps": round(esz * N / (vms * 1e-3) / 1e9, 2),
                             "pct_hbm_peak": round(100 * (vsb + vrb) / (vms * 1e-3) / (HBM_PEAK_GBPS * 1e9), 3),
                             "send_ms": round(vev[0], 5), "recv_ms": round(vev[1], 5)}
-    boundary = esz * N
+    both = main_codec[0] == "fwdbwd"            # a step carries both directions' tensors
+    boundary = esz * N * (2 if both else 1)
     value = boundary / (ms_per_step * 1e-3) / 1e9
     dominant = "send" if send_ms >= recv_ms else "recv"
     dom_bytes, dom_ms = (sb, send_ms) if dominant == "send" else (rb, recv_ms)
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    kname = f"{name}_ef_{dominant}"
+    tag = args.codec.replace(":", "_") if args.codec else "ef"
+    kname = f"{name}_{tag}_{dominant}"
 
+    # ---- CPU baseline: the oracle on the main codec (TopK + EF) of the same
+    # tensors, on all host threads, then on one
     cpu = None
-    if not args.no_cpu:
+    if not args.no_cpu and main_codec[0] in ("topk", "fwdbwd"):
         import oracle
         cores = cpu_cores()
-        k = tc.topk_count(L, cfg["main"][1], cfg["main"][2])
-        xr = xs[0].cpu()
-        xr = xr.numpy() if tdt == torch.float32 else xr.view(torch.int16).numpy().view(np.uint16)
-        e_np = np.zeros((n_seg, L), np.float32)
-        t1 = time.perf_counter()
-        done = 0
-        while done < 1 or (time.perf_counter() - t1 < args.cpu_seconds and done < 50):
-            oi, ov, e_np = oracle.ef_topk(xr, cfg["dtype"], e_np, n_seg, L, k, threads=cores)
-            oracle.topk_decompress(oi, ov, cfg["dtype"], n_seg, L, k)
-            done += 1
-        spent = time.perf_counter() - t1
+        k = tc.topk_count(L, main_codec[1], main_codec[2])
+
+        def host(t):
+            t = t.cpu()
+            return t.numpy() if tdt == torch.float32 else t.view(torch.int16).numpy().view(np.uint16)
+        tensors = [host(xs[0])]
+        if both:
+            tensors.append(host(W.normal_gradient((n_seg, L), cfg["grad_sigma"], args.seed, 2000,
+                                                  device=dev).to(tdt)))
+
+        def sample(threads, budget, cap):
+            res = [np.zeros((n_seg, L), np.float32) for _ in tensors]
+            t1 = time.perf_counter()
+            done = 0
+            while done < 1 or (time.perf_counter() - t1 < budget and done < cap):
+                for i, xr in enumerate(tensors):
+                    oi, ov, res[i] = oracle.ef_topk(xr, cfg["dtype"], res[i], n_seg, L, k, threads=threads)
+                    oracle.topk_decompress(oi, ov, cfg["dtype"], n_seg, L, k)
+                done += 1
+            return done, time.perf_counter() - t1
+        done, spent = sample(cores, args.cpu_seconds, 100000)
+        done1, spent1 = sample(1, args.cpu_seconds / 3, done)
+        what = "forward and backward tensors" if both else "tensors"
         cpu = {"value": round(boundary * done / spent / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
-               "sample": f"{done} tensors of the same workload ({label}), sender + receiver, {spent:.1f} s on "
-                         f"{platform.processor() or platform.machine()}"}
+               "sample": f"{done} steps of the same workload ({what} of the first rotating set, "
+                         f"TopK {100 * main_codec[1] // main_codec[2]} % + EF), sender + receiver, {spent:.1f} s "
+                         f"on {cores} threads",
+               "single_thread": {"value": round(boundary * done1 / spent1 / 1e9, 4), "unit": "GB/s",
+                                 "sample": f"{done1} such steps, {spent1:.1f} s on one thread"},
+               "cpu_model": cpu_model()}
     return {
         "metric": "boundary-tensor GB/s through compress+decompress+EF; % of HBM peak",
         "value": round(value, 3),
@@ -711,6 +822,7 @@ def run_ef(args, dev, name):
         "effective_GBps": round((sb + rb) / (ms_per_step * 1e-3) / 1e9, 2),
         "algorithmic_bytes_per_step": sb + rb,
         "kernels_ms": {"send": round(send_ms, 5), "recv": round(recv_ms, 5)},
+        "wall_ms_per_step": round(wall_ms[label], 5),
         "variants": variants,
         "device_copy_GBps": device_copy_gbps(dev),
         "roofline": {"bound": "hbm", "kernel": kname, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
@@ -795,13 +907,22 @@ def run_lm(args, dev):
     recv_ms = float(np.mean([a[2].elapsed_time(a[3]) for a in ev]))
 
     # ---- timed region: K micro-batches, compress(j+1) || decompress(j)
+    cur = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    e0.record(cur)
+    sA.wait_stream(cur)
+    sB.wait_stream(cur)
     stream_steps(j, steps); j += steps
+    cur.wait_stream(sA)
+    cur.wait_stream(sB)
+    e1.record(cur)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     check_errors("in the timed region")
-    ms_per_step = wall * 1e3 / steps
+    ms_per_step = e0.elapsed_time(e1) / steps
+    wall_ms_per_step = wall * 1e3 / steps
 
     N = L
     boundary_bytes = 2 * N
@@ -831,6 +952,7 @@ def run_lm(args, dev):
             done += 1
         spent = time.perf_counter() - t1
         cpu = {"value": round(2 * n_s * done / spent / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "cpu_model": cpu_model(),
                "sample": f"{done} x one eighth of a micro-batch (2^24 bf16, TopK 10 %, 4-bit kept list, EF), "
                          f"sender + receiver, {spent:.1f} s on {platform.processor() or platform.machine()}; "
                          f"one segment, so the oracle runs on one thread"}
@@ -856,7 +978,9 @@ def run_lm(args, dev):
             "seg_len": L,
             "k": k,
             "bits": bits,
+            "timed_region": "K micro-batches eager on two streams, HIP events on a stream that both join",
         },
+        "wall_ms_per_step": round(wall_ms_per_step, 5),
         "pct_hbm_peak": round(100.0 * b_alg / (ms_per_step * 1e-3) / (HBM_PEAK_GBPS * 1e9), 3),
         "effective_GBps": round(b_alg / (ms_per_step * 1e-3) / 1e9, 2),
         "algorithmic_bytes_per_step": b_alg,
