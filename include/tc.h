@@ -167,6 +167,14 @@ const char* tc_last_error(void);
  * sticky TC_KERR_* bits of the kernels run on it. */
 tc_status tc_device_errors(uint32_t* bits, int clear);
 
+/* For tests of the recovery path: synchronizes the current device and ORs
+ * `bits` (TC_KERR_* only, else TC_ERR_ARG) into its sticky bits, as a kernel
+ * would.  With TC_KERR_TIMEOUT set, every later cross-workgroup wait gives up
+ * after about a thousand polls instead of its full bound (a wait its group
+ * satisfies sooner completes as usual); results are invalid until the bit is
+ * cleared and the workspaces are zero-filled again, as after a real timeout. */
+tc_status tc_raise_device_errors(uint32_t bits);
+
 /* ------------------------------------------------------------------ TopK */
 
 /* Sec. 2.3 sender: per segment, the k entries of x with the largest |x|; ties

@@ -380,6 +380,18 @@ TC_API tc_status tc_device_errors(uint32_t* bits, int clear) {
   return TC_OK;
 }
 
+TC_API tc_status tc_raise_device_errors(uint32_t bits) {
+  if (bits & ~(uint32_t)(TC_KERR_TIMEOUT | TC_KERR_BAD_ID | TC_KERR_BAD_INDEX | TC_KERR_INTERNAL))
+    return fail(TC_ERR_ARG, "bits %#x: unknown kernel error bits", bits);
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  if ((e = tc::errors_topk_raise(bits)) != hipSuccess) return hip_fail(e, "error word (topk)");
+  if ((e = tc::errors_quant_raise(bits)) != hipSuccess) return hip_fail(e, "error word (quant)");
+  if ((e = tc::errors_scatter_raise(bits)) != hipSuccess) return hip_fail(e, "error word (scatter)");
+  if ((e = tc::errors_global_raise(bits)) != hipSuccess) return hip_fail(e, "error word (global)");
+  return TC_OK;
+}
+
 TC_API tc_status tc_topk_compress(const tc_codec* c, const void* x, int dt, const tc_payload* out, void* ws,
                                   size_t ws_bytes, void* stream) {
   tc_status s = check_codec(c, 1 << TC_TOPK);

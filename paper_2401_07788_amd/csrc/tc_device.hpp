@@ -438,6 +438,16 @@ __device__ __forceinline__ uint64_t ld_agent64(const uint64_t* p) {
                              hipMemcpyHostToDevice);                                        \
     }                                                                                       \
     return st;                                                                              \
+  }                                                                                         \
+  /* ORs bits into the word from the host (device idle: the caller synchronizes) */         \
+  hipError_t fn##_raise(uint32_t bits) {                                                    \
+    uint32_t v = 0;                                                                         \
+    hipError_t st = hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_kernel_errors), sizeof(v), 0,      \
+                                        hipMemcpyDeviceToHost);                             \
+    if (st != hipSuccess) return st;                                                        \
+    v |= bits;                                                                              \
+    return hipMemcpyToSymbol(HIP_SYMBOL(g_kernel_errors), &v, sizeof(v), 0,                 \
+                             hipMemcpyHostToDevice);                                        \
   }
 
 }  // namespace tc

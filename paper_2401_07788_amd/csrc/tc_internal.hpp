@@ -159,6 +159,11 @@ hipError_t errors_topk(uint32_t* bits, bool clear);
 hipError_t errors_quant(uint32_t* bits, bool clear);
 hipError_t errors_scatter(uint32_t* bits, bool clear);
 hipError_t errors_global(uint32_t* bits, bool clear);
+// the same words set from the host (tests of the recovery path)
+hipError_t errors_topk_raise(uint32_t bits);
+hipError_t errors_quant_raise(uint32_t bits);
+hipError_t errors_scatter_raise(uint32_t bits);
+hipError_t errors_global_raise(uint32_t bits);
 
 // device properties (cached per device)
 int device_cus();

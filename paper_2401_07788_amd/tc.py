@@ -95,6 +95,7 @@ EXPORTS = {
                                        C.c_void_p]),
     "tc_aqsgd_step": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.c_void_p, C.c_uint64, C.c_void_p,
                                 C.c_uint32, C.POINTER(Payload), C.c_void_p, C.c_size_t, C.c_void_p]),
+    "tc_raise_device_errors": (C.c_int, [C.c_uint32]),
     "tc_aqsgd_step_noalloc": (C.c_int, [C.POINTER(Codec), C.c_void_p, C.c_int, C.c_void_p, C.c_uint64,
                                         C.c_void_p, C.c_uint32, C.POINTER(Payload), C.c_void_p]),
     "tc_aqsgd_reconstruct": (C.c_int, [C.POINTER(Codec), C.POINTER(Payload), C.c_void_p, C.c_int, C.c_uint64,
@@ -247,6 +248,12 @@ def device_errors(clear: bool = True) -> int:
             ws.zero_()
         torch.cuda.synchronize()
     return int(bits.value)
+
+
+def raise_device_errors(bits: int) -> None:
+    """set sticky TC_KERR_* bits on the current device from the host, as a
+    kernel would (tests of the recovery path)"""
+    _check(lib().tc_raise_device_errors(int(bits)), "tc_raise_device_errors")
 
 
 def _ws_args(c, device, ws):

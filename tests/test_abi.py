@@ -127,3 +127,9 @@ def test_noalloc_refuses_shapes_beyond_its_scratch(tcmod):
     assert R.tc_aqsgd_step_noalloc(C.byref(c), a, 2, m, 0, ids, n_ids, C.byref(p), None) == 2
     assert R.tc_aqsgd_step_noalloc(None, a, 2, m, 1000, ids, n_ids, C.byref(p), None) == 1
     assert tcmod.NOALLOC_SCRATCH_BYTES == 4 << 20
+
+
+def test_raise_device_errors_checks_bits_first(tcmod):
+    R = tcmod.load(tcmod.LIB_PATH)
+    assert R.tc_raise_device_errors(0x10) == tcmod.TC_ERR_ARG
+    assert b"unknown" in R.tc_last_error()
