@@ -840,11 +840,18 @@ __global__ __launch_bounds__(G_NT) void k_g_emit(GlobalArgs a) {
     scale = __uint_as_float(st[ST_SCALE]);
   }
   float kmin = __builtin_inff(), kmax = -__builtin_inff();
+  // Tiles from the last to the first: the band pass read them first to
+  // last, so the last 256 MB it read are still in the on-package cache when
+  // this pass starts (and the next micro-batch's band pass, which reads the
+  // residual written here, starts where this pass ends).  Each tile's
+  // payload offset comes from tcount, so the order is free.
+  auto rev = [&](uint64_t i) { return a.n_tiles - 1 - i; };
   const bool pf = tiles_prefetchable(a);
   TileRaw<InT, EF> nxt;
-  bool have = pf && tile_whole(a, blockIdx.x);
-  if (have) tile_fetch<InT, EF>(a, blockIdx.x, nxt);
-  for (uint64_t tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
+  bool have = pf && tile_whole(a, rev(blockIdx.x));
+  if (have) tile_fetch<InT, EF>(a, rev(blockIdx.x), nxt);
+  for (uint64_t it = blockIdx.x; it < a.n_tiles; it += gridDim.x) {
+    const uint64_t tile = rev(it);
     // the tile's offset (from tcount), loaded together with its data
     uint32_t gt_before = 0, eq_before = 0, rec_gt = 0, rec_eq = 0;
     if (!none) {
@@ -862,8 +869,8 @@ __global__ __launch_bounds__(G_NT) void k_g_emit(GlobalArgs a) {
     float v[G_VPT];
     if (have) tile_values<InT, EF>(nxt, v);
     else load_tile_values<InT, EF>(a, t0, nv, v);
-    have = pf && tile_whole(a, tile + gridDim.x);
-    if (have) tile_fetch<InT, EF>(a, tile + gridDim.x, nxt);
+    have = pf && it + gridDim.x < a.n_tiles && tile_whole(a, rev(it + gridDim.x));
+    if (have) tile_fetch<InT, EF>(a, rev(it + gridDim.x), nxt);
     // ---- (1) keys > T and == T as bit masks (bit i: element i); keys
     // and T stay below 2^31, so the sign bit of a difference compares them
     uint32_t gm = 0, em = 0;
