@@ -515,31 +515,36 @@ def run_aqsgd(args, dev):
 
 
 EF_WORKLOADS = {
-    # ResNet-18 boundary: post-ReLU activations 128 x 128x16x16 fp32, one
-    # segment / group per sample; TopK 10 % + EF, variants TopK 30 %, Q2/4/8 + EF,
-    # the backward direction (gradients 1e-3 * N(0, 1), TopK 10 % + EF),
-    # EF21 + TopK 10 % (one fp32 buffer row per sample on each side) and
-    # EF-mixed TopK 10 % (half of the budget on x, half on the fp32 buffer)
-    "resnet": dict(desc="ResNet-18 boundary: 128 x 128x16x16 fp32 post-ReLU activations, per-sample segments",
+    # ResNet-18 boundary: post-ReLU activations 128 x 128x16x16 fp32 forward
+    # and gradients 1e-3 * N(0, 1) backward, one segment / group per sample;
+    # a step is both directions, TopK 10 % + EF each; variants the forward
+    # direction alone with TopK 10 % and 30 %, Q2/4/8 + EF, the backward
+    # direction alone, EF21 + TopK 10 % (one fp32 buffer row per sample on
+    # each side) and EF-mixed TopK 10 % (half of the budget on x, half on the
+    # fp32 buffer)
+    "resnet": dict(desc="ResNet-18 boundary: 128 x 128x16x16 fp32 post-ReLU activations and 1e-3 N(0, 1) "
+                        "gradients, per-sample segments",
                    shape=(128, 128, 16, 16), n_seg=128, gen="relu", dtype="f32", grad_sigma=1e-3,
-                   main=("topk", 1, 10),
-                   variants=[("topk", 3, 10), ("quant", 2), ("quant", 4), ("quant", 8), ("grad", 1, 10),
-                             ("ef21", 1, 10), ("efmix", 1, 10)]),
-    # transformer boundary: bf16 hidden states 8 x 512 x 768 with outlier
-    # channels, one segment / group per token row; TopK 10 % + EF, variants
-    # Q4 + EF, the backward gradient (1e-4 N(0, 1)) with its own TopK 10 % +
-    # EF, and the same gradient compressed at the activations' kept indices,
-    # alone and with EF
+                   main=("fwdbwd", 1, 10),
+                   variants=[("topk", 1, 10), ("topk", 3, 10), ("quant", 2), ("quant", 4), ("quant", 8),
+                             ("grad", 1, 10), ("ef21", 1, 10), ("efmix", 1, 10)]),
     # the tiny CNN boundary: post-ReLU activations 32 x 256x8x8 fp32 forward
     # and gradients 1e-3 * N(0, 1) backward, TopK 10 % + EF per sample on
     # both; one step = both directions, sender and receiver of each
     "cnn": dict(desc="tiny CNN boundary: 32 x 256x8x8 fp32 post-ReLU activations and 1e-3 N(0, 1) gradients, "
                      "per-sample segments", shape=(32, 256, 8, 8), n_seg=32, gen="relu", dtype="f32",
                 grad_sigma=1e-3, main=("fwdbwd", 1, 10), variants=[]),
-    "transformer": dict(desc="GPT-2-small boundary: 8 x 512 x 768 bf16 hidden states with 4 outlier channels x20, "
-                             "per-token-row segments", shape=(8, 512, 768), n_seg=8 * 512, gen="hidden",
-                        dtype="bf16", grad_sigma=1e-4, main=("topk", 1, 10),
-                        variants=[("quant", 4), ("grad", 1, 10), ("reuse", 1, 10, False), ("reuse", 1, 10, True)]),
+    # transformer boundary: bf16 hidden states 8 x 512 x 768 with outlier
+    # channels forward and bf16 gradients 1e-4 N(0, 1) backward, one segment /
+    # group per token row; a step is both directions, TopK 10 % + EF each;
+    # variants the forward direction alone with TopK 10 % and with Q4 + EF,
+    # the backward direction alone, and the gradient compressed at the
+    # activations' kept indices, alone and with EF
+    "transformer": dict(desc="GPT-2-small boundary: 8 x 512 x 768 bf16 hidden states with 4 outlier channels x20 "
+                             "and bf16(1e-4 N(0, 1)) gradients, per-token-row segments", shape=(8, 512, 768),
+                        n_seg=8 * 512, gen="hidden", dtype="bf16", grad_sigma=1e-4, main=("fwdbwd", 1, 10),
+                        variants=[("topk", 1, 10), ("quant", 4), ("grad", 1, 10), ("reuse", 1, 10, False),
+                                  ("reuse", 1, 10, True)]),
 }
 
 
@@ -607,8 +612,12 @@ def run_ef(args, dev, name):
             side = torch.cuda.Stream(dev)
             ws_side = {}
 
+            # kernels that wait for each other across workgroups (a workspace)
+            # must not share the device with another launch: those run in turn
+            may_overlap = ws is None
+
             def both(f_fwd, f_bwd, fork, join):
-                if not mode["concurrent"]:
+                if not (mode["concurrent"] and may_overlap):
                     f_fwd(ws)
                     f_bwd(ws)
                     return
@@ -635,7 +644,7 @@ def run_ef(args, dev, name):
                      lambda w: tc.topk_decompress(pls[1], L, out=ys[1]),
                      False, True)
             label = f"forward and backward, TopK {100 * codec[1] // codec[2]} % + EF each"
-            concurrent_dirs[0] = True
+            concurrent_dirs[0] = may_overlap
             send_bytes = 2 * (esz * N + 8 * N + payload)
             recv_bytes = 2 * (payload + esz * N)
             return send, recv, send_bytes, recv_bytes, label
