@@ -863,46 +863,60 @@ __device__ __forceinline__ void lds_pass_list(const uint32_t* s_list, uint32_t n
 // the first digit's bin go to a short list for the last two passes (else
 // those passes read the whole segment, which the two selections of EF-mixed
 // find faster).
+// hist_ready: s_h already holds the first digit's counts of every key (the
+// load loop counted them as the values arrived); only the search is left.
 template <int NT, bool LIST = true>
 __device__ __forceinline__ void lds_threshold(const uint32_t* s_v, uint32_t L, uint32_t k, uint32_t* s_h,
                                               uint32_t* s_list, uint32_t* scratch, uint32_t* found, uint32_t& T,
-                                              uint32_t& r) {
+                                              uint32_t& r, bool hist_ready = false) {
   const uint32_t t = threadIdx.x;
   T = 0x7FFFFFFFu;
   r = 0u;
   if (k > 0) {
     uint32_t need = k, d1, d2, d3;
-    lds_pass<NT, 4096>(s_v, L, 19, 0u, s_h, scratch, found, need, d1);
+    if (hist_ready) {
+      find_bin<NT, 4096>(s_h, need, scratch, found);
+      d1 = found[0];
+      need -= found[1];
+      __syncthreads();
+    } else {
+      lds_pass<NT, 4096>(s_v, L, 19, 0u, s_h, scratch, found, need, d1);
+    }
     uint32_t nl = LDS_LIST + 1u;
     if constexpr (LIST) {
-      // the keys of bin d1 into a short list (wavefront-aggregated appends),
-      // so that the last two passes read only them; a bin holding more
-      // than the list takes the passes over the whole segment
+      // the keys of bin d1 into a short list, so that the last two passes
+      // read only them (a bin holding more than the list takes the passes
+      // over the whole segment): each thread marks its matches in one mask
+      // (bit 4j + c: element c of its piece j), one wavefront scan and one
+      // append per wavefront place them, and the few matches are read again
       if (t == 0) found[0] = 0u;
       __syncthreads();
-      // (every lane runs every iteration: the scans below need whole wavefronts)
+      uint32_t mask = 0;
+#pragma unroll
       for (uint32_t j = 0; j < LDS_PIECES; ++j) {
         const uint32_t q = j * NT + t;
+        if (q * 4 >= L) continue;
         const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[q * 4]);
         uint32_t in = 0;
 #pragma unroll
         for (int c = 0; c < 4; ++c) in |= ((((w[c] & 0x7FFFFFFFu) >> 19) == d1) ? 1u : 0u) << c;
-        if (q * 4 >= L) in = 0u;
-        else if (q * 4 + 4 > L) in &= (1u << (L - q * 4)) - 1u;
-        const uint32_t n = (uint32_t)__builtin_popcount(in);
-        const uint32_t incl = wave_incl_scan(n);
-        const uint32_t tot_w = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1);
-        uint32_t base = 0;
-        if (tot_w) {
-          if (lane_id() == 0) base = atomicAdd(&found[0], tot_w);
-          base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
-        }
-        uint32_t o = base + incl - n;
-        for (uint32_t m = in; m; m &= m - 1u) {
-          const uint32_t c = (uint32_t)__builtin_ctz(m);
-          if (o < LDS_LIST) s_list[o] = w[c] & 0x7FFFFFFFu;
-          ++o;
-        }
+        if (q * 4 + 4 > L) in &= (1u << (L - q * 4)) - 1u;
+        mask |= in << (4 * j);
+      }
+      const uint32_t n = (uint32_t)__builtin_popcount(mask);
+      const uint32_t incl = wave_incl_scan(n);
+      const uint32_t tot_w = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1);
+      uint32_t base = 0;
+      if (tot_w) {
+        if (lane_id() == 0) base = atomicAdd(&found[0], tot_w);
+        base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
+      }
+      uint32_t o = base + incl - n;
+      for (uint32_t m = mask; m; m &= m - 1u) {
+        const uint32_t bit = (uint32_t)__builtin_ctz(m);
+        const uint32_t i = ((bit >> 2) * NT + t) * 4 + (bit & 3u);
+        if (o < LDS_LIST) s_list[o] = s_v[i] & 0x7FFFFFFFu;
+        ++o;
       }
       __syncthreads();
       nl = found[0];
@@ -987,7 +1001,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
   using Raw = typename Elem<InT>::raw;
   constexpr int NT = LDS_NT;
   __shared__ __attribute__((aligned(16))) uint32_t s_v[LDS_MAX];   // the segment's values (binary32 bits)
-  __shared__ uint32_t s_h[HIST_BINS];
+  __shared__ uint32_t s_h[HIST_BINS + WAVE];   // histograms (the last WAVE words: per-lane dummies)
   __shared__ uint32_t s_list[LDS_LIST];   // keys of the first pass's bin
   __shared__ uint32_t scratch[NT / WAVE + 2];
   __shared__ uint32_t found[2];
@@ -1008,7 +1022,20 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
       ms = (Raw*)a.m + (uint64_t)id * a.L;
     }
     // ---- values into LDS: piece q = 4 elements, lanes consecutive; loads
-    // go out four pieces at a time (the registers of 1024 threads)
+    // go out four pieces at a time (the registers of 1024 threads).  The
+    // first digit pass (key bits 30..19) is counted here, from registers, as
+    // the values arrive; exact zeros are counted apart and added once per
+    // wavefront (padding past the segment's end is not counted)
+    for (uint32_t b = t; b < (uint32_t)HIST_BINS; b += NT) s_h[b] = 0u;
+    __syncthreads();
+    const uint32_t dummy = HIST_BINS + (uint32_t)lane_id();
+    uint32_t zc = 0;
+    auto count = [&](uint32_t bits) {
+      const uint32_t kk = bits & 0x7FFFFFFFu;
+      const uint32_t z = eq31(kk, 0u);
+      zc += z;
+      atomicAdd(&s_h[pick(z, dummy, kk >> 19)], 1u);
+    };
     if (vec) {
 #pragma unroll
       for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
@@ -1035,6 +1062,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
               if constexpr (SEL == SEL_EF) x = x + er[j][c];
               if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(mr[j][c]);
               w[c] = __float_as_uint(x);
+              count(w[c]);
             }
             *reinterpret_cast<u32x4*>(&s_v[i0]) = w;
           }
@@ -1053,17 +1081,22 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
             x = Elem<InT>::up(xs[i]);
             if constexpr (SEL == SEL_EF) x = x + es[i];
             if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(ms[i]);
+            count(__float_as_uint(x));
           }
           w[c] = __float_as_uint(x);
         }
         *reinterpret_cast<u32x4*>(&s_v[i0]) = w;
       }
     }
+    {
+      const uint32_t zs = wave_sum(zc);
+      if (lane_id() == 0 && zs) atomicAdd(&s_h[0], zs);
+    }
     __syncthreads();
 
     // ---- T and the tie quota r, then the kept entries of thread t's run
     uint32_t T, r;
-    lds_threshold<NT, SEL != SEL_EFMIX>(s_v, L, (uint32_t)a.k, s_h, s_list, scratch, found, T, r);
+    lds_threshold<NT, SEL != SEL_EFMIX>(s_v, L, (uint32_t)a.k, s_h, s_list, scratch, found, T, r, true);
     const uint32_t b0 = t * LDS_RUN;
     const uint32_t nr = (b0 < L) ? min(LDS_RUN, L - b0) : 0u;
     const uint32_t km = lds_place<InT, NT>(s_v, L, b0, nr, T, r, (uint32_t)a.k, a.idx + seg * a.k,
