@@ -123,9 +123,10 @@ __device__ __forceinline__ void zero_lds(uint32_t* h, int n) {
 
 // Exact threshold for a segment held entirely by one wavefront (NT == 64):
 // radix select over 8-bit digits of the key from bit 23 down, then its last
-// 7 bits, with one 256-bin histogram in LDS private to the wavefront (`hist`,
-// 16-byte aligned); each digit is found with one wavefront scan (lane l owns
-// bins 4l..4l+3).
+// 7 bits, with 256-bin histograms in LDS private to the wavefront (`hist`,
+// 16-byte aligned, RADIX_CP * 256 words); each digit is found with one
+// wavefront scan (lane l owns bins 4l..4l+3).
+constexpr int RADIX_CP = 4;
 template <int VPT>
 __device__ __forceinline__ SelResult wave_radix_select(const uint32_t (&key)[VPT], int nv, uint32_t k,
                                                        uint32_t* hist) {
@@ -135,13 +136,28 @@ __device__ __forceinline__ SelResult wave_radix_select(const uint32_t (&key)[VPT
   for (int pass = 0; pass < 4; ++pass) {
     const uint32_t width = (pass < 3) ? 8u : 7u;
     const uint32_t shift = 31u - pbits - width;
-    reinterpret_cast<u32x4*>(hist)[lane] = u32x4{0u, 0u, 0u, 0u};
+    // the first digit (the exponent) takes few values, so the lanes count in
+    // RADIX_CP copies (lane mod RADIX_CP) and meet at most a quarter as often
+    // on one word; the later digits are spread out and use one copy
+    constexpr int CP = RADIX_CP;
+#pragma unroll
+    for (int c = 0; c < (pass == 0 ? CP : 1); ++c)
+      reinterpret_cast<u32x4*>(hist)[c * (256 / 4) + lane] = u32x4{0u, 0u, 0u, 0u};
     __syncthreads();
+    const uint32_t base = (pass == 0) ? (lane % CP) * 256u : 0u;
 #pragma unroll
     for (int i = 0; i < VPT; ++i)
-      if (i < nv && (key[i] >> (shift + width)) == prefix) atomicAdd(&hist[(key[i] >> shift) & ((1u << width) - 1u)], 1u);
+      if (i < nv && (key[i] >> (shift + width)) == prefix)
+        atomicAdd(&hist[base + ((key[i] >> shift) & ((1u << width) - 1u))], 1u);
     __syncthreads();
-    const u32x4 h = reinterpret_cast<const u32x4*>(hist)[lane];
+    u32x4 h = reinterpret_cast<const u32x4*>(hist)[lane];
+    if (pass == 0) {
+#pragma unroll
+      for (int c = 1; c < CP; ++c) {
+        const u32x4 hc = reinterpret_cast<const u32x4*>(hist)[c * (256 / 4) + lane];
+        h = h + hc;
+      }
+    }
     const uint32_t sum = h[0] + h[1] + h[2] + h[3];
     const uint32_t incl = wave_incl_scan(sum);
     uint32_t acc = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1) - incl;   // bins of higher lanes
