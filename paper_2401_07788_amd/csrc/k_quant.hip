@@ -195,6 +195,58 @@ __global__ __launch_bounds__(NT) void k_quant_unpack(UnpackArgs a) {
   }
 }
 
+// The same receiver in pieces of one 16-byte store each (4 binary32 or 8
+// 16-bit outputs), lanes consecutive, for the bit widths whose piece codes
+// fill whole bytes (b = 2, 4, 8, 32): every load and store instruction of a
+// wavefront then covers contiguous memory.  Needs G a multiple of the piece
+// and 16-byte aligned arrays (the launcher checks).  One piece per thread:
+// more pieces per thread in flight measured slower (fewer workgroups).
+template <int BYTES>
+__device__ __forceinline__ void load_piece_codes(const uint8_t* p, uint32_t (&w)[(BYTES + 3) / 4]) {
+  if constexpr (BYTES == 1) w[0] = *p;
+  else if constexpr (BYTES == 2) w[0] = *reinterpret_cast<const uint16_t*>(p);
+  else if constexpr (BYTES == 4) w[0] = *reinterpret_cast<const uint32_t*>(p);
+  else if constexpr (BYTES == 8) {
+    const u32x2 v = *reinterpret_cast<const u32x2*>(p);
+    w[0] = v[0]; w[1] = v[1];
+  } else {
+#pragma unroll
+    for (int h = 0; h < BYTES / 16; ++h) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(p + 16 * h);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[4 * h + i] = v[i];
+    }
+  }
+}
+
+template <typename OutT, int B, int NT>
+__global__ __launch_bounds__(NT) void k_quant_unpack_pc(UnpackArgs a) {
+  using R = typename Elem<OutT>::raw;
+  constexpr int PE = 16 / (int)sizeof(R);               // elements per piece
+  constexpr int CB = PE * B / 8;                        // code bytes per piece
+  const uint64_t ppg = a.G / PE;                        // pieces per group
+  const uint64_t n_pieces = a.n_grp * ppg;
+  for (uint64_t q = (uint64_t)blockIdx.x * NT + threadIdx.x; q < n_pieces; q += (uint64_t)gridDim.x * NT) {
+    const uint64_t grp = q / ppg, p = q - grp * ppg;
+    uint32_t c[(CB + 3) / 4];
+    load_piece_codes<CB>(reinterpret_cast<const uint8_t*>(a.codes + grp * a.wpg) + p * (uint64_t)CB, c);
+    R y[PE];
+    if constexpr (B == 32) {
+#pragma unroll
+      for (int i = 0; i < PE; ++i) y[i] = Elem<OutT>::down(__uint_as_float(c[i]));
+    } else {
+      const float lo = a.meta[2 * grp], scale = a.meta[2 * grp + 1];
+#pragma unroll
+      for (int i = 0; i < PE; ++i) {
+        const uint32_t code = (c[(i * B) / 32] >> ((i * B) % 32)) & ((1u << B) - 1u);
+        const float prod = (float)code * scale;
+        y[i] = Elem<OutT>::down(lo + prod);
+      }
+    }
+    store_run<R, PE, true>((R*)a.y + q * PE, y);
+  }
+}
+
 // ------------------------------------------------------------------ plans
 namespace {
 
@@ -280,7 +332,36 @@ hipError_t launch_quant(int dt, int out_dt, uint32_t bits, bool ef, const SegPla
   return hipLaunchKernel(fn, dim3(plan.grid), dim3(plan.nt), params, 0, st);
 }
 
+template <typename OutT>
+const void* unpack_pc_ptr(uint32_t b) {
+  switch (b) {
+    case 2: return (const void*)k_quant_unpack_pc<OutT, 2, 256>;
+    case 4: return (const void*)k_quant_unpack_pc<OutT, 4, 256>;
+    case 8: return (const void*)k_quant_unpack_pc<OutT, 8, 256>;
+    case 32: return (const void*)k_quant_unpack_pc<OutT, 32, 256>;
+  }
+  return nullptr;
+}
+
 hipError_t launch_unpack(int out_dt, uint32_t bits, const UnpackArgs& args, hipStream_t st) {
+  // whole 16-byte pieces: whole-byte codes, groups of whole pieces, aligned
+  // arrays, and every group's codes aligned to a piece's code load (up to 16
+  // bytes)
+  const uint64_t pe = 16 / dt_size(out_dt);
+  const uint64_t cb = pe * bits / 8;
+  const bool pieces = (bits == 2 || bits == 4 || bits == 8 || bits == 32) && (args.G % pe) == 0 &&
+                      (((uintptr_t)args.y | (uintptr_t)args.codes) & 15u) == 0 &&
+                      ((args.wpg * 4) % std::min<uint64_t>(cb, 16)) == 0;
+  if (pieces) {
+    const void* f = (out_dt == DT_F32) ? unpack_pc_ptr<float>(bits)
+                  : (out_dt == DT_BF16) ? unpack_pc_ptr<bf16_t>(bits) : unpack_pc_ptr<f16_t>(bits);
+    const uint64_t n_pieces = args.n_grp * (args.G / pe);
+    const uint64_t work = (n_pieces + 255) / 256;   // workgroups of 256 pieces
+    const uint64_t grid = std::max<uint64_t>(1, std::min<uint64_t>(work, (uint64_t)device_cus() * 16));
+    UnpackArgs a = args;
+    void* params[] = {&a};
+    return hipLaunchKernel(f, dim3((uint32_t)grid), dim3(256), params, 0, st);
+  }
   const void* fn = (out_dt == DT_F32) ? unpack_ptr<float>(bits)
                  : (out_dt == DT_BF16) ? unpack_ptr<bf16_t>(bits) : unpack_ptr<f16_t>(bits);
   if (!fn) return hipErrorInvalidValue;

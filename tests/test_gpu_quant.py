@@ -1,7 +1,9 @@
 """GPU parity: min-max quantization sender and receiver (Sec. 2.2) against the
 CPU oracle: packed code bytes and (lo, scale) bit for bit, reconstruction bit
 for bit, for every bit width 1..8 and 32, group lengths with ragged words and
-tails, groups spread over several workgroups, and constant groups."""
+tails, groups spread over several workgroups, and constant groups.  Both
+receiver forms run: 16-byte output pieces (b = 2, 4, 8, 32 and groups of
+whole pieces) and per-thread runs (everything else)."""
 import numpy as np
 import pytest
 import torch
@@ -35,8 +37,8 @@ def test_quant_parity_f32(tc, orc, b, G):
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f16"])
-@pytest.mark.parametrize("b", [2, 4, 6, 8])
-@pytest.mark.parametrize("G", [768, 32768])
+@pytest.mark.parametrize("b", [2, 4, 6, 8, 32])
+@pytest.mark.parametrize("G", [36, 768, 1000, 32768])
 def test_quant_parity_half(tc, orc, dt, b, G):
     n_grp = 4
     x = W.randn((n_grp, G), seed=3, tensor_id=b).to(TORCH[dt])
@@ -48,3 +50,12 @@ def test_quant_constant_and_relu_groups(tc, orc):
     x[1] = 2.5
     x[2] = -0.0
     run_case(tc, orc, x.contiguous(), 4, 32768, 4)
+
+
+@pytest.mark.parametrize("b", [2, 8])
+def test_quant_receiver_grid_stride(tc, orc, b):
+    # more 16-byte pieces than the receiver's grid holds threads: each thread
+    # takes several pieces
+    n_grp, G = 40, 131072
+    x = W.randn((n_grp, G), seed=9, tensor_id=b)
+    run_case(tc, orc, x, n_grp, G, b)
