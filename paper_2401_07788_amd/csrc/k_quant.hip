@@ -45,12 +45,23 @@ __device__ __forceinline__ void unpack_codes(const uint32_t (&w)[QVPT * B / 32],
   }
 }
 
+// Sender.  Loads, the residual and binary32 codes (b = 32) go in pieces of
+// QPE consecutive elements, lanes consecutive, so that every wavefront
+// instruction covers contiguous memory; piece j of thread t is element
+// (j * NT + t) * QPE of the workgroup's chunk.  Codes of b < 32 bits are
+// staged in LDS (one byte per element) and packed by thread t for chunk
+// elements [QVPT t, QVPT t + QVPT): QVPT b bits are a whole number of words
+// for every b.
+constexpr int QPE = 4;                 // elements per piece
+constexpr int QNP = QVPT / QPE;        // pieces per thread
+
 template <typename InT, typename OutT, int B, bool EF, int NT>
 __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
   using R = typename Elem<InT>::raw;
-  constexpr int WPT = (B == 32) ? QVPT : QVPT * B / 32;
+  constexpr int WPT = QVPT * B / 32;   // code words of one packing run (b < 32)
   constexpr uint64_t CH = (uint64_t)NT * QVPT;
   __shared__ float mm[2 * (NT / WAVE)];
+  __shared__ uint32_t s_codes[(B == 32) ? 1 : NT * QNP];   // 4 code bytes per word, one word per piece
 
   const uint32_t P = a.P;
   const uint32_t group = blockIdx.x / P, part = blockIdx.x % P;
@@ -61,38 +72,58 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
     bar = a.ws + (uint64_t)group * quant_group_mem_words(P);
     slots = bar + 64;
   }
+  const uint64_t base = (uint64_t)part * CH;   // the chunk's first element in its group
+  auto piece_at = [&](int j) -> uint64_t { return base + ((uint64_t)j * NT + threadIdx.x) * QPE; };
+  auto piece_n = [&](int j) -> int { return (int)min((uint64_t)QPE, sat_sub(a.G, piece_at(j))); };
 
   for (uint64_t grp = group; grp < a.n_grp; grp += n_groups) {
-    const uint64_t c0 = (uint64_t)part * CH + (uint64_t)threadIdx.x * QVPT;
-    const int nv = (int)min((uint64_t)QVPT, sat_sub(a.G, c0));
-    const uint64_t off = grp * a.G + c0;
+    const uint64_t goff = grp * a.G;
     float v[QVPT];
-    {
-      R xr[QVPT];
-      if (nv > 0) load_run_partial<R, QVPT, false>((const R*)a.x + off, nv, R{}, xr);
-      if constexpr (EF) {
-        float er[QVPT];
-        if (nv > 0) load_run_partial<float, QVPT, false>(a.e + off, nv, 0.0f, er);
 #pragma unroll
-        for (int i = 0; i < QVPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) + er[i] : 0.0f;
-      } else {
+    for (int j = 0; j < QNP; ++j) {
+      const int n = piece_n(j);
+      R xr[QPE];
+      float er[QPE];
+      if (n > 0) {
+        load_run_partial<R, QPE, false>((const R*)a.x + goff + piece_at(j), n, R{}, xr);
+        if constexpr (EF) load_run_partial<float, QPE, false>(a.e + goff + piece_at(j), n, 0.0f, er);
+      }
 #pragma unroll
-        for (int i = 0; i < QVPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) : 0.0f;
+      for (int i = 0; i < QPE; ++i) {
+        float t = 0.0f;
+        if (i < n) {
+          t = Elem<InT>::up(xr[i]);
+          if constexpr (EF) t = t + er[i];
+        }
+        v[j * QPE + i] = t;
       }
     }
 
-    uint32_t w[WPT];
     float lo = 0.0f, scale = 0.0f;
     if constexpr (B == 32) {
 #pragma unroll
-      for (int i = 0; i < QVPT; ++i) w[i] = __float_as_uint(v[i]);
+      for (int j = 0; j < QNP; ++j) {
+        const int n = piece_n(j);
+        uint32_t w[QPE];
+#pragma unroll
+        for (int i = 0; i < QPE; ++i) w[i] = __float_as_uint(v[j * QPE + i]);
+        if (n > 0) store_run_partial<uint32_t, QPE, false>(a.codes + grp * a.wpg + piece_at(j), n, w);
+        if constexpr (EF) {
+#pragma unroll
+          for (int i = 0; i < QPE; ++i) v[j * QPE + i] = v[j * QPE + i] - through<OutT>(v[j * QPE + i]);
+        }
+      }
     } else {
       // ---- min / max of the group
       lo = __int_as_float(0x7F800000);    // +inf
       float hi = __int_as_float(0xFF800000);  // -inf
 #pragma unroll
-      for (int i = 0; i < QVPT; ++i)
-        if (i < nv) { lo = fminf(lo, v[i]); hi = fmaxf(hi, v[i]); }
+      for (int j = 0; j < QNP; ++j) {
+        const int n = piece_n(j);
+#pragma unroll
+        for (int i = 0; i < QPE; ++i)
+          if (i < n) { lo = fminf(lo, v[j * QPE + i]); hi = fmaxf(hi, v[j * QPE + i]); }
+      }
       block_minmax<NT>(lo, hi, mm);
       if (P > 1) {
         if (threadIdx.x == 0) {
@@ -113,47 +144,60 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
       lo = lo + 0.0f;   // -0 reads as +0
       hi = hi + 0.0f;
       constexpr uint32_t LV = (1u << B) - 1u;
+      const bool flat = (hi == lo);
+      const float range = hi - lo;
+      scale = flat ? 0.0f : range / (float)LV;
+#pragma unroll
+      for (int j = 0; j < QNP; ++j) {
+        const int n = piece_n(j);
+        uint32_t word = 0u;
+#pragma unroll
+        for (int i = 0; i < QPE; ++i) {
+          uint32_t c = 0u;
+          if (!flat) {
+            const float u = (v[j * QPE + i] - lo) / range;
+            const float t = u * (float)LV;
+            c = min((uint32_t)rintf(t), LV);
+          }
+          if (i >= n) c = 0u;
+          word |= c << (8 * i);
+          if constexpr (EF) {
+            const float prod = (float)c * scale;
+            const float xh = lo + prod;
+            v[j * QPE + i] = v[j * QPE + i] - through<OutT>(xh);   // the residual, in place
+          }
+        }
+        s_codes[j * NT + threadIdx.x] = word;
+      }
+      __syncthreads();
+      // ---- pack: thread t takes chunk elements [QVPT t, QVPT t + QVPT)
       uint32_t c[QVPT];
-      if (hi == lo) {
 #pragma unroll
-        for (int i = 0; i < QVPT; ++i) c[i] = 0u;
-        scale = 0.0f;
-      } else {
-        const float range = hi - lo;
-        scale = range / (float)LV;
+      for (int q = 0; q < QVPT / 4; ++q) {
+        const uint32_t word = s_codes[threadIdx.x * (QVPT / 4) + q];
 #pragma unroll
-        for (int i = 0; i < QVPT; ++i) {
-          const float u = (v[i] - lo) / range;
-          const float t = u * (float)LV;
-          const uint32_t q = (uint32_t)rintf(t);
-          c[i] = (i < nv) ? min(q, LV) : 0u;
-        }
+        for (int i = 0; i < 4; ++i) c[4 * q + i] = (word >> (8 * i)) & 0xFFu;
       }
+      __syncthreads();   // the words are rewritten for the next group
+      uint32_t w[WPT];
       pack_codes<B>(c, w);
-      if constexpr (EF) {
-#pragma unroll
-        for (int i = 0; i < QVPT; ++i) {
-          const float prod = (float)c[i] * scale;
-          const float xh = lo + prod;
-          v[i] = v[i] - through<OutT>(xh);      // the residual, in place
-        }
-      }
+      const uint64_t wo = ((base + (uint64_t)threadIdx.x * QVPT) * (uint64_t)B) / 32u;
+      const int nw = (int)min((uint64_t)WPT, sat_sub(a.wpg, wo));
+      if (nw > 0) store_run_partial<uint32_t, WPT, false>(a.codes + grp * a.wpg + wo, nw, w);
     }
-    if constexpr (B == 32 && EF) {
-#pragma unroll
-      for (int i = 0; i < QVPT; ++i) v[i] = v[i] - through<OutT>(v[i]);
-    }
-
-    // ---- outputs
-    const uint64_t wo = (B == 32) ? c0 : (c0 * (uint64_t)B) / 32u;
-    const int nw = (int)min((uint64_t)WPT, sat_sub(a.wpg, wo));
-    if (nw > 0) store_run_partial<uint32_t, WPT, false>(a.codes + grp * a.wpg + wo, nw, w);
     if (part == 0 && threadIdx.x == 0) {
       a.meta[2 * grp] = lo;
       a.meta[2 * grp + 1] = scale;
     }
     if constexpr (EF) {
-      if (nv > 0) store_run_partial<float, QVPT, false>(a.e + off, nv, v);
+#pragma unroll
+      for (int j = 0; j < QNP; ++j) {
+        const int n = piece_n(j);
+        float r[QPE];
+#pragma unroll
+        for (int i = 0; i < QPE; ++i) r[i] = v[j * QPE + i];
+        if (n > 0) store_run_partial<float, QPE, false>(a.e + goff + piece_at(j), n, r);
+      }
     }
   }
   if (P > 1) group_exit<NT>(bar, P, slots, 2ull * P);
