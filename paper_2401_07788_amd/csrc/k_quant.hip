@@ -45,6 +45,36 @@ __device__ __forceinline__ void unpack_codes(const uint32_t (&w)[QVPT * B / 32],
   }
 }
 
+// The code of v in a group with minimum lo and range hi - lo > 0:
+// min(rint((v - lo) / range * LV), LV) with the division correctly rounded.
+// For range in [2^-125, 2^125] the quotient is first taken as
+// (v - lo) * RN(1 / range).  The t = quotient * LV of that form and of the
+// direct one differ by at most five roundings of 2^-24 relative each; with
+// (v - lo) <= range, t <= 255, so the two lie within 2^-13 of each other and
+// round to the same integer unless t is within 2^-10 of a half-integer.
+// Those values, and ranges outside the interval, take the division.
+template <uint32_t LV>
+struct MinMaxCode {
+  float lo, range, rcp;
+  bool fast;
+  __device__ __forceinline__ MinMaxCode(float lo_, float range_) : lo(lo_), range(range_) {
+    fast = range >= 0x1p-125f && range <= 0x1p125f;
+    rcp = 1.0f / range;
+  }
+  __device__ __forceinline__ uint32_t operator()(float v) const {
+    const float n = v - lo;
+    if (fast) {
+      const float u = n * rcp;
+      const float t = u * (float)LV;
+      const float r = rintf(t);
+      if (fabsf(t - r) < 0.5f - 0x1p-10f) return min((uint32_t)r, LV);
+    }
+    const float u = n / range;
+    const float t = u * (float)LV;
+    return min((uint32_t)rintf(t), LV);
+  }
+};
+
 // Sender.  Loads, the residual and binary32 codes (b = 32) go in pieces of
 // QPE consecutive elements, lanes consecutive, so that every wavefront
 // instruction covers contiguous memory; piece j of thread t is element
@@ -147,6 +177,7 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
       const bool flat = (hi == lo);
       const float range = hi - lo;
       scale = flat ? 0.0f : range / (float)LV;
+      const MinMaxCode<LV> code_of(lo, flat ? 1.0f : range);
 #pragma unroll
       for (int j = 0; j < QNP; ++j) {
         const int n = piece_n(j);
@@ -154,11 +185,7 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
 #pragma unroll
         for (int i = 0; i < QPE; ++i) {
           uint32_t c = 0u;
-          if (!flat) {
-            const float u = (v[j * QPE + i] - lo) / range;
-            const float t = u * (float)LV;
-            c = min((uint32_t)rintf(t), LV);
-          }
+          if (!flat) c = code_of(v[j * QPE + i]);
           if (i >= n) c = 0u;
           word |= c << (8 * i);
           if constexpr (EF) {

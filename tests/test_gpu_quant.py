@@ -59,3 +59,24 @@ def test_quant_receiver_grid_stride(tc, orc, b):
     n_grp, G = 40, 131072
     x = W.randn((n_grp, G), seed=9, tensor_id=b)
     run_case(tc, orc, x, n_grp, G, b)
+
+
+@pytest.mark.parametrize("b", [2, 4, 8])
+@pytest.mark.parametrize("R", [1.0, 1.7, 3.0e-3, 6.5e4])
+def test_quant_codes_at_rounding_ties(tc, orc, b, R):
+    # values whose scaled position (v - lo) / (hi - lo) * (2^b - 1) lies on,
+    # or a few ulps either side of, a half-integer: the code there depends on
+    # every rounding of the quotient
+    LV = (1 << b) - 1
+    G = 8192
+    half = (np.arange(G, dtype=np.float64) % LV + 0.5) * (np.float32(R) / LV)
+    v = half.astype(np.float32)
+    steps = (np.arange(G) % 7) - 3
+    for _ in range(3):
+        up, dn = steps > 0, steps < 0
+        v[up] = np.nextafter(v[up], np.float32(np.inf))
+        v[dn] = np.nextafter(v[dn], np.float32(-np.inf))
+        steps = steps - np.sign(steps)
+    v[0], v[1] = 0.0, np.float32(R)
+    x = torch.from_numpy(np.stack([v, v[::-1].copy()]))
+    run_case(tc, orc, x, 2, G, b)
