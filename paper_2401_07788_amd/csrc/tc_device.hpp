@@ -279,6 +279,19 @@ __device__ __forceinline__ float wave_minmax(float x) {
 __device__ __forceinline__ float wave_min(float x) { return wave_minmax<false>(x); }
 __device__ __forceinline__ float wave_max(float x) { return wave_minmax<true>(x); }
 
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_uminmax(uint32_t x) {
+  const uint32_t id = MAX ? 0u : 0xFFFFFFFFu;
+  auto op = [](uint32_t a, uint32_t b) { return MAX ? max(a, b) : min(a, b); };
+  x = op(x, dpp_u32<DPP_ROW_SHR1, 0xF>(id, x));
+  x = op(x, dpp_u32<DPP_ROW_SHR2, 0xF>(id, x));
+  x = op(x, dpp_u32<DPP_ROW_SHR4, 0xF>(id, x));
+  x = op(x, dpp_u32<DPP_ROW_SHR8, 0xF>(id, x));
+  x = op(x, dpp_u32<DPP_ROW_BCAST15, 0xA>(id, x));
+  x = op(x, dpp_u32<DPP_ROW_BCAST31, 0xC>(id, x));
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, WAVE - 1);
+}
+
 // ------------------------------------------------------- workgroup helpers
 // scratch must hold NT/64 + 1 words of LDS.  All threads of the workgroup
 // must call these (they contain barriers).  Wave totals go through LDS once;

@@ -125,7 +125,11 @@ __device__ __forceinline__ void zero_lds(uint32_t* h, int n) {
 // radix select over 8-bit digits of the key from bit 23 down, then its last
 // 7 bits, with 256-bin histograms in LDS private to the wavefront (`hist`,
 // 16-byte aligned, RADIX_CP * 256 words); each digit is found with one
-// wavefront scan (lane l owns bins 4l..4l+3).
+// wavefront scan (lane l owns bins 4l..4l+3).  Once the chosen bin must give
+// up only its largest key (one more needed) or all of its keys, the rest of
+// T is that largest or smallest key, found by one wavefront reduction
+// instead of the remaining passes (after two digits a row's bin holds about
+// one key).
 constexpr int RADIX_CP = 4;
 template <int VPT>
 __device__ __forceinline__ SelResult wave_radix_select(const uint32_t (&key)[VPT], int nv, uint32_t k,
@@ -161,22 +165,45 @@ __device__ __forceinline__ SelResult wave_radix_select(const uint32_t (&key)[VPT
     const uint32_t sum = h[0] + h[1] + h[2] + h[3];
     const uint32_t incl = wave_incl_scan(sum);
     uint32_t acc = (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1) - incl;   // bins of higher lanes
-    uint32_t d = 0u;
+    uint32_t d = 0u, cnt = 0u;
     const bool here = acc < need && need <= acc + sum;
     if (here) {
 #pragma unroll
       for (int c = 3; c >= 0; --c) {
-        if (acc + h[c] >= need) { d = 4u * lane + (uint32_t)c; break; }
+        if (acc + h[c] >= need) { d = 4u * lane + (uint32_t)c; cnt = h[c]; break; }
         acc += h[c];
       }
     }
     const int src = __builtin_ctzll(__ballot(here));
     d = (uint32_t)__builtin_amdgcn_readlane((int)d, src);
     acc = (uint32_t)__builtin_amdgcn_readlane((int)acc, src);
+    cnt = (uint32_t)__builtin_amdgcn_readlane((int)cnt, src);
     prefix = (prefix << width) | d;
     need -= acc;
     pbits += width;
     __syncthreads();
+    if (pass < 3 && (need == 1u || need == cnt)) {
+      // need == 1: T is the bin's largest key, one of its copies kept;
+      // need == cnt: every key of the bin is kept, T is the smallest and
+      // all of its copies are kept
+      const bool top = need == 1u;
+      const uint32_t sh = 31u - pbits;
+      uint32_t best = top ? 0u : 0xFFFFFFFFu;
+#pragma unroll
+      for (int i = 0; i < VPT; ++i)
+        if (i < nv && (key[i] >> sh) == prefix) best = top ? max(best, key[i]) : min(best, key[i]);
+      SelResult res;
+      res.T = top ? wave_uminmax<true>(best) : wave_uminmax<false>(best);
+      uint32_t eq = 0u;
+      if (!top) {
+#pragma unroll
+        for (int i = 0; i < VPT; ++i) eq += (i < nv && key[i] == res.T) ? 1u : 0u;
+      }
+      res.r = top ? 1u : wave_sum(eq);
+      res.gt_before = 0u;
+      res.eq_before = 0u;
+      return res;
+    }
   }
   SelResult res;
   res.T = prefix;

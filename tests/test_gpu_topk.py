@@ -176,3 +176,24 @@ def test_decompress_rows_several_per_wavefront(tc, orc):
     assert tc.device_errors() == 0
     oi, ov = orc.topk_compress(raw(x), "f16", n_seg, L, k)
     assert_bits_equal(raw(y), orc.topk_decompress(oi, ov, "f16", n_seg, L, k), "dense")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_topk_row_threshold_bin_shortcuts(tc, orc, dt):
+    # rows where the bin chosen by the first digits holds a few keys with
+    # ties among them (values 1 + j * 2^-20 share their top 16 key bits in
+    # fp32; in bf16 they collapse to one value), swept over k so that the
+    # selection ends needing one key of the bin, all of it, or something
+    # in between
+    n_seg, L = 6, 768
+    g = torch.Generator().manual_seed(5)
+    x = torch.rand((n_seg, L), generator=g) * 0.4 - 0.2
+    pick = torch.rand((n_seg, L), generator=g) < 0.01
+    j = torch.randint(0, 4, (n_seg, L), generator=g).to(torch.float64)
+    x = torch.where(pick, (1.0 + j * 2.0 ** -20).to(torch.float32), x)
+    x[:, 5] = 3.0
+    x[:, 700] = -3.0
+    x = x.to(TORCH[dt]).contiguous()
+    n_big = int(pick.sum(dim=1).max()) + 2
+    for k in range(1, n_big + 4):
+        run_case(tc, orc, x, n_seg, L, k)
