@@ -51,7 +51,7 @@ template <typename InT, int SEL, int VPT>
 __global__ __launch_bounds__(WAVE) void k_topk_row(TopkArgs a) {
   using R = typename Elem<InT>::raw;
   __shared__ uint32_t scratch[2];
-  __shared__ __attribute__((aligned(16))) uint32_t hist[RADIX_CP * 256];
+  __shared__ __attribute__((aligned(16))) uint32_t hist[RADIX_CP * RADIX_HS];
   for (uint64_t seg = blockIdx.x; seg < a.n_seg; seg += gridDim.x) {
     const uint64_t c0 = (uint64_t)threadIdx.x * VPT;
     const int nv = (int)min((uint64_t)VPT, sat_sub(a.L, c0));

@@ -124,31 +124,95 @@ __device__ __forceinline__ void zero_lds(uint32_t* h, int n) {
 // Exact threshold for a segment held entirely by one wavefront (NT == 64):
 // radix select over 8-bit digits of the key from bit 23 down, then its last
 // 7 bits, with 256-bin histograms in LDS private to the wavefront (`hist`,
-// 16-byte aligned, RADIX_CP * 256 words); each digit is found with one
-// wavefront scan (lane l owns bins 4l..4l+3).  Once the chosen bin must give
-// up only its largest key (one more needed) or all of its keys, the rest of
-// T is that largest or smallest key, found by one wavefront reduction
-// instead of the remaining passes (after two digits a row's bin holds about
-// one key).
+// 16-byte aligned, RADIX_CP * RADIX_HS words); each digit is found with one
+// wavefront scan (lane l owns bins 4l..4l+3).
+//  - The first digit is the exponent.  With at most 15 keys per lane it is
+//    counted in registers first: a 4-bit counter per lane for each of the
+//    eight digits at and below the segment's largest, summed over the
+//    wavefront in four words.  Only when T's digit lies further down does
+//    the histogram pass run.
+//  - In that pass the exponent takes few values, so the lanes count in
+//    RADIX_CP copies (lane mod RADIX_CP), RADIX_HS words apart: an odd
+//    number of 4-word bank groups, so that one bin's copies sit in distinct
+//    LDS banks.
+//  - Once the chosen bin must give up only its largest key (one more
+//    needed) or all of its keys, the rest of T is that largest or smallest
+//    key, found by one wavefront reduction instead of the remaining passes
+//    (after two digits a row's bin holds about one key).
 constexpr int RADIX_CP = 4;
+constexpr int RADIX_HS = 260;
 template <int VPT>
 __device__ __forceinline__ SelResult wave_radix_select(const uint32_t (&key)[VPT], int nv, uint32_t k,
                                                        uint32_t* hist) {
   const uint32_t lane = (uint32_t)lane_id();
   uint32_t prefix = 0u, need = k, pbits = 0u;
+  // T from the keys under `prefix` (pbits bits): their largest (one copy
+  // kept) or their smallest (all copies kept)
+  auto settle = [&](bool top) {
+    const uint32_t sh = 31u - pbits;
+    uint32_t best = top ? 0u : 0xFFFFFFFFu;
+#pragma unroll
+    for (int i = 0; i < VPT; ++i)
+      if (i < nv && (key[i] >> sh) == prefix) best = top ? max(best, key[i]) : min(best, key[i]);
+    SelResult res;
+    res.T = top ? wave_uminmax<true>(best) : wave_uminmax<false>(best);
+    uint32_t eq = 0u;
+    if (!top) {
+#pragma unroll
+      for (int i = 0; i < VPT; ++i) eq += (i < nv && key[i] == res.T) ? 1u : 0u;
+    }
+    res.r = top ? 1u : wave_sum(eq);
+    res.gt_before = 0u;
+    res.eq_before = 0u;
+    return res;
+  };
+  int first = 0;   // digit passes already done
+  if constexpr (VPT <= 15) {
+    uint32_t dm = 0u;
+#pragma unroll
+    for (int i = 0; i < VPT; ++i)
+      if (i < nv) dm = max(dm, key[i] >> 23);
+    dm = wave_uminmax<true>(dm);
+    uint32_t w = 0u;   // nibble o: keys of digit dm - o
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const uint32_t off = dm - (key[i] >> 23);
+      w += (i < nv && off < 8u) ? (1u << (off << 2)) : 0u;
+    }
+    // widened to 16-bit fields before the sums: words hold digits (0, 4),
+    // (2, 6), (1, 5), (3, 7)
+    const uint32_t ev = w & 0x0F0F0F0Fu, od = (w >> 4) & 0x0F0F0F0Fu;
+    const uint32_t s04 = wave_sum(ev & 0x00FF00FFu), s26 = wave_sum((ev >> 8) & 0x00FF00FFu);
+    const uint32_t s15 = wave_sum(od & 0x00FF00FFu), s37 = wave_sum((od >> 8) & 0x00FF00FFu);
+    const uint32_t c8[8] = {s04 & 0xFFFFu, s15 & 0xFFFFu, s26 & 0xFFFFu, s37 & 0xFFFFu,
+                            s04 >> 16,     s15 >> 16,     s26 >> 16,     s37 >> 16};
+    uint32_t acc = 0u, cnt = 0u;
+#pragma unroll
+    for (int o = 0; o < 8; ++o) {
+      if (first == 0 && acc < need && need <= acc + c8[o]) {
+        first = 1;
+        prefix = dm - (uint32_t)o;
+        need -= acc;
+        cnt = c8[o];
+      }
+      acc += c8[o];
+    }
+    if (first) {
+      pbits = 8u;
+      if (need == 1u || need == cnt) return settle(need == 1u);
+    }
+  }
 #pragma unroll
   for (int pass = 0; pass < 4; ++pass) {
+    if (pass < first) continue;
     const uint32_t width = (pass < 3) ? 8u : 7u;
     const uint32_t shift = 31u - pbits - width;
-    // the first digit (the exponent) takes few values, so the lanes count in
-    // RADIX_CP copies (lane mod RADIX_CP) and meet at most a quarter as often
-    // on one word; the later digits are spread out and use one copy
     constexpr int CP = RADIX_CP;
 #pragma unroll
     for (int c = 0; c < (pass == 0 ? CP : 1); ++c)
-      reinterpret_cast<u32x4*>(hist)[c * (256 / 4) + lane] = u32x4{0u, 0u, 0u, 0u};
+      reinterpret_cast<u32x4*>(hist)[c * (RADIX_HS / 4) + lane] = u32x4{0u, 0u, 0u, 0u};
     __syncthreads();
-    const uint32_t base = (pass == 0) ? (lane % CP) * 256u : 0u;
+    const uint32_t base = (pass == 0) ? (lane % CP) * (uint32_t)RADIX_HS : 0u;
 #pragma unroll
     for (int i = 0; i < VPT; ++i)
       if (i < nv && (key[i] >> (shift + width)) == prefix)
@@ -158,7 +222,7 @@ __device__ __forceinline__ SelResult wave_radix_select(const uint32_t (&key)[VPT
     if (pass == 0) {
 #pragma unroll
       for (int c = 1; c < CP; ++c) {
-        const u32x4 hc = reinterpret_cast<const u32x4*>(hist)[c * (256 / 4) + lane];
+        const u32x4 hc = reinterpret_cast<const u32x4*>(hist)[c * (RADIX_HS / 4) + lane];
         h = h + hc;
       }
     }
@@ -182,28 +246,7 @@ __device__ __forceinline__ SelResult wave_radix_select(const uint32_t (&key)[VPT
     need -= acc;
     pbits += width;
     __syncthreads();
-    if (pass < 3 && (need == 1u || need == cnt)) {
-      // need == 1: T is the bin's largest key, one of its copies kept;
-      // need == cnt: every key of the bin is kept, T is the smallest and
-      // all of its copies are kept
-      const bool top = need == 1u;
-      const uint32_t sh = 31u - pbits;
-      uint32_t best = top ? 0u : 0xFFFFFFFFu;
-#pragma unroll
-      for (int i = 0; i < VPT; ++i)
-        if (i < nv && (key[i] >> sh) == prefix) best = top ? max(best, key[i]) : min(best, key[i]);
-      SelResult res;
-      res.T = top ? wave_uminmax<true>(best) : wave_uminmax<false>(best);
-      uint32_t eq = 0u;
-      if (!top) {
-#pragma unroll
-        for (int i = 0; i < VPT; ++i) eq += (i < nv && key[i] == res.T) ? 1u : 0u;
-      }
-      res.r = top ? 1u : wave_sum(eq);
-      res.gt_before = 0u;
-      res.eq_before = 0u;
-      return res;
-    }
+    if (pass < 3 && (need == 1u || need == cnt)) return settle(need == 1u);
   }
   SelResult res;
   res.T = prefix;

@@ -197,3 +197,22 @@ def test_topk_row_threshold_bin_shortcuts(tc, orc, dt):
     n_big = int(pick.sum(dim=1).max()) + 2
     for k in range(1, n_big + 4):
         run_case(tc, orc, x, n_seg, L, k)
+
+
+@pytest.mark.parametrize("L", [64, 768, 960])
+@pytest.mark.parametrize("spread", [1.0, 30.0, 1e6])
+def test_topk_row_first_digit_window(tc, orc, L, spread):
+    # the first digit (the exponent) is counted for the eight binades below
+    # the row's largest key; with a few entries `spread` times larger, T's
+    # binade lies inside that window (1, 30) or far below it (1e6: the
+    # histogram pass); rows of subnormal values and of exact zeros too
+    n_seg = 8
+    g = torch.Generator().manual_seed(int(L + spread))
+    x = torch.randn((n_seg, L), generator=g)
+    big = torch.rand((n_seg, L), generator=g) < 0.01
+    x = torch.where(big, x * spread, x)
+    x[6] = torch.randn(L, generator=g) * 1e-40
+    x[7] = 0.0
+    x = x.contiguous()
+    for num, den in [(1, 100), (1, 10), (3, 10), (9, 10)]:
+        run_case(tc, orc, x, n_seg, L, tc.topk_count(L, num, den))
