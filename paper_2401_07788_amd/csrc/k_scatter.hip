@@ -324,10 +324,33 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
         reinterpret_cast<u32x4*>(buf)[q * SC_NT + threadIdx.x] = w;
       }
       __syncthreads();
+      // the held groups' entries: every read of the chunk goes out before
+      // any write (a chunk's indices are distinct), one LDS round trip
+      // rather than one per entry
+      R old[GPT][8];
 #pragma unroll
       for (int r = 0; r < GPT; ++r) {
         const uint32_t gq = threadIdx.x + (uint32_t)r * SC_NT;
-        if (gq < ng) apply_group<T>(pg[r], A0 + 8ull * gq, J0, J1, c0, c1, buf);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint64_t J = A0 + 8ull * gq + (uint64_t)e;
+          const uint32_t i = pg[r].idx[e];
+          old[r][e] = R{};
+          if (gq < ng && J >= J0 && J < J1 && i >= c0 && i < c1) old[r][e] = buf[i - c0];
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < GPT; ++r) {
+        const uint32_t gq = threadIdx.x + (uint32_t)r * SC_NT;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint64_t J = A0 + 8ull * gq + (uint64_t)e;
+          if (gq < ng && J >= J0 && J < J1) {
+            const uint32_t i = pg[r].idx[e];
+            if (i < c0 || i >= c1) raise_error(KERR_BAD_INDEX);
+            else buf[i - c0] = Elem<T>::down(Elem<T>::up(old[r][e]) + Elem<T>::up(pg[r].val[e]));
+          }
+        }
       }
       // a chunk with more entries than the registers hold: the rest in turns
       for (uint32_t gq = threadIdx.x + GPT * SC_NT; gq < ng; gq += SC_NT) {
