@@ -1,7 +1,9 @@
 """GPU parity over a seeded sweep of random cases, against the CPU oracle,
 bit for bit: TopK (Sec. 2.3) sender and receiver, TopK and min-max
 quantization (Sec. 2.2) inside error feedback (Sec. 2.4) over two carried
-steps, plain quantization, and AQ-SGD (Sec. 2.5) over two micro-batches.
+steps, plain quantization, TopK with its kept list quantized, a tensor sent
+at another's TopK indices (alone and inside EF), EF-mixed (Sec. 2.4), and
+AQ-SGD (Sec. 2.5) over two micro-batches.
 Each case draws its segment count and length (so that every engine runs:
 rows of up to 2048 elements, segments held in LDS, segments spread over
 several workgroups), its dtype, its K or bit width and the kind of data
@@ -143,3 +145,68 @@ def test_sweep_aqsgd(tc, orc, seed):
         assert_bits_equal(raw(a_hat), oa, f"a_hat step {t} {c}")
         assert_bits_equal(raw(m_s), mo, f"m_s step {t} {c}")
         assert_bits_equal(raw(m_r), mo_r, f"m_r step {t} {c}")
+
+
+@pytest.mark.parametrize("seed", range(N_CASES))
+def test_sweep_topk_quant_and_gather(tc, orc, seed):
+    c = draw(seed)
+    n_seg, L, dt, k, b = c["n_seg"], c["L"], c["dt"], c["k"], c["bits"]
+    # TopK with the kept list quantized (one group per segment), inside EF
+    n_q = min(n_seg, 4)
+    e = torch.zeros(n_q * L, dtype=torch.float32, device="cuda")
+    eo = np.zeros((n_q, L), np.float32)
+    for t in range(2):
+        xt = make(c["kind"], (n_q, L), dt, seed * 13 + t)
+        pq = tc.ef_step_topk_quant(xt.cuda(), e, k, b, n_q)
+        y = tc.topk_quant_decompress(pq, L, out_dtype=xt.dtype)
+        torch.cuda.synchronize()
+        assert tc.device_errors() == 0, c
+        oi, oc, om, eo = orc.ef_topk_quant(raw(xt), dt, eo, n_q, L, k, b)
+        assert_bits_equal(raw(pq.idx), oi, f"TopK-Q idx step {t} {c}")
+        assert_bits_equal(raw(pq.codes), oc, f"TopK-Q codes step {t} {c}")
+        assert_bits_equal(raw(pq.meta), om, f"TopK-Q meta step {t} {c}")
+        assert_bits_equal(raw(e).reshape(n_q, L), eo, f"TopK-Q e step {t} {c}")
+        assert_bits_equal(raw(y), orc.topk_quant_decompress(oi, oc, om, n_q, L, k, b, dt), f"TopK-Q dense {t} {c}")
+    # a second tensor at the first one's TopK indices, alone and inside EF
+    x = make(c["kind"], (n_seg, L), dt, seed)
+    p = tc.topk_compress(x.cuda(), k, n_seg)
+    oi, _ = orc.topk_compress(raw(x), dt, n_seg, L, k, threads=8)
+    g0 = make("normal", (n_seg, L), dt, seed + 99)
+    val = tc.topk_gather(p, g0.cuda())
+    torch.cuda.synchronize()
+    assert tc.device_errors() == 0, c
+    assert_bits_equal(raw(val), orc.topk_gather(raw(g0), dt, oi, n_seg, L, k), f"gather {c}")
+    e = torch.zeros(n_seg * L, dtype=torch.float32, device="cuda")
+    eo = np.zeros((n_seg, L), np.float32)
+    for t in range(2):
+        gt = make("normal", (n_seg, L), dt, seed + 100 + t)
+        val = tc.topk_gather(p, gt.cuda(), e=e, use_blk=(t == 0))
+        torch.cuda.synchronize()
+        assert tc.device_errors() == 0, c
+        ov, eo = orc.topk_gather(raw(gt), dt, oi, n_seg, L, k, e=eo)
+        assert_bits_equal(raw(val), ov, f"gather EF val step {t} {c}")
+        assert_bits_equal(raw(e).reshape(n_seg, L), eo, f"gather EF e step {t} {c}")
+
+
+@pytest.mark.parametrize("seed", range(N_CASES))
+def test_sweep_efmix(tc, orc, seed):
+    c = draw(seed)
+    n_seg, dt = c["n_seg"], c["dt"]
+    L = c["L"] if c["L"] <= 32768 else 1 + c["L"] % 32768   # one workgroup per segment
+    k = min(c["k"], L)
+    e = torch.zeros(n_seg * L, dtype=torch.float32, device="cuda")
+    eo = np.zeros((n_seg, L), np.float32)
+    for t in range(2):
+        xt = make(c["kind"], (n_seg, L), dt, seed * 17 + t)
+        px, pe = tc.efmix_step(xt.cuda(), e, k, n_seg)
+        y = tc.efmix_reconstruct(px, pe, L)
+        torch.cuda.synchronize()
+        assert tc.device_errors() == 0, c
+        oix, ovx, oie, ove, eo = orc.efmix_send(raw(xt), dt, eo, n_seg, L, k)
+        assert_bits_equal(raw(px.idx), oix, f"EF-mixed idx_x step {t} {c}")
+        assert_bits_equal(raw(px.val), ovx, f"EF-mixed val_x step {t} {c}")
+        assert_bits_equal(raw(pe.idx), oie, f"EF-mixed idx_e step {t} {c}")
+        assert_bits_equal(raw(pe.val), ove, f"EF-mixed val_e step {t} {c}")
+        assert_bits_equal(raw(e).reshape(n_seg, L), eo, f"EF-mixed e step {t} {c}")
+        assert_bits_equal(raw(y), orc.efmix_recv(oix, ovx, oie, ove, dt, n_seg, L, k, out_dt=dt),
+                          f"EF-mixed dense step {t} {c}")
