@@ -55,7 +55,8 @@ SOURCES_HASHED = {
                "paper_2401_07788_amd/csrc/tc_select.hpp", "paper_2401_07788_amd/csrc/tc_device.hpp",
                "paper_2401_07788_amd/csrc/k_scatter.hip", "paper_2401_07788_amd/csrc/k_quant.hip"],
     "transformer": ["paper_2401_07788_amd/csrc/k_topk.hip", "paper_2401_07788_amd/csrc/tc_select.hpp",
-                    "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip"],
+                    "paper_2401_07788_amd/csrc/tc_device.hpp", "paper_2401_07788_amd/csrc/k_scatter.hip",
+                    "paper_2401_07788_amd/csrc/k_quant.hip"],
 }
 SOURCES_HASHED["cnn"] = SOURCES_HASHED["resnet"]
 
