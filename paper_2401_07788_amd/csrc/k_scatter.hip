@@ -8,8 +8,9 @@
 // cooperative search of the ascending index list), builds the chunk in LDS,
 // and writes it out with full-width stores, so the dense output is written
 // exactly once.  Rows of up to 2048 elements take one wavefront each
-// instead.  Also here: the EF-mixed receiver (two lists, the second added)
-// and TopK at given indices (index reuse for gradients).
+// instead.  Also here: the EF-mixed receiver (two lists, the second added),
+// the EF-mixed sender's residual, and TopK at given indices (index reuse for
+// gradients).
 #include <algorithm>
 
 #include "tc_internal.hpp"
@@ -477,6 +478,117 @@ __global__ __launch_bounds__(SC_NT) void k_efmix_scatter(ScatterArgs a) {
   }
 }
 
+// EF-mixed residual (Sec. 2.4), the sender's second kernel, after both
+// selections: e <- (x minus what was sent of it) + (e minus what was sent
+// of it).  x is exact in its dtype, so its share is x off the input's list
+// and +0 on it.  Where both lists hold an index the receiver rounds
+// u = x + wire(e) (binary32) once to the wire dtype, and the part that
+// rounding drops, u - wire(u), stays in the buffer too.  Workgroup
+// iteration = one 4096-element chunk: its x and e are loaded first
+// (lane-consecutive pieces of four), both lists' entries in the chunk set
+// bits of two LDS masks (ranges from the block tables, else a search of the
+// ascending indices), then e is written in the same pieces.
+template <typename InT>
+__global__ __launch_bounds__(SC_NT) void k_efmix_resid(EfmixResidArgs a) {
+  using R = typename Elem<InT>::raw;
+  constexpr int QPT = (int)(SC_CH / 4 / SC_NT);   // pieces per thread
+  __shared__ uint32_t msk[2][SC_CH / 32];
+  __shared__ uint32_t scratch[SC_NT / WAVE + 2];
+  const uint64_t nch = (a.L + SC_CH - 1) / SC_CH;
+  const uint64_t nbt = n_blocks(a.L) + 1;
+  const uint32_t t = threadIdx.x;
+  const bool vec = ((((uintptr_t)a.x | (uintptr_t)a.e) & 15u) == 0) && (a.L % 4u) == 0;
+  for (uint64_t wi = blockIdx.x; wi < a.n_seg * nch; wi += gridDim.x) {
+    const uint64_t seg = wi / nch, c0 = (wi % nch) * SC_CH;
+    const uint64_t c1 = min(a.L, c0 + SC_CH);
+    const uint32_t n = (uint32_t)(c1 - c0);
+    const R* xc = (const R*)a.x + seg * a.L + c0;
+    float* ec = a.e + seg * a.L + c0;
+    R xr[QPT][4];
+    float er[QPT][4];
+#pragma unroll
+    for (int q = 0; q < QPT; ++q) {
+      const uint32_t i0 = ((uint32_t)q * SC_NT + t) * 4;
+      if (vec && i0 + 4 <= n) {
+        load_run<R, 4, false>(xc + i0, xr[q]);
+        load_run<float, 4, false>(ec + i0, er[q]);
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          xr[q][c] = (i0 + (uint32_t)c < n) ? xc[i0 + c] : R{};
+          er[q][c] = (i0 + (uint32_t)c < n) ? ec[i0 + c] : 0.0f;
+        }
+      }
+    }
+    const uint64_t kk[2] = {a.k, a.k2};
+    const uint32_t* ixl[2] = {a.idx + seg * a.k, a.idx2 + seg * a.k2};
+    const uint32_t* btl[2] = {a.blk ? a.blk + seg * nbt : nullptr, a.blk2 ? a.blk2 + seg * nbt : nullptr};
+    for (uint32_t i = t; i < 2 * (SC_CH / 32); i += SC_NT) (&msk[0][0])[i] = 0u;
+    // both lists' ranges in the chunk (block tables: one round trip for both)
+    uint32_t r0[2] = {0u, 0u}, r1[2] = {0u, 0u};
+    if (btl[0] && btl[1]) {
+      const uint64_t c = c0 / SC_CH;
+#pragma unroll
+      for (int l = 0; l < 2; ++l) { r0[l] = btl[l][c]; r1[l] = btl[l][c + 1]; }
+#pragma unroll
+      for (int l = 0; l < 2; ++l) {
+        if (r0[l] > r1[l] || r1[l] > kk[l] || r1[l] - r0[l] > n) {
+          if (t == 0) raise_error(KERR_BAD_INDEX);
+          r0[l] = r1[l] = 0u;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int l = 0; l < 2; ++l)
+        if (kk[l] > 0) chunk_range(ixl[l], btl[l], kk[l], c0, c1, scratch, r0[l], r1[l]);
+    }
+    // entries past the segment's end belong to no chunk: the last chunk flags them
+#pragma unroll
+    for (int l = 0; l < 2; ++l)
+      if (c1 == a.L && r1[l] < kk[l] && t == 0) raise_error(KERR_BAD_INDEX);
+    __syncthreads();   // the zeroed masks
+#pragma unroll
+    for (int l = 0; l < 2; ++l) {
+      for (uint32_t j = r0[l] + t; j < r1[l]; j += SC_NT) {
+        const uint32_t i = ixl[l][j];
+        if (!btl[l] && j > r0[l] && ixl[l][j - 1] >= i) raise_error(KERR_BAD_INDEX);
+        if (i < c0 || i >= c1) raise_error(KERR_BAD_INDEX);
+        else atomicOr(&msk[l][(i - c0) >> 5], 1u << ((i - c0) & 31u));
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < QPT; ++q) {
+      const uint32_t i0 = ((uint32_t)q * SC_NT + t) * 4;
+      if (i0 >= n) continue;
+      const uint32_t kx4 = msk[0][i0 >> 5] >> (i0 & 31u), ke4 = msk[1][i0 >> 5] >> (i0 & 31u);
+      float o[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const float xv = Elem<InT>::up(xr[q][c]);
+        const bool in_x = (kx4 >> c) & 1u, in_e = (ke4 >> c) & 1u;
+        const float rx = xv - (in_x ? xv : 0.0f);
+        const float v = er[q][c];
+        const float ve = through<InT>(v);
+        float re = v - (in_e ? ve : 0.0f);
+        if (in_x && in_e) {
+          const float u = xv + ve;
+          re = re + (u - through<InT>(u));
+        }
+        o[c] = rx + re;
+      }
+      if (vec && i0 + 4 <= n) {
+        store_run<float, 4, true>(ec + i0, o);
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          if (i0 + (uint32_t)c < n) ec[i0 + c] = o[c];
+      }
+    }
+    __syncthreads();   // the masks are cleared for the next chunk
+  }
+}
+
 // AQ-SGD receiver for rows of up to SR_MAX elements (one buffer row per
 // token row): one wavefront per row, in a slice of LDS of its own.  The row's
 // payload entries do not depend on the id, so they are loaded with the id;
@@ -725,6 +837,14 @@ hipError_t launch_efmix_recv(int wire, int out_dt, const ScatterArgs& args, hipS
   const void* fn = (wire == DT_F32) ? efmix_ptr<float>(out_dt)
                  : (wire == DT_BF16) ? efmix_ptr<bf16_t>(out_dt) : efmix_ptr<f16_t>(out_dt);
   ScatterArgs a = args;
+  void* params[] = {&a};
+  return hipLaunchKernel(fn, dim3(scatter_grid(a.n_seg, a.L)), dim3(SC_NT), params, 0, st);
+}
+
+hipError_t launch_efmix_resid(int dt, const EfmixResidArgs& args, hipStream_t st) {
+  const void* fn = (dt == DT_F32) ? (const void*)k_efmix_resid<float>
+                 : (dt == DT_BF16) ? (const void*)k_efmix_resid<bf16_t> : (const void*)k_efmix_resid<f16_t>;
+  EfmixResidArgs a = args;
   void* params[] = {&a};
   return hipLaunchKernel(fn, dim3(scatter_grid(a.n_seg, a.L)), dim3(SC_NT), params, 0, st);
 }

@@ -6,12 +6,13 @@
 //   EF    : v = x + e                              -> payload, e <- v - r
 //           r = what the receiver gets: wire(v) at kept entries, +0 elsewhere
 //   AQSGD : v = a - m[id]                          -> payload, m[id][kept] += wire(v)
-// and, in the LDS engine only, two selections (EF-mixed, Sec. 2.4):
+// and, in the LDS engine only, the two selections of EF-mixed (Sec. 2.4):
 //   EFMIX : TopK(x) and TopK(e) over halves of the budget -> two payloads,
-//           e <- (x - r_x) + (e - r_e)
+//           one workgroup each (they are independent); the residual
+//           e <- (x - r_x) + (e - r_e) is k_efmix_resid's (k_scatter.hip)
 // The segment (a sample, a token row, a whole example) stays in registers or
-// LDS for the whole kernel: inputs are read once (EF-mixed reads x twice),
-// the selection works on registers and LDS, and the outputs are written once.
+// LDS for the whole kernel: inputs are read once, the selection works on
+// registers and LDS, and the outputs are written once.
 //
 // Three engines:
 //   k_topk_row : one wavefront per segment of up to 2048 elements (token
@@ -861,8 +862,7 @@ __device__ __forceinline__ void lds_pass_list(const uint32_t* s_list, uint32_t n
 // the number of keys equal to T that are kept (k == 0: T above every
 // finite key).  Ends with every thread past a barrier.  LIST: the keys of
 // the first digit's bin go to a short list for the last two passes (else
-// those passes read the whole segment, which the two selections of EF-mixed
-// find faster).
+// those passes read the whole segment).
 // hist_ready: s_h already holds the first digit's counts of every key (the
 // load loop counted them as the values arrived); only the search is left.
 template <int NT, bool LIST = true>
@@ -1008,7 +1008,13 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
   const uint32_t t = threadIdx.x;
   const uint32_t L = (uint32_t)a.L;   // <= LDS_MAX (the plan guarantees it)
   const bool vec = ((((uintptr_t)a.x | (uintptr_t)a.e | (uintptr_t)a.m) & 15u) == 0) && (L % 4u) == 0;
-  for (uint64_t seg = blockIdx.x; seg < a.n_seg; seg += gridDim.x) {
+  // EF-mixed: two work items per segment, the input's selection (even) and
+  // the buffer's (odd), independent of each other; the residual follows in
+  // a kernel of its own
+  const uint64_t n_items = (SEL == SEL_EFMIX) ? 2 * a.n_seg : a.n_seg;
+  for (uint64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const uint64_t seg = (SEL == SEL_EFMIX) ? item >> 1 : item;
+    const bool buf_list = (SEL == SEL_EFMIX) && (item & 1u);
     const Raw* xs = (const Raw*)a.x + seg * a.L;
     float* es = (SEL == SEL_EF || SEL == SEL_EFMIX) ? a.e + seg * a.L : nullptr;
     // AQ-SGD: the example's buffer row; v = a - m
@@ -1045,8 +1051,14 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
         for (uint32_t j = 0; j < 4; ++j) {
           const uint32_t i0 = ((h + j) * NT + t) * 4;
           if (i0 < L) {
-            // (EF-mixed reads x again at the end: cached loads keep it in L2)
-            load_run<Raw, 4, SEL != SEL_EFMIX>(xs + i0, xr[j]);
+            if constexpr (SEL == SEL_EFMIX) {
+              // one array per workgroup: x, or the buffer e; cached loads,
+              // as the residual kernel reads both again
+              if (buf_list) load_run<float, 4, false>(es + i0, er[j]);
+              else load_run<Raw, 4, false>(xs + i0, xr[j]);
+            } else {
+              load_run<Raw, 4, true>(xs + i0, xr[j]);
+            }
             if constexpr (SEL == SEL_EF) load_run<float, 4, true>(es + i0, er[j]);
             if constexpr (SEL == SEL_AQSGD) load_run<Raw, 4, true>(ms + i0, mr[j]);
           }
@@ -1058,7 +1070,9 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
             u32x4 w;
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
-              float x = Elem<InT>::up(xr[j][c]);
+              float x;
+              if constexpr (SEL == SEL_EFMIX) x = buf_list ? er[j][c] : Elem<InT>::up(xr[j][c]);
+              else x = Elem<InT>::up(xr[j][c]);
               if constexpr (SEL == SEL_EF) x = x + er[j][c];
               if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(mr[j][c]);
               w[c] = __float_as_uint(x);
@@ -1078,7 +1092,8 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
           const uint32_t i = i0 + (uint32_t)c;
           float x = 0.0f;
           if (i < L) {
-            x = Elem<InT>::up(xs[i]);
+            if constexpr (SEL == SEL_EFMIX) x = buf_list ? es[i] : Elem<InT>::up(xs[i]);
+            else x = Elem<InT>::up(xs[i]);
             if constexpr (SEL == SEL_EF) x = x + es[i];
             if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(ms[i]);
             count(__float_as_uint(x));
@@ -1096,12 +1111,15 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
 
     // ---- T and the tie quota r, then the kept entries of thread t's run
     uint32_t T, r;
-    lds_threshold<NT, SEL != SEL_EFMIX>(s_v, L, (uint32_t)a.k, s_h, s_list, scratch, found, T, r, true);
+    const uint64_t kk = buf_list ? a.k2 : a.k;
+    uint32_t* const lidx = buf_list ? a.idx2 : a.idx;
+    Raw* const lval = (Raw*)(buf_list ? a.val2 : a.val);
+    uint32_t* const lblk = buf_list ? a.blk2 : a.blk;
+    lds_threshold<NT, true>(s_v, L, (uint32_t)kk, s_h, s_list, scratch, found, T, r, true);
     const uint32_t b0 = t * LDS_RUN;
     const uint32_t nr = (b0 < L) ? min(LDS_RUN, L - b0) : 0u;
-    const uint32_t km = lds_place<InT, NT>(s_v, L, b0, nr, T, r, (uint32_t)a.k, a.idx + seg * a.k,
-                                           (Raw*)a.val + seg * a.k,
-                                           a.blk ? a.blk + seg * (n_blocks(a.L) + 1) : nullptr, scratch);
+    const uint32_t km = lds_place<InT, NT>(s_v, L, b0, nr, T, r, (uint32_t)kk, lidx + seg * kk, lval + seg * kk,
+                                           lblk ? lblk + seg * (n_blocks(a.L) + 1) : nullptr, scratch);
     // AQ-SGD: the buffer row moves by the sent values at the kept entries
     // only; per half of the run, that half's buffer values are loaded at once
     if constexpr (SEL == SEL_AQSGD) {
@@ -1150,108 +1168,6 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
 #pragma unroll
           for (int c = 0; c < 4; ++c)
             if (i0 + (uint32_t)c < L) es[i0 + c] = o[c];
-        }
-      }
-    }
-    // EF-mixed (Sec. 2.4): the buffer takes the LDS for its own selection;
-    // then e' = (x minus what was sent of it) + (e minus what was sent of
-    // e).  x is exact in its dtype, so its share is x off the kept entries
-    // and +0 on them; x is read again for it rather than held in registers
-    // through the second selection.  Where both lists hold an index the
-    // receiver rounds u = x + wire(e) (binary32) once to the wire dtype, and
-    // the part that rounding drops, u - wire(u), stays in the buffer too.
-    if constexpr (SEL == SEL_EFMIX) {
-      __syncthreads();
-      // the buffer into LDS, in the input's piece layout
-      if (vec) {
-#pragma unroll
-        for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
-          float er[4][4];
-#pragma unroll
-          for (uint32_t j = 0; j < 4; ++j) {
-            const uint32_t i0 = ((h + j) * NT + t) * 4;
-            if (i0 < L) load_run<float, 4, true>(es + i0, er[j]);
-          }
-#pragma unroll
-          for (uint32_t j = 0; j < 4; ++j) {
-            const uint32_t i0 = ((h + j) * NT + t) * 4;
-            if (i0 < L)
-              *reinterpret_cast<u32x4*>(&s_v[i0]) = u32x4{__float_as_uint(er[j][0]), __float_as_uint(er[j][1]),
-                                                          __float_as_uint(er[j][2]), __float_as_uint(er[j][3])};
-          }
-        }
-      } else {
-        for (uint32_t j = 0; j < LDS_PIECES; ++j) {
-          const uint32_t i0 = (j * NT + t) * 4;
-          if (i0 >= L) break;
-          u32x4 w;
-#pragma unroll
-          for (int c = 0; c < 4; ++c) w[c] = __float_as_uint((i0 + (uint32_t)c < L) ? es[i0 + c] : 0.0f);
-          *reinterpret_cast<u32x4*>(&s_v[i0]) = w;
-        }
-      }
-      __syncthreads();
-      uint32_t T2, r2;
-      lds_threshold<NT, false>(s_v, L, (uint32_t)a.k2, s_h, s_list, scratch, found, T2, r2);
-      const uint32_t km2 = lds_place<InT, NT>(s_v, L, b0, nr, T2, r2, (uint32_t)a.k2, a.idx2 + seg * a.k2,
-                                              (Raw*)a.val2 + seg * a.k2,
-                                              a.blk2 ? a.blk2 + seg * (n_blocks(a.L) + 1) : nullptr, scratch);
-      // the residual in the load's layout (piece q = 4 elements, lanes
-      // consecutive: whole lines per wavefront access); the kept masks of
-      // the runs go through LDS, x is loaded for all pieces first
-      s_h[t] = km;
-      s_h[NT + t] = km2;
-      // (opaque copies of the row pointer and of the thread index: the
-      // addresses below are neither merged with the first loads of x nor
-      // computed ahead of the loop, either of which holds registers through
-      // both selections)
-      uint64_t xa = (uint64_t)(uintptr_t)xs;
-      uint32_t tq = t;
-      asm volatile("" : "+s"(xa), "+v"(tq));
-      const Raw* xs2 = (const Raw*)(uintptr_t)xa;
-      __syncthreads();
-      // four pieces at a time: their loads of x go out together
-#pragma unroll
-      for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
-        Raw xr[4][4];
-#pragma unroll
-        for (uint32_t j = 0; j < 4; ++j) {
-          const uint32_t i0 = ((h + j) * NT + tq) * 4;
-          if (vec) {
-            if (i0 < L) load_run<Raw, 4, false>(xs2 + i0, xr[j]);
-          } else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) xr[j][c] = (i0 + (uint32_t)c < L) ? xs2[i0 + c] : Raw{};
-          }
-        }
-#pragma unroll
-        for (uint32_t j = 0; j < 4; ++j) {
-          const uint32_t i0 = ((h + j) * NT + tq) * 4;
-          if (i0 >= L) continue;
-          const u32x4 w = *reinterpret_cast<const u32x4*>(&s_v[i0]);
-          const uint32_t sh = i0 % LDS_RUN;
-          const uint32_t kx4 = s_h[i0 / LDS_RUN] >> sh, ke4 = s_h[NT + i0 / LDS_RUN] >> sh;
-          float o[4];
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const float xv = Elem<InT>::up(xr[j][c]);
-            const bool in_x = (kx4 >> c) & 1u, in_e = (ke4 >> c) & 1u;
-            const float rx = xv - (in_x ? xv : 0.0f);
-            const float v = __uint_as_float(w[c]);
-            const float ve = through<InT>(v);
-            float re = v - (in_e ? ve : 0.0f);
-            if (in_x && in_e) {
-              const float u = xv + ve;
-              re = re + (u - through<InT>(u));
-            }
-            o[c] = rx + re;
-          }
-          if (vec) store_run<float, 4, true>(es + i0, o);
-          else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-              if (i0 + (uint32_t)c < L) es[i0 + c] = o[c];
-          }
         }
       }
     }

@@ -554,7 +554,8 @@ TC_API tc_status tc_efmix_step(const tc_codec* c, const void* x, int dt, float* 
                                   {out_e->val, bytes_of(c->n_seg * ke, dt), "buffer list val"},
                                   {out_e->blk, 4 * c->n_seg * nb, "buffer list blk"}}));
   TC_PRECONDITION(check_values(dt, x, e, n, stream));
-  const tc::SegPlan p = tc::plan_lds(tc::SEL_EFMIX, dt, c->n_seg);
+  // the two selections (two workgroups per segment), then the residual
+  const tc::SegPlan p = tc::plan_lds(tc::SEL_EFMIX, dt, 2 * c->n_seg);
   tc::TopkArgs a{};
   a.x = x;
   a.e = e;
@@ -570,6 +571,19 @@ TC_API tc_status tc_efmix_step(const tc_codec* c, const void* x, int dt, float* 
   a.L = c->seg_len;
   hipError_t he = tc::launch_topk(tc::SEL_EFMIX, dt, p, a, (hipStream_t)stream);
   if (he != hipSuccess) return hip_fail(he, "efmix launch");
+  tc::EfmixResidArgs r{};
+  r.x = x;
+  r.e = e;
+  r.idx = out_x->idx;
+  r.blk = out_x->blk;
+  r.idx2 = out_e->idx;
+  r.blk2 = out_e->blk;
+  r.n_seg = c->n_seg;
+  r.L = c->seg_len;
+  r.k = kx;
+  r.k2 = ke;
+  he = tc::launch_efmix_resid(dt, r, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "efmix residual launch");
   return TC_OK;
 }
 

@@ -104,6 +104,18 @@ struct ScatterArgs {
 hipError_t launch_topk_decompress(int wire, int out_dt, const ScatterArgs& a, hipStream_t st);
 hipError_t launch_efmix_recv(int wire, int out_dt, const ScatterArgs& a, hipStream_t st);
 
+// EF-mixed residual after both selections (the sender's second kernel)
+struct EfmixResidArgs {
+  const void* x;         // [n_seg][L] input
+  float* e;              // [n_seg][L] residual (in-out)
+  const uint32_t* idx;   // the input's list [n_seg][k]
+  const uint32_t* blk;   // its block table or nullptr
+  const uint32_t* idx2;  // the buffer's list [n_seg][k2]
+  const uint32_t* blk2;  // its block table or nullptr
+  uint64_t n_seg, L, k, k2;
+};
+hipError_t launch_efmix_resid(int dt, const EfmixResidArgs& a, hipStream_t st);
+
 // TopK at given indices (another tensor's TopK payload), optionally inside
 // error feedback
 struct GatherArgs {
