@@ -1042,7 +1042,60 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
       zc += z;
       atomicAdd(&s_h[pick(z, dummy, kk >> 19)], 1u);
     };
-    if (vec) {
+    if constexpr (SEL == SEL_EFMIX) {
+      // one array per workgroup, x or the buffer e, the source chosen once
+      // (a choice per piece would put each load in a branch of its own and
+      // serialise them); cached loads, as the residual kernel reads both
+      // again
+      auto fill = [&](auto from_e) {
+        constexpr bool FE = decltype(from_e)::value;
+#pragma unroll
+        for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
+          float f[4][4];
+#pragma unroll
+          for (uint32_t j = 0; j < 4; ++j) {
+            const uint32_t i0 = ((h + j) * NT + t) * 4;
+            if (vec) {
+              if (i0 < L) {
+                // (vec: the pieces are aligned, no alignment branches)
+                if constexpr (FE) {
+                  load16<float, 4, false>(es + i0, f[j]);
+                } else if constexpr (sizeof(Raw) == 4) {
+                  load16<float, 4, false>(reinterpret_cast<const float*>(xs) + i0, f[j]);
+                } else {
+                  Raw xr[4];
+                  load_run<Raw, 4, false>(xs + i0, xr);
+#pragma unroll
+                  for (int c = 0; c < 4; ++c) f[j][c] = Elem<InT>::up(xr[c]);
+                }
+              }
+            } else {
+#pragma unroll
+              for (int c = 0; c < 4; ++c) {
+                const uint32_t i = i0 + (uint32_t)c;
+                if constexpr (FE) f[j][c] = (i < L) ? es[i] : 0.0f;
+                else f[j][c] = (i < L) ? Elem<InT>::up(xs[i]) : 0.0f;
+              }
+            }
+          }
+#pragma unroll
+          for (uint32_t j = 0; j < 4; ++j) {
+            const uint32_t i0 = ((h + j) * NT + t) * 4;
+            if (i0 < L) {
+              u32x4 w;
+#pragma unroll
+              for (int c = 0; c < 4; ++c) {
+                w[c] = __float_as_uint(f[j][c]);
+                if (i0 + (uint32_t)c < L) count(w[c]);
+              }
+              *reinterpret_cast<u32x4*>(&s_v[i0]) = w;
+            }
+          }
+        }
+      };
+      if (buf_list) fill(std::true_type{});
+      else fill(std::false_type{});
+    } else if (vec) {
 #pragma unroll
       for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
         Raw xr[4][4], mr[4][4];
@@ -1051,14 +1104,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
         for (uint32_t j = 0; j < 4; ++j) {
           const uint32_t i0 = ((h + j) * NT + t) * 4;
           if (i0 < L) {
-            if constexpr (SEL == SEL_EFMIX) {
-              // one array per workgroup: x, or the buffer e; cached loads,
-              // as the residual kernel reads both again
-              if (buf_list) load_run<float, 4, false>(es + i0, er[j]);
-              else load_run<Raw, 4, false>(xs + i0, xr[j]);
-            } else {
-              load_run<Raw, 4, true>(xs + i0, xr[j]);
-            }
+            load_run<Raw, 4, true>(xs + i0, xr[j]);
             if constexpr (SEL == SEL_EF) load_run<float, 4, true>(es + i0, er[j]);
             if constexpr (SEL == SEL_AQSGD) load_run<Raw, 4, true>(ms + i0, mr[j]);
           }
@@ -1070,9 +1116,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
             u32x4 w;
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
-              float x;
-              if constexpr (SEL == SEL_EFMIX) x = buf_list ? er[j][c] : Elem<InT>::up(xr[j][c]);
-              else x = Elem<InT>::up(xr[j][c]);
+              float x = Elem<InT>::up(xr[j][c]);
               if constexpr (SEL == SEL_EF) x = x + er[j][c];
               if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(mr[j][c]);
               w[c] = __float_as_uint(x);
@@ -1092,8 +1136,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
           const uint32_t i = i0 + (uint32_t)c;
           float x = 0.0f;
           if (i < L) {
-            if constexpr (SEL == SEL_EFMIX) x = buf_list ? es[i] : Elem<InT>::up(xs[i]);
-            else x = Elem<InT>::up(xs[i]);
+            x = Elem<InT>::up(xs[i]);
             if constexpr (SEL == SEL_EF) x = x + es[i];
             if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(ms[i]);
             count(__float_as_uint(x));
