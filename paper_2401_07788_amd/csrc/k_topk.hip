@@ -153,6 +153,25 @@ __device__ __forceinline__ void load16(const Raw* p, Raw (&out)[E]) {
   const u32x4 w = vload<STREAM>(reinterpret_cast<const u32x4*>(p));
   __builtin_memcpy(out, &w, 16);
 }
+// one 16-byte run at base + off when `in`, else the run at base (one the
+// caller knows to be in bounds, and discards): the address is a select, so
+// that no branch stands between the loads
+template <typename Raw, int E, bool STREAM>
+__device__ __forceinline__ void load16_in(const Raw* base, uint32_t off, bool in, Raw (&out)[E]) {
+  load16<Raw, E, STREAM>(base + (in ? off : 0u), out);
+}
+// one 4-element piece (16 bytes of fp32, 8 of a 16-bit format), which the
+// caller has aligned: no alignment test
+template <typename Raw, bool STREAM>
+__device__ __forceinline__ void load_piece(const Raw* p, Raw (&out)[4]) {
+  if constexpr (sizeof(Raw) == 4) {
+    const u32x4 w = vload<STREAM>(reinterpret_cast<const u32x4*>(p));
+    __builtin_memcpy(out, &w, 16);
+  } else {
+    const u32x2 w = vload<STREAM>(reinterpret_cast<const u32x2*>(p));
+    __builtin_memcpy(out, &w, 8);
+  }
+}
 template <typename Raw, int E, bool STREAM>
 __device__ __forceinline__ void store16(Raw* p, const Raw (&in)[E]) {
   static_assert(E * sizeof(Raw) == 16, "one 16-byte access");
@@ -517,47 +536,66 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
 
   // ---- producer: run j of this thread starts at chunk offset (j*NT + t)*E;
   // all loads are issued before any is used, the input's before the buffer
-  // row's address (AQSGD: the example id) is waited for
+  // row's address (AQSGD: the example id) is waited for.  With every buffer
+  // 16-byte aligned and L a multiple of E (vec), a run lies wholly inside or
+  // wholly past the segment's end: one past it reads the chunk's first run
+  // (in bounds, as c0 < L) and its values become +0 below, so that the loads
+  // carry no branch (a branch per run that writes the same registers on
+  // both sides makes each load wait for the one before).  Otherwise runs
+  // load element by element, and land before the paths join.
   int n[R];
   Raw xr[R][E];
   Raw mr[R][E];               // AQSGD: the buffer row, kept for the update
   float er[R][E];             // EF: the residual
+  // AQSGD: the example id, a scalar read, is waited for apart from the
+  // input's loads
+  int64_t id = 0;
+  if constexpr (SEL == SEL_AQSGD) id = load_uniform(a.ids + seg);
+  auto load_x = [&](auto vec_c) {
+    constexpr bool VEC = decltype(vec_c)::value;
 #pragma unroll
-  for (int j = 0; j < R; ++j) {
-    const uint32_t off = (uint32_t)(j * NT + t) * E;
-    n[j] = (int)min((uint32_t)E, (uint32_t)sat_sub(a.L, c0 + off));   // L < 2^32
-    if (vec && n[j] == E) load16<Raw, E, true>(xs + off, xr[j]);
-    else if (n[j] > 0) load_run_partial<Raw, E, true>(xs + off, n[j], Raw{}, xr[j]);
-    else {
+    for (int j = 0; j < R; ++j) {
+      const uint32_t off = (uint32_t)(j * NT + t) * E;
+      n[j] = (int)min((uint32_t)E, (uint32_t)sat_sub(a.L, c0 + off));   // L < 2^32
+      if constexpr (VEC) {
+        load16_in<Raw, E, true>(xs, off, n[j] > 0, xr[j]);
+      } else if (n[j] > 0) {
+        load_run_partial<Raw, E, true>(xs + off, n[j], Raw{}, xr[j]);
+      } else {
 #pragma unroll
-      for (int i = 0; i < E; ++i) xr[j][i] = Raw{};
+        for (int i = 0; i < E; ++i) xr[j][i] = Raw{};
+      }
     }
-  }
+    if constexpr (!VEC) __builtin_amdgcn_s_waitcnt(0);
+  };
+  if (vec) load_x(std::true_type{});
+  else load_x(std::false_type{});
   Raw* ms = nullptr;
   if constexpr (SEL == SEL_AQSGD) {
-    const int64_t id = a.ids[seg];
     if (id < 0 || (uint64_t)id >= a.n_samples) {
       if (t == 0 && part == 0) raise_error(KERR_BAD_ID);
       return;                  // every workgroup of the group skips alike
     }
     ms = (Raw*)a.m + (uint64_t)id * a.L + c0;
   }
+  auto load_me = [&](auto vec_c) {
+    constexpr bool VEC = decltype(vec_c)::value;
 #pragma unroll
-  for (int j = 0; j < R; ++j) {
-    const uint32_t off = (uint32_t)(j * NT + t) * E;
-    if (vec && n[j] == E) {
-      if constexpr (SEL == SEL_AQSGD) load16<Raw, E, true>(ms + off, mr[j]);
-      if constexpr (SEL == SEL_EF) {
-        if constexpr (E == 4) {
-          load16<float, 4, true>(es + off, *reinterpret_cast<float(*)[4]>(&er[j][0]));
-        } else {
-          load16<float, 4, false>(es + off, *reinterpret_cast<float(*)[4]>(&er[j][0]));
-          load16<float, 4, false>(es + off + 4, *reinterpret_cast<float(*)[4]>(&er[j][4]));
+    for (int j = 0; j < R; ++j) {
+      const uint32_t off = (uint32_t)(j * NT + t) * E;
+      if constexpr (VEC) {
+        const bool in = n[j] > 0;
+        if constexpr (SEL == SEL_AQSGD) load16_in<Raw, E, true>(ms, off, in, mr[j]);
+        if constexpr (SEL == SEL_EF) {
+          if constexpr (E == 4) {
+            load16_in<float, 4, true>(es, off, in, *reinterpret_cast<float(*)[4]>(&er[j][0]));
+          } else {
+            load16_in<float, 4, false>(es, off, in, *reinterpret_cast<float(*)[4]>(&er[j][0]));
+            load16_in<float, 4, false>(es + 4, off, in, *reinterpret_cast<float(*)[4]>(&er[j][4]));
+          }
         }
-      }
-    } else {
-      // elements past the segment's end read as +0 (x, m and e alike)
-      if (n[j] > 0) {
+      } else if (n[j] > 0) {
+        // elements past the segment's end read as +0 (x, m and e alike)
         if constexpr (SEL == SEL_AQSGD) load_run_partial<Raw, E, true>(ms + off, n[j], Raw{}, mr[j]);
         if constexpr (SEL == SEL_EF) load_run_partial<float, E, true>(es + off, n[j], 0.0f, er[j]);
       } else {
@@ -565,7 +603,10 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
         for (int i = 0; i < E; ++i) { mr[j][i] = Raw{}; er[j][i] = 0.0f; }
       }
     }
-  }
+    if constexpr (!VEC) __builtin_amdgcn_s_waitcnt(0);
+  };
+  if (vec) load_me(std::true_type{});
+  else load_me(std::false_type{});
   float v[R][E];
 #pragma unroll
   for (int j = 0; j < R; ++j)
@@ -574,10 +615,11 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
       float x = Elem<InT>::up(xr[j][i]);
       if constexpr (SEL == SEL_EF) x = x + er[j][i];
       if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(mr[j][i]);
-      v[j][i] = x;     // past the segment's end: +0 - +0 or +0 + 0 = +0
+      v[j][i] = (n[j] > 0) ? x : 0.0f;     // +0 past the segment's end
     }
   // AQSGD: the buffer row waits in LDS for the update (it is not needed
-  // before), which keeps it out of registers during the selection
+  // before), which keeps it out of registers during the selection; a run
+  // past the segment's end is never stored back
   if constexpr (SEL == SEL_AQSGD) {
 #pragma unroll
     for (int j = 0; j < R; ++j) store16<Raw, E, false>(mlds + (uint32_t)(j * NT + t) * E, mr[j]);
@@ -1020,7 +1062,7 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
     // AQ-SGD: the example's buffer row; v = a - m
     Raw* ms = nullptr;
     if constexpr (SEL == SEL_AQSGD) {
-      const int64_t id = a.ids[seg];
+      const int64_t id = load_uniform(a.ids + seg);
       if (id < 0 || (uint64_t)id >= a.n_samples) {
         if (t == 0) raise_error(KERR_BAD_ID);
         continue;                  // every thread skips alike
@@ -1043,31 +1085,32 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
       atomicAdd(&s_h[pick(z, dummy, kk >> 19)], 1u);
     };
     if constexpr (SEL == SEL_EFMIX) {
-      // one array per workgroup, x or the buffer e, the source chosen once
-      // (a choice per piece would put each load in a branch of its own and
-      // serialise them); cached loads, as the residual kernel reads both
-      // again
-      auto fill = [&](auto from_e) {
+      // one array per workgroup, x or the buffer e, the source and the
+      // alignment case chosen once (a choice per piece would put each load
+      // in a branch of its own and serialise them); cached loads, as the
+      // residual kernel reads both again
+      auto fill = [&](auto from_e, auto vec_c) {
         constexpr bool FE = decltype(from_e)::value;
+        constexpr bool VEC = decltype(vec_c)::value;
 #pragma unroll
         for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
           float f[4][4];
 #pragma unroll
           for (uint32_t j = 0; j < 4; ++j) {
             const uint32_t i0 = ((h + j) * NT + t) * 4;
-            if (vec) {
-              if (i0 < L) {
-                // (vec: the pieces are aligned, no alignment branches)
-                if constexpr (FE) {
-                  load16<float, 4, false>(es + i0, f[j]);
-                } else if constexpr (sizeof(Raw) == 4) {
-                  load16<float, 4, false>(reinterpret_cast<const float*>(xs) + i0, f[j]);
-                } else {
-                  Raw xr[4];
-                  load_run<Raw, 4, false>(xs + i0, xr);
+            if constexpr (VEC) {
+              // a piece past the segment's end reads the first piece
+              // (unused), so that no branch stands between the loads
+              const uint32_t ia = (i0 < L) ? i0 : 0u;
+              if constexpr (FE) {
+                load16<float, 4, false>(es + ia, f[j]);
+              } else if constexpr (sizeof(Raw) == 4) {
+                load16<float, 4, false>(reinterpret_cast<const float*>(xs) + ia, f[j]);
+              } else {
+                Raw xr[4];
+                load_piece<Raw, false>(xs + ia, xr);
 #pragma unroll
-                  for (int c = 0; c < 4; ++c) f[j][c] = Elem<InT>::up(xr[c]);
-                }
+                for (int c = 0; c < 4; ++c) f[j][c] = Elem<InT>::up(xr[c]);
               }
             } else {
 #pragma unroll
@@ -1093,8 +1136,13 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
           }
         }
       };
-      if (buf_list) fill(std::true_type{});
-      else fill(std::false_type{});
+      if (buf_list) {
+        if (vec) fill(std::true_type{}, std::true_type{});
+        else fill(std::true_type{}, std::false_type{});
+      } else {
+        if (vec) fill(std::false_type{}, std::true_type{});
+        else fill(std::false_type{}, std::false_type{});
+      }
     } else if (vec) {
 #pragma unroll
       for (uint32_t h = 0; h < LDS_PIECES; h += 4) {
@@ -1102,12 +1150,14 @@ __global__ __launch_bounds__(LDS_NT) void k_topk_lds(TopkArgs a) {
         float er[4][4];
 #pragma unroll
         for (uint32_t j = 0; j < 4; ++j) {
+          // (vec: pieces aligned and whole; one past the segment's end
+          // reads the first piece, unused, so that no branch stands between
+          // the loads)
           const uint32_t i0 = ((h + j) * NT + t) * 4;
-          if (i0 < L) {
-            load_run<Raw, 4, true>(xs + i0, xr[j]);
-            if constexpr (SEL == SEL_EF) load_run<float, 4, true>(es + i0, er[j]);
-            if constexpr (SEL == SEL_AQSGD) load_run<Raw, 4, true>(ms + i0, mr[j]);
-          }
+          const uint32_t ia = (i0 < L) ? i0 : 0u;
+          load_piece<Raw, true>(xs + ia, xr[j]);
+          if constexpr (SEL == SEL_EF) load_piece<float, true>(es + ia, er[j]);
+          if constexpr (SEL == SEL_AQSGD) load_piece<Raw, true>(ms + ia, mr[j]);
         }
 #pragma unroll
         for (uint32_t j = 0; j < 4; ++j) {

@@ -104,6 +104,14 @@ __device__ __forceinline__ void vstore(V* p, V v) {
   else *p = v;
 }
 
+// A workgroup-uniform read of memory that no kernel in flight writes, in
+// the constant address space: the scalar unit serves it, counted apart from
+// the vector loads, so that waiting for it does not wait for them.
+template <typename T>
+__device__ __forceinline__ T load_uniform(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)p;
+}
+
 template <typename R, int N, bool STREAM = false>
 __device__ __forceinline__ void load_run(const R* __restrict__ p, R (&out)[N]) {
   constexpr int BYTES = N * (int)sizeof(R);
