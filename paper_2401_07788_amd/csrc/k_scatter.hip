@@ -12,6 +12,7 @@
 // the EF-mixed sender's residual, and TopK at given indices (index reuse for
 // gradients).
 #include <algorithm>
+#include <type_traits>
 
 #include "tc_internal.hpp"
 #include "tc_select.hpp"
@@ -150,10 +151,51 @@ constexpr uint32_t SR_MAX = 2048;
 constexpr int SR_WAVES = SC_NT / WAVE;
 static_assert(SR_MAX <= BLOCK_LEN, "a row is one block of the block table");
 
+// A row's entries j0 + r*WAVE + lane (r < EPL), all loads issued before any
+// is used: the index, the index before it (checked by the caller: indices
+// ascend) and the value's bits, one register each (two 16-bit values packed
+// in one register, or a use between two entries' loads, would make each
+// load wait for the one before).  Entries at or past k read as index
+// 0xFFFFFFFF for the check.
+template <typename W>
+using wire_bits_t = typename std::conditional<sizeof(W) == 4, uint32_t, uint16_t>::type;
+
+template <int EPL, typename UW>
+__device__ __forceinline__ void row_entries(const uint32_t* ix, const UW* vv, uint32_t j0, uint32_t k, uint32_t lane,
+                                            uint32_t (&ei)[EPL], uint32_t (&ep)[EPL], uint32_t (&ev)[EPL]) {
+  // (k >= 1: an entry at or past k reads entry 0 instead, and the caller
+  // skips it; no branch stands between the loads)
+#pragma unroll
+  for (int r = 0; r < EPL; ++r) {
+    const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
+    const uint32_t jj = (j < k) ? j : 0u;
+    ei[r] = ix[jj];
+    ev[r] = vv[jj];
+    ep[r] = ix[(jj > 0u) ? jj - 1u : 0u];
+  }
+}
+
+// the two block-table words of a row (a table of one block per row), or
+// zeros without a table; one address either way, so that the read carries
+// no branch
+static __device__ const uint32_t g_no_table[2] = {0u, 0u};
+__device__ __forceinline__ const uint32_t* row_table(const uint32_t* blk, uint64_t s, uint64_t L) {
+  return blk ? blk + s * (n_blocks(L) + 1) : g_no_table;
+}
+
+template <typename RW>
+__device__ __forceinline__ RW wire_value(uint32_t bits) {
+  const wire_bits_t<RW> u = (wire_bits_t<RW>)bits;
+  RW x;
+  __builtin_memcpy(&x, &u, sizeof(RW));
+  return x;
+}
+
 template <typename WireT, typename OutT>
 __global__ __launch_bounds__(SC_NT) void k_topk_scatter_row(ScatterArgs a) {
   using RW = typename Elem<WireT>::raw;
   using RO = typename Elem<OutT>::raw;
+  using UW = wire_bits_t<RW>;
   constexpr uint32_t PER = 16 / sizeof(RO);
   constexpr int EPL = 4;   // entries per lane per round, loads in flight together
   __shared__ __attribute__((aligned(16))) RO buf[SR_WAVES][SR_MAX];
@@ -164,36 +206,27 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter_row(ScatterArgs a) {
   const uint64_t stride = (uint64_t)gridDim.x * SR_WAVES;
   for (uint64_t s = (uint64_t)blockIdx.x * SR_WAVES + w; s < a.n_seg; s += stride) {
     const uint32_t* ix = a.idx + s * a.k;
-    const RW* vv = (const RW*)a.val + s * a.k;
-    // a block table, when given, must describe the row's one block
-    if (a.blk && lane == 0) {
-      const uint32_t* bt = a.blk + s * (n_blocks(a.L) + 1);
-      if (bt[0] != 0u || bt[1] != k) raise_error(KERR_BAD_INDEX);
-    }
+    const UW* vv = (const UW*)a.val + s * a.k;
+    // a block table, when given, must describe the row's one block; it is
+    // read with the first round of entries and checked after it
+    const uint32_t* bt = row_table(a.blk, s, a.L);
+    const uint32_t bt0 = bt[0], bt1 = bt[1];
+    uint32_t bad = 0u;
     for (uint32_t q = lane; q * PER < L; q += WAVE) reinterpret_cast<u32x4*>(b)[q] = u32x4{0u, 0u, 0u, 0u};
     for (uint32_t j0 = 0; j0 < k; j0 += EPL * WAVE) {
-      uint32_t ei[EPL], ep[EPL];
-      RW ev[EPL];
-#pragma unroll
-      for (int r = 0; r < EPL; ++r) {
-        const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
-        ei[r] = 0xFFFFFFFFu;
-        ep[r] = 0u;
-        if (j < k) {
-          ei[r] = ix[j];
-          ev[r] = vv[j];
-          if (j > 0) ep[r] = ix[j - 1] + 1u;   // the smallest index allowed here
-        }
-      }
+      uint32_t ei[EPL], ep[EPL], ev[EPL];
+      row_entries<EPL>(ix, vv, j0, k, lane, ei, ep, ev);
 #pragma unroll
       for (int r = 0; r < EPL; ++r) {
         const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
         if (j < k) {
-          if (ei[r] >= L || ei[r] < ep[r]) raise_error(KERR_BAD_INDEX);
-          else b[ei[r]] = Elem<OutT>::down(Elem<WireT>::up(ev[r]));
+          if (ei[r] >= L || (j > 0 && ei[r] <= ep[r])) bad = 1u;
+          else b[ei[r]] = Elem<OutT>::down(Elem<WireT>::up(wire_value<RW>(ev[r])));
         }
       }
     }
+    if (a.blk && (bt0 != 0u || bt1 != k)) bad = 1u;
+    if (bad) raise_error(KERR_BAD_INDEX);
     // (a wavefront's LDS accesses complete in program order)
     __builtin_amdgcn_wave_barrier();
     RO* yr = (RO*)a.y + s * a.L;
@@ -598,6 +631,7 @@ __global__ __launch_bounds__(SC_NT) void k_efmix_resid(EfmixResidArgs a) {
 template <typename T>
 __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv_row(ScatterArgs a) {
   using R = typename Elem<T>::raw;
+  using UW = wire_bits_t<R>;
   constexpr uint32_t PER = 16 / sizeof(R);
   constexpr int EPL = 4;   // entries per lane per round
   __shared__ __attribute__((aligned(16))) R buf[SR_WAVES][SR_MAX];
@@ -608,30 +642,19 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv_row(ScatterArgs a) {
   const uint64_t stride = (uint64_t)gridDim.x * SR_WAVES;
   for (uint64_t s = (uint64_t)blockIdx.x * SR_WAVES + w; s < a.n_seg; s += stride) {
     const uint32_t* ix = a.idx + s * a.k;
-    const R* vv = (const R*)a.val + s * a.k;
+    const UW* vv = (const UW*)a.val + s * a.k;
     const int64_t id = a.ids[s];
-    // the first round of entries goes out with the id
-    uint32_t ei[EPL], ep[EPL];
-    R ev[EPL];
-#pragma unroll
-    for (int r = 0; r < EPL; ++r) {
-      const uint32_t j = (uint32_t)r * WAVE + lane;
-      ei[r] = 0xFFFFFFFFu;
-      ep[r] = 0u;
-      if (j < k) {
-        ei[r] = ix[j];
-        ev[r] = vv[j];
-        if (j > 0) ep[r] = ix[j - 1] + 1u;   // the smallest index allowed here
-      }
-    }
+    // the first round of entries, and the block table's two words, go out
+    // with the id
+    const uint32_t* bt = row_table(a.blk, s, a.L);
+    const uint32_t bt0 = bt[0], bt1 = bt[1];
+    uint32_t ei[EPL], ep[EPL], ev[EPL];
+    if (k > 0) row_entries<EPL>(ix, vv, 0u, k, lane, ei, ep, ev);
     if (id < 0 || (uint64_t)id >= a.n_samples) {
       if (lane == 0) raise_error(KERR_BAD_ID);
       continue;
     }
-    if (a.blk && lane == 0) {
-      const uint32_t* bt = a.blk + s * (n_blocks(a.L) + 1);
-      if (bt[0] != 0u || bt[1] != k) raise_error(KERR_BAD_INDEX);
-    }
+    uint32_t bad = (a.blk && (bt0 != 0u || bt1 != k)) ? 1u : 0u;
     R* row = (R*)a.m + (uint64_t)id * a.L;
     for (uint32_t q = lane; q * PER < L; q += WAVE) {
       if (vec && q * PER + PER <= L) {
@@ -642,28 +665,17 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv_row(ScatterArgs a) {
     }
     // (a wavefront's LDS accesses complete in program order)
     for (uint32_t j0 = 0; j0 < k; j0 += EPL * WAVE) {
-      if (j0 > 0) {
-#pragma unroll
-        for (int r = 0; r < EPL; ++r) {
-          const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
-          ei[r] = 0xFFFFFFFFu;
-          ep[r] = 0u;
-          if (j < k) {
-            ei[r] = ix[j];
-            ev[r] = vv[j];
-            ep[r] = ix[j - 1] + 1u;
-          }
-        }
-      }
+      if (j0 > 0) row_entries<EPL>(ix, vv, j0, k, lane, ei, ep, ev);
 #pragma unroll
       for (int r = 0; r < EPL; ++r) {
         const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
         if (j < k) {
-          if (ei[r] >= L || ei[r] < ep[r]) raise_error(KERR_BAD_INDEX);
-          else b[ei[r]] = Elem<T>::down(Elem<T>::up(b[ei[r]]) + Elem<T>::up(ev[r]));
+          if (ei[r] >= L || (j > 0 && ei[r] <= ep[r])) bad = 1u;
+          else b[ei[r]] = Elem<T>::down(Elem<T>::up(b[ei[r]]) + Elem<T>::up(wire_value<R>(ev[r])));
         }
       }
     }
+    if (bad) raise_error(KERR_BAD_INDEX);
     __builtin_amdgcn_wave_barrier();
     R* out = (R*)a.y + s * a.L;
     for (uint32_t q = lane; q * PER < L; q += WAVE) {
