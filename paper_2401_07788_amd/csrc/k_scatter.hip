@@ -539,20 +539,29 @@ __global__ __launch_bounds__(SC_NT) void k_efmix_resid(EfmixResidArgs a) {
     float* ec = a.e + seg * a.L + c0;
     R xr[QPT][4];
     float er[QPT][4];
+    auto load_chunk = [&](auto vec_c) {
+      constexpr bool VEC = decltype(vec_c)::value;
 #pragma unroll
-    for (int q = 0; q < QPT; ++q) {
-      const uint32_t i0 = ((uint32_t)q * SC_NT + t) * 4;
-      if (vec && i0 + 4 <= n) {
-        load_run<R, 4, false>(xc + i0, xr[q]);
-        load_run<float, 4, false>(ec + i0, er[q]);
-      } else {
+      for (int q = 0; q < QPT; ++q) {
+        const uint32_t i0 = ((uint32_t)q * SC_NT + t) * 4;
+        if constexpr (VEC) {
+          // (vec: pieces aligned and whole; one past the chunk's end reads
+          // the chunk's first piece, unused, so that no branch stands
+          // between the loads)
+          const uint32_t ia = (i0 < n) ? i0 : 0u;
+          load_piece<R, false>(xc + ia, xr[q]);
+          load_piece<float, false>(ec + ia, er[q]);
+        } else {
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          xr[q][c] = (i0 + (uint32_t)c < n) ? xc[i0 + c] : R{};
-          er[q][c] = (i0 + (uint32_t)c < n) ? ec[i0 + c] : 0.0f;
+          for (int c = 0; c < 4; ++c) {
+            xr[q][c] = (i0 + (uint32_t)c < n) ? xc[i0 + c] : R{};
+            er[q][c] = (i0 + (uint32_t)c < n) ? ec[i0 + c] : 0.0f;
+          }
         }
       }
-    }
+    };
+    if (vec) load_chunk(std::true_type{});
+    else load_chunk(std::false_type{});
     const uint64_t kk[2] = {a.k, a.k2};
     const uint32_t* ixl[2] = {a.idx + seg * a.k, a.idx2 + seg * a.k2};
     const uint32_t* btl[2] = {a.blk ? a.blk + seg * nbt : nullptr, a.blk2 ? a.blk2 + seg * nbt : nullptr};

@@ -160,18 +160,6 @@ template <typename Raw, int E, bool STREAM>
 __device__ __forceinline__ void load16_in(const Raw* base, uint32_t off, bool in, Raw (&out)[E]) {
   load16<Raw, E, STREAM>(base + (in ? off : 0u), out);
 }
-// one 4-element piece (16 bytes of fp32, 8 of a 16-bit format), which the
-// caller has aligned: no alignment test
-template <typename Raw, bool STREAM>
-__device__ __forceinline__ void load_piece(const Raw* p, Raw (&out)[4]) {
-  if constexpr (sizeof(Raw) == 4) {
-    const u32x4 w = vload<STREAM>(reinterpret_cast<const u32x4*>(p));
-    __builtin_memcpy(out, &w, 16);
-  } else {
-    const u32x2 w = vload<STREAM>(reinterpret_cast<const u32x2*>(p));
-    __builtin_memcpy(out, &w, 8);
-  }
-}
 template <typename Raw, int E, bool STREAM>
 __device__ __forceinline__ void store16(Raw* p, const Raw (&in)[E]) {
   static_assert(E * sizeof(Raw) == 16, "one 16-byte access");

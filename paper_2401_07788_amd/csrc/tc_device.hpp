@@ -174,6 +174,19 @@ __device__ __forceinline__ void store_run(R* __restrict__ p, const R (&in)[N]) {
   for (int i = 0; i < N; ++i) p[i] = in[i];
 }
 
+// one 4-element piece (16 bytes of fp32, 8 of a 16-bit format), which the
+// caller has aligned: no alignment test
+template <typename Raw, bool STREAM>
+__device__ __forceinline__ void load_piece(const Raw* p, Raw (&out)[4]) {
+  if constexpr (sizeof(Raw) == 4) {
+    const u32x4 w = vload<STREAM>(reinterpret_cast<const u32x4*>(p));
+    __builtin_memcpy(out, &w, 16);
+  } else {
+    const u32x2 w = vload<STREAM>(reinterpret_cast<const u32x2*>(p));
+    __builtin_memcpy(out, &w, 8);
+  }
+}
+
 // Load a run that may be cut short at `n` valid elements (n <= N); elements
 // past n are left as `fill`.
 template <typename R, int N, bool STREAM = false>
