@@ -906,39 +906,54 @@ __global__ __launch_bounds__(SC_NT) void k_gather_ef_row(GatherArgs a) {
     R* vo = (R*)a.val + s * a.k;
     const R* xs = (const R*)a.x + s * a.L;
     float* es = a.e + s * a.L;
-    if (a.blk && lane == 0) {
-      const uint32_t* bt = a.blk + s * (n_blocks(a.L) + 1);
-      if (bt[0] != 0u || bt[1] != k) raise_error(KERR_BAD_INDEX);
-    }
-    // X = x + e into the slice, four elements per piece
-    for (uint32_t q = lane; q * 4 < L; q += WAVE) {
+    // a block table, when given, must describe the row's one block; it is
+    // read with the first loads and checked after the entries
+    const uint32_t* bt = row_table(a.blk, s, a.L);
+    const uint32_t bt0 = bt[0], bt1 = bt[1];
+    uint32_t bad = 0u;
+    // X = x + e into the slice, four elements per piece, a round of four
+    // pieces per lane loaded before any is used (vec: a piece past the
+    // row's end reads the first piece, unused)
+    constexpr int PPL = 4;
+    for (uint32_t q0 = 0; q0 * 4 < L; q0 += PPL * WAVE) {
       if (vec) {
-        R xr[4];
-        float er[4];
-        load_run<R, 4, false>(xs + q * 4, xr);
-        load_run<float, 4, false>(es + q * 4, er);
-        float o[4];
+        R xr[PPL][4];
+        float er[PPL][4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) o[c] = Elem<T>::up(xr[c]) + er[c];
-        u32x4 v4;
-        __builtin_memcpy(&v4, o, 16);
-        reinterpret_cast<u32x4*>(b)[q] = v4;
+        for (int p = 0; p < PPL; ++p) {
+          const uint32_t q = q0 + (uint32_t)p * WAVE + lane;
+          const uint32_t qa = (q * 4 < L) ? q : 0u;
+          load_piece<R, false>(xs + qa * 4, xr[p]);
+          load_piece<float, false>(es + qa * 4, er[p]);
+        }
+#pragma unroll
+        for (int p = 0; p < PPL; ++p) {
+          const uint32_t q = q0 + (uint32_t)p * WAVE + lane;
+          if (q * 4 < L) {
+            float o[4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) o[c] = Elem<T>::up(xr[p][c]) + er[p][c];
+            u32x4 v4;
+            __builtin_memcpy(&v4, o, 16);
+            reinterpret_cast<u32x4*>(b)[q] = v4;
+          }
+        }
       } else {
-        for (uint32_t c = q * 4; c < min(L, q * 4 + 4); ++c) b[c] = Elem<T>::up(xs[c]) + es[c];
+        for (uint32_t q = q0 + lane; q < q0 + PPL * WAVE && q * 4 < L; q += WAVE)
+          for (uint32_t c = q * 4; c < min(L, q * 4 + 4); ++c) b[c] = Elem<T>::up(xs[c]) + es[c];
       }
     }
     // (a wavefront's LDS accesses complete in program order)
     for (uint32_t j0 = 0; j0 < k; j0 += EPL * WAVE) {
+      // (k >= 1: an entry at or past k reads entry 0 and is skipped; no
+      // branch stands between the loads)
       uint32_t ei[EPL], ep[EPL];
 #pragma unroll
       for (int r = 0; r < EPL; ++r) {
         const uint32_t j = j0 + (uint32_t)r * WAVE + lane;
-        ei[r] = 0xFFFFFFFFu;
-        ep[r] = 0u;
-        if (j < k) {
-          ei[r] = ix[j];
-          if (j > 0) ep[r] = ix[j - 1] + 1u;   // the smallest index allowed here
-        }
+        const uint32_t jj = (j < k) ? j : 0u;
+        ei[r] = ix[jj];
+        ep[r] = ix[(jj > 0u) ? jj - 1u : 0u];
       }
 #pragma unroll
       for (int r = 0; r < EPL; ++r) {
@@ -946,10 +961,10 @@ __global__ __launch_bounds__(SC_NT) void k_gather_ef_row(GatherArgs a) {
         if (j < k) {
           const uint32_t i = ei[r];
           if (i >= L) {
-            raise_error(KERR_BAD_INDEX);
+            bad = 1u;
             vo[j] = R{};
           } else {
-            if (i < ep[r]) raise_error(KERR_BAD_INDEX);
+            if (j > 0 && i <= ep[r]) bad = 1u;   // not ascending
             const float X = b[i];
             vo[j] = Elem<T>::down(X);
             b[i] = X - through<T>(X);
@@ -957,6 +972,8 @@ __global__ __launch_bounds__(SC_NT) void k_gather_ef_row(GatherArgs a) {
         }
       }
     }
+    if (a.blk && (bt0 != 0u || bt1 != k)) bad = 1u;
+    if (bad) raise_error(KERR_BAD_INDEX);
     __builtin_amdgcn_wave_barrier();
     for (uint32_t q = lane; q * 4 < L; q += WAVE) {
       if (vec) {
