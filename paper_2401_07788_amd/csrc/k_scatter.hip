@@ -312,9 +312,10 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv(ScatterArgs a) {
     const uint64_t b = wi / nch, ci = wi % nch, c0 = ci * SC_CH;
     const uint64_t c1 = min(a.L, c0 + SC_CH);
     // the id and (with a block table) the payload range, in one round trip
-    const int64_t id = a.ids[b];
+    // of the scalar unit
+    const int64_t id = load_uniform(a.ids + b);
     uint32_t bj0 = 0, bj1 = 0;
-    if (a.blk) { bj0 = a.blk[b * nbt + ci]; bj1 = a.blk[b * nbt + ci + 1]; }
+    if (a.blk) { bj0 = load_uniform(a.blk + b * nbt + ci); bj1 = load_uniform(a.blk + b * nbt + ci + 1); }
     if (id < 0 || (uint64_t)id >= a.n_samples) {
       if (threadIdx.x == 0) raise_error(KERR_BAD_ID);
       continue;
