@@ -51,8 +51,8 @@ __device__ __forceinline__ void chunk_range(const uint32_t* ix, const uint32_t* 
                                             uint64_t c1, uint32_t* scratch, uint32_t& j0, uint32_t& j1) {
   if (bt) {
     const uint64_t c = c0 / SC_CH;
-    j0 = bt[c];
-    j1 = bt[c + 1];
+    j0 = load_uniform(bt + c);        // (c0 is the same for the whole workgroup)
+    j1 = load_uniform(bt + c + 1);
     if (j0 > j1 || j1 > k || j1 - j0 > c1 - c0) {
       if (threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
       j0 = j1 = 0;
@@ -91,7 +91,7 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter(ScatterArgs a) {
     // entries past the segment's end belong to no chunk: the last chunk flags them
     if (c1 == a.L && j1 < a.k && threadIdx.x == 0) raise_error(KERR_BAD_INDEX);
     float lo = 0.0f, scale = 0.0f;
-    if constexpr (MODE == MODE_CODES) { lo = a.meta[2 * seg]; scale = a.meta[2 * seg + 1]; }
+    if constexpr (MODE == MODE_CODES) { lo = load_uniform(a.meta + 2 * seg); scale = load_uniform(a.meta + 2 * seg + 1); }
     // this thread's entries j0 + t + r*SC_NT, all loaded first
     uint32_t ei[SC_EPT];
     float ex[SC_EPT];
@@ -459,7 +459,7 @@ __global__ __launch_bounds__(SC_NT) void k_efmix_scatter(ScatterArgs a) {
     if (btl[0] && btl[1]) {
       const uint64_t c = c0 / SC_CH;
 #pragma unroll
-      for (int l = 0; l < 2; ++l) { r0[l] = btl[l][c]; r1[l] = btl[l][c + 1]; }
+      for (int l = 0; l < 2; ++l) { r0[l] = load_uniform(btl[l] + c); r1[l] = load_uniform(btl[l] + c + 1); }
 #pragma unroll
       for (int l = 0; l < 2; ++l) {
         if (r0[l] > r1[l] || r1[l] > kk[l] || r1[l] - r0[l] > n) {
@@ -572,7 +572,7 @@ __global__ __launch_bounds__(SC_NT) void k_efmix_resid(EfmixResidArgs a) {
     if (btl[0] && btl[1]) {
       const uint64_t c = c0 / SC_CH;
 #pragma unroll
-      for (int l = 0; l < 2; ++l) { r0[l] = btl[l][c]; r1[l] = btl[l][c + 1]; }
+      for (int l = 0; l < 2; ++l) { r0[l] = load_uniform(btl[l] + c); r1[l] = load_uniform(btl[l] + c + 1); }
 #pragma unroll
       for (int l = 0; l < 2; ++l) {
         if (r0[l] > r1[l] || r1[l] > kk[l] || r1[l] - r0[l] > n) {
