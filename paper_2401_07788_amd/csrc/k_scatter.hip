@@ -199,7 +199,9 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter_row(ScatterArgs a) {
   constexpr uint32_t PER = 16 / sizeof(RO);
   constexpr int EPL = 4;   // entries per lane per round, loads in flight together
   __shared__ __attribute__((aligned(16))) RO buf[SR_WAVES][SR_MAX];
-  const uint32_t w = threadIdx.x / WAVE, lane = (uint32_t)lane_id();
+  // (the wavefront's number as a scalar: a row's table words are read
+  // through the scalar unit)
+  const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x / WAVE)), lane = (uint32_t)lane_id();
   RO* b = buf[w];
   const uint32_t L = (uint32_t)a.L, k = (uint32_t)a.k;   // k <= L <= SR_MAX (the launcher checks)
   const bool vec = (((uintptr_t)a.y | (L * sizeof(RO))) & 15u) == 0;
@@ -210,7 +212,7 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter_row(ScatterArgs a) {
     // a block table, when given, must describe the row's one block; it is
     // read with the first round of entries and checked after it
     const uint32_t* bt = row_table(a.blk, s, a.L);
-    const uint32_t bt0 = bt[0], bt1 = bt[1];
+    const uint32_t bt0 = load_uniform(bt), bt1 = load_uniform(bt + 1);
     uint32_t bad = 0u;
     for (uint32_t q = lane; q * PER < L; q += WAVE) reinterpret_cast<u32x4*>(b)[q] = u32x4{0u, 0u, 0u, 0u};
     for (uint32_t j0 = 0; j0 < k; j0 += EPL * WAVE) {
@@ -645,7 +647,9 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv_row(ScatterArgs a) {
   constexpr uint32_t PER = 16 / sizeof(R);
   constexpr int EPL = 4;   // entries per lane per round
   __shared__ __attribute__((aligned(16))) R buf[SR_WAVES][SR_MAX];
-  const uint32_t w = threadIdx.x / WAVE, lane = (uint32_t)lane_id();
+  // (the wavefront's number as a scalar: a row's id and table words are read
+  // through the scalar unit)
+  const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x / WAVE)), lane = (uint32_t)lane_id();
   R* b = buf[w];
   const uint32_t L = (uint32_t)a.L, k = (uint32_t)a.k;   // k <= L <= SR_MAX (the launcher checks)
   const bool vec = (((uintptr_t)a.m | (uintptr_t)a.y | (L * sizeof(R))) & 15u) == 0;
@@ -653,11 +657,11 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv_row(ScatterArgs a) {
   for (uint64_t s = (uint64_t)blockIdx.x * SR_WAVES + w; s < a.n_seg; s += stride) {
     const uint32_t* ix = a.idx + s * a.k;
     const UW* vv = (const UW*)a.val + s * a.k;
-    const int64_t id = a.ids[s];
+    const int64_t id = load_uniform(a.ids + s);
     // the first round of entries, and the block table's two words, go out
     // with the id
     const uint32_t* bt = row_table(a.blk, s, a.L);
-    const uint32_t bt0 = bt[0], bt1 = bt[1];
+    const uint32_t bt0 = load_uniform(bt), bt1 = load_uniform(bt + 1);
     uint32_t ei[EPL], ep[EPL], ev[EPL];
     if (k > 0) row_entries<EPL>(ix, vv, 0u, k, lane, ei, ep, ev);
     if (id < 0 || (uint64_t)id >= a.n_samples) {
@@ -897,7 +901,9 @@ __global__ __launch_bounds__(SC_NT) void k_gather_ef_row(GatherArgs a) {
   using R = typename Elem<T>::raw;
   constexpr int EPL = 4;   // entries per lane per round
   __shared__ __attribute__((aligned(16))) float buf[SR_WAVES][SR_MAX];
-  const uint32_t w = threadIdx.x / WAVE, lane = (uint32_t)lane_id();
+  // (the wavefront's number as a scalar: a row's table words are read
+  // through the scalar unit)
+  const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x / WAVE)), lane = (uint32_t)lane_id();
   float* b = buf[w];
   const uint32_t L = (uint32_t)a.L, k = (uint32_t)a.k;   // k <= L <= SR_MAX (the launcher checks)
   const bool vec = ((((uintptr_t)a.x | (uintptr_t)a.e) & 15u) == 0) && (L % 4u) == 0;
@@ -910,7 +916,7 @@ __global__ __launch_bounds__(SC_NT) void k_gather_ef_row(GatherArgs a) {
     // a block table, when given, must describe the row's one block; it is
     // read with the first loads and checked after the entries
     const uint32_t* bt = row_table(a.blk, s, a.L);
-    const uint32_t bt0 = bt[0], bt1 = bt[1];
+    const uint32_t bt0 = load_uniform(bt), bt1 = load_uniform(bt + 1);
     uint32_t bad = 0u;
     // X = x + e into the slice, four elements per piece, a round of four
     // pieces per lane loaded before any is used (vec: a piece past the

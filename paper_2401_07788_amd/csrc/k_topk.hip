@@ -62,7 +62,7 @@ __global__ __launch_bounds__(WAVE) void k_topk_row(TopkArgs a) {
     R mr[VPT];                 // AQSGD: the buffer row, kept for the update
     uint64_t mrow = 0;
     if constexpr (SEL == SEL_AQSGD) {
-      const int64_t id = a.ids[seg];
+      const int64_t id = load_uniform(a.ids + seg);
       if (id < 0 || (uint64_t)id >= a.n_samples) {
         if (threadIdx.x == 0) raise_error(KERR_BAD_ID);
         continue;
