@@ -155,8 +155,7 @@ static_assert(SR_MAX <= BLOCK_LEN, "a row is one block of the block table");
 // is used: the index, the index before it (checked by the caller: indices
 // ascend) and the value's bits, one register each (two 16-bit values packed
 // in one register, or a use between two entries' loads, would make each
-// load wait for the one before).  Entries at or past k read as index
-// 0xFFFFFFFF for the check.
+// load wait for the one before).
 template <typename W>
 using wire_bits_t = typename std::conditional<sizeof(W) == 4, uint32_t, uint16_t>::type;
 

@@ -104,9 +104,10 @@ __device__ __forceinline__ void vstore(V* p, V v) {
   else *p = v;
 }
 
-// A workgroup-uniform read of memory that no kernel in flight writes, in
-// the constant address space: the scalar unit serves it, counted apart from
-// the vector loads, so that waiting for it does not wait for them.
+// A read at an address that is the same for the whole wavefront, of memory
+// that no kernel in flight writes, in the constant address space: the scalar
+// unit serves it, counted apart from the vector loads, so that waiting for
+// it does not wait for them.
 template <typename T>
 __device__ __forceinline__ T load_uniform(const T* p) {
   return *(const __attribute__((address_space(4))) T*)p;
