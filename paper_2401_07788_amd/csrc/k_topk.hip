@@ -595,9 +595,14 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
   };
   if (vec) load_me(std::true_type{});
   else load_me(std::false_type{});
+  // while the loads are in flight, exchange A's first histogram is cleared;
+  // each run's keys go into it as soon as that run has landed
+  const bool select = a.k != 0;
+  if (select) grp_hist_clear<NT>(sh.sel, sm);
   float v[R][E];
+  uint32_t zc = 0;
 #pragma unroll
-  for (int j = 0; j < R; ++j)
+  for (int j = 0; j < R; ++j) {
 #pragma unroll
     for (int i = 0; i < E; ++i) {
       float x = Elem<InT>::up(xr[j][i]);
@@ -605,6 +610,11 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
       if constexpr (SEL == SEL_AQSGD) x = x - Elem<InT>::up(mr[j][i]);
       v[j][i] = (n[j] > 0) ? x : 0.0f;     // +0 past the segment's end
     }
+    if (select) {
+#pragma unroll
+      for (int i = 0; i < E; ++i) grp_hist_add(sh.sel, mag_key(v[j][i]), zc);
+    }
+  }
   // AQSGD: the buffer row waits in LDS for the update (it is not needed
   // before), which keeps it out of registers during the selection; a run
   // past the segment's end is never stored back
@@ -621,12 +631,12 @@ __device__ __forceinline__ void grp_segment(const TopkArgs& a, bool vec, uint64_
   SelResult sr;
   uint32_t ticket = 0;
   const bool exiting = P > 1 && last_seg;
-  if (a.k == 0) {
+  if (!select) {
     // T above every finite key (the keys of finite values are at most
     // 0x7F800000), so that nothing is kept
     sr.T = 0x7FFFFFFFu; sr.r = 0; sr.gt_before = 0; sr.eq_before = 0;
   } else {
-    const SelA A = grp_exchange_a<NT, R, E, CH>(v, (uint32_t)a.k, a.L, P, part, gm, sh.sel, sm, gs);
+    const SelA A = grp_exchange_a<NT, R, E, CH>(v, zc, (uint32_t)a.k, a.L, P, part, gm, sh.sel, sm, gs);
     refresh(v);
     bool cleared = false;
     if (EARLY && A.fine && P <= REC_P_MAX) {

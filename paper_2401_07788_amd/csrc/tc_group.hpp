@@ -228,30 +228,36 @@ __device__ __forceinline__ void grp_clear_a(const GrpMem& g, uint32_t par, uint3
 // the highest indices, so with k <= L they rank after every real element and
 // are never kept; the counts below need no bounds checks.  L: the segment's
 // length, rounded to what the group covers when the guess scales k.
+// Exchange A's first histogram (bits 30..19 of every key) and its window
+// counts, cleared before the workgroup's values arrive, so that the keys of
+// each run can be counted as soon as that run's loads land.
+template <int NT, typename SH>
+__device__ __forceinline__ void grp_hist_clear(SH& sh, GrpSmall& sm) {
+  zero_lds<NT>(sh.hist, HIST_BINS);
+  if (threadIdx.x < 3 * 16) sm.fwin[threadIdx.x] = 0u;
+  __syncthreads();
+}
+// One key into it; exact zeros (common after a ReLU, and the padding) are
+// counted in the thread's zc and added once per wave by exchange A, off one
+// hot bin.
+template <typename SH>
+__device__ __forceinline__ void grp_hist_add(SH& sh, uint32_t kk, uint32_t& zc) {
+  const uint32_t z = eq31(kk, 0u);
+  zc += z;
+  atomicAdd(&sh.hist[pick(z, HIST_BINS + (uint32_t)lane_id(), kk >> 19)], 1u);
+}
+
+// Exchange A proper: every key of the workgroup is in the first histogram
+// (grp_hist_clear, then grp_hist_add per key; zc: this thread's exact zeros).
 template <int NT, int R, int E, uint32_t CH>
-__device__ __forceinline__ SelA grp_exchange_a(float (&v)[R][E], uint32_t k, uint64_t L, uint32_t P,
+__device__ __forceinline__ SelA grp_exchange_a(float (&v)[R][E], uint32_t zc, uint32_t k, uint64_t L, uint32_t P,
                                                uint32_t part, const GrpMem& g,
                                                GrpSelShared<grp_local_cap(CH)>& sh, GrpSmall& sm, GrpState& gs) {
   const int t = (int)threadIdx.x;
-  const uint32_t dummy = HIST_BINS + (uint32_t)lane_id();
   auto key = [&](int j, int i) { return mag_key(v[j][i]); };
   const uint32_t par = gs.iter & 1u;
 
-  // ---- A: bits 30..19 of every key; exact zeros (common after a ReLU, and
-  // the padding) are counted in registers and added once per wave, off one hot bin
-  zero_lds<NT>(sh.hist, HIST_BINS);
-  if (t < 3 * 16) sm.fwin[t] = 0u;
-  __syncthreads();
-  uint32_t zc = 0;
-#pragma unroll
-  for (int j = 0; j < R; ++j)
-#pragma unroll
-    for (int i = 0; i < E; ++i) {
-      const uint32_t kk = key(j, i);
-      const uint32_t z = eq31(kk, 0u);
-      zc += z;
-      atomicAdd(&sh.hist[pick(z, dummy, kk >> 19)], 1u);
-    }
+  // ---- A: the exact zeros into the first histogram, once per wave
   const uint32_t zs = wave_sum(zc);
   if (lane_id() == 0 && zs) atomicAdd(&sh.hist[0], zs);
   __syncthreads();
