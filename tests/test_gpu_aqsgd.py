@@ -53,6 +53,20 @@ def test_aqsgd_small(tc, orc, dt, L):
              check_rows=np.arange(n_samples))
 
 
+def test_aqsgd_aligned_ragged_tail(tc, orc):
+    """8 examples of 394,016 binary16 elements (a multiple of the 8-element
+    run, not of the 12,288-element chunk): three runs per thread, 33
+    workgroups per example, so the last chunk's later runs lie wholly past
+    the example's end; more examples than resident groups, so a group takes
+    a second example"""
+    n_samples, L, B = 24, 394016, 8
+    m0 = W.randn((n_samples, L), 3, 0).to(torch.float16)
+    ids = W.epoch_ids(n_samples, B, seed=2)
+    acts = [W.drifted_activation(m0, ids[t], 1, 20 + t) for t in range(2)]
+    aq_steps(tc, orc, m0, [ids[t] for t in range(2)], acts, tc.topk_count(L, 3, 10),
+             check_rows=np.arange(n_samples))
+
+
 def test_aqsgd_revisit_and_k_edges(tc, orc):
     # the same ids again (the buffer has moved), and k = 0 / k = L
     n_samples, L = 8, 50000

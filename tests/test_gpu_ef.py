@@ -105,6 +105,14 @@ def test_ef_ragged(tc, orc, dt):
     ef_quant_steps(tc, orc, ys, 5, 999, 3)
 
 
+def test_ef_group_aligned_ragged_tail(tc, orc):
+    """fp32 EF over 8 segments of 394,016 elements: six 16-byte runs per
+    thread, 33 workgroups per segment, the last chunk's later runs wholly
+    past the segment's end"""
+    xs = [W.randn((8, 394016), 6, t) for t in range(2)]
+    ef_topk_steps(tc, orc, xs, 8, 394016, tc.topk_count(394016, 1, 10))
+
+
 @pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("L", [4099, 32768])
 def test_ef_lds_engine(tc, orc, dt, L):

@@ -61,6 +61,17 @@ def test_topk_parity(tc, orc, dt, L, kind):
         run_case(tc, orc, x, n_seg, L, tc.topk_count(L, num, den))
 
 
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_topk_group_aligned_ragged_tail(tc, orc, dt):
+    """8 segments of 394,016 elements (whole 16-byte runs, not whole chunks):
+    the most runs per thread, 33 workgroups per segment, more segments than
+    resident groups, and a last chunk whose later runs lie wholly past the
+    segment's end"""
+    n_seg, L = 8, 394016
+    x = make_input("normal", n_seg, L, dt, seed=7)
+    run_case(tc, orc, x, n_seg, L, tc.topk_count(L, 1, 10))
+
+
 @pytest.mark.parametrize("L", [768, 16384, 50001])
 @pytest.mark.parametrize("kind", ["relu", "ties", "const", "zeros"])
 def test_topk_edges(tc, orc, L, kind):
