@@ -223,7 +223,7 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
         float r[QPE];
 #pragma unroll
         for (int i = 0; i < QPE; ++i) r[i] = v[j * QPE + i];
-        if (n > 0) store_run_partial<float, QPE, false>(a.e + goff + piece_at(j), n, r);
+        if (n > 0) store_run_partial<float, QPE, true>(a.e + goff + piece_at(j), n, r);
       }
     }
   }
