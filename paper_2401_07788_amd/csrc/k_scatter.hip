@@ -233,7 +233,7 @@ __global__ __launch_bounds__(SC_NT) void k_topk_scatter_row(ScatterArgs a) {
     RO* yr = (RO*)a.y + s * a.L;
     for (uint32_t q = lane; q * PER < L; q += WAVE) {
       if (vec && q * PER + PER <= L) {
-        reinterpret_cast<u32x4*>(yr)[q] = reinterpret_cast<const u32x4*>(b)[q];
+        vstore<true>(reinterpret_cast<u32x4*>(yr) + q, reinterpret_cast<const u32x4*>(b)[q]);
       } else {
         for (uint32_t c = q * PER; c < min(L, q * PER + PER); ++c) yr[c] = b[c];
       }
@@ -694,8 +694,8 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv_row(ScatterArgs a) {
     for (uint32_t q = lane; q * PER < L; q += WAVE) {
       if (vec && q * PER + PER <= L) {
         const u32x4 v4 = reinterpret_cast<const u32x4*>(b)[q];
-        reinterpret_cast<u32x4*>(row)[q] = v4;
-        reinterpret_cast<u32x4*>(out)[q] = v4;
+        vstore<true>(reinterpret_cast<u32x4*>(row) + q, v4);
+        vstore<true>(reinterpret_cast<u32x4*>(out) + q, v4);
       } else {
         for (uint32_t c = q * PER; c < min(L, q * PER + PER); ++c) {
           row[c] = b[c];
