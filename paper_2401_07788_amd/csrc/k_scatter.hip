@@ -507,7 +507,7 @@ __global__ __launch_bounds__(SC_NT) void k_efmix_scatter(ScatterArgs a) {
       RO o[4];
 #pragma unroll
       for (int c = 0; c < 4; ++c) o[c] = Elem<OutT>::down(buf[q * 4 + c]);
-      store_run_partial<RO, 4, false>(yc + q * 4, nv, o);
+      store_run_partial<RO, 4, true>(yc + q * 4, nv, o);
     }
     __syncthreads();
   }
