@@ -118,7 +118,7 @@ __global__ __launch_bounds__(WAVE) void k_topk_row(TopkArgs a) {
       if constexpr (SEL == SEL_EF) eo[i] = v[i] - (kept ? through<InT>(v[i]) : 0.0f);
     }
     if constexpr (SEL == SEL_EF) {
-      if (nv > 0) store_run_partial<float, VPT, false>(a.e + seg * a.L + c0, nv, eo);
+      if (nv > 0) store_run_partial<float, VPT, true>(a.e + seg * a.L + c0, nv, eo);
     }
     if constexpr (SEL == SEL_AQSGD) {
       if (nv > 0 && a.k > 0) store_run_partial<R, VPT, false>((R*)a.m + mrow + c0, nv, mr);
