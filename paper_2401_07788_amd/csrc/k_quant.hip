@@ -115,8 +115,8 @@ __global__ __launch_bounds__(NT) void k_quant_pack(QuantArgs a) {
       R xr[QPE];
       float er[QPE];
       if (n > 0) {
-        load_run_partial<R, QPE, false>((const R*)a.x + goff + piece_at(j), n, R{}, xr);
-        if constexpr (EF) load_run_partial<float, QPE, false>(a.e + goff + piece_at(j), n, 0.0f, er);
+        load_run_partial<R, QPE, true>((const R*)a.x + goff + piece_at(j), n, R{}, xr);
+        if constexpr (EF) load_run_partial<float, QPE, true>(a.e + goff + piece_at(j), n, 0.0f, er);
       }
 #pragma unroll
       for (int i = 0; i < QPE; ++i) {
