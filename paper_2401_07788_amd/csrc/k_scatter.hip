@@ -551,8 +551,8 @@ __global__ __launch_bounds__(SC_NT) void k_efmix_resid(EfmixResidArgs a) {
           // the chunk's first piece, unused, so that no branch stands
           // between the loads)
           const uint32_t ia = (i0 < n) ? i0 : 0u;
-          load_piece<R, false>(xc + ia, xr[q]);
-          load_piece<float, false>(ec + ia, er[q]);
+          load_piece<R, true>(xc + ia, xr[q]);
+          load_piece<float, true>(ec + ia, er[q]);
         } else {
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
@@ -929,8 +929,8 @@ __global__ __launch_bounds__(SC_NT) void k_gather_ef_row(GatherArgs a) {
         for (int p = 0; p < PPL; ++p) {
           const uint32_t q = q0 + (uint32_t)p * WAVE + lane;
           const uint32_t qa = (q * 4 < L) ? q : 0u;
-          load_piece<R, false>(xs + qa * 4, xr[p]);
-          load_piece<float, false>(es + qa * 4, er[p]);
+          load_piece<R, true>(xs + qa * 4, xr[p]);
+          load_piece<float, true>(es + qa * 4, er[p]);
         }
 #pragma unroll
         for (int p = 0; p < PPL; ++p) {

@@ -72,14 +72,14 @@ __global__ __launch_bounds__(WAVE) void k_topk_row(TopkArgs a) {
     {
       R xr[VPT];
       const uint64_t off = seg * a.L + c0;
-      if (nv > 0) load_run_partial<R, VPT, false>((const R*)a.x + off, nv, R{}, xr);
+      if (nv > 0) load_run_partial<R, VPT, true>((const R*)a.x + off, nv, R{}, xr);
       if constexpr (SEL == SEL_EF) {
         float er[VPT];
-        if (nv > 0) load_run_partial<float, VPT, false>(a.e + off, nv, 0.0f, er);
+        if (nv > 0) load_run_partial<float, VPT, true>(a.e + off, nv, 0.0f, er);
 #pragma unroll
         for (int i = 0; i < VPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) + er[i] : 0.0f;
       } else if constexpr (SEL == SEL_AQSGD) {
-        if (nv > 0) load_run_partial<R, VPT, false>((const R*)a.m + mrow + c0, nv, R{}, mr);
+        if (nv > 0) load_run_partial<R, VPT, true>((const R*)a.m + mrow + c0, nv, R{}, mr);
 #pragma unroll
         for (int i = 0; i < VPT; ++i) v[i] = (i < nv) ? Elem<InT>::up(xr[i]) - Elem<InT>::up(mr[i]) : 0.0f;
       } else {
