@@ -671,7 +671,7 @@ __global__ __launch_bounds__(SC_NT) void k_aqsgd_recv_row(ScatterArgs a) {
     R* row = (R*)a.m + (uint64_t)id * a.L;
     for (uint32_t q = lane; q * PER < L; q += WAVE) {
       if (vec && q * PER + PER <= L) {
-        reinterpret_cast<u32x4*>(b)[q] = reinterpret_cast<const u32x4*>(row)[q];
+        reinterpret_cast<u32x4*>(b)[q] = vload<true>(reinterpret_cast<const u32x4*>(row) + q);
       } else {
         for (uint32_t c = q * PER; c < min(L, q * PER + PER); ++c) b[c] = row[c];
       }
